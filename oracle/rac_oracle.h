@@ -1,0 +1,95 @@
+/*
+ * rac_oracle.h - plain single-threaded CPU oracle of the RAC aligned residual
+ * codec (Section "Quality- and Cost-Constrained Aligned Residual Encoding":
+ * Eq. affine-fit, Eq. aligned-residual, Eq. residual-quantization, the outlier
+ * paragraph, Eq. residual-reconstruction).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may call this library.  The product path (the
+ * HIP library under paper_2608_04991_amd/) never links, loads or calls it, and
+ * the two share no source, header, table or helper.
+ *
+ * Every function here takes HOST pointers.  bf16 tensors are passed as their
+ * raw 16-bit patterns (uint16_t), row-major [tokens][hidden].
+ *
+ * Parity status of each function is stated in its comment in rac_oracle.c.
+ */
+#ifndef RAC_ORACLE_H
+#define RAC_ORACLE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    ORC_OK = 0,
+    ORC_ERR_INVALID = 1,   /* configuration outside the supported domain   */
+    ORC_ERR_CAPACITY = 3,  /* wire buffer smaller than the encoded size    */
+    ORC_ERR_FORMAT = 5,    /* wire header does not describe this config    */
+    ORC_ERR_NONFINITE = 6  /* an input element is NaN or infinite          */
+};
+
+enum {
+    ORC_FLAG_FIXED_STEP = 1u << 0, /* calibrated per-channel-group step table */
+    ORC_FLAG_XHAT_BF16 = 1u << 1   /* reconstruction written as bf16 (RNE)    */
+};
+
+typedef struct {
+    int64_t tokens;       /* T: flattened token rows (B*N)                 */
+    int32_t hidden;       /* d                                             */
+    int32_t group_align;  /* g_a, power of two, divides d                  */
+    int32_t group_quant;  /* g_q, power of two, divides d                  */
+    int32_t bits;         /* q in {2,3,4,8}                                */
+    int32_t outlier_k;    /* outliers per token row, 0..min(64,d)          */
+    uint32_t flags;       /* ORC_FLAG_*                                    */
+} orc_config;
+
+/* Byte offsets of the wire sections (all 256-byte aligned). */
+typedef struct {
+    uint64_t off_coef, off_scale, off_codes, off_outl, total;
+} orc_layout;
+
+int orc_layout_of(const orc_config* cfg, orc_layout* out);
+
+/* Full encode: header + coefficients + scales + codes + outliers, and the
+ * sender-side reconstruction into xhat (may be NULL).  ref may be NULL (a zero
+ * reference).  steps is read only with ORC_FLAG_FIXED_STEP ([d/g_q] floats). */
+int orc_encode(const orc_config* cfg, const uint16_t* x, const uint16_t* ref,
+               const float* steps, uint8_t* wire, size_t wire_cap, void* xhat);
+
+/* Receiver reconstruction from a wire and the receiver's own reference. */
+int orc_decode(const orc_config* cfg, const uint8_t* wire, const uint16_t* ref,
+               const float* steps, void* xhat);
+
+/* ---- Pieces exposed so tests can pin them one at a time ---------------- */
+
+/* Exact widening of a bf16 pattern. */
+float orc_bf16_to_f32(uint16_t h);
+/* Round-to-nearest-even fp32 -> bf16 pattern. */
+uint16_t orc_f32_to_bf16(float f);
+/* Exact value of an fp16 pattern. */
+float orc_f16_to_f32(uint16_t h);
+/* Round-to-nearest-even fp32 -> fp16 pattern, magnitudes above 65504 clamp to
+ * 65504 (the largest finite fp16). */
+uint16_t orc_f16_rne_sat(float f);
+/* Smallest positive fp16 h with value(h)*qmax >= m (m >= 0 finite, qmax >= 1);
+ * 0x7BFF (65504) when no finite fp16 satisfies it. */
+uint16_t orc_scale_roundup(float m, int32_t qmax);
+/* Smallest positive fp16 h with value(h) >= step; 0x7BFF when step > 65504. */
+uint16_t orc_step_roundup(float step);
+/* Canonical pairwise sum over n = power-of-two elements. */
+float orc_tsum(const float* v, int32_t n);
+/* Affine fit of one group before wire rounding: alpha*, beta*. */
+void orc_fit_group(const float* r, const float* x, int32_t g, float* alpha_star,
+                   float* beta_star);
+/* Per-token outlier choice: the k channels with the largest |e| (ties to the
+ * lower channel), written ascending into idx[k]. */
+void orc_topk_row(const float* e, int32_t d, int32_t k, uint16_t* idx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

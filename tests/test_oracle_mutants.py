@@ -1,0 +1,75 @@
+"""Mutation check of the oracle's pins.
+
+Each case plants one plausible mistake in a temporary copy of the oracle
+source (on the CPU), builds it with gcc, and runs the pin tests against that
+build: at least one pin must fail.  This is what makes the pins a check of the
+oracle rather than a restatement of it.
+"""
+from __future__ import annotations
+
+import os
+import shutil
+import subprocess
+
+import pytest
+
+import oracle
+from tests import test_oracle_pins as pins
+
+# (name, text in rac_oracle.c, replacement)
+MUTANTS = [
+    ("beta_sign", "*beta_star = mx - a * mr;", "*beta_star = mx + a * mr;"),
+    ("uncentred_fit", "const float u = r[c] - mr;", "const float u = r[c];"),
+    ("transposed_alpha", "const float a = crx / crr;", "const float a = crr / crx;"),
+    ("zero_variance_beta", "*beta_star = mx;\n", "*beta_star = 0.0f;\n"),
+    ("scale_round_down", "    return (uint16_t)lo;\n}\n\nuint16_t orc_step_roundup",
+     "    return (uint16_t)(lo - 1);\n}\n\nuint16_t orc_step_roundup"),
+    ("half_away_from_zero", "float rq = rintf(tq);", "float rq = roundf(tq);"),
+    ("qmax_off_by_one", "const int32_t qmax = (1 << (bits - 1)) - 1;",
+     "const int32_t qmax = (1 << (bits - 1));"),
+    ("msb_first_packing", "row[pos / 8] |= (uint8_t)(1u << (pos % 8));",
+     "row[pos / 8] |= (uint8_t)(1u << (7 - pos % 8));"),
+    ("outlier_ties_to_higher", "return (a->idx < b->idx) ? -1 : (a->idx > b->idx);",
+     "return (a->idx > b->idx) ? -1 : (a->idx < b->idx);"),
+    ("outlier_left_in_dense", "                ed[c] = 0.0f;\n", "\n"),
+    ("aligned_ref_drops_beta", "                rt[c] = a * r[c] + b0;", "                rt[c] = a * r[c];"),
+    ("decoder_drops_outliers", "eh[c] = orc_f16_to_f32((uint16_t)(w >> 16));", "(void)c;"),
+    ("alpha_beta_swapped", "put16(coef + 4 * j, ah);", "put16(coef + 4 * j, bh);"),
+    ("outlier_value_unrounded_recon", "? orc_f16_to_f32(oval[c]) :", "? e[c] :"),
+    ("f16_ties_up", "p = (lo & 1u) ? lo + 1 : lo; /* tie: even fraction */",
+     "p = lo + 1; /* tie: even fraction */"),
+]
+
+PINS = [
+    pins.test_f16_rne_matches_numpy_including_ties_and_subnormals,
+    lambda: pins.test_scale_roundup_is_smallest_fp16_covering_the_max(7),
+    lambda: pins.test_fit_matches_exact_rational_least_squares(16),
+    pins.test_fit_zero_variance_reference_gives_alpha_zero_beta_mean,
+    pins.test_topk_matches_brute_force_with_ties,
+    pins.test_hand_worked_example_bit_exact,
+    lambda: pins.test_pack_known_answers_via_zero_reference(4, [1, -1, 7, -7, 0, 0, 0, 0], "f1970000"),
+    pins.test_quantizer_rounds_half_to_even,
+    pins.test_exact_affine_rows_give_zero_codes_and_exact_reconstruction,
+    pins.test_zero_reference_is_textbook_grouped_absmax_quantization,
+    lambda: pins.test_error_bound_and_equivalence_on_uplink_rows(4, 8),
+    pins.test_sender_reconstruction_equals_receiver_decode_bitwise,
+]
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_planted_mistake_fails_a_pin(tmp_path, name, old, new):
+    src = open(oracle._SRC).read()
+    assert src.count(old) == 1, f"mutation site for {name} not unique"
+    shutil.copy(os.path.join(os.path.dirname(oracle._SRC), "rac_oracle.h"), tmp_path)
+    (tmp_path / "m.c").write_text(src.replace(old, new))
+    so = str(tmp_path / "libm.so")
+    subprocess.run(["gcc", "-std=c11", "-O2", "-ffp-contract=off", "-fPIC", "-shared", "-o", so,
+                    str(tmp_path / "m.c"), "-lm"], check=True)
+    caught = []
+    with oracle.swapped_library(so):
+        for pin in PINS:
+            try:
+                pin()
+            except AssertionError:
+                caught.append(getattr(pin, "__name__", "lambda"))
+    assert caught, f"no pin caught mutant {name}"

@@ -1,0 +1,465 @@
+"""Pins of the CPU oracle against things other than itself.
+
+Each test checks the oracle against what the paper and plain mathematics fix:
+a hand-derived worked example, closed forms (exact affine data, zero-variance
+references), exact rational least squares, library number-format conversions
+(numpy float16, torch bfloat16), the error bound of Eq. error-bound, the
+error equivalence of Eq. error-equivalence, brute force on tiny inputs, and
+metamorphic relations.  A mistake such as a dropped term, a wrong sign or
+index, a transposed operand, a round-down scale, a swapped nibble order or the
+wrong tie rule fails at least one of them.
+"""
+from __future__ import annotations
+
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_04991_amd import workloads as wl
+from tests import wirefmt
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+QMAX = {2: 1, 3: 3, 4: 7, 8: 127}
+
+
+def f16val(bits):
+    return np.asarray(bits, dtype=np.uint16).view(np.float16).astype(np.float32)
+
+
+def cfgd(T, d, ga, gq, b, k=0, flags=0):
+    return dict(tokens=T, hidden=d, group_align=ga, group_quant=gq, bits=b, outlier_k=k,
+                flags=flags)
+
+
+# ---------------------------------------------------------------------------
+# Number formats, against numpy / torch conversions
+
+def test_f16_decode_all_patterns_match_numpy():
+    pats = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    finite = np.isfinite(pats.view(np.float16))
+    want = pats.view(np.float16).astype(np.float32)
+    got = np.array([oracle.f16_to_f32(int(p)) for p in pats[finite][::7]], dtype=np.float32)
+    np.testing.assert_array_equal(got.view(np.uint32), want[finite][::7].view(np.uint32))
+
+
+def test_f16_rne_matches_numpy_including_ties_and_subnormals():
+    rng = np.random.default_rng(1)
+    vals = np.concatenate([
+        rng.standard_normal(3000).astype(np.float32) * 10.0 ** rng.integers(-9, 5, 3000),
+        # exact midpoints between adjacent fp16 values (ties)
+        ((np.arange(1, 400, dtype=np.float32) + 0.5) * np.float32(2.0 ** -24)),
+        ((np.arange(1024, 1200, dtype=np.float32) + 0.5) * np.float32(2.0 ** -10)),
+        np.float32([0.0, -0.0, 65504.0, 65519.0, 6.1e-5, 5.96e-8, 2.98e-8, 2.99e-8]),
+    ]).astype(np.float32)
+    vals = np.concatenate([vals, -vals])
+    want = np.clip(vals, -65504, 65504).astype(np.float16).view(np.uint16)
+    got = np.array([oracle.f16_rne_sat(float(v)) for v in vals], dtype=np.uint16)
+    np.testing.assert_array_equal(got, want)
+
+
+def test_f16_saturates_instead_of_overflowing():
+    assert oracle.f16_rne_sat(1e6) == 0x7BFF
+    assert oracle.f16_rne_sat(-65520.0) == 0xFBFF
+
+
+def test_bf16_round_trip_matches_torch():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(2)
+    vals = rng.standard_normal(4000).astype(np.float32) * 10.0 ** rng.integers(-30, 30, 4000)
+    ties = (np.arange(1, 300, dtype=np.uint32) << 16 | 0x8000).view(np.float32)
+    vals = np.concatenate([vals, ties, -ties]).astype(np.float32)
+    want = torch.from_numpy(vals).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    got = np.array([oracle.f32_to_bf16(float(v)) for v in vals], dtype=np.uint16)
+    np.testing.assert_array_equal(got, want)
+    for h in [0x3F80, 0xC2F7, 0x0001, 0x7F7F]:
+        b = np.uint32(h) << 16
+        assert oracle.bf16_to_f32(h) == float(np.array([b], np.uint32).view(np.float32)[0])
+
+
+@pytest.mark.parametrize("q", [1, 3, 7, 127])
+def test_scale_roundup_is_smallest_fp16_covering_the_max(q):
+    rng = np.random.default_rng(3 + q)
+    ms = np.concatenate([rng.random(600) * 10.0 ** rng.integers(-8, 6, 600),
+                         [1e-12, 7.0, 0.25, 1.5, 65504.0 * q]]).astype(np.float32)
+    allf16 = np.arange(1, 0x7C00, dtype=np.uint16).view(np.float16).astype(np.float64)
+    for m in ms:
+        h = oracle.scale_roundup(float(m), q)
+        # independent brute force over every positive finite fp16 (float64 math)
+        ok = allf16 * q >= float(m)
+        want = int(np.argmax(ok)) + 1 if ok.any() else 0x7BFF
+        assert h == want, (m, q, hex(h), hex(want))
+
+
+def test_scale_roundup_saturates():
+    assert oracle.scale_roundup(1e9, 7) == 0x7BFF
+
+
+def test_step_roundup_is_smallest_fp16_not_below_step():
+    allf16 = np.arange(1, 0x7C00, dtype=np.uint16).view(np.float16).astype(np.float64)
+    for s in [0.01, 0.0333, 1.0, 3.14159, 1e-7, 0.0, 70000.0]:
+        h = oracle.step_roundup(s)
+        ok = allf16 >= np.float32(s)
+        want = int(np.argmax(ok)) + 1 if ok.any() else 0x7BFF
+        assert h == want
+
+
+# ---------------------------------------------------------------------------
+# Canonical sum
+
+def test_tsum_is_exact_on_integers_and_follows_the_pairwise_tree():
+    v = np.arange(-37, 27, dtype=np.float32)
+    assert oracle.tsum(v) == float(v.sum(dtype=np.float64))
+    # order-sensitive input: pairwise ((a+b)+(c+d)) differs from left-to-right
+    v = np.float32([1e8, 1.0, -1e8, 1.0])
+    pair = (np.float32(1e8) + np.float32(1.0)) + (np.float32(-1e8) + np.float32(1.0))
+    assert oracle.tsum(v) == float(pair) == 0.0
+    v8 = np.float32([3e7, 1, 1, 1, -3e7, 1, 1, 1])
+    l = (v8[0] + v8[1]) + (v8[2] + v8[3])
+    r = (v8[4] + v8[5]) + (v8[6] + v8[7])
+    assert oracle.tsum(v8) == float(np.float32(l + r))
+
+
+# ---------------------------------------------------------------------------
+# Affine fit (Eq. affine-fit)
+
+def _exact_ls(r, x):
+    r = [Fraction(float(v)) for v in r]
+    x = [Fraction(float(v)) for v in x]
+    n = len(r)
+    mr, mx = sum(r) / n, sum(x) / n
+    crr = sum((a - mr) ** 2 for a in r)
+    crx = sum((a - mr) * (b - mx) for a, b in zip(r, x))
+    alpha = crx / crr
+    return alpha, mx - alpha * mr
+
+
+@pytest.mark.parametrize("g", [8, 16, 64, 128])
+def test_fit_matches_exact_rational_least_squares(g):
+    rng = np.random.default_rng(10 + g)
+    for trial in range(12):
+        r = wl.bf16_bits_to_f32(wl.f32_to_bf16_bits(rng.standard_normal(g) * rng.uniform(0.1, 5)))
+        a0, b0 = rng.uniform(-2, 2), rng.normal()
+        x = wl.bf16_bits_to_f32(wl.f32_to_bf16_bits(a0 * r + b0 + 0.3 * rng.standard_normal(g)))
+        al, be = oracle.fit_group(r, x)
+        ea, eb = _exact_ls(r, x)
+        assert abs(al - float(ea)) <= 2e-5 * (1 + abs(float(ea)))
+        assert abs(be - float(eb)) <= 2e-5 * (1 + abs(float(eb)))
+        # the least-squares residual is orthogonal to [1, r] (normal equations)
+        res = [Fraction(float(xv)) - ea * Fraction(float(rv)) - eb for rv, xv in zip(r, x)]
+        assert sum(res) == 0
+
+
+def test_fit_zero_variance_reference_gives_alpha_zero_beta_mean():
+    x = np.float32([0.5, 1.5, 0.5, 1.5, 0.5, 1.5, 0.5, 9.5])
+    al, be = oracle.fit_group(np.full(8, -1.0, np.float32), x)
+    assert al == 0.0 and be == 2.0
+
+
+def test_fit_exact_affine_dyadic_data_is_exact():
+    rng = np.random.default_rng(5)
+    r = rng.integers(-32, 33, 64).astype(np.float32) / 4
+    x = np.float32(1.25) * r - np.float32(0.5)
+    al, be = oracle.fit_group(r, x)
+    assert oracle.f16_rne_sat(al) == 0x3D00  # 1.25
+    assert oracle.f16_rne_sat(be) == 0xB800  # -0.5
+
+
+# ---------------------------------------------------------------------------
+# Outlier choice
+
+def test_topk_matches_brute_force_with_ties():
+    rng = np.random.default_rng(7)
+    for trial in range(50):
+        d = 24
+        e = rng.integers(-5, 6, d).astype(np.float32) / 2  # many ties, signed zeros
+        e[rng.integers(0, d)] = -0.0
+        k = int(rng.integers(1, 9))
+        got = oracle.topk_row(e, k)
+        order = sorted(range(d), key=lambda c: (-abs(float(e[c])), c))
+        assert list(got) == sorted(order[:k])
+
+
+# ---------------------------------------------------------------------------
+# Whole codec: worked example, known answers, closed forms
+
+def test_hand_worked_example_bit_exact():
+    ex = json.load(open(os.path.join(GOLDEN, "worked_example_d16.json")))
+    c = ex["config"]
+    x = wl.f32_to_bf16_bits(np.float32(ex["x"]).reshape(1, -1))
+    ref = wl.f32_to_bf16_bits(np.float32(ex["ref"]).reshape(1, -1))
+    rc, wire, xhat = oracle.encode(x, ref, **c)
+    assert rc == 0
+    s = wirefmt.sections(wire)
+    coef = [[f"{v:04X}" for v in grp] for grp in s["coef"][0]]
+    assert coef == ex["coef_f16_hex"]
+    assert [f"{v:04X}" for v in s["scale"][0]] == ex["scale_f16_hex"]
+    assert s["codes"][0].tobytes().hex() == ex["code_bytes_hex"]
+    assert list(wirefmt.unpack_codes(s["codes"], 16, 4)[0]) == ex["codes"]
+    assert [[int(w & 0xFFFF), f"{int(w >> 16):04X}"] for w in s["outl"][0]] == ex["outliers"]
+    np.testing.assert_array_equal(xhat[0], np.float32(ex["xhat"]))
+    rc, xdec = oracle.decode(wire, ref, **c)
+    assert rc == 0
+    np.testing.assert_array_equal(xdec.view(np.uint32), xhat.view(np.uint32))
+
+
+@pytest.mark.parametrize("bits,codes,hexbytes", [
+    (4, [1, -1, 7, -7, 0, 0, 0, 0], "f1970000"),
+    (2, [1, -1, 0, 1, -1, 0, 0, 0], "4d03"),
+    (3, [1, -1, 3, -3, 2, 0, -1, -1], "f92afc"),
+    (8, [1, -1, 127, -127, 5, 0, 0, -5], "01ff7f810500 00fb".replace(" ", "")),
+])
+def test_pack_known_answers_via_zero_reference(bits, codes, hexbytes):
+    # zero reference => alpha = 0, beta = mean(x) = 0 here; max |x| = Qmax
+    # makes the scale exactly 1, so the codes equal x
+    q = QMAX[bits]
+    x = np.float32(codes) * (np.float32(1.0))
+    assert abs(x).max() == q and x.sum() == 0
+    xb = wl.f32_to_bf16_bits(x.reshape(1, 8))
+    rc, wire, xhat = oracle.encode(xb, None, **cfgd(1, 8, 8, 8, bits))
+    assert rc == 0
+    s = wirefmt.sections(wire)
+    assert s["scale"][0, 0] == 0x3C00
+    assert s["codes"][0].tobytes().hex() == hexbytes
+    np.testing.assert_array_equal(xhat[0], x)
+
+
+def test_quantizer_rounds_half_to_even():
+    x = np.float32([7, -7, 2.5, -2.5, 1.5, 0, 0.5, -2.0])  # mean 0, max 7 -> scale 1
+    xb = wl.f32_to_bf16_bits(x.reshape(1, 8))
+    rc, wire, xhat = oracle.encode(xb, None, **cfgd(1, 8, 8, 8, 4))
+    got = wirefmt.unpack_codes(wirefmt.sections(wire)["codes"], 8, 4)[0]
+    assert list(got) == [7, -7, 2, -2, 2, 0, 0, -2]
+
+
+def test_exact_affine_rows_give_zero_codes_and_exact_reconstruction():
+    rng = np.random.default_rng(11)
+    T, d = 6, 256
+    r = rng.integers(-32, 33, (T, d)).astype(np.float32) / 4
+    x = np.float32(1.25) * r - np.float32(0.5)
+    xb, rb = wl.f32_to_bf16_bits(x), wl.f32_to_bf16_bits(r)
+    assert np.array_equal(wl.bf16_bits_to_f32(xb), x)
+    for k in (0, 5):
+        c = cfgd(T, d, 64, 32, 4, k)
+        rc, wire, xhat = oracle.encode(xb, rb, **c)
+        assert rc == 0
+        s = wirefmt.sections(wire)
+        assert np.all(s["coef"][..., 0] == 0x3D00) and np.all(s["coef"][..., 1] == 0xB800)
+        assert np.all(s["scale"] == 0) and np.all(s["codes"] == 0)
+        np.testing.assert_array_equal(xhat, x)
+        if k:  # all residuals tie at zero: the lowest channels are chosen
+            assert np.all((s["outl"] & 0xFFFF) == np.arange(k))
+            assert np.all((s["outl"] >> 16) == 0)
+
+
+def test_zero_reference_is_textbook_grouped_absmax_quantization():
+    """ref = 0 reduces to symmetric absmax quantization of x - mean per group
+    (the zero-variance rule), written here from the textbook in float64."""
+    rng = np.random.default_rng(12)
+    T, d, g, bits = 8, 128, 32, 4
+    q = QMAX[bits]
+    xb = wl.f32_to_bf16_bits(rng.standard_normal((T, d)) * 3 + 0.7)
+    x = wl.bf16_bits_to_f32(xb).astype(np.float64)
+    rc, wire, xhat = oracle.encode(xb, None, **cfgd(T, d, g, g, bits))
+    s = wirefmt.sections(wire)
+    xg = x.reshape(T, d // g, g)
+    beta = xg.mean(axis=2).astype(np.float16)                # fp16 of the mean
+    e = xg - beta.astype(np.float64)[..., None]
+    m = np.abs(e).max(axis=2)
+    allf16 = np.arange(1, 0x7C00, dtype=np.uint16).view(np.float16).astype(np.float64)
+    scale = allf16[np.searchsorted(allf16 * q, m)]           # round the scale up
+    codes = np.clip(np.rint(e / scale[..., None]), -q, q)
+    assert np.array_equal(s["coef"][..., 0], np.zeros((T, d // g), np.uint16))
+    assert np.array_equal(s["coef"][..., 1], beta.view(np.uint16))
+    assert np.array_equal(f16val(s["scale"]), scale.astype(np.float32))
+    assert np.array_equal(wirefmt.unpack_codes(s["codes"], d, bits), codes.reshape(T, d))
+    want = beta.astype(np.float64)[..., None] + codes * scale[..., None]
+    np.testing.assert_allclose(xhat, want.reshape(T, d), rtol=1e-6, atol=1e-6)
+
+
+# ---------------------------------------------------------------------------
+# Bounds and identities on generator data
+
+def _recompute(wire, xb, rb, T, d, ga, gq, bits, k):
+    """E, E-hat and the dense mask from the wire, in numpy binary32."""
+    s = wirefmt.sections(wire)
+    x = wl.bf16_bits_to_f32(xb)
+    r = np.zeros_like(x) if rb is None else wl.bf16_bits_to_f32(rb)
+    a = np.repeat(f16val(s["coef"][..., 0]), ga, axis=1)
+    b = np.repeat(f16val(s["coef"][..., 1]), ga, axis=1)
+    rt = a * r + b                       # numpy float32: two roundings, no FMA
+    e = x - rt
+    sc = np.repeat(f16val(s["scale"]), gq, axis=1)
+    codes = wirefmt.unpack_codes(s["codes"], d, bits)
+    eh = codes.astype(np.float32) * sc
+    dense = np.ones((T, d), bool)
+    if k:
+        idx = (s["outl"] & 0xFFFF).astype(np.int64)
+        val = f16val((s["outl"] >> 16).astype(np.uint16))
+        rows = np.repeat(np.arange(T), k)
+        dense[rows, idx.ravel()] = False
+        eh[rows, idx.ravel()] = val.ravel()
+    return dict(x=x, rt=rt, e=e, eh=eh, sc=sc, codes=codes, dense=dense, s=s)
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4, 8])
+@pytest.mark.parametrize("k", [0, 8])
+def test_error_bound_and_equivalence_on_uplink_rows(bits, k):
+    T, d, g = 24, 1024, 128
+    xb, rb, _ = wl.prefill_uplink(0, rows=(0, T), hidden=d)
+    rc, wire, xhat = oracle.encode(xb, rb, **cfgd(T, d, g, g, bits, k))
+    assert rc == 0
+    v = _recompute(wire, xb, rb, T, d, g, g, bits, k)
+    q = QMAX[bits]
+    # Eq. error-equivalence: H - H_hat = E - E_hat (one binary32 rounding apart)
+    ulp = np.spacing(np.abs(xhat)) + np.spacing(np.abs(v["x"]))
+    assert np.all(np.abs((v["x"] - xhat) - (v["e"] - v["eh"])) <= ulp)
+    # Eq. error-bound per dense element: |E - DQ(q)| <= s/2 (+ binary32 slack)
+    err = np.abs(v["x"].astype(np.float64) - xhat)
+    slack = v["sc"] * q * 2.0 ** -22 + np.spacing(np.abs(v["e"])) + np.spacing(np.abs(xhat))
+    dense = v["dense"]
+    assert np.all(err[dense] <= v["sc"][dense] / 2 + slack[dense])
+    # no dense clipping: |code| <= Qmax and every nonzero group reaches Qmax
+    assert np.abs(v["codes"]).max() <= q
+    cg = np.abs(v["codes"]).reshape(T, d // g, g).max(axis=2)
+    sg = v["s"]["scale"]
+    normal = f16val(sg) >= 2.0 ** -14
+    assert np.all(cg[normal] == q)
+    # the scale is the smallest fp16 covering the dense max
+    ed = np.where(dense, v["e"], 0).reshape(T, d // g, g)
+    m = np.abs(ed).max(axis=2)
+    assert np.all(f16val(sg) * q >= m)
+    below = (sg.astype(np.int32) - 1).clip(0).astype(np.uint16)
+    assert np.all((f16val(below) * q < m) | (sg <= 1))
+    # outliers: exact fp16 of E, chosen as the k largest |E| per row
+    if k:
+        idx = (v["s"]["outl"] & 0xFFFF).astype(np.int64)
+        assert np.all(np.diff(idx, axis=1) > 0)
+        vals = (v["s"]["outl"] >> 16).astype(np.uint16)
+        e_at = np.take_along_axis(v["e"], idx, axis=1)
+        assert np.array_equal(vals, np.clip(e_at, -65504, 65504).astype(np.float16).view(np.uint16))
+        ae = np.abs(v["e"])
+        kth = np.sort(ae, axis=1)[:, -k]
+        assert np.all(np.take_along_axis(ae, idx, axis=1) >= kth[:, None])
+        assert np.all(ae[dense].reshape(T, d - k) <= kth[:, None])
+        err_o = np.abs(v["x"] - xhat)[~dense].reshape(T, k)
+        assert np.all(err_o <= np.abs(e_at - f16val(vals)) + np.spacing(np.abs(xhat[~dense]).reshape(T, k)) * 2)
+
+
+def test_sender_reconstruction_equals_receiver_decode_bitwise():
+    T, d = 16, 512
+    xb, rb, _ = wl.prefill_uplink(3, rows=(0, T), hidden=d)
+    for flags in (0, oracle.FLAG_XHAT_BF16):
+        c = cfgd(T, d, 64, 128, 4, 4, flags)
+        rc, wire, xhat = oracle.encode(xb, rb, **c)
+        rc2, xdec = oracle.decode(wire, rb, **c)
+        assert rc == rc2 == 0
+        assert np.array_equal(xhat.view(np.uint8), xdec.view(np.uint8))
+    # the bf16 output is the RNE rounding of the fp32 output
+    rc, w32, x32 = oracle.encode(xb, rb, **cfgd(T, d, 64, 128, 4, 4, 0))
+    assert np.array_equal(xhat, wl.f32_to_bf16_bits(x32))
+
+
+def test_wire_layout_closed_form_and_zero_padding():
+    for c in [cfgd(4096, 4096, 128, 128, 4, 8), cfgd(3, 520, 8, 8, 3, 64),
+              cfgd(0, 64, 64, 64, 2), cfgd(5, 256, 32, 16, 8, 0, oracle.FLAG_FIXED_STEP)]:
+        assert oracle.layout(**c) == wirefmt.expected_layout(**c)
+    assert oracle.layout(**cfgd(4096, 4096, 128, 128, 4, 8))["total"] == 9306368  # 27.7% of bf16
+    T, d = 5, 520
+    xb, rb, _ = wl.affine_pair(wl.AffineRecipe(T, d, 8), 0)
+    rc, wire, _ = oracle.encode(xb, rb, **cfgd(T, d, 8, 8, 3, 7))
+    h = wirefmt.header(wire)
+    assert h["magic"] == wirefmt.MAGIC and h["version"] == 1 and h["flags"] == 1
+    assert wirefmt.padding_is_zero(wire)
+
+
+def test_metamorphic_power_of_two_scaling():
+    """Scaling x and ref by 2^p leaves codes, alpha and outlier channels
+    unchanged and scales beta, the scales, the outlier values and x-hat by
+    2^p.  Exact only away from fp16 subnormals, so rows holding a serialized
+    beta or scale below 2^-10 are left out."""
+    T, d, g = 32, 512, 64
+    xb, rb, _ = wl.tiny(0, rows=(0, T))
+    c = cfgd(T, d, g, g, 4, 3)
+    rc, w1, h1 = oracle.encode(xb, rb, **c)
+    s1 = wirefmt.sections(w1)
+    beta = np.abs(f16val(s1["coef"][..., 1]))
+    safe = np.all((beta >= 2.0 ** -10) | (beta == 0), axis=1) & np.all(
+        f16val(s1["scale"]) >= 2.0 ** -10, axis=1)
+    assert safe.sum() >= 8
+    for p in (-3, 2):
+        f = np.float32(2.0 ** p)
+        xs = wl.f32_to_bf16_bits(wl.bf16_bits_to_f32(xb) * f)
+        rs = wl.f32_to_bf16_bits(wl.bf16_bits_to_f32(rb) * f)
+        rc, w2, h2 = oracle.encode(xs, rs, **c)
+        s2 = wirefmt.sections(w2)
+        assert np.array_equal(s1["codes"][safe], s2["codes"][safe])
+        assert np.array_equal(s1["coef"][safe, :, 0], s2["coef"][safe, :, 0])     # alpha
+        np.testing.assert_array_equal(f16val(s1["coef"][safe, :, 1]) * f,
+                                      f16val(s2["coef"][safe, :, 1]))
+        np.testing.assert_array_equal(f16val(s1["scale"][safe]) * f, f16val(s2["scale"][safe]))
+        assert np.array_equal(s1["outl"][safe] & 0xFFFF, s2["outl"][safe] & 0xFFFF)
+        np.testing.assert_array_equal(h1[safe] * f, h2[safe])
+
+
+def test_metamorphic_token_permutation():
+    T, d = 12, 512
+    xb, rb, _ = wl.prefill_uplink(1, rows=(0, T), hidden=d)
+    c = cfgd(T, d, 128, 128, 4, 8)
+    perm = np.random.default_rng(0).permutation(T)
+    _, w1, h1 = oracle.encode(xb, rb, **c)
+    _, w2, h2 = oracle.encode(xb[perm], rb[perm], **c)
+    s1, s2 = wirefmt.sections(w1), wirefmt.sections(w2)
+    for key in ("coef", "scale", "codes", "outl"):
+        assert np.array_equal(s1[key][perm], s2[key])
+    assert np.array_equal(h1[perm], h2)
+
+
+def test_fixed_step_mode_clips_and_bounds_unclipped_error():
+    T, d, g, bits = 16, 512, 64, 4
+    xb, rb, _ = wl.tiny(0, rows=(0, T))
+    steps = np.full(d // g, 0.02, np.float32)
+    c = cfgd(T, d, g, g, bits, 0, oracle.FLAG_FIXED_STEP)
+    rc, wire, xhat = oracle.encode(xb, rb, steps, **c)
+    assert rc == 0 and wirefmt.sections(wire)["scale"] is None
+    s = wirefmt.sections(wire)
+    codes = wirefmt.unpack_codes(s["codes"], d, bits)
+    step = f16val(oracle.step_roundup(0.02))
+    assert step >= np.float32(0.02)
+    x = wl.bf16_bits_to_f32(xb)
+    a = np.repeat(f16val(s["coef"][..., 0]), g, axis=1)
+    b = np.repeat(f16val(s["coef"][..., 1]), g, axis=1)
+    e = x - (a * wl.bf16_bits_to_f32(rb) + b)
+    unclipped = np.abs(codes) < QMAX[bits]
+    assert np.all(np.abs(e - codes * step)[unclipped] <= step / 2 * (1 + 1e-6) + 1e-6)
+    assert np.all(np.sign(codes[~unclipped]) == np.sign(e[~unclipped]))
+    rc, xdec = oracle.decode(wire, rb, steps, **c)
+    assert np.array_equal(xdec, xhat)
+
+
+# ---------------------------------------------------------------------------
+# Error paths
+
+def test_error_paths():
+    xb = np.zeros((2, 64), np.uint16)
+    good = cfgd(2, 64, 64, 64, 4)
+    for bad in [dict(bits=5), dict(group_align=48), dict(group_quant=128), dict(outlier_k=65),
+                dict(hidden=60), dict(tokens=-1), dict(flags=8)]:
+        c = dict(good, **bad)
+        with pytest.raises(ValueError):
+            oracle.layout(**c)
+    lay = oracle.layout(**good)
+    rc, _, _ = oracle.encode(xb, None, wire_cap=lay["total"] - 1, **good)
+    assert rc == oracle.ORC_ERR_CAPACITY
+    xn = xb.copy()
+    xn[1, 3] = 0x7FC0  # NaN
+    rc, _, _ = oracle.encode(xn, None, **good)
+    assert rc == oracle.ORC_ERR_NONFINITE
+    rc, wire, _ = oracle.encode(xb, None, **good)
+    bad = wire.copy()
+    bad[0] ^= 1
+    assert oracle.decode(bad, None, **good)[0] == oracle.ORC_ERR_FORMAT
+    assert oracle.decode(wire, None, **dict(good, bits=8))[0] == oracle.ORC_ERR_FORMAT

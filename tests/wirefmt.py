@@ -1,0 +1,94 @@
+"""Test-side reader of the RAC wire format (header + sections), in numpy.
+
+Written against the documented layout only, so tests can inspect wires from
+either the oracle or the HIP library without trusting either one's code:
+
+  0  u32 magic 'RAC1'   4 u16 version   6 u16 flags (1 outliers, 2 fixed step,
+                                                      4 zero reference)
+  8  u32 tokens        12 u32 hidden   16 u32 g_a   20 u32 g_q
+  24 u8 bits  25 u8 coef fmt  26 u8 scale fmt  27 u8 outlier fmt  28 u16 k
+  32 u64 off_coef  40 off_scale  48 off_codes  56 off_outl  64 total
+  sections 256-byte aligned, zero padded.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+MAGIC = 0x31434152
+
+
+def up256(v: int) -> int:
+    return (v + 255) // 256 * 256
+
+
+def expected_layout(tokens, hidden, group_align, group_quant, bits, outlier_k=0, flags=0):
+    coef = tokens * (hidden // group_align) * 4
+    scale = 0 if (flags & 1) else tokens * (hidden // group_quant) * 2
+    codes = tokens * hidden * bits // 8
+    outl = tokens * outlier_k * 4
+    off_coef = 256
+    off_scale = up256(off_coef + coef)
+    off_codes = up256(off_scale + scale)
+    off_outl = up256(off_codes + codes)
+    total = up256(off_outl + outl)
+    return dict(off_coef=off_coef, off_scale=off_scale, off_codes=off_codes,
+                off_outl=off_outl, total=total)
+
+
+def header(wire: np.ndarray) -> dict:
+    w = np.asarray(wire, dtype=np.uint8)
+    u32 = lambda o: int(w[o:o + 4].view(np.uint32)[0])
+    u16 = lambda o: int(w[o:o + 2].view(np.uint16)[0])
+    u64 = lambda o: int(w[o:o + 8].view(np.uint64)[0])
+    return dict(magic=u32(0), version=u16(4), flags=u16(6), tokens=u32(8), hidden=u32(12),
+                group_align=u32(16), group_quant=u32(20), bits=int(w[24]), coef_fmt=int(w[25]),
+                scale_fmt=int(w[26]), outl_fmt=int(w[27]), outlier_k=u16(28),
+                off_coef=u64(32), off_scale=u64(40), off_codes=u64(48), off_outl=u64(56),
+                total=u64(64))
+
+
+def sections(wire: np.ndarray) -> dict:
+    """Split a wire into typed per-row arrays (views)."""
+    w = np.asarray(wire, dtype=np.uint8)
+    h = header(w)
+    T, d, ga, gq, b, k = (h["tokens"], h["hidden"], h["group_align"], h["group_quant"],
+                          h["bits"], h["outlier_k"])
+    fixed = bool(h["flags"] & 2)
+    out = {"header": h}
+    n = T * (d // ga) * 2
+    out["coef"] = w[h["off_coef"]:h["off_coef"] + 2 * n].view(np.uint16).reshape(T, d // ga, 2)
+    if fixed:
+        out["scale"] = None
+    else:
+        n = T * (d // gq)
+        out["scale"] = w[h["off_scale"]:h["off_scale"] + 2 * n].view(np.uint16).reshape(T, d // gq)
+    n = T * d * b // 8
+    out["codes"] = w[h["off_codes"]:h["off_codes"] + n].reshape(T, d * b // 8)
+    n = T * k
+    out["outl"] = w[h["off_outl"]:h["off_outl"] + 4 * n].view(np.uint32).reshape(T, k)
+    return out
+
+
+def unpack_codes(code_rows: np.ndarray, hidden: int, bits: int) -> np.ndarray:
+    """Signed integer codes [T, hidden] from packed rows (LSB-first bit string)."""
+    rows = np.asarray(code_rows, dtype=np.uint8)
+    bitstr = np.unpackbits(rows, axis=1, bitorder="little")[:, :hidden * bits]
+    bitstr = bitstr.reshape(rows.shape[0], hidden, bits).astype(np.int64)
+    u = (bitstr << np.arange(bits, dtype=np.int64)).sum(axis=2)
+    return np.where(u >= (1 << (bits - 1)), u - (1 << bits), u)
+
+
+def padding_is_zero(wire: np.ndarray) -> bool:
+    """Every byte outside the header fields and the sections is zero."""
+    w = np.asarray(wire, dtype=np.uint8)
+    h = header(w)
+    T, d, ga, gq, b, k = (h["tokens"], h["hidden"], h["group_align"], h["group_quant"],
+                          h["bits"], h["outlier_k"])
+    used = np.zeros(w.size, dtype=bool)
+    used[:72] = True
+    used[h["off_coef"]:h["off_coef"] + T * (d // ga) * 4] = True
+    if not (h["flags"] & 2):
+        used[h["off_scale"]:h["off_scale"] + T * (d // gq) * 2] = True
+    used[h["off_codes"]:h["off_codes"] + T * d * b // 8] = True
+    used[h["off_outl"]:h["off_outl"] + T * k * 4] = True
+    return bool(np.all(w[~used] == 0)) and bool(np.all(w[30:32] == 0))
