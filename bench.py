@@ -1,0 +1,235 @@
+"""Benchmark of the RAC codec hot path on one MI355X.
+
+One step = one pass of the whole hot path over one batch of the prefill-uplink
+workload (Llama-3-8B-shaped boundary state: 4096 tokens x 4096 hidden bf16,
+alignment/quantization group 128, 4-bit codes, top-8 outliers per token):
+rac_encode with the fused sender reconstruction, then the receiver's
+rac_decode, on one stream.  Inputs are resident in HBM before timing starts;
+batches rotate through enough buffer sets (> 1 GB) that no step finds its
+inputs in the 256 MB Infinity Cache.
+
+Prints ONE JSON line:
+  value       bf16 activation bytes processed per second (2*T*d per step), GB/s
+  roofline    the encode kernel (the dominant one): algorithmic bytes per
+              launch / its average HIP-event duration, against 8 TB/s
+  cpu_baseline the CPU oracle (single thread) on the same step
+  extras      encode-only and decode-only rates, decode-phase µs per call at
+              batch 1/16/64/256 (GLM-4-9B-shaped, 4096 hidden)
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "encode_prefill_uplink_4096x4096_traffic.json")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(T, d, wire_bytes, xhat_bytes_per_elem=4, encode=True):
+    """Minimum bytes one launch must move: encode reads x and ref and writes
+    the wire and x-hat; decode reads the wire and ref and writes x-hat."""
+    elems = T * d
+    if encode:
+        return elems * 2 + elems * 2 + wire_bytes + elems * xhat_bytes_per_elem
+    return wire_bytes + elems * 2 + elems * xhat_bytes_per_elem
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the codec shards by token rows with no "
+              "exchange between GPUs, so multi-GPU runs are not part of this benchmark.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2608_04991_amd as rac
+    from paper_2608_04991_amd import workloads as wl
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    rac.library()
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda()
+
+    T, d, g, b, k = 4096, 4096, 128, 4, 8
+    cfg = rac.RacConfig(T, d, g, g, b, k)
+    wbytes = rac.rac_wire_size(cfg)
+    log("[bench] generating the prefill-uplink workload")
+    xb, rb, _ = wl.prefill_uplink(0)
+    x0, r0 = dev(xb), dev(rb)
+    set_bytes = 2 * T * d * 2 + 2 * T * d * 4 + wbytes
+    nsets = max(2, int(np.ceil(1.2e9 / set_bytes)))
+    sets = []
+    for i in range(nsets):
+        sets.append(dict(x=x0.clone(), ref=r0.clone(),
+                         wire=torch.empty(wbytes, dtype=torch.uint8, device="cuda"),
+                         xhat=torch.empty(T, d, dtype=torch.float32, device="cuda"),
+                         xdec=torch.empty(T, d, dtype=torch.float32, device="cuda")))
+    stream = torch.cuda.current_stream()
+
+    def step(i, ev=None):
+        s = sets[i % nsets]
+        if ev is not None:
+            ev[0].record(stream)
+        rac.rac_encode(cfg, s["x"], s["ref"], None, s["wire"], s["xhat"], stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        rac.rac_decode(cfg, s["wire"], s["ref"], None, s["xdec"], stream=stream)
+        if ev is not None:
+            ev[2].record(stream)
+
+    log(f"[bench] warmup {args.warmup} steps ({nsets} rotating buffer sets)")
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    log(f"[bench] timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i, evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    enc_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    dec_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
+    ms_per_step = wall * 1e3 / args.steps
+    act_bytes = T * d * 2
+    value = act_bytes / (ms_per_step * 1e-3) / 1e9
+
+    # parity spot check of the timed configuration (first rows) vs the sender
+    s0 = sets[0]
+    assert torch.equal(s0["xhat"], s0["xdec"]), "sender and receiver reconstructions differ"
+
+    enc_alg = algorithmic_bytes(T, d, wbytes)
+    dec_alg = algorithmic_bytes(T, d, wbytes, encode=False)
+    enc_avg_s = float(enc_ms.mean()) * 1e-3
+    achieved = enc_alg / enc_avg_s / 1e9
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        try:
+            traffic = json.load(open(TRAFFIC_FILE)).get("bytes_per_launch")
+        except Exception:
+            traffic = None
+    out = {
+        "metric": "encode+reconstruct GB/s of bf16 activation & % HBM peak; decode-step µs/call",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "prefill uplink, Llama-3-8B-shaped: x,ref bf16 4096 tokens x 4096 hidden, "
+                               "group 128, 4-bit, top-8 outliers/token; step = rac_encode (fused sender "
+                               "reconstruction, fp32) + rac_decode",
+                   "tokens": T, "hidden": d, "group": g, "bits": b, "outlier_k": k,
+                   "wire_bytes": wbytes, "rotating_buffer_sets": nsets},
+        "roofline": {"kernel": "rac_encode_kernel<4,8>", "bound": "hbm",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                     "algorithmic_bytes_per_launch": enc_alg,
+                     "avg_launch_us": round(enc_avg_s * 1e6, 3)},
+    }
+    extras = {
+        "encode_recon_GBps_activation": round(act_bytes / enc_avg_s / 1e9, 1),
+        "encode_us": round(enc_avg_s * 1e6, 2),
+        "decode_us": round(float(dec_ms.mean()) * 1e3, 2),
+        "decode_GBps_activation": round(act_bytes / (float(dec_ms.mean()) * 1e-3) / 1e9, 1),
+        "decode_hbm_frac": round(dec_alg / (float(dec_ms.mean()) * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+    }
+    if not args.no_extras:
+        extras["decode_step"] = decode_step_latency(torch, rac, wl, dev, stream)
+    out["extras"] = extras
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(xb, rb, cfg)
+    print(json.dumps(out), flush=True)
+
+
+def decode_step_latency(torch, rac, wl, dev, stream):
+    """µs per call of rac_encode and rac_decode for decode-phase batches
+    (1 token per sequence, 4096 hidden, group 128, 4-bit, no outliers):
+    wall time per call with back-to-back launches, and kernel time from
+    HIP events."""
+    res = {}
+    for B in (1, 16, 64, 256):
+        cfg = rac.RacConfig(B, 4096, 128, 128, 4, 0)
+        xb, rb = wl.decode_step(B)
+        x, ref = dev(xb), dev(rb)
+        wire = torch.empty(rac.rac_wire_size(cfg), dtype=torch.uint8, device="cuda")
+        xh = torch.empty(B, 4096, dtype=torch.float32, device="cuda")
+        xd = torch.empty_like(xh)
+        for _ in range(20):
+            rac.rac_encode(cfg, x, ref, None, wire, xh, stream=stream)
+            rac.rac_decode(cfg, wire, ref, None, xd, stream=stream)
+        torch.cuda.synchronize()
+        n = 200
+        t0 = time.perf_counter()
+        for _ in range(n):
+            rac.rac_encode(cfg, x, ref, None, wire, xh, stream=stream)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for _ in range(n):
+            rac.rac_decode(cfg, wire, ref, None, xd, stream=stream)
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ke, kd = [], []
+        for _ in range(20):
+            e[0].record(stream)
+            rac.rac_encode(cfg, x, ref, None, wire, xh, stream=stream)
+            e[1].record(stream)
+            rac.rac_decode(cfg, wire, ref, None, xd, stream=stream)
+            e[2].record(stream)
+            torch.cuda.synchronize()
+            ke.append(e[0].elapsed_time(e[1]))
+            kd.append(e[1].elapsed_time(e[2]))
+        res[f"B{B}"] = {"encode_us_per_call": round((t1 - t0) / n * 1e6, 2),
+                        "decode_us_per_call": round((t2 - t1) / n * 1e6, 2),
+                        "encode_event_us": round(float(np.median(ke)) * 1e3, 2),
+                        "decode_event_us": round(float(np.median(kd)) * 1e3, 2)}
+    return res
+
+
+def cpu_baseline(xb, rb, cfg):
+    """The CPU oracle, single-threaded, on the same step (all 4096 rows:
+    encode with sender reconstruction, then decode)."""
+    import oracle
+    c = dict(tokens=cfg.tokens, hidden=cfg.hidden, group_align=cfg.group_align,
+             group_quant=cfg.group_quant, bits=cfg.bits, outlier_k=cfg.outlier_k, flags=cfg.flags)
+    log("[bench] CPU oracle baseline (one step, single thread)")
+    t0 = time.perf_counter()
+    rc, wire, _ = oracle.encode(xb, rb, **c)
+    rc2, _ = oracle.decode(wire, rb, **c)
+    dt = time.perf_counter() - t0
+    assert rc == 0 and rc2 == 0
+    return {"value": round(cfg.tokens * cfg.hidden * 2 / dt / 1e9, 5), "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"one full step: {cfg.tokens}x{cfg.hidden} encode (with sender reconstruction) "
+                      f"+ decode, {dt:.2f} s on {os.cpu_count()} visible cores, 1 used"}
+
+
+if __name__ == "__main__":
+    main()

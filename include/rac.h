@@ -1,0 +1,165 @@
+/*
+ * rac.h - C ABI of the MI355X (gfx950) RAC aligned residual codec.
+ *
+ * The codec is the one of the paper's Section "Quality- and Cost-Constrained
+ * Aligned Residual Encoding".  A boundary hidden state H ([tokens x hidden],
+ * bf16, row-major) is coded against a reference R of the same shape:
+ *
+ *   1. grouped affine alignment (Eq. affine-fit): for every token row and
+ *      every group of g_a channels, the least-squares pair (alpha*, beta*) of
+ *      x ~ alpha*r + beta; a zero-variance reference group gives alpha* = 0,
+ *      beta* = mean(x).  Both ends use the fp16-serialized pair.
+ *   2. aligned residual (Eq. aligned-residual): E = H - (alpha R + beta).
+ *   3. outliers (paragraph "Outlier Metadata and Calibration"): optionally the
+ *      k largest |E| of each token row leave the dense base and travel as
+ *      (channel, fp16 value); ties go to the lower channel.
+ *   4. grouped symmetric quantization (Eq. residual-quantization): per group of
+ *      g_q channels, Qmax = 2^(q-1)-1, the scale is the smallest fp16 s with
+ *      s*Qmax >= max|E^d| (rounded up, so nothing clips), codes are
+ *      round-half-even(E^d / s); an all-zero group carries scale 0.
+ *   5. reconstruction (Eq. residual-reconstruction): H-hat = R~ + E-hat, with
+ *      E-hat = q*s on the dense base and the fp16 value at outliers.
+ *
+ * Arithmetic is IEEE binary32 with a fixed evaluation order (pairwise sums
+ * over channel order, two-pass centred moments, no fused multiply-add), so the
+ * sender's reconstruction, the receiver's decode and an independent CPU
+ * implementation agree bit for bit.
+ *
+ * Conventions shared by every entry point:
+ *   - All tensor and wire pointers are DEVICE pointers on the current HIP
+ *     device; the caller owns every buffer.  The library allocates nothing,
+ *     frees nothing, never synchronizes and keeps no global state.
+ *   - bf16 tensors (x, ref) are passed as raw 16-bit patterns, row-major
+ *     [tokens][hidden]; x, ref and xhat must be 16-byte aligned and the wire
+ *     256-byte aligned.
+ *   - Work is enqueued on `stream` (a hipStream_t; 0 is the null stream) and
+ *     is stream-ordered; calls are reentrant.  Calls on different streams may
+ *     run concurrently as long as their output buffers do not overlap.
+ *   - Argument errors are reported synchronously, before anything is
+ *     enqueued.  RAC_ERR_HIP reports a failed kernel launch.  Kernels never
+ *     trap; inputs must be finite (results for NaN/Inf inputs are unspecified
+ *     but every memory access stays in bounds).
+ *   - Saturation: coefficients, scales and outlier values are fp16; values
+ *     beyond 65504 in magnitude are clamped to +-65504, which the caller can
+ *     detect in the wire.
+ *
+ * Wire format (little-endian, self-describing, all padding zero):
+ *   header (256 B): u32 magic 'RAC1', u16 version 1, u16 flags (1 outliers,
+ *     2 fixed step, 4 encoded against a zero reference), u32 tokens,
+ *     u32 hidden, u32 g_a, u32 g_q, u8 bits, u8 coef fmt (1 = fp16 pair),
+ *     u8 scale fmt (1 = fp16, 0 = absent), u8 outlier fmt (1 = u16 channel in
+ *     the low half and fp16 value in the high half of a u32, 0 = absent),
+ *     u16 k, u16 0, then u64 offsets of the coef, scale, code and outlier
+ *     sections and the total size; sections start at 256-byte boundaries.
+ *   coef   : fp16 [tokens][hidden/g_a][2]   (alpha, beta)
+ *   scale  : fp16 [tokens][hidden/g_q]      (absent with RAC_FLAG_FIXED_STEP)
+ *   codes  : u8   [tokens][hidden*bits/8]   channel c of a row occupies bits
+ *            [c*bits, c*bits+bits) of the row's little-endian bit string, as
+ *            bits-wide two's complement (INT4: two values per byte, even
+ *            channel in the low nibble)
+ *   outl   : u32  [tokens][k]               ascending channel per row
+ */
+#ifndef RAC_H
+#define RAC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* rac_stream_t; /* identical to hipStream_t */
+
+typedef enum {
+    RAC_OK = 0,
+    RAC_ERR_INVALID = 1,     /* configuration or pointer argument invalid        */
+    RAC_ERR_ALIGN = 2,       /* a pointer breaks the alignment rules above       */
+    RAC_ERR_CAPACITY = 3,    /* wire buffer smaller than rac_wire_size()         */
+    RAC_ERR_HIP = 4,         /* the HIP runtime refused the kernel launch        */
+    RAC_ERR_FORMAT = 5,      /* a wire header does not parse                     */
+    RAC_ERR_UNSUPPORTED = 6  /* valid codec configuration the kernels do not
+                                implement (hidden above 8192)                   */
+} rac_status;
+
+enum {
+    /* Quantize with a calibrated step per channel group instead of the
+     * per-(token, group) max-abs scale: s = smallest fp16 >= fixed_steps[g],
+     * codes clip to +-Qmax, the wire carries no scale section. */
+    RAC_FLAG_FIXED_STEP = 1u << 0,
+    /* Write the reconstruction as bf16 (round to nearest even of the fp32
+     * value) instead of fp32. */
+    RAC_FLAG_XHAT_BF16 = 1u << 1
+};
+
+typedef struct {
+    int64_t tokens;      /* T = B*N token rows, 0 <= T < 2^32                      */
+    int32_t hidden;      /* d: multiple of 8, 8 <= d <= 65535 (kernels: <= 8192)  */
+    int32_t group_align; /* g_a: power of two, 8 <= g_a <= d, divides d           */
+    int32_t group_quant; /* g_q: power of two, 8 <= g_q <= d, divides d           */
+    int32_t bits;        /* q in {2, 3, 4, 8}; Qmax = 2^(q-1) - 1                  */
+    int32_t outlier_k;   /* outliers per token row, 0 <= k <= min(64, d)          */
+    uint32_t flags;      /* RAC_FLAG_*                                            */
+} rac_config;
+
+typedef struct {
+    uint64_t off_coef, off_scale, off_codes, off_outl, total; /* bytes */
+} rac_layout;
+
+/* Host-only, pure.  Section offsets and total wire size for `cfg`.
+ * Returns RAC_ERR_INVALID for a configuration outside the ranges above. */
+rac_status rac_wire_layout(const rac_config* cfg, rac_layout* out);
+
+/* Host-only, pure.  Total wire bytes for `cfg`, or 0 if it is invalid. */
+size_t rac_wire_size(const rac_config* cfg);
+
+/* Host-only, pure.  Parse a wire header the caller has copied to HOST memory
+ * (at least 256 bytes) into `out` (flags gets RAC_FLAG_FIXED_STEP when the
+ * wire carries no scales).  Checks magic, version, field ranges and that the
+ * recorded offsets match the layout of the parsed configuration; returns
+ * RAC_ERR_FORMAT otherwise.  `zero_ref` (may be NULL) receives 1 when the
+ * wire was encoded against a zero reference. */
+rac_status rac_parse_header(const void* header_host, size_t len, rac_config* out,
+                            int* zero_ref);
+
+/* Sender side: encode x against ref into `wire`, and optionally write the
+ * sender-side reconstruction H-hat into `xhat` in the same pass (the paper's
+ * sender reconstruction, which keeps later references in sync with the
+ * receiver).
+ *   x           : bf16 [T][d]                          (required if T > 0)
+ *   ref         : bf16 [T][d], or NULL for a zero reference
+ *   fixed_steps : fp32 [d/g_q], only with RAC_FLAG_FIXED_STEP, else ignored
+ *   wire        : u8 [wire_cap], wire_cap >= rac_wire_size(cfg); the first
+ *                 rac_wire_size(cfg) bytes are written, header included
+ *   xhat        : fp32 [T][d] (bf16 with RAC_FLAG_XHAT_BF16), or NULL
+ * One kernel launch. */
+rac_status rac_encode(const rac_config* cfg, const void* x, const void* ref,
+                      const float* fixed_steps, void* wire, size_t wire_cap, void* xhat,
+                      rac_stream_t stream);
+
+/* Sender side: H-hat from a wire this sender produced (same definition and
+ * same kernel as rac_decode, so the result is bit-identical to the fused
+ * reconstruction of rac_encode and to the receiver's rac_decode).
+ * Arguments as in rac_decode. */
+rac_status rac_reconstruct(const rac_config* cfg, const void* wire, const void* ref,
+                           const float* fixed_steps, void* xhat, rac_stream_t stream);
+
+/* Receiver side (Eq. residual-reconstruction): H-hat = alpha*R + beta + E-hat
+ * from the wire and the receiver's own reference.
+ *   wire        : a wire produced for exactly `cfg` (device memory); the
+ *                 header is not re-read on the device - a receiver that got
+ *                 the wire from elsewhere checks it with rac_parse_header
+ *   ref         : bf16 [T][d], or NULL for a zero reference
+ *   fixed_steps : fp32 [d/g_q] with RAC_FLAG_FIXED_STEP, else ignored
+ *   xhat        : fp32 [T][d] (bf16 with RAC_FLAG_XHAT_BF16)
+ * Outlier entries whose channel is >= d are ignored.  One kernel launch. */
+rac_status rac_decode(const rac_config* cfg, const void* wire, const void* ref,
+                      const float* fixed_steps, void* xhat, rac_stream_t stream);
+
+/* Static string naming a status code. */
+const char* rac_status_string(rac_status s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* RAC_H */

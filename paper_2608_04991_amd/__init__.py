@@ -1,0 +1,174 @@
+"""MI355X (gfx950) RAC aligned residual codec: Python binding of librac.so.
+
+This module only marshals arguments to the C ABI declared in include/rac.h
+(same names, same semantics); every step of the codec runs in the HIP
+kernels of csrc/rac.hip.  PyTorch supplies device memory and the stream.
+
+    cfg = RacConfig(tokens=T, hidden=d, group_align=128, group_quant=128,
+                    bits=4, outlier_k=8)
+    wire = torch.empty(rac_wire_size(cfg), dtype=torch.uint8, device="cuda")
+    rac_encode(cfg, x, ref, None, wire, xhat)          # x, ref: bf16 [T, d]
+    rac_decode(cfg, wire, ref, None, xhat_receiver)
+
+There is no fallback: if librac.so is missing the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+__all__ = [
+    "RacConfig", "RacError", "RAC_FLAG_FIXED_STEP", "RAC_FLAG_XHAT_BF16", "STATUS",
+    "library", "library_path", "rac_wire_layout", "rac_wire_size", "rac_parse_header",
+    "rac_encode", "rac_reconstruct", "rac_decode", "rac_status_string",
+]
+
+RAC_FLAG_FIXED_STEP = 1
+RAC_FLAG_XHAT_BF16 = 2
+STATUS = {0: "RAC_OK", 1: "RAC_ERR_INVALID", 2: "RAC_ERR_ALIGN", 3: "RAC_ERR_CAPACITY",
+          4: "RAC_ERR_HIP", 5: "RAC_ERR_FORMAT", 6: "RAC_ERR_UNSUPPORTED"}
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def library_path() -> str:
+    return os.path.join(_HERE, "lib", "librac.so")
+
+
+class RacError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {STATUS.get(status, status)} ({rac_status_string(status)})")
+        self.status = status
+
+
+class _Config(ctypes.Structure):
+    _fields_ = [("tokens", ctypes.c_int64), ("hidden", ctypes.c_int32),
+                ("group_align", ctypes.c_int32), ("group_quant", ctypes.c_int32),
+                ("bits", ctypes.c_int32), ("outlier_k", ctypes.c_int32),
+                ("flags", ctypes.c_uint32)]
+
+
+class _Layout(ctypes.Structure):
+    _fields_ = [("off_coef", ctypes.c_uint64), ("off_scale", ctypes.c_uint64),
+                ("off_codes", ctypes.c_uint64), ("off_outl", ctypes.c_uint64),
+                ("total", ctypes.c_uint64)]
+
+
+@dataclass(frozen=True)
+class RacConfig:
+    tokens: int
+    hidden: int
+    group_align: int
+    group_quant: int
+    bits: int
+    outlier_k: int = 0
+    flags: int = 0
+
+    def _c(self) -> _Config:
+        return _Config(self.tokens, self.hidden, self.group_align, self.group_quant, self.bits,
+                       self.outlier_k, self.flags)
+
+
+_lib = None
+
+
+def library():
+    """Load librac.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        path = library_path()
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is missing: build it with `python -m paper_2608_04991_amd.build`")
+        L = ctypes.CDLL(path)
+        cp = ctypes.POINTER(_Config)
+        vp = ctypes.c_void_p
+        L.rac_wire_layout.argtypes = [cp, ctypes.POINTER(_Layout)]
+        L.rac_wire_layout.restype = ctypes.c_int
+        L.rac_wire_size.argtypes = [cp]
+        L.rac_wire_size.restype = ctypes.c_size_t
+        L.rac_parse_header.argtypes = [vp, ctypes.c_size_t, cp, ctypes.POINTER(ctypes.c_int)]
+        L.rac_parse_header.restype = ctypes.c_int
+        L.rac_encode.argtypes = [cp, vp, vp, vp, vp, ctypes.c_size_t, vp, vp]
+        L.rac_encode.restype = ctypes.c_int
+        L.rac_reconstruct.argtypes = [cp, vp, vp, vp, vp, vp]
+        L.rac_reconstruct.restype = ctypes.c_int
+        L.rac_decode.argtypes = [cp, vp, vp, vp, vp, vp]
+        L.rac_decode.restype = ctypes.c_int
+        L.rac_status_string.argtypes = [ctypes.c_int]
+        L.rac_status_string.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _ptr(t):
+    """Device address of a tensor (or an int address, or None)."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _nbytes(t) -> int:
+    return t.numel() * t.element_size()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(status: int, what: str):
+    if status != 0:
+        raise RacError(status, what)
+
+
+def rac_status_string(status: int) -> str:
+    return library().rac_status_string(int(status)).decode()
+
+
+def rac_wire_layout(cfg: RacConfig) -> dict:
+    out = _Layout()
+    _check(library().rac_wire_layout(ctypes.byref(cfg._c()), ctypes.byref(out)), "rac_wire_layout")
+    return {f: int(getattr(out, f)) for f, _ in _Layout._fields_}
+
+
+def rac_wire_size(cfg: RacConfig) -> int:
+    return int(library().rac_wire_size(ctypes.byref(cfg._c())))
+
+
+def rac_parse_header(header: bytes):
+    """Parse a host copy of a wire header; returns (RacConfig, zero_ref)."""
+    buf = ctypes.create_string_buffer(bytes(header), len(header))
+    c = _Config()
+    zr = ctypes.c_int(0)
+    _check(library().rac_parse_header(buf, len(header), ctypes.byref(c), ctypes.byref(zr)),
+           "rac_parse_header")
+    return RacConfig(c.tokens, c.hidden, c.group_align, c.group_quant, c.bits, c.outlier_k,
+                     c.flags), bool(zr.value)
+
+
+def rac_encode(cfg: RacConfig, x, ref, fixed_steps, wire, xhat=None, stream=None,
+               wire_cap: int | None = None) -> None:
+    """Encode x against ref into wire (+ fused sender reconstruction)."""
+    cap = wire_cap if wire_cap is not None else (_nbytes(wire) if not isinstance(wire, int) else 0)
+    _check(library().rac_encode(ctypes.byref(cfg._c()), _ptr(x), _ptr(ref), _ptr(fixed_steps),
+                                _ptr(wire), cap, _ptr(xhat), _stream(stream)), "rac_encode")
+
+
+def rac_reconstruct(cfg: RacConfig, wire, ref, fixed_steps, xhat, stream=None) -> None:
+    """Sender-side reconstruction from the sender's own wire."""
+    _check(library().rac_reconstruct(ctypes.byref(cfg._c()), _ptr(wire), _ptr(ref),
+                                     _ptr(fixed_steps), _ptr(xhat), _stream(stream)),
+           "rac_reconstruct")
+
+
+def rac_decode(cfg: RacConfig, wire, ref, fixed_steps, xhat, stream=None) -> None:
+    """Receiver-side reconstruction from a wire and the receiver's reference."""
+    _check(library().rac_decode(ctypes.byref(cfg._c()), _ptr(wire), _ptr(ref),
+                                _ptr(fixed_steps), _ptr(xhat), _stream(stream)), "rac_decode")

@@ -1,0 +1,147 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/rac.h declares, and its host-only logic (layout, header parsing,
+argument validation that returns before any launch) behaves as documented.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2608_04991_amd as rac
+from paper_2608_04991_amd import workloads as wl
+from tests import wirefmt
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "rac.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rac_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(rac.library_path()):
+        pytest.fail("librac.so is not built; run __graft_entry__.build()")
+    return rac.library()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared_functions()
+    assert set(names) == {"rac_wire_layout", "rac_wire_size", "rac_parse_header", "rac_encode",
+                          "rac_reconstruct", "rac_decode", "rac_status_string"}
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    for s in range(7):
+        assert rac.rac_status_string(s) != "unknown status"
+    assert rac.rac_status_string(99) == "unknown status"
+
+
+CFGS = [
+    dict(tokens=4096, hidden=4096, group_align=128, group_quant=128, bits=4, outlier_k=8),
+    dict(tokens=65536, hidden=3584, group_align=128, group_quant=128, bits=4, outlier_k=4),
+    dict(tokens=256, hidden=4096, group_align=128, group_quant=4096, bits=2),
+    dict(tokens=32768, hidden=4096, group_align=64, group_quant=64, bits=3, outlier_k=16),
+    dict(tokens=0, hidden=512, group_align=64, group_quant=64, bits=8),
+    dict(tokens=7, hidden=520, group_align=8, group_quant=8, bits=3, outlier_k=64,
+         flags=rac.RAC_FLAG_FIXED_STEP),
+]
+
+
+@pytest.mark.parametrize("c", CFGS)
+def test_layout_matches_documented_format(lib, c):
+    cfg = rac.RacConfig(**c)
+    assert rac.rac_wire_layout(cfg) == wirefmt.expected_layout(**c)
+    assert rac.rac_wire_size(cfg) == wirefmt.expected_layout(**c)["total"]
+
+
+def test_payload_ratio_of_the_prefill_uplink_shape(lib):
+    cfg = rac.RacConfig(4096, 4096, 128, 128, 4, 8)
+    ratio = rac.rac_wire_size(cfg) / (4096 * 4096 * 2)
+    assert abs(ratio - 0.2774) < 5e-4   # 4-bit codes + fp16 scale/coef + 8 outliers per row
+
+
+@pytest.mark.parametrize("bad", [dict(bits=5), dict(group_align=96), dict(group_quant=4),
+                                 dict(hidden=100), dict(outlier_k=65), dict(tokens=-1),
+                                 dict(flags=16), dict(group_align=1024)])
+def test_invalid_configs_are_rejected(lib, bad):
+    c = dict(tokens=4, hidden=512, group_align=64, group_quant=64, bits=4)
+    c.update(bad)
+    cfg = rac.RacConfig(**c)
+    assert rac.rac_wire_size(cfg) == 0
+    with pytest.raises(rac.RacError) as e:
+        rac.rac_wire_layout(cfg)
+    assert e.value.status == 1
+
+
+def test_parse_header_reads_oracle_headers(lib):
+    for c in CFGS[:4] + CFGS[5:]:
+        small = dict(c, tokens=3)
+        T, d = 3, small["hidden"]
+        xb, rb, _ = wl.affine_pair(wl.AffineRecipe(T, d, small["group_align"]), 0)
+        steps = np.full(d // small["group_quant"], 0.05, np.float32)
+        for ref in (rb, None):
+            rc, wire, _ = oracle.encode(xb, ref, steps, want_xhat=False, **small)
+            assert rc == 0
+            cfg, zero_ref = rac.rac_parse_header(wire[:256].tobytes())
+            want = dict(small, flags=small.get("flags", 0) & rac.RAC_FLAG_FIXED_STEP)
+            want.setdefault("outlier_k", 0)
+            assert cfg == rac.RacConfig(**want)
+            assert zero_ref == (ref is None)
+
+
+def test_parse_header_rejects_corruption(lib):
+    c = dict(tokens=2, hidden=64, group_align=64, group_quant=64, bits=4, outlier_k=2)
+    xb = wl.f32_to_bf16_bits(np.random.default_rng(0).standard_normal((2, 64)))
+    rc, wire, _ = oracle.encode(xb, None, want_xhat=False, **c)
+    good = wire[:256].tobytes()
+    rac.rac_parse_header(good)
+    for off, val in [(0, 0x00), (4, 2), (24, 5), (28, 0), (40, 0x11), (100, 1), (6, 0x08), (25, 2)]:
+        bad = bytearray(good)
+        bad[off] = val
+        with pytest.raises(rac.RacError) as e:
+            rac.rac_parse_header(bytes(bad))
+        assert e.value.status == 5, off
+    with pytest.raises(rac.RacError):
+        rac.rac_parse_header(good[:200])
+
+
+# Argument checks happen on the host before anything is enqueued, so they can
+# be exercised with fake (never dereferenced) addresses.
+FAKE = 1 << 40
+
+
+def _encode(cfg, x=FAKE, ref=FAKE, steps=None, wire=FAKE, cap=1 << 40, xhat=FAKE):
+    return rac.library().rac_encode(ctypes.byref(cfg._c()), x, ref, steps, wire, cap, xhat, 0)
+
+
+def _decode(cfg, wire=FAKE, ref=FAKE, steps=None, xhat=FAKE):
+    return rac.library().rac_decode(ctypes.byref(cfg._c()), wire, ref, steps, xhat, 0)
+
+
+def test_argument_errors_are_synchronous(lib):
+    good = rac.RacConfig(64, 512, 64, 64, 4)
+    assert _encode(rac.RacConfig(64, 512, 64, 64, 5)) == 1              # invalid bits
+    assert _encode(good, x=None) == 1                                    # x required
+    assert _encode(good, x=FAKE + 2) == 2                                # x misaligned
+    assert _encode(good, ref=FAKE + 8) == 2                              # ref misaligned
+    assert _encode(good, wire=FAKE + 16) == 2                            # wire needs 256 B
+    assert _encode(good, xhat=FAKE + 4) == 2                             # xhat misaligned
+    assert _encode(good, cap=rac.rac_wire_size(good) - 1) == 3           # capacity
+    fixed = rac.RacConfig(64, 512, 64, 64, 4, 0, rac.RAC_FLAG_FIXED_STEP)
+    assert _encode(fixed, steps=None) == 1                               # steps required
+    big = rac.RacConfig(4, 16384, 128, 128, 4)
+    assert _encode(big) == 6                                             # kernels cap d at 8192
+    assert _decode(rac.RacConfig(64, 512, 64, 64, 5)) == 1
+    assert _decode(good, wire=FAKE + 128) == 2
+    assert _decode(good, xhat=None) == 1
+    assert rac.library().rac_reconstruct(ctypes.byref(good._c()), FAKE, FAKE, None, FAKE + 1, 0) == 2

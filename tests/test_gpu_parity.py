@@ -1,0 +1,239 @@
+"""GPU parity of the HIP codec against the CPU oracle, through the C ABI.
+
+Small cases run the oracle on every row; they span several wavefront tiles
+(four rows per block), ragged row counts, a partial last 512-channel chunk,
+every bit width, groups below and above one chunk, per-token outliers with
+ties (both selection paths), zero references, bf16 output and the fixed-step
+mode.  The full benchmark shapes are checked on sampled rows, which the
+oracle can compute one by one because rows are independent.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2608_04991_amd as rac
+from paper_2608_04991_amd import workloads as wl
+from tests import wirefmt
+from tests.gpu_util import assert_parity, cfgd, gpu_run, oracle_run, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    rac.library()
+
+
+def _zero_sum_integer_rows(T, d, g, n_big, big, seed):
+    """Rows of integers in [-2, 2] built from (v, -v) pairs inside every
+    group (so each group mean is exactly 0); in n_big groups of each row one
+    pair is (big, -big).  Against a zero reference the residual is the row
+    itself, full of ties."""
+    rng = np.random.default_rng(seed)
+    x = np.zeros((T, d), np.float32)
+    for t in range(T):
+        big_groups = set(rng.choice(d // g, n_big, replace=False).tolist()) if n_big else set()
+        for j in range(d // g):
+            v = rng.integers(-2, 3, g // 2).astype(np.float32)
+            if j in big_groups:
+                v[0] = big
+            grp = np.concatenate([v, -v])
+            rng.shuffle(grp)
+            x[t, j * g:(j + 1) * g] = grp
+    return x
+
+
+def _dyadic_exact_rows(T, d, seed):
+    rng = np.random.default_rng(seed)
+    r = rng.integers(-32, 33, (T, d)).astype(np.float32) / 4
+    x = np.float32(1.25) * r - np.float32(0.5)
+    return wl.f32_to_bf16_bits(x), wl.f32_to_bf16_bits(r)
+
+
+def _downlink_rows(T, d, seed=0):
+    """Downlink inputs whose reference is the oracle's reconstruction of a
+    synthetic uplink (the same-round reference of the prefill downlink)."""
+    xu, ru, _ = wl.prefill_downlink_uplink(seed, rows=(0, T), tokens=T, hidden=d)
+    rc, _, uhat = oracle.encode(xu, ru, **cfgd(T, d, 128, 128, 4, 4))
+    assert rc == 0
+    ref = wl.f32_to_bf16_bits(uhat)
+    return wl.prefill_downlink(ref, seed, rows=(0, T), tokens=T, hidden=d), ref
+
+
+def _affine(T, d, g, seed=0, **kw):
+    x, r, _ = wl.affine_pair(wl.AffineRecipe(T, d, g, **kw), seed)
+    return x, r
+
+
+CASES = {
+    "tiny_64x512_g64_b4": (cfgd(64, 512, 64, 64, 4), lambda: wl.tiny(0)[:2]),
+    "uplink_37x4096_g128_b4_k8": (cfgd(37, 4096, 128, 128, 4, 8),
+                                  lambda: wl.prefill_uplink(0, rows=(0, 37))[:2]),
+    "uplink_21x4096_ga64_gq128_b8_k16": (cfgd(21, 4096, 64, 128, 8, 16),
+                                         lambda: wl.prefill_uplink(1, rows=(100, 121))[:2]),
+    "downlink_40x3584_g128_b4_k4": (cfgd(40, 3584, 128, 128, 4, 4), lambda: _downlink_rows(40, 3584)),
+    "long_29x4096_g64_b3_k16": (cfgd(29, 4096, 64, 64, 3, 16),
+                                lambda: wl.long_context(0, rows=(0, 29), group=64)[:2]),
+    "long_29x4096_g128_b2_k16": (cfgd(29, 4096, 128, 128, 2, 16),
+                                 lambda: wl.long_context(0, rows=(0, 29), group=128)[:2]),
+    "long_13x4096_g128_b8_k16": (cfgd(13, 4096, 128, 128, 8, 16),
+                                 lambda: wl.long_context(2, rows=(500, 513), group=128)[:2]),
+    "partial_chunk_13x2880_ga64_gq32_b4_k5": (cfgd(13, 2880, 64, 32, 4, 5), lambda: _affine(13, 2880, 64)),
+    "bytewise3_11x2888_g8_b3_k3": (cfgd(11, 2888, 8, 8, 3, 3), lambda: _affine(11, 2888, 8)),
+    "d8192_9x8192_ga128_gq256_b4_k8": (cfgd(9, 8192, 128, 256, 4, 8), lambda: _affine(9, 8192, 128)),
+    "large_groups_10x4096_ga1024_gq2048_b4_k8": (cfgd(10, 4096, 1024, 2048, 4, 8),
+                                                 lambda: _affine(10, 4096, 1024)),
+    "gq_eq_d_16x4096_b4": (cfgd(16, 4096, 128, 4096, 4), lambda: wl.decode_step(16)),
+    "all_outliers_12x64_ga8_gq16_k64": (cfgd(12, 64, 8, 16, 4, 64), lambda: _affine(12, 64, 8)),
+    "smallest_5x8_b4_k2": (cfgd(5, 8, 8, 8, 4, 2), lambda: _affine(5, 8, 8)),
+    "zero_reference_19x1024_b4_k4": (cfgd(19, 1024, 128, 64, 4, 4),
+                                     lambda: (_affine(19, 1024, 128)[0], None)),
+    "ties_fast_path_9x4096_zero_ref_k8": (cfgd(9, 4096, 128, 128, 4, 8),
+                                          lambda: (wl.f32_to_bf16_bits(_zero_sum_integer_rows(9, 4096, 128, 5, 3.0, 0)), None)),
+    "ties_slow_path_exact_affine_7x1024_k5": (cfgd(7, 1024, 64, 32, 4, 5), lambda: _dyadic_exact_rows(7, 1024, 3)),
+    "ties_heavy_zero_ref_6x512_k12": (cfgd(6, 512, 64, 64, 4, 12),
+                                      lambda: (wl.f32_to_bf16_bits(_zero_sum_integer_rows(6, 512, 64, 0, 0.0, 1)), None)),
+    "bf16_out_25x4096_g128_b4_k8": (cfgd(25, 4096, 128, 128, 4, 8, rac.RAC_FLAG_XHAT_BF16),
+                                    lambda: wl.prefill_uplink(0, rows=(7, 32))[:2]),
+}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_small_parity(name):
+    c, gen = CASES[name]
+    xb, rb = gen()
+    say(f"[gpu] {name}: T={c['tokens']} d={c['hidden']} ga={c['group_align']} gq={c['group_quant']} "
+        f"b={c['bits']} k={c['outlier_k']} flags={c['flags']}")
+    ow, ox = oracle_run(c, xb, rb)
+    gw, gx, gd, gr = gpu_run(c, xb, rb)
+    assert_parity(c, gw, gx, ow, ox)
+    # sender reconstruction == receiver decode == standalone reconstruct, bitwise
+    assert np.array_equal(gx.view(np.uint8), gd.view(np.uint8))
+    assert np.array_equal(gx.view(np.uint8), gr.view(np.uint8))
+
+
+def _fixed_steps(d, g, seed=1):
+    """Calibrated steps of the tiny workload: 2 std(E) / (2^4 - 1) per channel
+    group, from the oracle's residuals on a separate seed."""
+    xb, rb, _ = wl.tiny(seed)
+    rc, wire, _ = oracle.encode(xb, rb, want_xhat=False, **cfgd(64, d, g, g, 4))
+    s = wirefmt.sections(wire)
+    a = np.repeat(s["coef"][..., 0].view(np.float16).astype(np.float32), g, axis=1)
+    b = np.repeat(s["coef"][..., 1].view(np.float16).astype(np.float32), g, axis=1)
+    e = wl.bf16_bits_to_f32(xb) - (a * wl.bf16_bits_to_f32(rb) + b)
+    return (2 * e.reshape(64, d // g, g).transpose(1, 0, 2).reshape(d // g, -1).std(axis=1)
+            / 15).astype(np.float32)
+
+
+def test_fixed_step_tiny():
+    c = cfgd(64, 512, 64, 64, 4, 0, rac.RAC_FLAG_FIXED_STEP)
+    steps = _fixed_steps(512, 64)
+    xb, rb, _ = wl.tiny(0)
+    say(f"[gpu] fixed step tiny: steps[:3]={steps[:3]}")
+    rc, ow, ox = oracle.encode(xb, rb, steps, **c)
+    assert rc == 0
+    gw, gx, gd, gr = gpu_run(c, xb, rb, steps)
+    assert_parity(c, gw, gx, ow, ox)
+    assert np.array_equal(gx, gd) and np.array_equal(gx, gr)
+
+
+@pytest.mark.parametrize("batch", [1, 16, 64, 256])
+@pytest.mark.parametrize("bits", [2, 4, 8])
+@pytest.mark.parametrize("gq", [128, 4096])
+def test_decode_step_batches(batch, bits, gq):
+    c = cfgd(batch, 4096, 128, gq, bits)
+    xb, rb = wl.decode_step(batch)
+    say(f"[gpu] decode step B={batch} b={bits} gq={gq}")
+    ow, ox = oracle_run(c, xb, rb)
+    gw, gx, gd, _ = gpu_run(c, xb, rb)
+    assert_parity(c, gw, gx, ow, ox)
+    assert np.array_equal(gx, gd)
+
+
+def test_empty_token_batch_writes_header_only():
+    c = cfgd(0, 512, 64, 64, 4, 2)
+    xb = np.zeros((0, 512), np.uint16)
+    for ref in (None, xb):
+        gw, gx, gd, _ = gpu_run(c, xb, ref)
+        ow, _ = oracle_run(c, xb, None)  # an empty device tensor has no address: zero reference
+        assert gw.size == 256 and np.array_equal(gw, ow)
+
+
+def test_without_xhat_and_on_a_side_stream_deterministic():
+    import torch
+    c = cfgd(33, 4096, 128, 128, 4, 8)
+    xb, rb, _ = wl.prefill_uplink(5, rows=(0, 33))
+    s = torch.cuda.Stream()
+    say("[gpu] side stream, no xhat, twice")
+    w1, _, d1, _ = gpu_run(c, xb, rb, stream=s, want_xhat=False)
+    w2, _, d2, _ = gpu_run(c, xb, rb, stream=s, want_xhat=False, garbage=0x11)
+    assert np.array_equal(w1, w2) and np.array_equal(d1, d2)
+    ow, ox = oracle_run(c, xb, rb)
+    assert_parity(c, w1, d1, ow, ox)
+
+
+# ---------------------------------------------------------------------------
+# Full benchmark shapes, sampled rows
+
+def _sample(T, n, seed=0):
+    rng = np.random.default_rng(seed)
+    rows = np.unique(np.concatenate([[0, 1, 2, 3, T - 2, T - 1], rng.choice(T, n, replace=False)]))
+    return rows
+
+
+def test_full_prefill_uplink_4096x4096_sampled():
+    c = cfgd(4096, 4096, 128, 128, 4, 8)
+    say("[gpu] full prefill uplink 4096x4096: generating")
+    xb, rb, _ = wl.prefill_uplink(0)
+    gw, gx, gd, _ = gpu_run(c, xb, rb)
+    assert np.array_equal(gx, gd)
+    rows = _sample(4096, 48)
+    ow, ox = oracle_run(dict(c, tokens=rows.size), xb[rows], rb[rows])
+    n = assert_parity(c, gw, gx, ow, ox, g_rows=rows, o_rows=slice(None))
+    assert n == rows.size
+    assert wirefmt.padding_is_zero(gw) and wirefmt.header(gw)["tokens"] == 4096
+
+
+def test_full_long_context_32768x4096_g128_b4_sampled():
+    c = cfgd(32768, 4096, 128, 128, 4, 16)
+    say("[gpu] full long context 32768x4096: generating")
+    xb, rb, _ = wl.long_context(0, group=128)
+    gw, gx, gd, _ = gpu_run(c, xb, rb)
+    assert np.array_equal(gx, gd)
+    rows = _sample(32768, 40, seed=1)
+    ow, ox = oracle_run(dict(c, tokens=rows.size), xb[rows], rb[rows])
+    assert_parity(c, gw, gx, ow, ox, g_rows=rows, o_rows=slice(None))
+    h = wirefmt.header(gw)
+    assert h["tokens"] == 32768 and wirefmt.padding_is_zero(gw)
+
+
+def test_full_prefill_downlink_65536x3584_sampled():
+    """The same-round reference: the GPU reconstructs the uplink of all rows;
+    on the sampled rows the oracle reconstructs it too (asserted equal) and
+    encodes the downlink from its own reference."""
+    import torch
+    T, d = 65536, 3584
+    cu = cfgd(T, d, 128, 128, 4, 4)
+    say("[gpu] full downlink 65536x3584: uplink generation")
+    xu, ru, _ = wl.prefill_downlink_uplink(0)
+    uw, uhat, _, _ = gpu_run(cu, xu, ru)
+    ref = wl.f32_to_bf16_bits(uhat)
+    del uw, uhat
+    say("[gpu] full downlink: downlink generation")
+    xd = wl.prefill_downlink(ref, 0)
+    gw, gx, gd, _ = gpu_run(cu, xd, ref)
+    assert np.array_equal(gx, gd)
+    rows = _sample(T, 32, seed=2)
+    rc, _, uhat_o = oracle.encode(xu[rows], ru[rows], **dict(cu, tokens=rows.size))
+    ref_o = wl.f32_to_bf16_bits(uhat_o)
+    assert np.array_equal(ref_o, ref[rows]), "uplink reconstruction differs from the oracle"
+    xd_o = wl.prefill_downlink(ref_o, 0, rows=rows)
+    assert np.array_equal(xd_o, xd[rows])
+    ow, ox = oracle_run(dict(cu, tokens=rows.size), xd_o, ref_o)
+    assert_parity(cu, gw, gx, ow, ox, g_rows=rows, o_rows=slice(None))
+    torch.cuda.empty_cache()
