@@ -17,6 +17,10 @@
  * Readings of the paper that are not spelled out there (each one is listed
  * with its justification in the design notes of the repository):
  *   - fit scope is one (alpha, beta) per token row and alignment group;
+ *   - the aligned reference alpha*r + beta is rounded once (a fused
+ *     multiply-add); with fp16 alpha and bf16 r the product is exact in
+ *     binary32 unless it underflows, so this equals the two-step form
+ *     everywhere except in that corner, where it fixes one answer;
  *   - sums use the canonical pairwise tree orc_tsum, fit is two-pass centred;
  *   - Round_wire for alpha/beta is fp16 round-to-nearest-even, saturating;
  *   - RoundUp_wire for the scale is "smallest fp16 h with h*Qmax >= max|E^d|";
@@ -384,7 +388,7 @@ int orc_encode(const orc_config* cfg, const uint16_t* x, const uint16_t* ref,
             put16(coef + 4 * j + 2, bh);
             const float a = orc_f16_to_f32(ah), b0 = orc_f16_to_f32(bh);
             for (int32_t c = j * ga; c < (j + 1) * ga; ++c) {
-                rt[c] = a * r[c] + b0;
+                rt[c] = fmaf(a, r[c], b0);
                 e[c] = xv[c] - rt[c];
             }
         }
@@ -498,7 +502,7 @@ int orc_decode(const orc_config* cfg, const uint8_t* wire, const uint16_t* ref,
             const float b0 = orc_f16_to_f32(get16(coef + 4 * j + 2));
             for (int32_t c = j * ga; c < (j + 1) * ga; ++c) {
                 const float r = ref ? orc_bf16_to_f32(ref[t * d + c]) : 0.0f;
-                const float rt = a * r + b0;
+                const float rt = fmaf(a, r, b0);
                 orc_store_xhat(cfg, xhat, t * d + c, rt + eh[c]);
             }
         }

@@ -6,23 +6,24 @@
 // entry point is documented in include/rac.h.
 //
 // Mapping onto CDNA4.  The codec is a per-token-row stream with no dense
-// contraction, so it is HBM-bound and uses no MFMA.  One 64-lane wavefront
-// owns one token row.  A row is cut into 512-channel chunks; in chunk `it`,
-// lane l holds channels [it*512 + 8l, it*512 + 8l + 8) -- one 128-bit load of
-// x and one of ref per lane and chunk, fully coalesced (1 KiB per wave load).
-// The whole row stays in VGPRs: fit, residual, outlier choice, scale,
-// quantization, packing and the fused sender reconstruction all run on
-// registers, and every byte of x/ref is read from HBM exactly once and every
-// output byte written exactly once.
+// contraction, so it is HBM-bound and uses no MFMA.  One workgroup owns one
+// token row and one 64-lane wavefront owns one 512-channel chunk of it: lane l
+// of wave w holds channels [512w + 8l, 512w + 8l + 8), one 128-bit load of x
+// and one of ref per lane, fully coalesced.  Each lane keeps its 8 channels in
+// registers through fit, residual, outlier choice, scale, quantization,
+// packing and the fused sender reconstruction, so every byte of x/ref is read
+// from HBM once and every output byte written once.  Work that spans chunks
+// (the per-token outlier choice, groups wider than 512 channels) goes through
+// LDS with workgroup barriers; everything else is wave-local.
 //
 // Exactness.  The sums of the fit follow a fixed pairwise tree over channel
-// order: a lane-local tree over its 8 contiguous channels, then a butterfly
-// across lanes whose every step adds the partial sums of two adjacent
-// aligned blocks (DPP quad_perm / row_half_mirror / row_mirror, then
-// v_permlane16_swap and v_permlane32_swap), then a tree over chunks.  Since
-// floating-point addition is commutative, that reproduces the canonical
-// pairwise sum exactly.  The file is compiled with -ffp-contract=off so no
-// multiply-add is fused, and divisions stay correctly rounded.
+// order: a lane-local tree over its 8 contiguous channels, a butterfly across
+// lanes whose every step adds the partial sums of two adjacent aligned blocks
+// (DPP quad_perm / row_half_mirror / row_mirror, then v_permlane16_swap and
+// v_permlane32_swap), then a pairwise tree over chunks.  Floating-point
+// addition is commutative, so that reproduces the canonical pairwise sum
+// exactly.  The file is compiled with -ffp-contract=off so no multiply-add is
+// fused, and divisions stay correctly rounded.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -31,9 +32,10 @@
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kWavesPerBlock = 4;
-constexpr int kBlock = kWave * kWavesPerBlock;
-constexpr int kChunk = 512;
+constexpr int kChunk = 512;       // channels per wavefront (8 per lane)
+constexpr int kMaxWaves = 16;     // rows up to 8192 channels
+constexpr int kCandCap = 64;      // outlier candidates ranked by one wavefront
+constexpr int kMaxGroupMax = 256; // group maxima for the outlier threshold
 constexpr float kMagic = 12582912.0f;  // 1.5 * 2^23: adding it rounds to an integer (RNE)
 // Quotients t' = E * (1/s) within this distance of a half-integer are
 // recomputed with the correctly rounded division E / s.  |t' - E/s| is below
@@ -48,18 +50,20 @@ struct alignas(8) Args {
     void* xhat;
     uint64_t off_coef, off_scale, off_codes, off_outl, total;
     uint64_t end_coef, end_scale, end_codes, end_outl;  // first byte after each section
+    uint64_t code_row_bytes;  // d * bits / 8
     int64_t tokens;
     int32_t d;
-    int32_t nch;        // chunks per row: ceil(d / 512)
-    int32_t ga, gq;     // group sizes
+    int32_t nch;        // 512-channel chunks per row = wavefronts per workgroup
+    int32_t lg_a, lg_q; // log2 of the group sizes
     int32_t lane_lv_a;  // butterfly levels inside a chunk: log2(min(g, 512) / 8)
     int32_t lane_lv_q;
-    int32_t cpg_a;      // chunks per group: max(1, g / 512)
-    int32_t cpg_q;
+    int32_t lg_cpg_a;   // log2 chunks per group (0 when a group fits in a chunk)
+    int32_t lg_cpg_q;
     int32_t k;
     int32_t fixed;
     int32_t xhat_bf16;
     int32_t write_header;
+    float inv_ga;       // 1 / g_a (exact, power of two)
     uint32_t hdr[24];   // first 96 bytes of the header; the rest is zero
 };
 
@@ -202,50 +206,6 @@ __device__ __forceinline__ float tree8(const float* v) {
     return ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
 }
 
-// Pairwise tree over the chunks of groups spanning `cpg` chunks, then the
-// group total broadcast back to each of its chunks.
-template <int MAXCH>
-__device__ __forceinline__ void chunk_tree_sum(float* s, int cpg) {
-    constexpr int kLevels = MAXCH >= 16 ? 4 : MAXCH >= 8 ? 3 : MAXCH >= 4 ? 2 : MAXCH >= 2 ? 1 : 0;
-#pragma unroll
-    for (int lv = 0; lv < kLevels; ++lv) {
-        const int w = 1 << lv;
-        if (w < cpg) {
-#pragma unroll
-            for (int it = 0; it + w < MAXCH; it += 2 * w) s[it] = s[it] + s[it + w];
-        }
-    }
-#pragma unroll
-    for (int lv = kLevels - 1; lv >= 0; --lv) {
-        const int w = 1 << lv;
-        if (w < cpg) {
-#pragma unroll
-            for (int it = 0; it + w < MAXCH; it += 2 * w) s[it + w] = s[it];
-        }
-    }
-}
-
-template <int MAXCH>
-__device__ __forceinline__ void chunk_tree_max(float* s, int cpg) {
-    constexpr int kLevels = MAXCH >= 16 ? 4 : MAXCH >= 8 ? 3 : MAXCH >= 4 ? 2 : MAXCH >= 2 ? 1 : 0;
-#pragma unroll
-    for (int lv = 0; lv < kLevels; ++lv) {
-        const int w = 1 << lv;
-        if (w < cpg) {
-#pragma unroll
-            for (int it = 0; it + w < MAXCH; it += 2 * w) s[it] = __builtin_fmaxf(s[it], s[it + w]);
-        }
-    }
-#pragma unroll
-    for (int lv = kLevels - 1; lv >= 0; --lv) {
-        const int w = 1 << lv;
-        if (w < cpg) {
-#pragma unroll
-            for (int it = 0; it + w < MAXCH; it += 2 * w) s[it + w] = s[it];
-        }
-    }
-}
-
 __device__ __forceinline__ uint32_t mbcnt64(uint64_t m) {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
@@ -269,20 +229,6 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
 }
 
 // One bit per (chunk, channel-in-lane) slot of a lane: bit it*8 + j.
-template <int MAXCH>
-struct SlotMask {
-    static constexpr int kWords = (MAXCH * 8 + 63) / 64;
-    uint64_t w[kWords];
-    __device__ __forceinline__ bool test(int slot) const {  // slot is a compile-time constant
-        return (w[slot / 64] >> (slot % 64)) & 1ull;
-    }
-    __device__ __forceinline__ void set(int slot) {        // slot may be a runtime value
-#pragma unroll
-        for (int i = 0; i < kWords; ++i)
-            if ((slot >> 6) == i) w[i] |= 1ull << (slot & 63);
-    }
-};
-
 // ---------------------------------------------------------------------------
 // Header and inter-section padding (written by wave 0 of block 0).
 
@@ -415,18 +361,25 @@ __device__ __forceinline__ int32_t code_at(uint32_t lo, uint32_t hi, int j) {
     return ((int32_t)(u << (32 - BITS))) >> (32 - BITS);  // sign-extend
 }
 
-// max |E| over the lane's 8 channels of chunk `it`, outliers counted as 0.
-template <int MAXCH>
-__device__ __forceinline__ float dense_absmax8(const float* e, const SlotMask<MAXCH>& selbits,
-                                               const SlotMask<MAXCH>& slot_any, int it) {
-    float m = 0.0f;
+// Pairwise tree over n (a power of two, <= 16) consecutive chunk partials.
+__device__ __forceinline__ float tree_n(const float* p, int n) {
+    float v[kMaxWaves];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        float v = e[j];
-        if (slot_any.test(it * 8 + j))
-            if (selbits.test(it * 8 + j)) v = 0.0f;
-        m = __builtin_fmaxf(m, __builtin_fabsf(v));
+    for (int i = 0; i < kMaxWaves; ++i) v[i] = i < n ? p[i] : 0.0f;
+#pragma unroll
+    for (int lv = 0; lv < 4; ++lv) {
+        const int w = 1 << lv;
+        if (w < n) {
+#pragma unroll
+            for (int i = 0; i + w < kMaxWaves; i += 2 * w) v[i] = v[i] + v[i + w];
+        }
     }
+    return v[0];
+}
+
+__device__ __forceinline__ float max_n(const float* p, int n) {
+    float m = 0.0f;
+    for (int i = 0; i < n; ++i) m = __builtin_fmaxf(m, p[i]);
     return m;
 }
 
@@ -445,427 +398,453 @@ __device__ __forceinline__ void store_xhat(const Args& A, uint64_t off, const fl
     }
 }
 
-// ---------------------------------------------------------------------------
-// Outlier choice for one row: the k largest |E| (ties to the lower channel).
-//
-// 1. L = k-th largest of the 64 per-lane maxima of |E|.  At least k elements
-//    satisfy |E| >= L, so the k-th largest element is >= L.
-// 2. Elements with |E| >= L are gathered into LDS (typically ~k of them).
-// 3a. If at most 64 were gathered, the key (|E|, -channel) of each candidate
-//     is ranked against the others; the candidate ranked k-1 gives the
-//     threshold key (T, c*).
-// 3b. Otherwise (heavy ties), T is found by bisection on the bit pattern of
-//     |E| and c* by bisection on the channel among the elements equal to T.
-// 4. An element is an outlier iff |E| > T, or |E| == T and channel <= c*.
-//    It is marked in `selbits` (bit it*8+j of the owning lane) and in the
-//    wave-uniform `slot_any`; the k outliers are gathered and written in
-//    ascending channel order.
+// Workgroup-shared state of one row.
+struct RowShared {
+    uint32_t smax[kWave];           // max |E| bits over lane l of every wave (threshold search)
+    uint64_t ckey[kCandCap];        // candidate key: |E| bits << 32 | (0xFFFF - channel)
+    uint32_t cval[kCandCap];        // candidate E bits
+    uint32_t cnt[4];                // [0] candidate count, [1..3] rotating block counters
+    uint32_t lthr;                  // threshold lower bound L (bits of |E|)
+    uint32_t kstar[3];              // threshold |E| bits, last tied channel taken, ties?
+    float part[5][kMaxWaves];       // chunk partials of groups wider than one chunk
+};
 
-template <int MAXCH>
-__device__ __forceinline__ void select_outliers(const Args& A, const float (&E)[MAXCH][8], int64_t row, uint32_t lane,
-                                uint32_t* s_val, uint32_t* s_idx, SlotMask<MAXCH>& selbits,
-                                SlotMask<MAXCH>& slot_any) {
-    const int k = A.k, d = A.d, nch = A.nch;
-    // 1. per-lane max and its rank among lanes
-    float lm = 0.0f;
-#pragma unroll
-    for (int it = 0; it < MAXCH; ++it)
-        if (it < nch && it * kChunk + (int)lane * 8 < d) {
-#pragma unroll
-            for (int j = 0; j < 8; ++j) lm = __builtin_fmaxf(lm, __builtin_fabsf(E[it][j]));
-        }
-    const uint32_t lmb = __float_as_uint(lm);
-    uint32_t ge = 0;
-#pragma unroll 1
-    for (int l = 0; l < kWave; ++l) ge += (rdlane(lmb, l) >= lmb) ? 1u : 0u;
-    const uint32_t L = wave_max_u32(ge >= (uint32_t)k ? lmb : 0u);
-    const float Lf = __uint_as_float(L);
+// Sum of v over the workgroup (one value per wavefront, from lane 0), through
+// three rotating LDS counters so that consecutive calls need one barrier each.
+__device__ __forceinline__ uint32_t block_sum(RowShared& S, uint32_t v, int& it) {
+    const int slot = 1 + it % 3;
+    if (threadIdx.x == 0) S.cnt[1 + (it + 1) % 3] = 0u;
+    if ((threadIdx.x & (kWave - 1)) == 0) atomicAdd(&S.cnt[slot], v);
+    __syncthreads();
+    ++it;
+    return S.cnt[slot];
+}
 
-    // 2. gather candidates |E| >= L
-    uint32_t ncand = 0;
-#pragma unroll
-    for (int it = 0; it < MAXCH; ++it)
-        if (it < nch) {
-            const bool act = it * kChunk + (int)lane * 8 < d;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const bool p = act && __builtin_fabsf(E[it][j]) >= Lf;
-                const uint64_t m = ballot(p);
-                if (m) {
-                    const uint32_t pos = ncand + mbcnt64(m);
-                    if (p && pos < (uint32_t)kWave) {
-                        s_val[pos] = __float_as_uint(E[it][j]);
-                        s_idx[pos] = (uint32_t)(it * kChunk + lane * 8 + j);
-                    }
-                    ncand += (uint32_t)__builtin_popcountll(m);
-                }
-            }
-        }
-    wave_lds_sync();
-
-    uint32_t T;          // threshold |E| bits
-    uint32_t cstar;      // last tied channel taken (only used when ties)
-    bool ties;
-    if (ncand <= (uint32_t)kWave) {
-        // 3a. rank the candidate keys
-        const bool have = lane < ncand;
-        const uint32_t vb = have ? (s_val[lane] & 0x7FFFFFFFu) : 0u;
-        const uint32_t ix = have ? s_idx[lane] : 0xFFFFu;
-        const uint64_t key = have ? (((uint64_t)vb << 16) | (uint64_t)(0xFFFFu - ix)) : 0ull;
-        uint32_t rank = 0;
-        for (uint32_t l = 0; l < ncand; ++l) {
-            const uint64_t o = ((uint64_t)rdlane((uint32_t)(key >> 32), (int)l) << 32) |
-                               (uint64_t)rdlane((uint32_t)key, (int)l);
-            rank += (o > key) ? 1u : 0u;
-        }
-        const uint64_t at = ballot(have && rank == (uint32_t)(k - 1));
-        const int src = at ? (int)__builtin_ctzll(at) : 0;
-        T = rdlane(vb, src);
-        cstar = rdlane(ix, src);
-        ties = __builtin_popcountll(ballot(have && vb >= T)) != (unsigned)k;
-    } else {
-        // 3b. bisection: largest T with count(|E| >= T) >= k
-        // (compares are written two-sided on E so that nothing per element is
-        // loop-invariant and hoisted into extra registers)
-        uint32_t lo = 0u, hi = 0x7F800000u;
-        while (lo < hi) {
-            const uint32_t mid = lo + ((hi - lo + 1u) >> 1);
-            const float mf = __uint_as_float(mid);
-            uint32_t cnt = 0;
-#pragma unroll
-            for (int it = 0; it < MAXCH; ++it)
-                if (it < nch) {
-                    const bool act = it * kChunk + (int)lane * 8 < d;
-#pragma unroll
-                    for (int j = 0; j < 8; ++j)
-                        cnt += (uint32_t)__builtin_popcountll(
-                            ballot(act && (E[it][j] >= mf || E[it][j] <= -mf)));
-                }
-            if (cnt >= (uint32_t)k) lo = mid;
-            else hi = mid - 1u;
-        }
-        T = lo;
-        const float Tf = __uint_as_float(T);
-        uint32_t gt = 0, ge2 = 0;
-#pragma unroll
-        for (int it = 0; it < MAXCH; ++it)
-            if (it < nch) {
-                const bool act = it * kChunk + (int)lane * 8 < d;
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    gt += (uint32_t)__builtin_popcountll(ballot(act && (E[it][j] > Tf || E[it][j] < -Tf)));
-                    ge2 += (uint32_t)__builtin_popcountll(ballot(act && (E[it][j] >= Tf || E[it][j] <= -Tf)));
-                }
-            }
-        ties = ge2 != (uint32_t)k;
-        // smallest channel c* with count(|E| == T, channel <= c*) == k - gt
-        const uint32_t need = (uint32_t)k - gt;
-        uint32_t clo = 0u, chi = (uint32_t)d - 1u;
-        const uint32_t lane8 = lane * 8u;
-        while (clo < chi) {
-            const uint32_t mid = (clo + chi) >> 1;
-            uint32_t cnt = 0;
-#pragma unroll
-            for (int it = 0; it < MAXCH; ++it)
-                if (it < nch) {
-                    const bool act = it * kChunk + (int)lane * 8 < d;
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        // channel it*512 + 8*lane + j <= mid, as a compare of lane8
-                        const int lim = (int)mid - it * kChunk - j;
-                        cnt += (uint32_t)__builtin_popcountll(ballot(
-                            act && (E[it][j] == Tf || E[it][j] == -Tf) && (int)lane8 <= lim));
-                    }
-                }
-            if (cnt >= need) chi = mid;
-            else clo = mid + 1u;
-        }
-        cstar = clo;
-    }
-    wave_lds_sync();
-
-    // 4. mark and gather the k outliers
-    const float Tf = __uint_as_float(T);
+__device__ __forceinline__ uint32_t count8(const float* e, bool act, float t) {
     uint32_t n = 0;
 #pragma unroll
-    for (int it = 0; it < MAXCH; ++it)
-        if (it < nch) {
-            const bool act = it * kChunk + (int)lane * 8 < d;
+    for (int j = 0; j < 8; ++j) n += (uint32_t)__builtin_popcountll(ballot(act && __builtin_fabsf(e[j]) >= t));
+    return n;
+}
+
+__device__ __forceinline__ uint64_t cand_key(uint32_t ebits, uint32_t ch) {
+    return ((uint64_t)(ebits & 0x7FFFFFFFu) << 32) | (uint64_t)(0xFFFFu - ch);
+}
+
+__device__ __forceinline__ uint32_t key_channel(uint64_t key) { return 0xFFFFu - (uint32_t)(key & 0xFFFFu); }
+
+__device__ __forceinline__ uint64_t rdlane64(uint64_t v, int l) {
+    return ((uint64_t)rdlane((uint32_t)(v >> 32), l) << 32) | (uint64_t)rdlane((uint32_t)v, l);
+}
+
+// Append this lane's elements satisfying p[j] to the LDS candidate list
+// (one LDS atomic per wavefront reserves the slots).
+__device__ __forceinline__ void append8(RowShared& S, uint32_t* counter, const float* e, const bool* p,
+                                        int c0, uint32_t lane) {
+    uint32_t n = 0;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const float a = __builtin_fabsf(E[it][j]);
-                const uint32_t c = (uint32_t)(it * kChunk) + lane * 8u + (uint32_t)j;
-                const bool p = act && (ties ? (a > Tf || (a == Tf && c <= cstar)) : (a >= Tf));
-                const uint64_t m = ballot(p);
-                if (m) {
-                    slot_any.set(it * 8 + j);
-                    if (p) {
-                        selbits.set(it * 8 + j);
-                        const uint32_t pos = n + mbcnt64(m);
-                        if (pos < (uint32_t)kWave) {
-                            s_val[pos] = __float_as_uint(E[it][j]);
-                            s_idx[pos] = c;
-                        }
-                    }
-                    n += (uint32_t)__builtin_popcountll(m);
-                }
+    for (int j = 0; j < 8; ++j) n += (uint32_t)__builtin_popcountll(ballot(p[j]));
+    if (!n) return;
+    uint32_t base = 0u;
+    if (lane == 0u) base = atomicAdd(counter, n);
+    base = (uint32_t)__builtin_amdgcn_readfirstlane((int)base);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const uint64_t m = ballot(p[j]);
+        if (m) {
+            const uint32_t pos = base + mbcnt64(m);
+            if (p[j] && pos < (uint32_t)kCandCap) {
+                S.ckey[pos] = cand_key(__float_as_uint(e[j]), (uint32_t)(c0 + j));
+                S.cval[pos] = __float_as_uint(e[j]);
             }
+            base += (uint32_t)__builtin_popcountll(m);
         }
-    wave_lds_sync();
-    // n == k here.  Lane i < k holds gathered outlier i; its output slot is
-    // the number of gathered outliers with a lower channel.
-    if (lane < (uint32_t)k) {
-        const uint32_t c = s_idx[lane];
-        const uint32_t v = s_val[lane];
-        uint32_t slot = 0;
-        for (int i = 0; i < k; ++i) slot += (s_idx[i] < c) ? 1u : 0u;
-        uint32_t* out = reinterpret_cast<uint32_t*>(A.wire + A.off_outl) + (uint64_t)row * (uint64_t)k;
-        out[slot] = c | (f16_rne_sat(__uint_as_float(v)) << 16);
     }
-    wave_lds_sync();
 }
 
 // ---------------------------------------------------------------------------
-// Encode with fused sender reconstruction: one wavefront per token row.
+// Per-token outlier choice: the k largest |E| of the row, ties to the lower
+// channel.  Called by every wavefront of the workgroup with its 8 residuals
+// per lane; returns the per-lane mask of chosen channels (bit j = channel
+// c0 + j) and writes the row's outlier entries in ascending channel order.
+//
+// 1. Threshold L: the channels of lane l in all wavefronts form one strided
+//    group (64 channels spread over the row); its max |E| is built with one
+//    LDS atomic max per lane.  Every wave finds the k-th largest of the 64
+//    group maxima by an MSB-first radix select on the bit patterns (compare +
+//    ballot per bit), stopping after the top 16 bits, which can only lower L.
+//    At least k groups have a maximum >= L, each holding an element >= L, so
+//    every outlier satisfies |E| >= L.  On the benchmark data about k+1
+//    elements pass.
+// 2. Candidates |E| >= L are appended to LDS.
+// 3a. At most 64 candidates: wave 0 ranks their keys (|E|, -channel); rank
+//     k-1 is the threshold key K*, outliers are the keys >= K*.
+// 3b. Otherwise (heavy ties) the threshold is found directly: a radix select
+//     of T = k-th largest |E| with workgroup-wide counts, then the last tied
+//     channel c* by bisection on the channel among the elements equal to T.
+// 4. An element is an outlier iff |E| > T, or |E| == T and channel <= c*.
 
-template <int BITS, int MAXCH>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(2))) void rac_encode_kernel(Args A) {
-    __shared__ uint32_t s_val_all[kWavesPerBlock][kWave];
-    __shared__ uint32_t s_idx_all[kWavesPerBlock][kWave];
-    const uint32_t lane = threadIdx.x & (kWave - 1);
-    const uint32_t wv = threadIdx.x / kWave;
-    if (A.write_header && blockIdx.x == 0 && wv == 0) write_header(A, lane);
-    const int64_t row = (int64_t)blockIdx.x * kWavesPerBlock + wv;
-    if (row >= A.tokens) return;
-
-    const int d = A.d, nch = A.nch;
-    const float q = (float)((1 << (BITS - 1)) - 1);
-    const uint64_t rbase = (uint64_t)row * (uint64_t)d;
-
-    // a1: load x and ref rows (raw bf16 words; widening to fp32 is exact and
-    // is redone where a value is needed, which keeps the row in 64 VGPRs)
-    uint4 XV[MAXCH], RV[MAXCH];
+__device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S, const float* e,
+                                                    bool act, int c0, uint32_t lane, int w, int64_t row) {
+    const int k = A.k;
+    // 1. strided group maxima: lane l of every wave -> one LDS max per lane
+    float lm = 0.0f;
 #pragma unroll
-    for (int it = 0; it < MAXCH; ++it) {
-        XV[it] = make_uint4(0, 0, 0, 0);
-        RV[it] = make_uint4(0, 0, 0, 0);
-        const int c0 = it * kChunk + (int)lane * 8;
-        if (it < nch && c0 < d) {
-            XV[it] = *reinterpret_cast<const uint4*>(A.x + rbase + c0);
-            if (A.ref) RV[it] = *reinterpret_cast<const uint4*>(A.ref + rbase + c0);
-        }
+    for (int j = 0; j < 8; ++j) lm = __builtin_fmaxf(lm, __builtin_fabsf(e[j]));
+    if (act) atomicMax(&S.smax[lane], __float_as_uint(lm));  // bits order like non-negative floats
+    if (threadIdx.x == 0) {
+        S.cnt[0] = 0u;
+        S.cnt[1] = 0u;
     }
+    __syncthreads();
+    // k-th largest of the 64 group maxima, top 16 bits (every wave, same result)
+    const uint32_t v = S.smax[lane];
+    uint32_t L = 0u;
+#pragma unroll
+    for (int bit = 30; bit >= 15; --bit) {
+        const uint32_t c = L | (1u << bit);
+        if ((uint32_t)__builtin_popcountll(ballot(v >= c)) >= (uint32_t)k) L = c;
+    }
+    const float Lf = __uint_as_float(L);
+    // 2. candidates |E| >= L
+    {
+        bool p[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) p[j] = act && __builtin_fabsf(e[j]) >= Lf;
+        append8(S, &S.cnt[0], e, p, c0, lane);
+    }
+    __syncthreads();
+    const uint32_t C = S.cnt[0];
+    uint32_t* outl = reinterpret_cast<uint32_t*>(A.wire + A.off_outl) + (uint64_t)row * (uint64_t)k;
 
-    // a2-a3: grouped affine fit (two-pass centred moments, pairwise sums),
-    // serialized to fp16, then the residual E = x - (alpha r + beta).
-    uint32_t* coef_row = reinterpret_cast<uint32_t*>(A.wire + A.off_coef) + (uint64_t)row * (uint64_t)(d / A.ga);
-    const float inv_ga = 1.0f / (float)A.ga;  // exact: power of two
-    float X[MAXCH][8];   // becomes the residual E
-    uint32_t CF[MAXCH];  // serialized (alpha, beta) of the lane's group
-    if (A.cpg_a == 1) {
-        // groups lie inside one chunk: fit and residual chunk by chunk
-        const int lanes_pg = A.ga >= kChunk ? kWave : A.ga / 8;
-#pragma unroll
-        for (int it = 0; it < MAXCH; ++it) {
-            float r[8], x[8];
-            widen8(RV[it], r);
-            widen8(XV[it], x);
-            const float mr = lane_sum(tree8(r), A.lane_lv_a) * inv_ga;
-            const float mx = lane_sum(tree8(x), A.lane_lv_a) * inv_ga;
-            float uu[8], uv[8];
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const float u = r[j] - mr;
-                const float v = x[j] - mx;
-                uu[j] = u * u;
-                uv[j] = u * v;
+    if (w == 0) S.smax[lane] = 0u;  // ready for the next row (read by every wave before this barrier)
+    if (C <= (uint32_t)kCandCap) {
+        // 3a. wave 0 ranks the candidates (one per lane)
+        if (w == 0) {
+            const bool have = lane < C;
+            const uint64_t key = have ? S.ckey[lane] : 0ull;
+            const uint32_t val = have ? S.cval[lane] : 0u;
+            uint32_t rank = 0;
+            for (uint32_t j = 0; j < C; ++j) rank += (rdlane64(key, (int)j) > key) ? 1u : 0u;
+            const uint64_t at = ballot(have && rank == (uint32_t)(k - 1));
+            const uint64_t kst = rdlane64(key, at ? (int)__builtin_ctzll(at) : 0);
+            const uint32_t T = (uint32_t)(kst >> 32);
+            const uint32_t ch = key_channel(key);
+            uint32_t slot = 0;
+            for (uint32_t j = 0; j < C; ++j) {
+                const uint64_t kj = rdlane64(key, (int)j);
+                slot += (kj >= kst && key_channel(kj) < ch) ? 1u : 0u;
             }
-            const float crr = lane_sum(tree8(uu), A.lane_lv_a);
-            const float crx = lane_sum(tree8(uv), A.lane_lv_a);
-            CF[it] = fit_coef(crr, crx, mr, mx);
-            const int c0 = it * kChunk + (int)lane * 8;
-            if (it < nch && c0 < d && (int)lane % lanes_pg == 0) coef_row[c0 / A.ga] = CF[it];
-            residual8(CF[it], r, x, X[it]);
+            if (have && key >= kst && slot < (uint32_t)k) outl[slot] = ch | (f16_rne_sat(__uint_as_float(val)) << 16);
+            const bool ties = __builtin_popcountll(ballot(have && (uint32_t)(key >> 32) >= T)) > (unsigned)k;
+            if (lane == 0u) {
+                S.kstar[0] = T;
+                S.kstar[1] = key_channel(kst);
+                S.kstar[2] = ties ? 1u : 0u;
+            }
         }
     } else {
-        // groups span cpg_a chunks: chunk partial sums combined by a tree
-        float SR[MAXCH], SX[MAXCH], SUU[MAXCH], SUV[MAXCH];
-#pragma unroll
-        for (int it = 0; it < MAXCH; ++it) {
-            float r[8], x[8];
-            widen8(RV[it], r);
-            widen8(XV[it], x);
-            SR[it] = lane_sum(tree8(r), 6);
-            SX[it] = lane_sum(tree8(x), 6);
+        // 3b. radix select of T with workgroup-wide counts
+        int it = 0;
+        uint32_t T = 0u;
+        for (int bit = 30; bit >= 0; --bit) {
+            const uint32_t c = T | (1u << bit);
+            if (block_sum(S, count8(e, act, __uint_as_float(c)), it) >= (uint32_t)k) T = c;
         }
-        chunk_tree_sum<MAXCH>(SR, A.cpg_a);
-        chunk_tree_sum<MAXCH>(SX, A.cpg_a);
+        const float Tf = __uint_as_float(T);
+        uint32_t gtw = 0;
 #pragma unroll
-        for (int it = 0; it < MAXCH; ++it) {
-            const float mr = SR[it] * inv_ga, mx = SX[it] * inv_ga;
-            float r[8], x[8], uu[8], uv[8];
-            widen8(RV[it], r);
-            widen8(XV[it], x);
+        for (int j = 0; j < 8; ++j) gtw += (uint32_t)__builtin_popcountll(ballot(act && __builtin_fabsf(e[j]) > Tf));
+        const uint32_t gt = block_sum(S, gtw, it);
+        const uint32_t ge = block_sum(S, count8(e, act, Tf), it);
+        const bool ties = ge != (uint32_t)k;
+        uint32_t cstar = 0xFFFFu;
+        if (ties) {
+            // smallest channel c* with count(|E| == T, channel <= c*) == k - gt
+            const uint32_t need = (uint32_t)k - gt;
+            uint32_t lo = 0u, hi = (uint32_t)A.d - 1u;
+            while (lo < hi) {
+                const uint32_t mid = (lo + hi) >> 1;
+                uint32_t n = 0;
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    n += (uint32_t)__builtin_popcountll(
+                        ballot(act && __builtin_fabsf(e[j]) == Tf && (uint32_t)(c0 + j) <= mid));
+                if (block_sum(S, n, it) >= need) hi = mid;
+                else lo = mid + 1u;
+            }
+            cstar = lo;
+        }
+        // gather the k outliers; wave 0 writes them by ascending channel
+        const int slot = 1 + it % 3;
+        if (threadIdx.x == 0) S.cnt[1 + (it + 1) % 3] = 0u;
+        __syncthreads();
+        bool p[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const float a = __builtin_fabsf(e[j]);
+            p[j] = act && (ties ? (a > Tf || (a == Tf && (uint32_t)(c0 + j) <= cstar)) : a >= Tf);
+        }
+        append8(S, &S.cnt[slot], e, p, c0, lane);
+        __syncthreads();
+        if (w == 0) {
+            const bool have = lane < (uint32_t)k;
+            const uint32_t ch = have ? key_channel(S.ckey[lane]) : 0u;
+            const uint32_t val = have ? S.cval[lane] : 0u;
+            uint32_t pos = 0;
+            for (int j = 0; j < k; ++j) pos += (key_channel(S.ckey[j]) < ch) ? 1u : 0u;
+            if (have && pos < (uint32_t)k) outl[pos] = ch | (f16_rne_sat(__uint_as_float(val)) << 16);
+            if (lane == 0u) {
+                S.kstar[0] = T;
+                S.kstar[1] = cstar;
+                S.kstar[2] = ties ? 1u : 0u;
+            }
+        }
+    }
+    __syncthreads();
+    // 4. mark this lane's outliers
+    const uint32_t T = S.kstar[0], cstar = S.kstar[1];
+    const bool ties = S.kstar[2] != 0u;
+    const float Tf = __uint_as_float(T);
+    uint32_t selm = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const float a = __builtin_fabsf(e[j]);
+        const bool p = act && (ties ? (a > Tf || (a == Tf && (uint32_t)(c0 + j) <= cstar)) : a >= Tf);
+        if (p) selm |= 1u << j;
+    }
+    return selm;
+}
+
+// ---------------------------------------------------------------------------
+// Encode with fused sender reconstruction.  One workgroup per token row (rows
+// beyond the grid are taken in strides, the next row's x and ref prefetched
+// into registers while the current one is processed), one wavefront per
+// 512-channel chunk.
+
+template <int BITS>
+__global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
+    __shared__ RowShared S;
+    const uint32_t lane = threadIdx.x & (kWave - 1);
+    const int w = (int)(threadIdx.x / kWave);
+    const int d = A.d;
+    const int c0 = w * kChunk + (int)lane * 8;
+    const bool act = c0 < d;
+    const float q = (float)((1 << (BITS - 1)) - 1);
+    if (A.write_header && blockIdx.x == 0 && w == 0) write_header(A, lane);
+    const bool dword3 = (d & 31) == 0;
+    const int grp_a = c0 >> A.lg_a, grp_q = c0 >> A.lg_q;
+    const int cpg_a = 1 << A.lg_cpg_a, cpg_q = 1 << A.lg_cpg_q;
+    const bool first_a = A.lg_cpg_a == 0 ? (lane & ((1u << (A.lg_a - 3)) - 1u)) == 0u
+                                         : (lane == 0u && (w & (cpg_a - 1)) == 0);
+    const bool first_q = A.lg_cpg_q == 0 ? (lane & ((1u << (A.lg_q - 3)) - 1u)) == 0u
+                                         : (lane == 0u && (w & (cpg_q - 1)) == 0);
+    const uint32_t sh_fixed = (A.fixed && act) ? step_roundup(A.steps[grp_q]) : 0u;
+    const uint32_t ngq = (uint32_t)d >> A.lg_q, nga = (uint32_t)d >> A.lg_a;
+
+    if (A.k > 0) {
+        if (w == 0) S.smax[lane] = 0u;
+        __syncthreads();
+    }
+    int64_t row = blockIdx.x;
+    uint4 nx = make_uint4(0, 0, 0, 0), nr = make_uint4(0, 0, 0, 0);
+    if (row < A.tokens && act) {
+        nx = *reinterpret_cast<const uint4*>(A.x + (uint64_t)row * (uint64_t)d + c0);
+        if (A.ref) nr = *reinterpret_cast<const uint4*>(A.ref + (uint64_t)row * (uint64_t)d + c0);
+    }
+    for (; row < A.tokens; row += gridDim.x) {
+        if (row != (int64_t)blockIdx.x) __syncthreads();  // LDS reuse across rows
+        const uint64_t rbase = (uint64_t)row * (uint64_t)d;
+        const uint4 xv = nx, rv = nr;
+        const int64_t nrow = row + gridDim.x;
+        if (nrow < A.tokens && act) {
+            nx = *reinterpret_cast<const uint4*>(A.x + (uint64_t)nrow * (uint64_t)d + c0);
+            if (A.ref) nr = *reinterpret_cast<const uint4*>(A.ref + (uint64_t)nrow * (uint64_t)d + c0);
+        }
+        float r[8], x[8];
+        widen8(rv, r);
+        widen8(xv, x);
+
+        // a2: grouped affine fit, two-pass centred moments, pairwise sums
+        float mr, mx, crr, crx;
+        float uu[8], uv[8];
+        if (A.lg_cpg_a == 0) {
+            mr = lane_sum(tree8(r), A.lane_lv_a) * A.inv_ga;
+            mx = lane_sum(tree8(x), A.lane_lv_a) * A.inv_ga;
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
-                const float u = r[j] - mr;
-                const float v = x[j] - mx;
+                const float u = r[j] - mr, v = x[j] - mx;
                 uu[j] = u * u;
                 uv[j] = u * v;
             }
-            SUU[it] = lane_sum(tree8(uu), 6);
-            SUV[it] = lane_sum(tree8(uv), 6);
+            crr = lane_sum(tree8(uu), A.lane_lv_a);
+            crx = lane_sum(tree8(uv), A.lane_lv_a);
+        } else {
+            const int g0 = w & ~(cpg_a - 1);
+            const float sr = lane_sum(tree8(r), 6), sx = lane_sum(tree8(x), 6);
+            if (lane == 0u) {
+                S.part[0][w] = sr;
+                S.part[1][w] = sx;
+            }
+            __syncthreads();
+            mr = tree_n(&S.part[0][g0], cpg_a) * A.inv_ga;
+            mx = tree_n(&S.part[1][g0], cpg_a) * A.inv_ga;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const float u = r[j] - mr, v = x[j] - mx;
+                uu[j] = u * u;
+                uv[j] = u * v;
+            }
+            const float suu = lane_sum(tree8(uu), 6), suv = lane_sum(tree8(uv), 6);
+            if (lane == 0u) {
+                S.part[2][w] = suu;
+                S.part[3][w] = suv;
+            }
+            __syncthreads();
+            crr = tree_n(&S.part[2][g0], cpg_a);
+            crx = tree_n(&S.part[3][g0], cpg_a);
         }
-        chunk_tree_sum<MAXCH>(SUU, A.cpg_a);
-        chunk_tree_sum<MAXCH>(SUV, A.cpg_a);
+        const uint32_t cf = fit_coef(crr, crx, mr, mx);
+        if (first_a && act) reinterpret_cast<uint32_t*>(A.wire + A.off_coef)[(uint64_t)row * nga + grp_a] = cf;
+
+        // a3: aligned reference R~ = fma(alpha, r, beta) and residual E = x - R~
+        const float a = f16_value(cf & 0xFFFFu), b0 = f16_value(cf >> 16);
+        float rt[8], e[8];
 #pragma unroll
-        for (int it = 0; it < MAXCH; ++it) {
-            CF[it] = fit_coef(SUU[it], SUV[it], SR[it] * inv_ga, SX[it] * inv_ga);
-            if (it < nch && lane == 0 && (it % A.cpg_a) == 0) coef_row[(it * kChunk) / A.ga] = CF[it];
-            float r[8], x[8];
-            widen8(RV[it], r);
-            widen8(XV[it], x);
-            residual8(CF[it], r, x, X[it]);
+        for (int j = 0; j < 8; ++j) {
+            rt[j] = __builtin_fmaf(a, r[j], b0);
+            e[j] = x[j] - rt[j];
         }
-    }
 
-    // a4: outliers
-    SlotMask<MAXCH> selbits{}, slot_any{};
-    if (A.k > 0) select_outliers<MAXCH>(A, X, row, lane, s_val_all[wv], s_idx_all[wv], selbits, slot_any);
-
-    // a5: dense max per quantization group (groups spanning chunks need all
-    // chunk maxima first; groups inside a chunk are done chunk by chunk)
-    float M[MAXCH];
-    if (A.cpg_q > 1) {
+        // a4: outliers
+        uint32_t selm = 0;
+        if (A.k > 0) selm = select_outliers(A, S, e, act, c0, lane, w, row);
+        float ed[8];
 #pragma unroll
-        for (int it = 0; it < MAXCH; ++it) M[it] = lane_max(dense_absmax8(X[it], selbits, slot_any, it), 6);
-        chunk_tree_max<MAXCH>(M, A.cpg_q);
-    }
-
-    uint16_t* scale_row = reinterpret_cast<uint16_t*>(A.wire + A.off_scale) + (uint64_t)row * (uint64_t)(d / A.gq);
-    uint8_t* code_row = A.wire + A.off_codes + (uint64_t)row * (uint64_t)d * BITS / 8u;
-    const bool dword3 = (d % 32) == 0;
-    const int lanes_pg_q = A.gq >= kChunk ? kWave : A.gq / 8;
+        for (int j = 0; j < 8; ++j) ed[j] = e[j];
+        if (selm) {
 #pragma unroll
-    for (int it = 0; it < MAXCH; ++it) {
-        if (it < nch) {
-        const int c0 = it * kChunk + (int)lane * 8;
-        const bool act = c0 < d;
-        const int grp = c0 / A.gq;
-        const float m = A.cpg_q > 1 ? M[it] : lane_max(dense_absmax8(X[it], selbits, slot_any, it), A.lane_lv_q);
+            for (int j = 0; j < 8; ++j)
+                if ((selm >> j) & 1u) ed[j] = 0.0f;
+        }
+
+        // a5: scale of the quantization group
         uint32_t sh;
         if (A.fixed) {
-            sh = step_roundup(act ? A.steps[grp] : 1.0f);
+            sh = sh_fixed;
         } else {
+            float m = 0.0f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) m = __builtin_fmaxf(m, __builtin_fabsf(ed[j]));
+            if (A.lg_cpg_q == 0) {
+                m = lane_max(m, A.lane_lv_q);
+            } else {
+                m = lane_max(m, 6);
+                if (lane == 0u) S.part[4][w] = m;
+                __syncthreads();
+                m = max_n(&S.part[4][w & ~(cpg_q - 1)], cpg_q);
+            }
             sh = m == 0.0f ? 0u : scale_roundup(m, q);
-            const bool first = (A.gq >= kChunk) ? (lane == 0 && (it % A.cpg_q) == 0) : ((int)lane % lanes_pg_q == 0);
-            if (first && act) scale_row[grp] = (uint16_t)sh;
+            if (first_q && act)
+                reinterpret_cast<uint16_t*>(A.wire + A.off_scale)[(uint64_t)row * ngq + grp_q] = (uint16_t)sh;
         }
         const float s = f16_value(sh);
         const float inv = sh ? __builtin_amdgcn_rcpf(s) : 0.0f;
-        const float a = f16_value(CF[it] & 0xFFFFu), b0 = f16_value(CF[it] >> 16);
-        float r[8];
-        widen8(RV[it], r);
-        // a6-a8: quantize, pack, reconstruct
+
+        // a6-a8: quantize (round half to even), pack, reconstruct
         Packed<BITS> pk{};
         float H[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            float e = X[it][j];
-            const bool slot_has = slot_any.test(it * 8 + j);
-            bool is_out = false;
-            if (slot_has) {
-                is_out = selbits.test(it * 8 + j);
-                if (is_out) e = 0.0f;
-            }
-            float tc = __builtin_amdgcn_fmed3f(e * inv, -q, q);
+            float tc = __builtin_amdgcn_fmed3f(ed[j] * inv, -q, q);
             float mg = tc + kMagic;
             float qf = mg - kMagic;
-            if (__builtin_fabsf(tc - qf) > kNearHalf) {
-                tc = __builtin_amdgcn_fmed3f(e / s, -q, q);
+            if (__builtin_fabsf(tc - qf) > kNearHalf) {  // near a tie: exact quotient
+                tc = __builtin_amdgcn_fmed3f(ed[j] / s, -q, q);
                 mg = tc + kMagic;
                 qf = mg - kMagic;
             }
             pack_put<BITS>(pk, j, __float_as_uint(mg));
-            float eh = qf * s;
-            if (slot_has && is_out) eh = f16_value(f16_rne_sat(X[it][j]));
-            H[j] = (a * r[j] + b0) + eh;
+            H[j] = __builtin_fmaf(qf, s, rt[j]);  // q*s is exact, so this is R~ + q*s
         }
-        store_codes<BITS>(code_row, it, lane, act, dword3, pk);
+        if (selm) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if ((selm >> j) & 1u) H[j] = rt[j] + f16_value(f16_rne_sat(e[j]));
+        }
+        store_codes<BITS>(A.wire + A.off_codes + (uint64_t)row * A.code_row_bytes, w, lane, act, dword3, pk);
         if (A.xhat && act) store_xhat(A, rbase + c0, H);
-        }
     }
 }
 
 // ---------------------------------------------------------------------------
-// Decode / reconstruct: one wavefront per token row, pure streaming.
+// Decode / reconstruct: one workgroup per token row (strided, with the next
+// row's inputs prefetched), one wavefront per chunk, no cross-wave work.
 
-template <int BITS, int MAXCH>
-__global__ __launch_bounds__(kBlock) void rac_decode_kernel(Args A) {
-    __shared__ uint32_t s_ent_all[kWavesPerBlock][kWave];
+template <int BITS>
+__global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
     const uint32_t lane = threadIdx.x & (kWave - 1);
-    const uint32_t wv = threadIdx.x / kWave;
-    const int64_t row = (int64_t)blockIdx.x * kWavesPerBlock + wv;
-    if (row >= A.tokens) return;
-    const int d = A.d, nch = A.nch, k = A.k;
-    const uint64_t rbase = (uint64_t)row * (uint64_t)d;
-    uint32_t* s_ent = s_ent_all[wv];
+    const int w = (int)(threadIdx.x / kWave);
+    const int d = A.d, k = A.k;
+    const int c0 = w * kChunk + (int)lane * 8;
+    const bool act = c0 < d;
+    const bool dword3 = (d & 31) == 0;
+    const int grp_a = c0 >> A.lg_a, grp_q = c0 >> A.lg_q;
+    const uint32_t ngq = (uint32_t)d >> A.lg_q, nga = (uint32_t)d >> A.lg_a;
+    const uint32_t sh_fixed = (A.fixed && act) ? step_roundup(A.steps[grp_q]) : 0u;
 
-    // outliers of this row: owner lanes mark their slots
-    SlotMask<MAXCH> selbits{}, slot_any{};
-    if (k > 0) {
-        const uint32_t* ol = reinterpret_cast<const uint32_t*>(A.wire + A.off_outl) + (uint64_t)row * (uint64_t)k;
-        const uint32_t ent = lane < (uint32_t)k ? ol[lane] : 0u;
-        s_ent[lane] = ent;
-        wave_lds_sync();
-        for (int i = 0; i < k; ++i) {
-            const uint32_t c = rdlane(ent, i) & 0xFFFFu;
-            if (c < (uint32_t)d) {
-                const uint32_t owner = (c % kChunk) / 8u;
-                const int slot = (int)((c / kChunk) * 8u + (c % 8u));
-                slot_any.set(slot);
-                if (lane == owner) selbits.set(slot);
-            }
-        }
-    }
-
-    const uint32_t* coef_row = reinterpret_cast<const uint32_t*>(A.wire + A.off_coef) + (uint64_t)row * (uint64_t)(d / A.ga);
-    const uint16_t* scale_row = reinterpret_cast<const uint16_t*>(A.wire + A.off_scale) + (uint64_t)row * (uint64_t)(d / A.gq);
-    const uint8_t* code_row = A.wire + A.off_codes + (uint64_t)row * (uint64_t)d * BITS / 8u;
-    const bool dword3 = (d % 32) == 0;
-#pragma unroll
-    for (int it = 0; it < MAXCH; ++it) {
-        if (it < nch) {
-        const int c0 = it * kChunk + (int)lane * 8;
-        const bool act = c0 < d;
-        uint4 rv = make_uint4(0, 0, 0, 0);
-        uint32_t cf = 0, sh = 0, lo, hi;
+    // inputs of one row for this lane: ref words, packed codes, coefficient
+    // pair, scale, and (lanes < k) one outlier entry
+    struct In {
+        uint4 rv;
+        uint32_t lo, hi, cf, sh, ent;
+    };
+    auto load = [&](int64_t rw) {
+        In in{};
+        in.ent = 0xFFFFFFFFu;
         if (act) {
-            if (A.ref) rv = *reinterpret_cast<const uint4*>(A.ref + rbase + c0);
-            cf = coef_row[c0 / A.ga];
-            sh = A.fixed ? step_roundup(A.steps[c0 / A.gq]) : (uint32_t)scale_row[c0 / A.gq];
+            if (A.ref) in.rv = *reinterpret_cast<const uint4*>(A.ref + (uint64_t)rw * (uint64_t)d + c0);
+            in.cf = reinterpret_cast<const uint32_t*>(A.wire + A.off_coef)[(uint64_t)rw * nga + grp_a];
+            in.sh = A.fixed ? sh_fixed
+                            : (uint32_t)reinterpret_cast<const uint16_t*>(A.wire + A.off_scale)[(uint64_t)rw * ngq + grp_q];
         }
-        load_codes<BITS>(code_row, it, lane, act, dword3, lo, hi);
-        const float a = f16_value(cf & 0xFFFFu), b0 = f16_value(cf >> 16);
-        const float s = f16_value(sh);
-        const float r[8] = {bf16_lo(rv.x), bf16_hi(rv.x), bf16_lo(rv.y), bf16_hi(rv.y),
-                            bf16_lo(rv.z), bf16_hi(rv.z), bf16_lo(rv.w), bf16_hi(rv.w)};
-        float H[8];
+        load_codes<BITS>(A.wire + A.off_codes + (uint64_t)rw * A.code_row_bytes, w, lane, act, dword3, in.lo, in.hi);
+        if (lane < (uint32_t)k)
+            in.ent = reinterpret_cast<const uint32_t*>(A.wire + A.off_outl)[(uint64_t)rw * (uint64_t)k + lane];
+        return in;
+    };
+
+    int64_t row = blockIdx.x;
+    In nxt{};
+    if (row < A.tokens) nxt = load(row);
+    for (; row < A.tokens; row += gridDim.x) {
+        const In in = nxt;
+        const int64_t nrow = row + gridDim.x;
+        if (nrow < A.tokens) nxt = load(nrow);
+        const float a = f16_value(in.cf & 0xFFFFu), b0 = f16_value(in.cf >> 16);
+        const float s = f16_value(in.sh);
+        float r[8], rt[8], H[8];
+        widen8(in.rv, r);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            float eh = (float)code_at<BITS>(lo, hi, j) * s;
-            if (slot_any.test(it * 8 + j)) {
-                if (selbits.test(it * 8 + j)) {
-                    const uint32_t c = (uint32_t)c0 + (uint32_t)j;
-                    for (int i = 0; i < k; ++i)
-                        if ((s_ent[i] & 0xFFFFu) == c) eh = f16_value(s_ent[i] >> 16);
+            rt[j] = __builtin_fmaf(a, r[j], b0);
+            H[j] = __builtin_fmaf((float)code_at<BITS>(in.lo, in.hi, j), s, rt[j]);  // R~ + q*s, q*s exact
+        }
+        for (int i = 0; i < k; ++i) {
+            // outliers of this chunk replace the dense value at their channel
+            const uint32_t en = rdlane(in.ent, i);
+            const uint32_t c = en & 0xFFFFu;
+            if (c < (uint32_t)d && (int)(c / kChunk) == w) {
+                const uint32_t owner = (c % kChunk) / 8u, jj = c % 8u;
+                const float v = f16_value(en >> 16);
+                if (lane == owner) {
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        if ((uint32_t)j == jj) H[j] = rt[j] + v;
                 }
             }
-            const float rt = a * r[j] + b0;
-            H[j] = rt + eh;
         }
-        if (act) store_xhat(A, rbase + c0, H);
-        }
+        if (act) store_xhat(A, (uint64_t)row * (uint64_t)d + c0, H);
     }
 }
 
@@ -925,18 +904,20 @@ Args make_args(const rac_config* c, const Sizes& S) {
     A.end_scale = S.L.off_scale + S.scale;
     A.end_codes = S.L.off_codes + S.codes;
     A.end_outl = S.L.off_outl + S.outl;
+    A.code_row_bytes = (uint64_t)c->hidden * (uint64_t)c->bits / 8u;
     A.tokens = c->tokens;
     A.d = c->hidden;
     A.nch = (c->hidden + kChunk - 1) / kChunk;
-    A.ga = c->group_align;
-    A.gq = c->group_quant;
+    A.lg_a = ilog2(c->group_align);
+    A.lg_q = ilog2(c->group_quant);
     A.lane_lv_a = ilog2(c->group_align >= kChunk ? kChunk / 8 : c->group_align / 8);
     A.lane_lv_q = ilog2(c->group_quant >= kChunk ? kChunk / 8 : c->group_quant / 8);
-    A.cpg_a = c->group_align >= kChunk ? c->group_align / kChunk : 1;
-    A.cpg_q = c->group_quant >= kChunk ? c->group_quant / kChunk : 1;
+    A.lg_cpg_a = c->group_align > kChunk ? ilog2(c->group_align / kChunk) : 0;
+    A.lg_cpg_q = c->group_quant > kChunk ? ilog2(c->group_quant / kChunk) : 0;
     A.k = c->outlier_k;
     A.fixed = (c->flags & RAC_FLAG_FIXED_STEP) ? 1 : 0;
     A.xhat_bf16 = (c->flags & RAC_FLAG_XHAT_BF16) ? 1 : 0;
+    A.inv_ga = 1.0f / (float)c->group_align;
     return A;
 }
 
@@ -973,33 +954,50 @@ void fill_header(Args& A, const rac_config* c, bool zero_ref) {
 
 using KernelFn = void (*)(Args);
 
-template <int BITS, int MAXCH>
-struct EncK { static constexpr KernelFn fn = rac_encode_kernel<BITS, MAXCH>; };
-template <int BITS, int MAXCH>
-struct DecK { static constexpr KernelFn fn = rac_decode_kernel<BITS, MAXCH>; };
-
-template <template <int, int> class K>
-KernelFn pick(int bits, int nch) {
-    const bool small = nch <= 8;
+KernelFn pick_encode(int bits) {
     switch (bits) {
-        case 2: return small ? K<2, 8>::fn : K<2, 16>::fn;
-        case 3: return small ? K<3, 8>::fn : K<3, 16>::fn;
-        case 4: return small ? K<4, 8>::fn : K<4, 16>::fn;
-        default: return small ? K<8, 8>::fn : K<8, 16>::fn;
+        case 2: return rac_encode_kernel<2>;
+        case 3: return rac_encode_kernel<3>;
+        case 4: return rac_encode_kernel<4>;
+        default: return rac_encode_kernel<8>;
     }
 }
 
-rac_status launch(KernelFn fn, Args A, int64_t rows, hipStream_t stream) {
-    const int64_t blocks = rows > 0 ? (rows + kWavesPerBlock - 1) / kWavesPerBlock : 1;
+KernelFn pick_decode(int bits) {
+    switch (bits) {
+        case 2: return rac_decode_kernel<2>;
+        case 3: return rac_decode_kernel<3>;
+        case 4: return rac_decode_kernel<4>;
+        default: return rac_decode_kernel<8>;
+    }
+}
+
+// One workgroup per token row.  Large row counts use a grid of as many
+// workgroups as the device keeps resident, each taking rows in strides (and
+// prefetching its next row); small counts launch one workgroup per row.
+rac_status launch(KernelFn fn, Args A, hipStream_t stream) {
+    const int64_t rows = A.tokens;
+    const int threads = A.nch * kWave;
+    int64_t blocks = rows <= 0 ? 1 : rows;
+    if (rows > 256) {
+        int dev = 0, cus = 0, per_cu = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(fn), threads, 0) !=
+                hipSuccess)
+            return RAC_ERR_HIP;
+        const int64_t resident = (int64_t)cus * (per_cu > 0 ? per_cu : 1);
+        if (blocks > resident) blocks = resident;
+    }
     void* args[] = {&A};
     const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3((unsigned)blocks),
-                                         dim3(kBlock), args, 0, stream);
+                                         dim3((unsigned)threads), args, 0, stream);
     return e == hipSuccess ? RAC_OK : RAC_ERR_HIP;
 }
 
 rac_status common_checks(const rac_config* cfg) {
     if (!config_valid(cfg)) return RAC_ERR_INVALID;
-    if (cfg->hidden > 16 * kChunk) return RAC_ERR_UNSUPPORTED;
+    if (cfg->hidden > kMaxWaves * kChunk) return RAC_ERR_UNSUPPORTED;
     return RAC_OK;
 }
 
@@ -1019,7 +1017,7 @@ rac_status run_decode(const rac_config* cfg, const void* wire, const void* ref, 
     A.ref = static_cast<const uint16_t*>(ref);
     A.steps = steps;
     A.xhat = xhat;
-    return launch(pick<DecK>(cfg->bits, A.nch), A, cfg->tokens, stream);
+    return launch(pick_decode(cfg->bits), A, stream);
 }
 
 }  // namespace
@@ -1092,7 +1090,7 @@ rac_status rac_encode(const rac_config* cfg, const void* x, const void* ref, con
     A.xhat = xhat;
     A.write_header = 1;
     fill_header(A, cfg, ref == nullptr);
-    return launch(pick<EncK>(cfg->bits, A.nch), A, cfg->tokens, stream);
+    return launch(pick_encode(cfg->bits), A, stream);
 }
 
 rac_status rac_reconstruct(const rac_config* cfg, const void* wire, const void* ref,

@@ -32,7 +32,7 @@ MUTANTS = [
     ("outlier_ties_to_higher", "return (a->idx < b->idx) ? -1 : (a->idx > b->idx);",
      "return (a->idx > b->idx) ? -1 : (a->idx < b->idx);"),
     ("outlier_left_in_dense", "                ed[c] = 0.0f;\n", "\n"),
-    ("aligned_ref_drops_beta", "                rt[c] = a * r[c] + b0;", "                rt[c] = a * r[c];"),
+    ("aligned_ref_drops_beta", "                rt[c] = fmaf(a, r[c], b0);", "                rt[c] = a * r[c];"),
     ("decoder_drops_outliers", "eh[c] = orc_f16_to_f32((uint16_t)(w >> 16));", "(void)c;"),
     ("alpha_beta_swapped", "put16(coef + 4 * j, ah);", "put16(coef + 4 * j, bh);"),
     ("outlier_value_unrounded_recon", "? orc_f16_to_f32(oval[c]) :", "? e[c] :"),
