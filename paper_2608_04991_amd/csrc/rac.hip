@@ -43,16 +43,18 @@ constexpr float kMagic = 12582912.0f;  // 1.5 * 2^23: adding it rounds to an int
 constexpr float kNearHalf = 0.5f - 0x1p-14f;
 
 struct alignas(8) Args {
+    // hot-path fields
     const uint16_t* x;
     const uint16_t* ref;
     const float* steps;
-    uint8_t* wire;
+    uint32_t* coef;     // wire sections
+    uint16_t* scale;
+    uint8_t* codes;
+    uint32_t* outl;
     void* xhat;
-    uint64_t off_coef, off_scale, off_codes, off_outl, total;
-    uint64_t end_coef, end_scale, end_codes, end_outl;  // first byte after each section
-    uint64_t code_row_bytes;  // d * bits / 8
     int64_t tokens;
     int32_t d;
+    int32_t code_row_bytes;  // d * bits / 8
     int32_t nch;        // 512-channel chunks per row = wavefronts per workgroup
     int32_t lg_a, lg_q; // log2 of the group sizes
     int32_t lane_lv_a;  // butterfly levels inside a chunk: log2(min(g, 512) / 8)
@@ -62,8 +64,12 @@ struct alignas(8) Args {
     int32_t k;
     int32_t fixed;
     int32_t xhat_bf16;
-    int32_t write_header;
     float inv_ga;       // 1 / g_a (exact, power of two)
+    // header and padding (written once, by the first wavefront)
+    int32_t write_header;
+    uint8_t* wire;
+    uint64_t off_scale, off_codes, off_outl, total;
+    uint64_t end_coef, end_scale, end_codes, end_outl;  // first byte after each section
     uint32_t hdr[24];   // first 96 bytes of the header; the rest is zero
 };
 
@@ -96,19 +102,17 @@ __device__ __forceinline__ uint32_t bf16_rne(float v) {
 }
 
 // Smallest positive fp16 h with value(h) * q >= m  (m > 0); 0x7BFF if none.
-// value(h) * q is exact in binary32, so the test is an exact comparison.  The
-// start point RNE(m / q) is within one fp16 step of the answer.
-__device__ __forceinline__ uint32_t scale_roundup(float m, float q) {
-    if (m > 65504.0f * q) return 0x7BFFu;
-    uint32_t h = f16_rne_sat(m / q);
-    if (h == 0u) h = 1u;
-#pragma unroll
-    for (int i = 0; i < 3; ++i)
-        if (h < 0x7BFFu && f16_value(h) * q < m) ++h;
-#pragma unroll
-    for (int i = 0; i < 3; ++i)
-        if (h > 1u && f16_value(h - 1u) * q >= m) --h;
-    return h;
+// value(h) * q is exact in binary32, so the test below is an exact
+// comparison.  y = m * fl(1/q) is within 2^-23 (relative) of m/q, so its RNE
+// fp16 rounding h0 is either the answer or one step below it: if value(h0)
+// >= m/q, then y was at least the midpoint below h0 and value(h0-1) < m/q; if
+// value(h0) < m/q, then y was at most the midpoint above h0 and
+// value(h0+1) >= m/q.
+__device__ __forceinline__ uint32_t scale_roundup(float m, float q, float inv_q) {
+    uint32_t h = f16_rne_sat(m * inv_q);
+    h = h < 1u ? 1u : h;
+    h = f16_value(h) * q >= m ? h : h + 1u;
+    return m > 65504.0f * q ? 0x7BFFu : h;
 }
 
 // Smallest positive fp16 h with value(h) >= step; 0x7BFF above 65504.
@@ -129,22 +133,10 @@ __device__ __forceinline__ uint32_t step_roundup(float step) {
 // alpha* = C_rx / C_rr, beta* = m_x - alpha* m_r; a zero-variance reference
 // gives (0, m_x).  Returns the fp16 pair (alpha | beta << 16).
 __device__ __forceinline__ uint32_t fit_coef(float crr, float crx, float mr, float mx) {
-    float as, bs;
-    if (crr == 0.0f) {
-        as = 0.0f;
-        bs = mx;
-    } else {
-        as = crx / crr;
-        bs = mx - as * mr;
-    }
+    const bool flat = crr == 0.0f;
+    const float as = flat ? 0.0f : crx / crr;
+    const float bs = flat ? mx : mx - as * mr;
     return f16_rne_sat(as) | (f16_rne_sat(bs) << 16);
-}
-
-// E = x - R~ with R~ = alpha r + beta from the serialized pair (two roundings).
-__device__ __forceinline__ void residual8(uint32_t cf, const float* r, const float* x, float* e) {
-    const float a = f16_value(cf & 0xFFFFu), b0 = f16_value(cf >> 16);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) e[j] = x[j] - (a * r[j] + b0);
 }
 
 // ---------------------------------------------------------------------------
@@ -200,6 +192,52 @@ __device__ __forceinline__ float lane_max(float v, int levels) {
     if (levels > 4) v = pair16_max(v);
     if (levels > 5) v = pair32_max(v);
     return v;
+}
+
+// Same with a compile-time depth (LV >= 0); LV < 0 falls back to `levels`.
+template <int LV>
+__device__ __forceinline__ float lsum(float v, int levels) {
+    if constexpr (LV < 0) {
+        return lane_sum(v, levels);
+    } else {
+        if constexpr (LV > 0) v = v + dpp<0xB1>(v);
+        if constexpr (LV > 1) v = v + dpp<0x4E>(v);
+        if constexpr (LV > 2) v = v + dpp<0x141>(v);
+        if constexpr (LV > 3) v = v + dpp<0x140>(v);
+        if constexpr (LV > 4) v = pair16_sum(v);
+        if constexpr (LV > 5) v = pair32_sum(v);
+        return v;
+    }
+}
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+
+// Max over the lanes of an aligned block of non-negative, non-NaN values: on
+// such values the unsigned order of the bit patterns is the float order, and
+// an integer max folds into one DPP instruction per level.
+template <int LV>
+__device__ __forceinline__ float lmax(float f, int levels) {
+    if constexpr (LV < 0) {
+        return lane_max(f, levels);
+    } else {
+        uint32_t v = __float_as_uint(f);
+        if constexpr (LV > 0) v = __builtin_elementwise_max(v, dpp_u<0xB1>(v));
+        if constexpr (LV > 1) v = __builtin_elementwise_max(v, dpp_u<0x4E>(v));
+        if constexpr (LV > 2) v = __builtin_elementwise_max(v, dpp_u<0x141>(v));
+        if constexpr (LV > 3) v = __builtin_elementwise_max(v, dpp_u<0x140>(v));
+        if constexpr (LV > 4) {
+            auto p = __builtin_amdgcn_permlane16_swap((int)v, (int)v, false, false);
+            v = __builtin_elementwise_max((uint32_t)p[0], (uint32_t)p[1]);
+        }
+        if constexpr (LV > 5) {
+            auto p = __builtin_amdgcn_permlane32_swap((int)v, (int)v, false, false);
+            v = __builtin_elementwise_max((uint32_t)p[0], (uint32_t)p[1]);
+        }
+        return __uint_as_float(v);
+    }
 }
 
 __device__ __forceinline__ float tree8(const float* v) {
@@ -404,8 +442,6 @@ struct RowShared {
     uint64_t ckey[kCandCap];        // candidate key: |E| bits << 32 | (0xFFFF - channel)
     uint32_t cval[kCandCap];        // candidate E bits
     uint32_t cnt[4];                // [0] candidate count, [1..3] rotating block counters
-    uint32_t lthr;                  // threshold lower bound L (bits of |E|)
-    uint32_t kstar[3];              // threshold |E| bits, last tied channel taken, ties?
     float part[5][kMaxWaves];       // chunk partials of groups wider than one chunk
 };
 
@@ -484,19 +520,22 @@ __device__ __forceinline__ void append8(RowShared& S, uint32_t* counter, const f
 //     channel c* by bisection on the channel among the elements equal to T.
 // 4. An element is an outlier iff |E| > T, or |E| == T and channel <= c*.
 
-__device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S, const float* e,
-                                                    bool act, int c0, uint32_t lane, int w, int64_t row) {
+__device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S, RowShared& Snext,
+                                                    const float* e, bool act, int c0, uint32_t lane, int w,
+                                                    int64_t row) {
     const int k = A.k;
     // 1. strided group maxima: lane l of every wave -> one LDS max per lane
     float lm = 0.0f;
 #pragma unroll
     for (int j = 0; j < 8; ++j) lm = __builtin_fmaxf(lm, __builtin_fabsf(e[j]));
     if (act) atomicMax(&S.smax[lane], __float_as_uint(lm));  // bits order like non-negative floats
-    if (threadIdx.x == 0) {
-        S.cnt[0] = 0u;
-        S.cnt[1] = 0u;
-    }
     __syncthreads();
+    // The other buffer was last used by the previous row, which every wave
+    // has finished: clear it for the next row.
+    if (w == 0) {
+        Snext.smax[lane] = 0u;
+        if (lane < 4u) Snext.cnt[lane] = 0u;
+    }
     // k-th largest of the 64 group maxima, top 16 bits (every wave, same result)
     const uint32_t v = S.smax[lane];
     uint32_t L = 0u;
@@ -515,38 +554,35 @@ __device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S,
     }
     __syncthreads();
     const uint32_t C = S.cnt[0];
-    uint32_t* outl = reinterpret_cast<uint32_t*>(A.wire + A.off_outl) + (uint64_t)row * (uint64_t)k;
-
-    if (w == 0) S.smax[lane] = 0u;  // ready for the next row (read by every wave before this barrier)
+    uint32_t* outl = A.outl + (uint64_t)row * (uint64_t)k;
+    uint32_t T, cstar;
+    bool ties;
     if (C <= (uint32_t)kCandCap) {
-        // 3a. wave 0 ranks the candidates (one per lane)
+        // 3a. every wave ranks the candidates (one per lane) and finds K*
+        const bool have = lane < C;
+        const uint64_t key = have ? S.ckey[lane] : 0ull;
+        uint32_t rank = 0;
+        for (uint32_t j = 0; j < C; ++j) rank += (rdlane64(key, (int)j) > key) ? 1u : 0u;
+        const uint64_t at = ballot(have && rank == (uint32_t)(k - 1));
+        const uint64_t kst = rdlane64(key, at ? (int)__builtin_ctzll(at) : 0);
+        T = (uint32_t)(kst >> 32);
+        cstar = key_channel(kst);
+        ties = __builtin_popcountll(ballot(have && (uint32_t)(key >> 32) >= T)) > (unsigned)k;
         if (w == 0) {
-            const bool have = lane < C;
-            const uint64_t key = have ? S.ckey[lane] : 0ull;
-            const uint32_t val = have ? S.cval[lane] : 0u;
-            uint32_t rank = 0;
-            for (uint32_t j = 0; j < C; ++j) rank += (rdlane64(key, (int)j) > key) ? 1u : 0u;
-            const uint64_t at = ballot(have && rank == (uint32_t)(k - 1));
-            const uint64_t kst = rdlane64(key, at ? (int)__builtin_ctzll(at) : 0);
-            const uint32_t T = (uint32_t)(kst >> 32);
+            // wave 0 writes the row's outliers in ascending channel order
             const uint32_t ch = key_channel(key);
             uint32_t slot = 0;
             for (uint32_t j = 0; j < C; ++j) {
                 const uint64_t kj = rdlane64(key, (int)j);
                 slot += (kj >= kst && key_channel(kj) < ch) ? 1u : 0u;
             }
-            if (have && key >= kst && slot < (uint32_t)k) outl[slot] = ch | (f16_rne_sat(__uint_as_float(val)) << 16);
-            const bool ties = __builtin_popcountll(ballot(have && (uint32_t)(key >> 32) >= T)) > (unsigned)k;
-            if (lane == 0u) {
-                S.kstar[0] = T;
-                S.kstar[1] = key_channel(kst);
-                S.kstar[2] = ties ? 1u : 0u;
-            }
+            if (have && key >= kst && slot < (uint32_t)k)
+                outl[slot] = ch | (f16_rne_sat(__uint_as_float(S.cval[lane])) << 16);
         }
     } else {
         // 3b. radix select of T with workgroup-wide counts
         int it = 0;
-        uint32_t T = 0u;
+        T = 0u;
         for (int bit = 30; bit >= 0; --bit) {
             const uint32_t c = T | (1u << bit);
             if (block_sum(S, count8(e, act, __uint_as_float(c)), it) >= (uint32_t)k) T = c;
@@ -557,8 +593,8 @@ __device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S,
         for (int j = 0; j < 8; ++j) gtw += (uint32_t)__builtin_popcountll(ballot(act && __builtin_fabsf(e[j]) > Tf));
         const uint32_t gt = block_sum(S, gtw, it);
         const uint32_t ge = block_sum(S, count8(e, act, Tf), it);
-        const bool ties = ge != (uint32_t)k;
-        uint32_t cstar = 0xFFFFu;
+        ties = ge != (uint32_t)k;
+        cstar = 0xFFFFu;
         if (ties) {
             // smallest channel c* with count(|E| == T, channel <= c*) == k - gt
             const uint32_t need = (uint32_t)k - gt;
@@ -594,17 +630,9 @@ __device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S,
             uint32_t pos = 0;
             for (int j = 0; j < k; ++j) pos += (key_channel(S.ckey[j]) < ch) ? 1u : 0u;
             if (have && pos < (uint32_t)k) outl[pos] = ch | (f16_rne_sat(__uint_as_float(val)) << 16);
-            if (lane == 0u) {
-                S.kstar[0] = T;
-                S.kstar[1] = cstar;
-                S.kstar[2] = ties ? 1u : 0u;
-            }
         }
     }
-    __syncthreads();
     // 4. mark this lane's outliers
-    const uint32_t T = S.kstar[0], cstar = S.kstar[1];
-    const bool ties = S.kstar[2] != 0u;
     const float Tf = __uint_as_float(T);
     uint32_t selm = 0;
 #pragma unroll
@@ -622,28 +650,43 @@ __device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S,
 // into registers while the current one is processed), one wavefront per
 // 512-channel chunk.
 
-template <int BITS>
+// GA / GQ select the group shape at compile time: 0..6 = groups inside one
+// chunk with that many butterfly levels, 7 = groups spanning chunks, -1 =
+// read from the arguments at run time.
+template <int BITS, int GA, int GQ, bool OUTL>
 __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
-    __shared__ RowShared S;
+    // LDS state of a row, double-buffered by row parity: every row that uses
+    // LDS has a workgroup barrier, so no wave is more than one row ahead.
+    __shared__ RowShared SS[2];
     const uint32_t lane = threadIdx.x & (kWave - 1);
     const int w = (int)(threadIdx.x / kWave);
     const int d = A.d;
     const int c0 = w * kChunk + (int)lane * 8;
     const bool act = c0 < d;
-    const float q = (float)((1 << (BITS - 1)) - 1);
+    constexpr float q = (float)((1 << (BITS - 1)) - 1);
+    constexpr float inv_q = 1.0f / q;
     if (A.write_header && blockIdx.x == 0 && w == 0) write_header(A, lane);
     const bool dword3 = (d & 31) == 0;
+    const bool multi_a = GA == 7 || (GA < 0 && A.lg_cpg_a > 0);
+    const bool multi_q = GQ == 7 || (GQ < 0 && A.lg_cpg_q > 0);
+    const int lv_a = GA >= 0 ? (GA == 7 ? 6 : GA) : A.lane_lv_a;
+    const int lv_q = GQ >= 0 ? (GQ == 7 ? 6 : GQ) : A.lane_lv_q;
     const int grp_a = c0 >> A.lg_a, grp_q = c0 >> A.lg_q;
     const int cpg_a = 1 << A.lg_cpg_a, cpg_q = 1 << A.lg_cpg_q;
-    const bool first_a = A.lg_cpg_a == 0 ? (lane & ((1u << (A.lg_a - 3)) - 1u)) == 0u
-                                         : (lane == 0u && (w & (cpg_a - 1)) == 0);
-    const bool first_q = A.lg_cpg_q == 0 ? (lane & ((1u << (A.lg_q - 3)) - 1u)) == 0u
-                                         : (lane == 0u && (w & (cpg_q - 1)) == 0);
+    const bool first_a = !multi_a ? (lane & ((1u << lv_a) - 1u)) == 0u : (lane == 0u && (w & (cpg_a - 1)) == 0);
+    const bool first_q = !multi_q ? (lane & ((1u << lv_q) - 1u)) == 0u : (lane == 0u && (w & (cpg_q - 1)) == 0);
     const uint32_t sh_fixed = (A.fixed && act) ? step_roundup(A.steps[grp_q]) : 0u;
     const uint32_t ngq = (uint32_t)d >> A.lg_q, nga = (uint32_t)d >> A.lg_a;
 
-    if (A.k > 0) {
-        if (w == 0) S.smax[lane] = 0u;
+    if (OUTL) {
+        if (w == 0) {
+            SS[0].smax[lane] = 0u;
+            SS[1].smax[lane] = 0u;
+            if (lane < 4u) {
+                SS[0].cnt[lane] = 0u;
+                SS[1].cnt[lane] = 0u;
+            }
+        }
         __syncthreads();
     }
     int64_t row = blockIdx.x;
@@ -652,8 +695,8 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
         nx = *reinterpret_cast<const uint4*>(A.x + (uint64_t)row * (uint64_t)d + c0);
         if (A.ref) nr = *reinterpret_cast<const uint4*>(A.ref + (uint64_t)row * (uint64_t)d + c0);
     }
-    for (; row < A.tokens; row += gridDim.x) {
-        if (row != (int64_t)blockIdx.x) __syncthreads();  // LDS reuse across rows
+    for (int64_t n = 0; row < A.tokens; row += gridDim.x, ++n) {
+        RowShared& S = SS[n & 1];
         const uint64_t rbase = (uint64_t)row * (uint64_t)d;
         const uint4 xv = nx, rv = nr;
         const int64_t nrow = row + gridDim.x;
@@ -668,20 +711,21 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
         // a2: grouped affine fit, two-pass centred moments, pairwise sums
         float mr, mx, crr, crx;
         float uu[8], uv[8];
-        if (A.lg_cpg_a == 0) {
-            mr = lane_sum(tree8(r), A.lane_lv_a) * A.inv_ga;
-            mx = lane_sum(tree8(x), A.lane_lv_a) * A.inv_ga;
+        if (!multi_a) {
+            constexpr int L = GA == 7 ? 6 : GA;
+            mr = lsum<L>(tree8(r), lv_a) * A.inv_ga;
+            mx = lsum<L>(tree8(x), lv_a) * A.inv_ga;
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 const float u = r[j] - mr, v = x[j] - mx;
                 uu[j] = u * u;
                 uv[j] = u * v;
             }
-            crr = lane_sum(tree8(uu), A.lane_lv_a);
-            crx = lane_sum(tree8(uv), A.lane_lv_a);
+            crr = lsum<L>(tree8(uu), lv_a);
+            crx = lsum<L>(tree8(uv), lv_a);
         } else {
             const int g0 = w & ~(cpg_a - 1);
-            const float sr = lane_sum(tree8(r), 6), sx = lane_sum(tree8(x), 6);
+            const float sr = lsum<6>(tree8(r), 6), sx = lsum<6>(tree8(x), 6);
             if (lane == 0u) {
                 S.part[0][w] = sr;
                 S.part[1][w] = sx;
@@ -695,7 +739,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
                 uu[j] = u * u;
                 uv[j] = u * v;
             }
-            const float suu = lane_sum(tree8(uu), 6), suv = lane_sum(tree8(uv), 6);
+            const float suu = lsum<6>(tree8(uu), 6), suv = lsum<6>(tree8(uv), 6);
             if (lane == 0u) {
                 S.part[2][w] = suu;
                 S.part[3][w] = suv;
@@ -705,7 +749,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
             crx = tree_n(&S.part[3][g0], cpg_a);
         }
         const uint32_t cf = fit_coef(crr, crx, mr, mx);
-        if (first_a && act) reinterpret_cast<uint32_t*>(A.wire + A.off_coef)[(uint64_t)row * nga + grp_a] = cf;
+        if (first_a && act) A.coef[(uint64_t)row * nga + grp_a] = cf;
 
         // a3: aligned reference R~ = fma(alpha, r, beta) and residual E = x - R~
         const float a = f16_value(cf & 0xFFFFu), b0 = f16_value(cf >> 16);
@@ -718,7 +762,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
 
         // a4: outliers
         uint32_t selm = 0;
-        if (A.k > 0) selm = select_outliers(A, S, e, act, c0, lane, w, row);
+        if constexpr (OUTL) selm = select_outliers(A, S, SS[(n + 1) & 1], e, act, c0, lane, w, row);
         float ed[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) ed[j] = e[j];
@@ -736,43 +780,53 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
             float m = 0.0f;
 #pragma unroll
             for (int j = 0; j < 8; ++j) m = __builtin_fmaxf(m, __builtin_fabsf(ed[j]));
-            if (A.lg_cpg_q == 0) {
-                m = lane_max(m, A.lane_lv_q);
+            if (!multi_q) {
+                m = lmax<GQ == 7 ? 6 : GQ>(m, lv_q);
             } else {
-                m = lane_max(m, 6);
+                m = lmax<6>(m, 6);
                 if (lane == 0u) S.part[4][w] = m;
                 __syncthreads();
                 m = max_n(&S.part[4][w & ~(cpg_q - 1)], cpg_q);
             }
-            sh = m == 0.0f ? 0u : scale_roundup(m, q);
+            sh = m == 0.0f ? 0u : scale_roundup(m, q, inv_q);
             if (first_q && act)
-                reinterpret_cast<uint16_t*>(A.wire + A.off_scale)[(uint64_t)row * ngq + grp_q] = (uint16_t)sh;
+                A.scale[(uint64_t)row * ngq + grp_q] = (uint16_t)sh;
         }
         const float s = f16_value(sh);
         const float inv = sh ? __builtin_amdgcn_rcpf(s) : 0.0f;
 
         // a6-a8: quantize (round half to even), pack, reconstruct
+        float tc[8], mg[8], qf[8];
+        float dist = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            tc[j] = __builtin_amdgcn_fmed3f(ed[j] * inv, -q, q);
+            mg[j] = tc[j] + kMagic;
+            qf[j] = mg[j] - kMagic;
+            dist = __builtin_fmaxf(dist, __builtin_fabsf(tc[j] - qf[j]));
+        }
+        if (dist > kNearHalf) {  // some quotient is near a tie: use the exact one
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (__builtin_fabsf(tc[j] - qf[j]) > kNearHalf) {
+                    tc[j] = __builtin_amdgcn_fmed3f(ed[j] / s, -q, q);
+                    mg[j] = tc[j] + kMagic;
+                    qf[j] = mg[j] - kMagic;
+                }
+        }
         Packed<BITS> pk{};
         float H[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            float tc = __builtin_amdgcn_fmed3f(ed[j] * inv, -q, q);
-            float mg = tc + kMagic;
-            float qf = mg - kMagic;
-            if (__builtin_fabsf(tc - qf) > kNearHalf) {  // near a tie: exact quotient
-                tc = __builtin_amdgcn_fmed3f(ed[j] / s, -q, q);
-                mg = tc + kMagic;
-                qf = mg - kMagic;
-            }
-            pack_put<BITS>(pk, j, __float_as_uint(mg));
-            H[j] = __builtin_fmaf(qf, s, rt[j]);  // q*s is exact, so this is R~ + q*s
+            pack_put<BITS>(pk, j, __float_as_uint(mg[j]));
+            H[j] = __builtin_fmaf(qf[j], s, rt[j]);  // q*s is exact, so this is R~ + q*s
         }
         if (selm) {
 #pragma unroll
             for (int j = 0; j < 8; ++j)
                 if ((selm >> j) & 1u) H[j] = rt[j] + f16_value(f16_rne_sat(e[j]));
         }
-        store_codes<BITS>(A.wire + A.off_codes + (uint64_t)row * A.code_row_bytes, w, lane, act, dword3, pk);
+        store_codes<BITS>(A.codes + (uint64_t)row * (uint64_t)A.code_row_bytes, w, lane, act, dword3, pk);
         if (A.xhat && act) store_xhat(A, rbase + c0, H);
     }
 }
@@ -804,13 +858,11 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
         in.ent = 0xFFFFFFFFu;
         if (act) {
             if (A.ref) in.rv = *reinterpret_cast<const uint4*>(A.ref + (uint64_t)rw * (uint64_t)d + c0);
-            in.cf = reinterpret_cast<const uint32_t*>(A.wire + A.off_coef)[(uint64_t)rw * nga + grp_a];
-            in.sh = A.fixed ? sh_fixed
-                            : (uint32_t)reinterpret_cast<const uint16_t*>(A.wire + A.off_scale)[(uint64_t)rw * ngq + grp_q];
+            in.cf = A.coef[(uint64_t)rw * nga + grp_a];
+            in.sh = A.fixed ? sh_fixed : (uint32_t)A.scale[(uint64_t)rw * ngq + grp_q];
         }
-        load_codes<BITS>(A.wire + A.off_codes + (uint64_t)rw * A.code_row_bytes, w, lane, act, dword3, in.lo, in.hi);
-        if (lane < (uint32_t)k)
-            in.ent = reinterpret_cast<const uint32_t*>(A.wire + A.off_outl)[(uint64_t)rw * (uint64_t)k + lane];
+        load_codes<BITS>(A.codes + (uint64_t)rw * (uint64_t)A.code_row_bytes, w, lane, act, dword3, in.lo, in.hi);
+        if (lane < (uint32_t)k) in.ent = A.outl[(uint64_t)rw * (uint64_t)k + lane];
         return in;
     };
 
@@ -895,7 +947,6 @@ bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p
 
 Args make_args(const rac_config* c, const Sizes& S) {
     Args A{};
-    A.off_coef = S.L.off_coef;
     A.off_scale = S.L.off_scale;
     A.off_codes = S.L.off_codes;
     A.off_outl = S.L.off_outl;
@@ -904,7 +955,7 @@ Args make_args(const rac_config* c, const Sizes& S) {
     A.end_scale = S.L.off_scale + S.scale;
     A.end_codes = S.L.off_codes + S.codes;
     A.end_outl = S.L.off_outl + S.outl;
-    A.code_row_bytes = (uint64_t)c->hidden * (uint64_t)c->bits / 8u;
+    A.code_row_bytes = c->hidden * c->bits / 8;
     A.tokens = c->tokens;
     A.d = c->hidden;
     A.nch = (c->hidden + kChunk - 1) / kChunk;
@@ -919,6 +970,13 @@ Args make_args(const rac_config* c, const Sizes& S) {
     A.xhat_bf16 = (c->flags & RAC_FLAG_XHAT_BF16) ? 1 : 0;
     A.inv_ga = 1.0f / (float)c->group_align;
     return A;
+}
+
+void set_sections(Args& A, const Sizes& S) {
+    A.coef = reinterpret_cast<uint32_t*>(A.wire + S.L.off_coef);
+    A.scale = reinterpret_cast<uint16_t*>(A.wire + S.L.off_scale);
+    A.codes = A.wire + S.L.off_codes;
+    A.outl = reinterpret_cast<uint32_t*>(A.wire + S.L.off_outl);
 }
 
 void fill_header(Args& A, const rac_config* c, bool zero_ref) {
@@ -942,7 +1000,7 @@ void fill_header(Args& A, const rac_config* c, bool zero_ref) {
     h[26] = (c->flags & RAC_FLAG_FIXED_STEP) ? 0 : 1;
     h[27] = c->outlier_k > 0 ? 1 : 0;
     put16(28, (uint32_t)c->outlier_k);
-    put64(32, A.off_coef);
+    put64(32, (uint64_t)256);
     put64(40, A.off_scale);
     put64(48, A.off_codes);
     put64(56, A.off_outl);
@@ -954,13 +1012,31 @@ void fill_header(Args& A, const rac_config* c, bool zero_ref) {
 
 using KernelFn = void (*)(Args);
 
-KernelFn pick_encode(int bits) {
+template <int GA, int GQ, bool OUTL>
+KernelFn encode_for_bits(int bits) {
     switch (bits) {
-        case 2: return rac_encode_kernel<2>;
-        case 3: return rac_encode_kernel<3>;
-        case 4: return rac_encode_kernel<4>;
-        default: return rac_encode_kernel<8>;
+        case 2: return rac_encode_kernel<2, GA, GQ, OUTL>;
+        case 3: return rac_encode_kernel<3, GA, GQ, OUTL>;
+        case 4: return rac_encode_kernel<4, GA, GQ, OUTL>;
+        default: return rac_encode_kernel<8, GA, GQ, OUTL>;
     }
+}
+
+template <int GA, int GQ>
+KernelFn encode_for(int bits, bool outl) {
+    return outl ? encode_for_bits<GA, GQ, true>(bits) : encode_for_bits<GA, GQ, false>(bits);
+}
+
+// Specialized group shapes: 64/64, 128/128 and 128 with one scale per row
+// of up to 8192 channels; anything else takes the generic kernel.
+KernelFn pick_encode(const Args& A, int bits) {
+    const int ga = A.lg_cpg_a > 0 ? 7 : A.lane_lv_a;
+    const int gq = A.lg_cpg_q > 0 ? 7 : A.lane_lv_q;
+    const bool outl = A.k > 0;
+    if (ga == 3 && gq == 3) return encode_for<3, 3>(bits, outl);
+    if (ga == 4 && gq == 4) return encode_for<4, 4>(bits, outl);
+    if (ga == 4 && gq == 7) return encode_for<4, 7>(bits, outl);
+    return encode_for<-1, -1>(bits, outl);
 }
 
 KernelFn pick_decode(int bits) {
@@ -1014,6 +1090,7 @@ rac_status run_decode(const rac_config* cfg, const void* wire, const void* ref, 
     const Sizes S = sizes_of(cfg);
     Args A = make_args(cfg, S);
     A.wire = const_cast<uint8_t*>(static_cast<const uint8_t*>(wire));
+    set_sections(A, S);
     A.ref = static_cast<const uint16_t*>(ref);
     A.steps = steps;
     A.xhat = xhat;
@@ -1087,10 +1164,11 @@ rac_status rac_encode(const rac_config* cfg, const void* x, const void* ref, con
     A.ref = static_cast<const uint16_t*>(ref);
     A.steps = (cfg->flags & RAC_FLAG_FIXED_STEP) ? fixed_steps : nullptr;
     A.wire = static_cast<uint8_t*>(wire);
+    set_sections(A, S);
     A.xhat = xhat;
     A.write_header = 1;
     fill_header(A, cfg, ref == nullptr);
-    return launch(pick_encode(cfg->bits), A, stream);
+    return launch(pick_encode(A, cfg->bits), A, stream);
 }
 
 rac_status rac_reconstruct(const rac_config* cfg, const void* wire, const void* ref,
