@@ -30,7 +30,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "encode_prefill_uplink_4096x4096_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "rac_encode_prefill_uplink_4096x4096_traffic.json")
 
 
 def log(msg):
@@ -53,6 +53,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run plain device copies of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the codec shards by token rows with no "
@@ -63,9 +65,19 @@ def main():
     import torch
     import paper_2608_04991_amd as rac
     from paper_2608_04991_amd import workloads as wl
+    from paper_2608_04991_amd import rocprof_summary
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] copied {n} bytes 5 times")
+        return
     rac.library()
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda()
 
@@ -122,12 +134,13 @@ def main():
     dec_alg = algorithmic_bytes(T, d, wbytes, encode=False)
     enc_avg_s = float(enc_ms.mean()) * 1e-3
     achieved = enc_alg / enc_avg_s / 1e9
+    # HBM bytes per launch from the committed rocprofv3 counter runs, valid
+    # only for the kernel source they were taken on
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
-        try:
-            traffic = json.load(open(TRAFFIC_FILE)).get("bytes_per_launch")
-        except Exception:
-            traffic = None
+        t = json.load(open(TRAFFIC_FILE))
+        if t.get("kernel_source_sha256_16") == rocprof_summary.source_hash():
+            traffic = round(t["bytes_per_launch"])
     out = {
         "metric": "encode+reconstruct GB/s of bf16 activation & % HBM peak; decode-step µs/call",
         "value": round(value, 2),
@@ -146,7 +159,7 @@ def main():
                                "reconstruction, fp32) + rac_decode",
                    "tokens": T, "hidden": d, "group": g, "bits": b, "outlier_k": k,
                    "wire_bytes": wbytes, "rotating_buffer_sets": nsets},
-        "roofline": {"kernel": "rac_encode_kernel<4,8>", "bound": "hbm",
+        "roofline": {"kernel": "rac_encode_kernel<4,4,4,true>", "bound": "hbm",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "algorithmic_bytes_per_launch": enc_alg,
@@ -214,21 +227,27 @@ def decode_step_latency(torch, rac, wl, dev, stream):
 
 
 def cpu_baseline(xb, rb, cfg):
-    """The CPU oracle, single-threaded, on the same step (all 4096 rows:
-    encode with sender reconstruction, then decode)."""
+    """The CPU oracle, single-threaded, on the same step (all rows: encode
+    with sender reconstruction, then decode), repeated until at least 10 s of
+    CPU time have been spent (at most 30 s)."""
     import oracle
     c = dict(tokens=cfg.tokens, hidden=cfg.hidden, group_align=cfg.group_align,
              group_quant=cfg.group_quant, bits=cfg.bits, outlier_k=cfg.outlier_k, flags=cfg.flags)
-    log("[bench] CPU oracle baseline (one step, single thread)")
-    t0 = time.perf_counter()
-    rc, wire, _ = oracle.encode(xb, rb, **c)
-    rc2, _ = oracle.decode(wire, rb, **c)
-    dt = time.perf_counter() - t0
-    assert rc == 0 and rc2 == 0
-    return {"value": round(cfg.tokens * cfg.hidden * 2 / dt / 1e9, 5), "unit": "GB/s", "cores": 1,
+    log("[bench] CPU oracle baseline (full steps, single thread)")
+    reps, dt = 0, 0.0
+    while dt < 10.0 and reps < 30:
+        t0 = time.perf_counter()
+        rc, wire, _ = oracle.encode(xb, rb, **c)
+        rc2, _ = oracle.decode(wire, rb, **c)
+        dt += time.perf_counter() - t0
+        reps += 1
+        assert rc == 0 and rc2 == 0
+        log(f"[bench] oracle step {reps}: {dt:.1f} s so far")
+    return {"value": round(reps * cfg.tokens * cfg.hidden * 2 / dt / 1e9, 5), "unit": "GB/s", "cores": 1,
             "kind": "oracle",
-            "sample": f"one full step: {cfg.tokens}x{cfg.hidden} encode (with sender reconstruction) "
-                      f"+ decode, {dt:.2f} s on {os.cpu_count()} visible cores, 1 used"}
+            "sample": f"{reps} full steps of the benchmark workload ({cfg.tokens}x{cfg.hidden} encode with "
+                      f"sender reconstruction + decode), {dt:.1f} s, single thread on a host with "
+                      f"{os.cpu_count()} visible cores"}
 
 
 if __name__ == "__main__":

@@ -21,9 +21,10 @@
  *      E-hat = q*s on the dense base and the fp16 value at outliers.
  *
  * Arithmetic is IEEE binary32 with a fixed evaluation order (pairwise sums
- * over channel order, two-pass centred moments, no fused multiply-add), so the
- * sender's reconstruction, the receiver's decode and an independent CPU
- * implementation agree bit for bit.
+ * over channel order, two-pass centred moments, no contraction except the
+ * aligned reference alpha*r + beta, which is rounded once), so the sender's
+ * reconstruction, the receiver's decode and an independent CPU implementation
+ * agree bit for bit.
  *
  * Conventions shared by every entry point:
  *   - All tensor and wire pointers are DEVICE pointers on the current HIP
