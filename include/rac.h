@@ -94,7 +94,7 @@ enum {
 };
 
 typedef struct {
-    int64_t tokens;      /* T = B*N token rows, 0 <= T < 2^32                      */
+    int64_t tokens;      /* T = B*N token rows, 0 <= T < 2^31                      */
     int32_t hidden;      /* d: multiple of 8, 8 <= d <= 65535 (kernels: <= 8192)  */
     int32_t group_align; /* g_a: power of two, 8 <= g_a <= d, divides d           */
     int32_t group_quant; /* g_q: power of two, 8 <= g_q <= d, divides d           */

@@ -3,12 +3,20 @@
 Flags: -ffp-contract=off keeps every multiply and add separately rounded (the
 codec's arithmetic is defined operation by operation); packed fp32 ops are
 disabled; divisions stay correctly rounded (hipcc's default).
+
+The device assembly is also generated and scanned for a known miscompile
+(see isa_check.py); a hit fails the build.
 """
 from __future__ import annotations
 
 import os
 import subprocess
 import sys
+
+try:
+    from . import isa_check
+except ImportError:  # run as a script
+    import isa_check
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
@@ -29,6 +37,15 @@ def build(verbose: bool = True) -> str:
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
+    asm = LIB + ".s"
+    dev = [HIPCC, *[f for f in FLAGS if f not in ("-fPIC", "-shared")], "--cuda-device-only", "-S",
+           "-I", INC, "-o", asm, SRC]
+    subprocess.run(dev, check=True)
+    bad = isa_check.scan(open(asm).read())
+    os.remove(asm)
+    if bad:
+        os.remove(tmp)
+        raise RuntimeError("miscompiled SCC use in librac:\n" + "\n".join(bad))
     os.replace(tmp, LIB)
     return LIB
 

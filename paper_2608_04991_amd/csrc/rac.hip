@@ -35,7 +35,6 @@ constexpr int kWave = 64;
 constexpr int kChunk = 512;       // channels per wavefront (8 per lane)
 constexpr int kMaxWaves = 16;     // rows up to 8192 channels
 constexpr int kCandCap = 64;      // outlier candidates ranked by one wavefront
-constexpr int kMaxGroupMax = 256; // group maxima for the outlier threshold
 constexpr float kMagic = 12582912.0f;  // 1.5 * 2^23: adding it rounds to an integer (RNE)
 // Quotients t' = E * (1/s) within this distance of a half-integer are
 // recomputed with the correctly rounded division E / s.  |t' - E/s| is below
@@ -52,7 +51,7 @@ struct alignas(8) Args {
     uint8_t* codes;
     uint32_t* outl;
     void* xhat;
-    int64_t tokens;
+    uint32_t tokens;    // < 2^31, so row + gridDim.x never wraps
     int32_t d;
     int32_t code_row_bytes;  // d * bits / 8
     int32_t nch;        // 512-channel chunks per row = wavefronts per workgroup
@@ -72,6 +71,64 @@ struct alignas(8) Args {
     uint64_t end_coef, end_scale, end_codes, end_outl;  // first byte after each section
     uint32_t hdr[24];   // first 96 bytes of the header; the rest is zero
 };
+
+// ---------------------------------------------------------------------------
+// Raw buffer access.  Each row section (x, ref, coef, scale, codes, outliers,
+// xhat of one token row) is addressed through a buffer resource whose range is
+// exactly that section; the hardware drops a store at an offset outside the
+// range and returns 0 for such a load.  Lanes without work (the tail of a
+// partial chunk, lanes that do not own a group's coefficient) take an offset
+// outside the range instead of a branch, so every store of a row is issued
+// unconditionally and the wait for the next row's prefetched loads does not
+// have to wait for this row's stores as well.
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr uint32_t kOut = 0x80000000u;       // an offset outside every range
+constexpr int kRawBufferWord3 = 0x00020000;  // untyped buffer, 32-bit data format field
+// s_waitcnt operand: vector memory count 0, export and LDS/scalar counts left
+// at their maxima (no wait on them)
+constexpr int kWaitVmem0 = 0x0F70;
+
+// Resource for `bytes` bytes at element `i` of array `p`.  The address is
+// formed in integer arithmetic: p may be null when the range is empty.
+template <class T>
+__device__ __forceinline__ Rsrc rsrc(const T* p, uint64_t i, uint32_t bytes) {
+    const uint64_t a = (uint64_t)(uintptr_t)p + i * sizeof(T);
+    return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(a), (short)0, (int)bytes, kRawBufferWord3);
+}
+__device__ __forceinline__ uint4 bload128(Rsrc r, uint32_t off) {
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ uint2 bload64(Rsrc r, uint32_t off) {
+    const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0);
+    return make_uint2(v.x, v.y);
+}
+__device__ __forceinline__ uint32_t bload32(Rsrc r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0);
+}
+__device__ __forceinline__ uint32_t bload16(Rsrc r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0);
+}
+__device__ __forceinline__ uint32_t bload8(Rsrc r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b8(r, (int)off, 0, 0);
+}
+__device__ __forceinline__ void bstore128(Rsrc r, uint32_t off, uint4 v) {
+    __builtin_amdgcn_raw_buffer_store_b128((u32x4){v.x, v.y, v.z, v.w}, r, (int)off, 0, 0);
+}
+__device__ __forceinline__ void bstore64(Rsrc r, uint32_t off, uint32_t lo, uint32_t hi) {
+    __builtin_amdgcn_raw_buffer_store_b64((u32x2){lo, hi}, r, (int)off, 0, 0);
+}
+__device__ __forceinline__ void bstore32(Rsrc r, uint32_t off, uint32_t v) {
+    __builtin_amdgcn_raw_buffer_store_b32(v, r, (int)off, 0, 0);
+}
+__device__ __forceinline__ void bstore16(Rsrc r, uint32_t off, uint32_t v) {
+    __builtin_amdgcn_raw_buffer_store_b16((uint16_t)v, r, (int)off, 0, 0);
+}
+__device__ __forceinline__ void bstore8(Rsrc r, uint32_t off, uint32_t v) {
+    __builtin_amdgcn_raw_buffer_store_b8((uint8_t)v, r, (int)off, 0, 0);
+}
 
 // ---------------------------------------------------------------------------
 // Number formats
@@ -250,23 +307,21 @@ __device__ __forceinline__ uint32_t mbcnt64(uint64_t m) {
 
 __device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
 
+// A value known to be equal in all lanes, moved to a scalar register.
+__device__ __forceinline__ uint32_t uniform(uint32_t v) { return (uint32_t)__builtin_amdgcn_readfirstlane((int)v); }
+
 __device__ __forceinline__ uint32_t rdlane(uint32_t v, int l) {
     return (uint32_t)__builtin_amdgcn_readlane((int)v, l);
 }
 
+// Orders this wavefront's LDS writes before its later LDS reads by other
+// lanes (LDS executes one wavefront's instructions in order; this keeps the
+// compiler from reordering them).
 __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
 }
 
-// Wave-wide max of unsigned values (all lanes get it).
-__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
-    float f = __uint_as_float(v);  // order-preserving for non-NaN patterns < 0x7F800000
-    f = lane_max(f, 6);
-    return __float_as_uint(f);
-}
-
-// One bit per (chunk, channel-in-lane) slot of a lane: bit it*8 + j.
 // ---------------------------------------------------------------------------
 // Header and inter-section padding (written by wave 0 of block 0).
 
@@ -318,75 +373,74 @@ __device__ __forceinline__ void pack_put<8>(Packed<8>& p, int j, uint32_t c) {
     else p.hi |= (c & 255u) << (8 * (j - 4));
 }
 
-// Store the packed codes of chunk `it` for this lane.  Lane l's 8 channels
-// occupy bytes [l*BITS, l*BITS + BITS) of the chunk's 64*BITS bytes.
+// Store the packed codes of chunk `it` for this lane into the row's code
+// section `rc`.  Lane l's 8 channels occupy bytes [l*BITS, l*BITS + BITS) of
+// the chunk's 64*BITS bytes; lanes past the end of the row fall outside the
+// section's range.
 template <int BITS>
-__device__ __forceinline__ void store_codes(uint8_t* row_codes, int it, uint32_t lane, bool active,
-                                            bool dword_ok, const Packed<BITS>& p);
+__device__ __forceinline__ void store_codes(Rsrc rc, int it, uint32_t lane, bool dword_ok, const Packed<BITS>& p);
 
 template <>
-__device__ __forceinline__ void store_codes<2>(uint8_t* rc, int it, uint32_t lane, bool active, bool,
-                                               const Packed<2>& p) {
-    if (active) *reinterpret_cast<uint16_t*>(rc + it * 128 + lane * 2) = (uint16_t)p.w;
+__device__ __forceinline__ void store_codes<2>(Rsrc rc, int it, uint32_t lane, bool, const Packed<2>& p) {
+    bstore16(rc, (uint32_t)it * 128u + lane * 2u, p.w);
 }
 template <>
-__device__ __forceinline__ void store_codes<4>(uint8_t* rc, int it, uint32_t lane, bool active, bool,
-                                               const Packed<4>& p) {
-    if (active) *reinterpret_cast<uint32_t*>(rc + it * 256 + lane * 4) = p.w;
+__device__ __forceinline__ void store_codes<4>(Rsrc rc, int it, uint32_t lane, bool, const Packed<4>& p) {
+    bstore32(rc, (uint32_t)it * 256u + lane * 4u, p.w);
 }
 template <>
-__device__ __forceinline__ void store_codes<8>(uint8_t* rc, int it, uint32_t lane, bool active, bool,
-                                               const Packed<8>& p) {
-    if (active) *reinterpret_cast<uint2*>(rc + it * 512 + lane * 8) = make_uint2(p.lo, p.hi);
+__device__ __forceinline__ void store_codes<8>(Rsrc rc, int it, uint32_t lane, bool, const Packed<8>& p) {
+    bstore64(rc, (uint32_t)it * 512u + lane * 8u, p.lo, p.hi);
 }
 template <>
-__device__ __forceinline__ void store_codes<3>(uint8_t* rc, int it, uint32_t lane, bool active,
-                                               bool dword_ok, const Packed<3>& p) {
+__device__ __forceinline__ void store_codes<3>(Rsrc rc, int it, uint32_t lane, bool dword_ok, const Packed<3>& p) {
     // Four lanes own 96 contiguous bits = 3 dwords; lane j of the quad writes
-    // dword j from its own 24 bits and the next lane's.
-    const uint32_t nxt = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)p.w, 0x39 /* quad_perm [1,2,3,0] */,
-                                                               0xF, 0xF, false);
-    uint8_t* base = rc + it * 192;
+    // dword j from its own 24 bits and the next lane's.  Rows whose length is
+    // not a multiple of 32 channels are written bytewise.
+    const uint32_t base = (uint32_t)it * 192u;
     if (dword_ok) {
+        const uint32_t nxt = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)p.w, 0x39 /* quad_perm [1,2,3,0] */,
+                                                                   0xF, 0xF, false);
         const uint32_t j = lane & 3u;
         const uint32_t dw = j == 0 ? (p.w | (nxt << 24))
                           : j == 1 ? ((p.w >> 8) | (nxt << 16))
                                    : ((p.w >> 16) | (nxt << 8));
-        if (active && j < 3u) *reinterpret_cast<uint32_t*>(base + ((lane >> 2) * 3u + j) * 4u) = dw;
-    } else if (active) {
-        base[lane * 3 + 0] = (uint8_t)p.w;
-        base[lane * 3 + 1] = (uint8_t)(p.w >> 8);
-        base[lane * 3 + 2] = (uint8_t)(p.w >> 16);
+        bstore32(rc, j < 3u ? base + ((lane >> 2) * 3u + j) * 4u : kOut, dw);
+    } else {
+        bstore8(rc, base + lane * 3u + 0u, p.w);
+        bstore8(rc, base + lane * 3u + 1u, p.w >> 8);
+        bstore8(rc, base + lane * 3u + 2u, p.w >> 16);
     }
 }
 
-// Load this lane's packed codes of chunk `it` (inverse of store_codes).
+// Load this lane's packed codes of chunk `it` from the row's code section
+// (inverse of store_codes; lanes past the end of the row read zeros).
 template <int BITS>
-__device__ __forceinline__ void load_codes(const uint8_t* rc, int it, uint32_t lane, bool active,
-                                           bool dword_ok, uint32_t& lo, uint32_t& hi) {
+__device__ __forceinline__ void load_codes(Rsrc rc, int it, uint32_t lane, bool dword_ok, uint32_t& lo,
+                                           uint32_t& hi) {
     lo = hi = 0;
-    if (!active) return;
     if constexpr (BITS == 2) {
-        lo = *reinterpret_cast<const uint16_t*>(rc + it * 128 + lane * 2);
+        lo = bload16(rc, (uint32_t)it * 128u + lane * 2u);
     } else if constexpr (BITS == 4) {
-        lo = *reinterpret_cast<const uint32_t*>(rc + it * 256 + lane * 4);
+        lo = bload32(rc, (uint32_t)it * 256u + lane * 4u);
     } else if constexpr (BITS == 8) {
-        const uint2 v = *reinterpret_cast<const uint2*>(rc + it * 512 + lane * 8);
+        const uint2 v = bload64(rc, (uint32_t)it * 512u + lane * 8u);
         lo = v.x;
         hi = v.y;
     } else {
-        const uint8_t* base = rc + it * 192;
+        const uint32_t base = (uint32_t)it * 192u;
         if (dword_ok) {
-            const uint32_t j = lane & 3u;
-            const uint32_t* dws = reinterpret_cast<const uint32_t*>(base) + (lane >> 2) * 3u;
             // lane j's 24 bits start at bit 24j of the quad's 96 bits
-            const uint32_t w0 = dws[(24u * j) >> 5];
-            const uint32_t w1 = j == 3u ? 0u : dws[((24u * j) >> 5) + 1u];
+            const uint32_t j = lane & 3u;
+            const uint32_t q0 = base + (lane >> 2) * 12u;
+            const uint32_t i0 = (24u * j) >> 5;
+            const uint32_t w0 = bload32(rc, q0 + i0 * 4u);
+            const uint32_t w1 = bload32(rc, j == 3u ? kOut : q0 + (i0 + 1u) * 4u);
             const uint32_t sh = (24u * j) & 31u;
             lo = (sh ? ((w0 >> sh) | (w1 << (32u - sh))) : w0) & 0xFFFFFFu;
         } else {
-            lo = (uint32_t)base[lane * 3] | ((uint32_t)base[lane * 3 + 1] << 8) |
-                 ((uint32_t)base[lane * 3 + 2] << 16);
+            lo = bload8(rc, base + lane * 3u) | (bload8(rc, base + lane * 3u + 1u) << 8) |
+                 (bload8(rc, base + lane * 3u + 2u) << 16);
         }
     }
 }
@@ -421,23 +475,41 @@ __device__ __forceinline__ float max_n(const float* p, int n) {
     return m;
 }
 
-__device__ __forceinline__ void store_xhat(const Args& A, uint64_t off, const float* H) {
-    if (A.xhat_bf16) {
-        uint4 o;
-        o.x = bf16_rne(H[0]) | (bf16_rne(H[1]) << 16);
-        o.y = bf16_rne(H[2]) | (bf16_rne(H[3]) << 16);
-        o.z = bf16_rne(H[4]) | (bf16_rne(H[5]) << 16);
-        o.w = bf16_rne(H[6]) | (bf16_rne(H[7]) << 16);
-        *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(A.xhat) + off) = o;
+// Store this lane's 8 reconstructed channels at element offset c0 of the
+// row's xhat section (fp32, or bf16 when bf16 is set).  Both forms issue two
+// stores (the bf16 form's second one outside the range), so the number of
+// stores per row does not depend on the format.
+__device__ __forceinline__ void store_xhat(Rsrc rx, bool bf16, uint32_t c0, const float* H) {
+    uint4 v0, v1;
+    uint32_t o0, o1;
+    if (bf16) {
+        v0.x = bf16_rne(H[0]) | (bf16_rne(H[1]) << 16);
+        v0.y = bf16_rne(H[2]) | (bf16_rne(H[3]) << 16);
+        v0.z = bf16_rne(H[4]) | (bf16_rne(H[5]) << 16);
+        v0.w = bf16_rne(H[6]) | (bf16_rne(H[7]) << 16);
+        v1 = v0;
+        o0 = c0 * 2u;
+        o1 = kOut;
     } else {
-        float* o = reinterpret_cast<float*>(A.xhat) + off;
-        *reinterpret_cast<float4*>(o) = make_float4(H[0], H[1], H[2], H[3]);
-        *reinterpret_cast<float4*>(o + 4) = make_float4(H[4], H[5], H[6], H[7]);
+        v0 = make_uint4(__float_as_uint(H[0]), __float_as_uint(H[1]), __float_as_uint(H[2]), __float_as_uint(H[3]));
+        v1 = make_uint4(__float_as_uint(H[4]), __float_as_uint(H[5]), __float_as_uint(H[6]), __float_as_uint(H[7]));
+        o0 = c0 * 4u;
+        o1 = c0 * 4u + 16u;
     }
+    bstore128(rx, o0, v0);
+    bstore128(rx, o1, v1);
+}
+
+// Buffer resource of one row of the reconstruction (range 0 when no
+// reconstruction is wanted, which drops its stores).
+__device__ __forceinline__ Rsrc xhat_row(const Args& A, uint32_t row) {
+    const uint32_t es = A.xhat_bf16 ? 2u : 4u;
+    return rsrc(static_cast<const uint8_t*>(A.xhat), (uint64_t)row * (uint64_t)A.d * es,
+                A.xhat ? (uint32_t)A.d * es : 0u);
 }
 
 // Workgroup-shared state of one row.
-struct RowShared {
+struct alignas(16) RowShared {
     uint32_t smax[kWave];           // max |E| bits over lane l of every wave (threshold search)
     uint64_t ckey[kCandCap];        // candidate key: |E| bits << 32 | (0xFFFF - channel)
     uint32_t cval[kCandCap];        // candidate E bits
@@ -522,7 +594,7 @@ __device__ __forceinline__ void append8(RowShared& S, uint32_t* counter, const f
 
 __device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S, RowShared& Snext,
                                                     const float* e, bool act, int c0, uint32_t lane, int w,
-                                                    int64_t row) {
+                                                    uint32_t row) {
     const int k = A.k;
     // 1. strided group maxima: lane l of every wave -> one LDS max per lane
     float lm = 0.0f;
@@ -554,15 +626,21 @@ __device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S,
     }
     __syncthreads();
     const uint32_t C = S.cnt[0];
-    uint32_t* outl = A.outl + (uint64_t)row * (uint64_t)k;
+    const Rsrc outl = rsrc(A.outl, (uint64_t)row * (uint64_t)k, (uint32_t)k * 4u);
     uint32_t T, cstar;
     bool ties;
     if (C <= (uint32_t)kCandCap) {
         // 3a. every wave ranks the candidates (one per lane) and finds K*
+        // (rank = number of larger keys; keys are distinct as they hold the
+        // channel; LDS broadcast reads, two keys at a time)
         const bool have = lane < C;
         const uint64_t key = have ? S.ckey[lane] : 0ull;
         uint32_t rank = 0;
-        for (uint32_t j = 0; j < C; ++j) rank += (rdlane64(key, (int)j) > key) ? 1u : 0u;
+        for (uint32_t j = 0; j < C; j += 2) {
+            const ulonglong2 kk = *reinterpret_cast<const ulonglong2*>(&S.ckey[j]);
+            rank += (kk.x > key) ? 1u : 0u;
+            rank += (j + 1u < C && kk.y > key) ? 1u : 0u;
+        }
         const uint64_t at = ballot(have && rank == (uint32_t)(k - 1));
         const uint64_t kst = rdlane64(key, at ? (int)__builtin_ctzll(at) : 0);
         T = (uint32_t)(kst >> 32);
@@ -570,14 +648,17 @@ __device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S,
         ties = __builtin_popcountll(ballot(have && (uint32_t)(key >> 32) >= T)) > (unsigned)k;
         if (w == 0) {
             // wave 0 writes the row's outliers in ascending channel order
+            // (slot = number of chosen keys of a lower channel, i.e. of a
+            // larger low word)
             const uint32_t ch = key_channel(key);
             uint32_t slot = 0;
-            for (uint32_t j = 0; j < C; ++j) {
-                const uint64_t kj = rdlane64(key, (int)j);
-                slot += (kj >= kst && key_channel(kj) < ch) ? 1u : 0u;
+            for (uint32_t j = 0; j < C; j += 2) {
+                const ulonglong2 kk = *reinterpret_cast<const ulonglong2*>(&S.ckey[j]);
+                slot += (kk.x >= kst && (uint32_t)kk.x > (uint32_t)key) ? 1u : 0u;
+                slot += (j + 1u < C && kk.y >= kst && (uint32_t)kk.y > (uint32_t)key) ? 1u : 0u;
             }
-            if (have && key >= kst && slot < (uint32_t)k)
-                outl[slot] = ch | (f16_rne_sat(__uint_as_float(S.cval[lane])) << 16);
+            bstore32(outl, (have && key >= kst && slot < (uint32_t)k) ? slot * 4u : kOut,
+                     ch | (f16_rne_sat(__uint_as_float(S.cval[lane])) << 16));
         }
     } else {
         // 3b. radix select of T with workgroup-wide counts
@@ -629,7 +710,8 @@ __device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S,
             const uint32_t val = have ? S.cval[lane] : 0u;
             uint32_t pos = 0;
             for (int j = 0; j < k; ++j) pos += (key_channel(S.ckey[j]) < ch) ? 1u : 0u;
-            if (have && pos < (uint32_t)k) outl[pos] = ch | (f16_rne_sat(__uint_as_float(val)) << 16);
+            bstore32(outl, (have && pos < (uint32_t)k) ? pos * 4u : kOut,
+                     ch | (f16_rne_sat(__uint_as_float(val)) << 16));
         }
     }
     // 4. mark this lane's outliers
@@ -689,21 +771,26 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
         }
         __syncthreads();
     }
-    int64_t row = blockIdx.x;
-    uint4 nx = make_uint4(0, 0, 0, 0), nr = make_uint4(0, 0, 0, 0);
-    if (row < A.tokens && act) {
-        nx = *reinterpret_cast<const uint4*>(A.x + (uint64_t)row * (uint64_t)d + c0);
-        if (A.ref) nr = *reinterpret_cast<const uint4*>(A.ref + (uint64_t)row * (uint64_t)d + c0);
-    }
-    for (int64_t n = 0; row < A.tokens; row += gridDim.x, ++n) {
+    // x and ref of row `rw` for this lane (zeros past the last row, past the
+    // end of the row and for a zero reference)
+    const uint32_t row_bytes = (uint32_t)d * 2u;
+    auto load_row = [&](uint32_t rw, uint4& vx, uint4& vr) {
+        const bool in = rw < A.tokens;
+        const uint64_t o = (uint64_t)(in ? rw : 0) * (uint64_t)d;
+        vx = bload128(rsrc(A.x, o, in ? row_bytes : 0u), (uint32_t)c0 * 2u);
+        vr = bload128(rsrc(A.ref, o, (in && A.ref) ? row_bytes : 0u), (uint32_t)c0 * 2u);
+    };
+    uint32_t row = blockIdx.x;
+    uint4 nx, nr;
+    load_row(row, nx, nr);
+    // Let the first row land before the loop: then the loop head holds no
+    // wait, and inside the loop only the prefetched loads are waited for
+    // (never the stores of the row before).
+    __builtin_amdgcn_s_waitcnt(kWaitVmem0);
+    for (uint32_t n = 0; row < A.tokens; row += gridDim.x, ++n) {
         RowShared& S = SS[n & 1];
-        const uint64_t rbase = (uint64_t)row * (uint64_t)d;
         const uint4 xv = nx, rv = nr;
-        const int64_t nrow = row + gridDim.x;
-        if (nrow < A.tokens && act) {
-            nx = *reinterpret_cast<const uint4*>(A.x + (uint64_t)nrow * (uint64_t)d + c0);
-            if (A.ref) nr = *reinterpret_cast<const uint4*>(A.ref + (uint64_t)nrow * (uint64_t)d + c0);
-        }
+        load_row(row + gridDim.x, nx, nr);
         float r[8], x[8];
         widen8(rv, r);
         widen8(xv, x);
@@ -749,7 +836,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
             crx = tree_n(&S.part[3][g0], cpg_a);
         }
         const uint32_t cf = fit_coef(crr, crx, mr, mx);
-        if (first_a && act) A.coef[(uint64_t)row * nga + grp_a] = cf;
+        bstore32(rsrc(A.coef, (uint64_t)row * nga, nga * 4u), first_a ? (uint32_t)grp_a * 4u : kOut, cf);
 
         // a3: aligned reference R~ = fma(alpha, r, beta) and residual E = x - R~
         const float a = f16_value(cf & 0xFFFFu), b0 = f16_value(cf >> 16);
@@ -789,8 +876,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
                 m = max_n(&S.part[4][w & ~(cpg_q - 1)], cpg_q);
             }
             sh = m == 0.0f ? 0u : scale_roundup(m, q, inv_q);
-            if (first_q && act)
-                A.scale[(uint64_t)row * ngq + grp_q] = (uint16_t)sh;
+            bstore16(rsrc(A.scale, (uint64_t)row * ngq, ngq * 2u), first_q ? (uint32_t)grp_q * 2u : kOut, sh);
         }
         const float s = f16_value(sh);
         const float inv = sh ? __builtin_amdgcn_rcpf(s) : 0.0f;
@@ -826,8 +912,329 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
             for (int j = 0; j < 8; ++j)
                 if ((selm >> j) & 1u) H[j] = rt[j] + f16_value(f16_rne_sat(e[j]));
         }
-        store_codes<BITS>(A.codes + (uint64_t)row * (uint64_t)A.code_row_bytes, w, lane, act, dword3, pk);
-        if (A.xhat && act) store_xhat(A, rbase + c0, H);
+        const uint32_t crb = (uint32_t)A.code_row_bytes;
+        store_codes<BITS>(rsrc(A.codes, (uint64_t)row * crb, crb), w, lane, dword3, pk);
+        store_xhat(xhat_row(A, row), A.xhat_bf16 != 0, (uint32_t)c0, H);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Encode with per-token outliers, two wavefronts per token row.  For rows of
+// at most 4096 channels whose groups lie inside a chunk, a workgroup of two
+// wavefronts owns one token row at a time and wavefront w holds chunks
+// [4w, 4w + 4): lane l keeps E, ref (as loaded) and the coefficient pair of
+// channels [512c + 8l, 512c + 8l + 8) of its four chunks in registers.  The
+// per-token outlier choice then costs two barriers between two wavefronts and
+// its threshold search and ranking run twice per row, where the
+// one-wavefront-per-chunk kernel runs them once per chunk.
+
+constexpr int kPairChunks = 4;                      // chunks per wavefront
+constexpr int kPairMaxD = 2 * kPairChunks * kChunk;  // channels per row
+
+struct alignas(16) PairShared {
+    uint64_t ckey[2][kCandCap];  // candidates of each wavefront: |E| bits << 32 | (0xFFFF - channel)
+    uint32_t cval[2][kCandCap];  // their E bits
+    uint32_t smax[2][kWave];     // lane maxima of |E| of each wavefront
+    uint32_t cnt[2];             // candidate count of each wavefront
+    uint32_t xcnt[2][2];         // exact search: element counts, [slot][wavefront]
+};
+
+// Append this lane's elements of one chunk whose |E| pattern is >= lo (and,
+// with use_key, whose key is >= kmin) to a candidate list; entries beyond
+// kCandCap are counted but not stored.  n is the running count (uniform).
+__device__ __forceinline__ uint32_t append_chunk(uint64_t* ckey, uint32_t* cval, const float* e, bool act,
+                                                 uint32_t c0, uint32_t lo, bool use_key, uint64_t kmin, uint32_t n) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const uint32_t eb = __float_as_uint(e[j]);
+        const bool p = act && (eb & 0x7FFFFFFFu) >= lo && (!use_key || cand_key(eb, c0 + j) >= kmin);
+        const uint64_t m = ballot(p);
+        if (m) {
+            const uint32_t pos = n + mbcnt64(m);
+            if (p && pos < (uint32_t)kCandCap) {
+                ckey[pos] = cand_key(eb, c0 + j);
+                cval[pos] = eb;
+            }
+            n += (uint32_t)__builtin_popcountll(m);
+        }
+    }
+    return n;
+}
+
+// Hide the held ref values from the optimizer before they are widened again
+// (a reused widening would keep 32 more registers alive across the row).
+__device__ __forceinline__ void opaque4(uint4 (&r)[kPairChunks]) {
+#pragma unroll
+    for (int i = 0; i < kPairChunks; ++i) asm volatile("" : "+v"(r[i].x), "+v"(r[i].y), "+v"(r[i].z), "+v"(r[i].w));
+}
+
+template <int BITS, int GA, int GQ>
+__global__ __launch_bounds__(2 * kWave) __attribute__((amdgpu_waves_per_eu(4))) void rac_encode_pair_kernel(Args A) {
+    __shared__ PairShared PS[2];  // by row parity (two barriers per row)
+    const uint32_t lane = threadIdx.x & (kWave - 1);
+    const int w = (int)uniform(threadIdx.x / kWave);
+    const int d = A.d, k = A.k;
+    constexpr float q = (float)((1 << (BITS - 1)) - 1);
+    constexpr float inv_q = 1.0f / q;
+    if (A.write_header && blockIdx.x == 0 && w == 0) write_header(A, lane);
+    const bool dword3 = (d & 31) == 0;
+    const int lv_a = GA >= 0 ? GA : A.lane_lv_a;
+    const int lv_q = GQ >= 0 ? GQ : A.lane_lv_q;
+    const bool first_a = (lane & ((1u << lv_a) - 1u)) == 0u;
+    const bool first_q = (lane & ((1u << lv_q) - 1u)) == 0u;
+    const uint32_t ngq = (uint32_t)d >> A.lg_q, nga = (uint32_t)d >> A.lg_a;
+    const uint32_t row_bytes = (uint32_t)d * 2u;
+    const uint32_t crb = (uint32_t)A.code_row_bytes;
+    const int wc0 = w * kPairChunks * kChunk;  // first channel of this wavefront's chunks
+
+    uint32_t n = 0;
+    for (uint32_t row = blockIdx.x; row < A.tokens; row += gridDim.x, ++n) {
+        PairShared& S = PS[n & 1];
+        // lane * 8, opaque inside the loop: otherwise every per-channel
+        // constant of the lane's 32 channels is hoisted out of the row loop
+        uint32_t l8 = lane * 8u;
+        asm volatile("" : "+v"(l8));
+        const uint64_t o = (uint64_t)row * (uint64_t)d;
+        const Rsrc rx = rsrc(A.x, o, row_bytes), rr = rsrc(A.ref, o, A.ref ? row_bytes : 0u);
+        uint4 xl[kPairChunks], rp[kPairChunks];
+        uint32_t cf[kPairChunks];
+#pragma unroll
+        for (int i = 0; i < kPairChunks; ++i) {
+            const uint32_t off = ((uint32_t)(wc0 + i * kChunk) + l8) * 2u;  // past the row: reads 0
+            xl[i] = bload128(rx, off);
+            rp[i] = bload128(rr, off);
+            cf[i] = 0u;
+        }
+
+        // a2-a3 per chunk: fit of the lane's group, E; lane maximum of |E|
+        const Rsrc rcoef = rsrc(A.coef, (uint64_t)row * nga, nga * 4u);
+        float e[kPairChunks][8];
+        float lmx = 0.0f;
+#pragma unroll
+        for (int i = 0; i < kPairChunks; ++i) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) e[i][j] = 0.0f;
+            if (wc0 + i * kChunk >= d) continue;
+            const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
+            float r[8], x[8], uu[8], uv[8];
+            widen8(rp[i], r);
+            widen8(xl[i], x);
+            const float mr = lsum<GA>(tree8(r), lv_a) * A.inv_ga;
+            const float mx = lsum<GA>(tree8(x), lv_a) * A.inv_ga;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const float u = r[j] - mr, v = x[j] - mx;
+                uu[j] = u * u;
+                uv[j] = u * v;
+            }
+            const float crr = lsum<GA>(tree8(uu), lv_a), crx = lsum<GA>(tree8(uv), lv_a);
+            cf[i] = fit_coef(crr, crx, mr, mx);
+            bstore32(rcoef, first_a ? (c0 >> A.lg_a) * 4u : kOut, cf[i]);
+            const float a = f16_value(cf[i] & 0xFFFFu), b0 = f16_value(cf[i] >> 16);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {  // E = 0 past the row
+                e[i][j] = x[j] - __builtin_fmaf(a, r[j], b0);
+                lmx = __builtin_fmaxf(lmx, __builtin_fabsf(e[i][j]));
+            }
+        }
+
+        // a4: the k largest |E| of the row (ties to the lower channel).
+        // Threshold L: the k-th largest of the 64 maxima of |E| over lane l
+        // of both wavefronts, cut to its top 16 bits (which can only lower
+        // it); each of >= k such groups holds an element >= L, so every
+        // outlier has |E| >= L.
+        S.smax[w][lane] = __float_as_uint(lmx);
+        __syncthreads();
+        const uint32_t v = __builtin_elementwise_max(S.smax[0][lane], S.smax[1][lane]);
+        uint32_t L = 0u;
+#pragma unroll
+        for (int bit = 30; bit >= 15; --bit) {
+            const uint32_t cnd = L | (1u << bit);
+            if ((uint32_t)__builtin_popcountll(ballot(v >= cnd)) >= (uint32_t)k) L = cnd;
+        }
+        uint32_t Cw = 0;
+#pragma unroll
+        for (int i = 0; i < kPairChunks; ++i) {
+            if (wc0 + i * kChunk >= d) continue;
+            const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
+            Cw = append_chunk(S.ckey[w], S.cval[w], e[i], c0 < (uint32_t)d, c0, L, false, 0ull, Cw);
+        }
+        if (lane == 0u) S.cnt[w] = Cw;
+        __syncthreads();
+        // (values read from LDS are the same in every lane: readfirstlane
+        // makes that visible, so the branches on them stay scalar)
+        uint32_t C0 = uniform(S.cnt[0]), C1 = uniform(S.cnt[1]);
+        const bool exact = C0 + C1 > (uint32_t)kCandCap;
+        uint64_t kst = 0ull;  // key of the k-th largest element: the outliers are the keys >= kst
+        if (exact) {
+            // Heavy ties: T = the k-th largest |E| pattern by a radix search
+            // over its bits, then the last tied channel by bisection; every
+            // step counts over both wavefronts (one barrier, two rotating
+            // slots).  The lists are then rebuilt from the k outliers.
+            uint32_t T = 0u, lo = 0u, hi = (uint32_t)d - 1u, need = (uint32_t)k;
+            int slot = 0;
+#pragma unroll 1
+            for (int step = 0;; ++step) {
+                uint32_t plo = T, phi = 0x7FFFFFFFu, pmax = 0xFFFFu;
+                if (step < 31) {
+                    plo = T | (1u << (30 - step));
+                } else if (step == 31) {
+                    if (T == 0x7FFFFFFFu) continue;
+                    plo = T + 1u;
+                } else {
+                    if (lo >= hi) break;
+                    phi = T;
+                    pmax = (lo + hi) >> 1;
+                }
+                uint32_t cntl = 0;
+#pragma unroll
+                for (int i = 0; i < kPairChunks; ++i) {
+                    const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        const uint32_t a = __float_as_uint(e[i][j]) & 0x7FFFFFFFu;
+                        cntl += (c0 < (uint32_t)d && a >= plo && a <= phi && c0 + j <= pmax) ? 1u : 0u;
+                    }
+                }
+                const uint32_t cw = (uint32_t)lsum<6>((float)cntl, 6);  // integer counts <= 2048: exact
+                if (lane == 0u) S.xcnt[slot][w] = cw;
+                __syncthreads();
+                const uint32_t cnt = uniform(S.xcnt[slot][0] + S.xcnt[slot][1]);
+                slot ^= 1;
+                if (step < 31) {
+                    if (cnt >= (uint32_t)k) T = plo;
+                } else if (step == 31) {
+                    need = (uint32_t)k - cnt;
+                } else if (cnt >= need) {
+                    hi = pmax;
+                } else {
+                    lo = pmax + 1u;
+                }
+            }
+            kst = ((uint64_t)T << 32) | (uint64_t)(0xFFFFu - lo);
+            Cw = 0;
+#pragma unroll
+            for (int i = 0; i < kPairChunks; ++i) {
+                const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
+                Cw = append_chunk(S.ckey[w], S.cval[w], e[i], c0 < (uint32_t)d, c0, T, true, kst, Cw);
+            }
+            if (lane == 0u) S.cnt[w] = Cw;
+            __syncthreads();
+            C0 = uniform(S.cnt[0]);
+            C1 = uniform(S.cnt[1]);  // C0 + C1 == k
+        }
+        // candidate `lane` of the concatenated lists
+        const uint32_t C = C0 + C1;
+        const bool have = lane < C;
+        const bool in0 = lane < C0;
+        const uint64_t key = have ? (in0 ? S.ckey[0][lane] : S.ckey[1][lane - C0]) : 0ull;
+        const uint32_t val = have ? (in0 ? S.cval[0][lane] : S.cval[1][lane - C0]) : 0u;
+        if (!exact) {
+            // rank = number of larger keys (keys are distinct; LDS broadcast reads)
+            uint32_t rank = 0;
+#pragma unroll
+            for (int li = 0; li < 2; ++li) {
+                const uint32_t cl = li ? C1 : C0;
+                for (uint32_t j = 0; j < cl; j += 2) {
+                    const ulonglong2 kk = *reinterpret_cast<const ulonglong2*>(&S.ckey[li][j]);
+                    rank += (kk.x > key) ? 1u : 0u;
+                    rank += (j + 1u < cl && kk.y > key) ? 1u : 0u;
+                }
+            }
+            const uint64_t at = ballot(have && rank == (uint32_t)(k - 1));
+            kst = rdlane64(key, at ? (int)__builtin_ctzll(at) : 0);
+        }
+        const uint32_t Tb = (uint32_t)(kst >> 32), cstar = key_channel(kst);
+        const float Tf = __uint_as_float(Tb);
+        // The channel rule matters only if another element has pattern Tb:
+        // on the fast path every such element is a candidate; the exact path
+        // always applies it.
+        const bool ties = exact || __builtin_popcountll(ballot(have && (uint32_t)(key >> 32) == Tb)) > 1;
+        if (w == 0) {
+            // the row's outliers in ascending channel order (slot = number of
+            // chosen keys of a lower channel, i.e. of a larger low word)
+            uint32_t slot = 0;
+#pragma unroll
+            for (int li = 0; li < 2; ++li) {
+                const uint32_t cl = li ? C1 : C0;
+                for (uint32_t j = 0; j < cl; j += 2) {
+                    const ulonglong2 kk = *reinterpret_cast<const ulonglong2*>(&S.ckey[li][j]);
+                    slot += (kk.x >= kst && (uint32_t)kk.x > (uint32_t)key) ? 1u : 0u;
+                    slot += (j + 1u < cl && kk.y >= kst && (uint32_t)kk.y > (uint32_t)key) ? 1u : 0u;
+                }
+            }
+            const Rsrc outl = rsrc(A.outl, (uint64_t)row * (uint64_t)k, (uint32_t)k * 4u);
+            bstore32(outl, (have && key >= kst && slot < (uint32_t)k) ? slot * 4u : kOut,
+                     key_channel(key) | (f16_rne_sat(__uint_as_float(val)) << 16));
+        }
+
+        // a5-a8 per chunk: scale, quantize, pack, reconstruct
+        opaque4(rp);
+        const Rsrc rsc = rsrc(A.scale, (uint64_t)row * ngq, ngq * 2u);
+        const Rsrc rcd = rsrc(A.codes, (uint64_t)row * crb, crb);
+        const Rsrc rxh = xhat_row(A, row);
+#pragma unroll
+        for (int i = 0; i < kPairChunks; ++i) {
+            if (wc0 + i * kChunk >= d) continue;
+            const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
+            const bool act = c0 < (uint32_t)d;
+            float rt[8], ed[8];
+            {
+                float r[8];
+                widen8(rp[i], r);
+                const float a = f16_value(cf[i] & 0xFFFFu), b0 = f16_value(cf[i] >> 16);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) rt[j] = __builtin_fmaf(a, r[j], b0);
+            }
+            uint32_t selm = 0;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const float ae = __builtin_fabsf(e[i][j]);
+                const bool sel = act && (ties ? (ae > Tf || (ae == Tf && c0 + j <= cstar)) : ae >= Tf);
+                selm |= sel ? 1u << j : 0u;
+                ed[j] = sel ? 0.0f : e[i][j];
+            }
+            float m = 0.0f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) m = __builtin_fmaxf(m, __builtin_fabsf(ed[j]));
+            m = lmax<GQ>(m, lv_q);
+            const uint32_t sh = m == 0.0f ? 0u : scale_roundup(m, q, inv_q);
+            bstore16(rsc, first_q ? (c0 >> A.lg_q) * 2u : kOut, sh);
+            const float s = f16_value(sh);
+            const float inv = sh ? __builtin_amdgcn_rcpf(s) : 0.0f;
+            float tc[8], mg[8], qf[8];
+            float dist = 0.0f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                tc[j] = __builtin_amdgcn_fmed3f(ed[j] * inv, -q, q);
+                mg[j] = tc[j] + kMagic;
+                qf[j] = mg[j] - kMagic;
+                dist = __builtin_fmaxf(dist, __builtin_fabsf(tc[j] - qf[j]));
+            }
+            if (dist > kNearHalf) {  // some quotient is near a tie: use the exact one
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    if (__builtin_fabsf(tc[j] - qf[j]) > kNearHalf) {
+                        tc[j] = __builtin_amdgcn_fmed3f(ed[j] / s, -q, q);
+                        mg[j] = tc[j] + kMagic;
+                        qf[j] = mg[j] - kMagic;
+                    }
+            }
+            Packed<BITS> pk{};
+            float H[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                pack_put<BITS>(pk, j, __float_as_uint(mg[j]));
+                H[j] = __builtin_fmaf(qf[j], s, rt[j]);  // q*s is exact, so this is R~ + q*s
+            }
+            if (selm) {
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    if ((selm >> j) & 1u) H[j] = rt[j] + f16_value(f16_rne_sat(e[i][j]));
+            }
+            store_codes<BITS>(rcd, (wc0 >> 9) + i, lane, dword3, pk);
+            store_xhat(rxh, A.xhat_bf16 != 0, c0, H);
+        }
     }
 }
 
@@ -853,26 +1260,29 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
         uint4 rv;
         uint32_t lo, hi, cf, sh, ent;
     };
-    auto load = [&](int64_t rw) {
-        In in{};
-        in.ent = 0xFFFFFFFFu;
-        if (act) {
-            if (A.ref) in.rv = *reinterpret_cast<const uint4*>(A.ref + (uint64_t)rw * (uint64_t)d + c0);
-            in.cf = A.coef[(uint64_t)rw * nga + grp_a];
-            in.sh = A.fixed ? sh_fixed : (uint32_t)A.scale[(uint64_t)rw * ngq + grp_q];
-        }
-        load_codes<BITS>(A.codes + (uint64_t)rw * (uint64_t)A.code_row_bytes, w, lane, act, dword3, in.lo, in.hi);
-        if (lane < (uint32_t)k) in.ent = A.outl[(uint64_t)rw * (uint64_t)k + lane];
+    // (zeros past the last row and past the end of the row; entries of lanes
+    // >= k are never read)
+    const uint32_t crb = (uint32_t)A.code_row_bytes;
+    auto load = [&](uint32_t rw) {
+        const bool in_range = rw < A.tokens;
+        const uint64_t r = (uint64_t)(in_range ? rw : 0);
+        In in;
+        in.rv = bload128(rsrc(A.ref, r * (uint64_t)d, (in_range && A.ref) ? (uint32_t)d * 2u : 0u),
+                         (uint32_t)c0 * 2u);
+        in.cf = bload32(rsrc(A.coef, r * nga, in_range ? nga * 4u : 0u), (uint32_t)grp_a * 4u);
+        in.sh = bload16(rsrc(A.scale, r * ngq, (in_range && !A.fixed) ? ngq * 2u : 0u), (uint32_t)grp_q * 2u);
+        if (A.fixed) in.sh = sh_fixed;
+        load_codes<BITS>(rsrc(A.codes, r * crb, in_range ? crb : 0u), w, lane, dword3, in.lo, in.hi);
+        in.ent = bload32(rsrc(A.outl, r * (uint64_t)k, in_range ? (uint32_t)k * 4u : 0u), lane * 4u);
         return in;
     };
 
-    int64_t row = blockIdx.x;
-    In nxt{};
-    if (row < A.tokens) nxt = load(row);
+    uint32_t row = blockIdx.x;
+    In nxt = load(row);
+    __builtin_amdgcn_s_waitcnt(kWaitVmem0);  // as in the encode kernel
     for (; row < A.tokens; row += gridDim.x) {
         const In in = nxt;
-        const int64_t nrow = row + gridDim.x;
-        if (nrow < A.tokens) nxt = load(nrow);
+        nxt = load(row + gridDim.x);
         const float a = f16_value(in.cf & 0xFFFFu), b0 = f16_value(in.cf >> 16);
         const float s = f16_value(in.sh);
         float r[8], rt[8], H[8];
@@ -896,7 +1306,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
                 }
             }
         }
-        if (act) store_xhat(A, (uint64_t)row * (uint64_t)d + c0, H);
+        store_xhat(xhat_row(A, row), A.xhat_bf16 != 0, (uint32_t)c0, H);
     }
 }
 
@@ -909,7 +1319,7 @@ uint64_t up256(uint64_t v) { return (v + 255u) & ~uint64_t(255); }
 
 bool config_valid(const rac_config* c) {
     if (!c) return false;
-    if (c->tokens < 0 || c->tokens > 0xFFFFFFFFll) return false;
+    if (c->tokens < 0 || c->tokens > 0x7FFFFFFFll) return false;
     if (c->hidden < 8 || c->hidden > 65535 || c->hidden % 8 != 0) return false;
     if (!is_pow2(c->group_align) || c->group_align < 8 || c->group_align > c->hidden ||
         c->hidden % c->group_align != 0)
@@ -956,7 +1366,7 @@ Args make_args(const rac_config* c, const Sizes& S) {
     A.end_codes = S.L.off_codes + S.codes;
     A.end_outl = S.L.off_outl + S.outl;
     A.code_row_bytes = c->hidden * c->bits / 8;
-    A.tokens = c->tokens;
+    A.tokens = (uint32_t)c->tokens;
     A.d = c->hidden;
     A.nch = (c->hidden + kChunk - 1) / kChunk;
     A.lg_a = ilog2(c->group_align);
@@ -1039,6 +1449,29 @@ KernelFn pick_encode(const Args& A, int bits) {
     return encode_for<-1, -1>(bits, outl);
 }
 
+template <int GA, int GQ>
+KernelFn pair_for(int bits) {
+    switch (bits) {
+        case 2: return rac_encode_pair_kernel<2, GA, GQ>;
+        case 3: return rac_encode_pair_kernel<3, GA, GQ>;
+        case 4: return rac_encode_pair_kernel<4, GA, GQ>;
+        default: return rac_encode_pair_kernel<8, GA, GQ>;
+    }
+}
+
+// Rows with outliers take the two-wavefront kernel when it holds the whole
+// row and both group sizes fit in a chunk (calibrated step tables take the
+// one-wavefront-per-chunk kernel).
+bool use_pair_kernel(const Args& A) {
+    return A.k > 0 && !A.fixed && A.d <= kPairMaxD && A.lg_cpg_a == 0 && A.lg_cpg_q == 0;
+}
+
+KernelFn pick_pair(const Args& A, int bits) {
+    if (A.lane_lv_a == 3 && A.lane_lv_q == 3) return pair_for<3, 3>(bits);
+    if (A.lane_lv_a == 4 && A.lane_lv_q == 4) return pair_for<4, 4>(bits);
+    return pair_for<-1, -1>(bits);
+}
+
 KernelFn pick_decode(int bits) {
     switch (bits) {
         case 2: return rac_decode_kernel<2>;
@@ -1051,9 +1484,9 @@ KernelFn pick_decode(int bits) {
 // One workgroup per token row.  Large row counts use a grid of as many
 // workgroups as the device keeps resident, each taking rows in strides (and
 // prefetching its next row); small counts launch one workgroup per row.
-rac_status launch(KernelFn fn, Args A, hipStream_t stream) {
+rac_status launch(KernelFn fn, Args A, hipStream_t stream, int threads = 0) {
     const int64_t rows = A.tokens;
-    const int threads = A.nch * kWave;
+    if (threads == 0) threads = A.nch * kWave;
     int64_t blocks = rows <= 0 ? 1 : rows;
     if (rows > 256) {
         int dev = 0, cus = 0, per_cu = 0;
@@ -1168,6 +1601,7 @@ rac_status rac_encode(const rac_config* cfg, const void* x, const void* ref, con
     A.xhat = xhat;
     A.write_header = 1;
     fill_header(A, cfg, ref == nullptr);
+    if (use_pair_kernel(A)) return launch(pick_pair(A, cfg->bits), A, stream, 2 * kWave);
     return launch(pick_encode(A, cfg->bits), A, stream);
 }
 

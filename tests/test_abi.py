@@ -72,7 +72,7 @@ def test_payload_ratio_of_the_prefill_uplink_shape(lib):
 
 @pytest.mark.parametrize("bad", [dict(bits=5), dict(group_align=96), dict(group_quant=4),
                                  dict(hidden=100), dict(outlier_k=65), dict(tokens=-1),
-                                 dict(flags=16), dict(group_align=1024)])
+                                 dict(tokens=2**31), dict(flags=16), dict(group_align=1024)])
 def test_invalid_configs_are_rejected(lib, bad):
     c = dict(tokens=4, hidden=512, group_align=64, group_quant=64, bits=4)
     c.update(bad)
