@@ -1128,7 +1128,6 @@ __global__ __launch_bounds__(2 * kWave) __attribute__((amdgpu_waves_per_eu(4))) 
         const bool have = lane < C;
         const bool in0 = lane < C0;
         const uint64_t key = have ? (in0 ? S.ckey[0][lane] : S.ckey[1][lane - C0]) : 0ull;
-        const uint32_t val = have ? (in0 ? S.cval[0][lane] : S.cval[1][lane - C0]) : 0u;
         if (!exact) {
             // rank = number of larger keys (keys are distinct; LDS broadcast reads)
             uint32_t rank = 0;
@@ -1149,7 +1148,9 @@ __global__ __launch_bounds__(2 * kWave) __attribute__((amdgpu_waves_per_eu(4))) 
         // The channel rule matters only if another element has pattern Tb:
         // on the fast path every such element is a candidate; the exact path
         // always applies it.
-        const bool ties = exact || __builtin_popcountll(ballot(have && (uint32_t)(key >> 32) == Tb)) > 1;
+        uint32_t khi = (uint32_t)(key >> 32);
+        asm volatile("" : "+v"(khi));  // (a 32-bit compare; widened, it cost a spilled register)
+        const bool ties = exact || __builtin_popcountll(ballot(have && khi == Tb)) > 1;
         if (w == 0) {
             // the row's outliers in ascending channel order (slot = number of
             // chosen keys of a lower channel, i.e. of a larger low word)
@@ -1163,6 +1164,7 @@ __global__ __launch_bounds__(2 * kWave) __attribute__((amdgpu_waves_per_eu(4))) 
                     slot += (j + 1u < cl && kk.y >= kst && (uint32_t)kk.y > (uint32_t)key) ? 1u : 0u;
                 }
             }
+            const uint32_t val = have ? (in0 ? S.cval[0][lane] : S.cval[1][lane - C0]) : 0u;
             const Rsrc outl = rsrc(A.outl, (uint64_t)row * (uint64_t)k, (uint32_t)k * 4u);
             bstore32(outl, (have && key >= kst && slot < (uint32_t)k) ? slot * 4u : kOut,
                      key_channel(key) | (f16_rne_sat(__uint_as_float(val)) << 16));
@@ -1292,18 +1294,21 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
             rt[j] = __builtin_fmaf(a, r[j], b0);
             H[j] = __builtin_fmaf((float)code_at<BITS>(in.lo, in.hi, j), s, rt[j]);  // R~ + q*s, q*s exact
         }
-        for (int i = 0; i < k; ++i) {
-            // outliers of this chunk replace the dense value at their channel
-            const uint32_t en = rdlane(in.ent, i);
+        // Outliers of this chunk replace the dense value at their channel.
+        // Lane i holds entry i; only the entries inside this wavefront's
+        // chunk are visited (about k / chunks of them).
+        const uint32_t ech = in.ent & 0xFFFFu;
+        uint64_t mine = ballot(lane < (uint32_t)k && ech < (uint32_t)d && (ech >> 9) == (uint32_t)w);
+        while (mine) {
+            const uint32_t en = rdlane(in.ent, (int)__builtin_ctzll(mine));
+            mine &= mine - 1u;
             const uint32_t c = en & 0xFFFFu;
-            if (c < (uint32_t)d && (int)(c / kChunk) == w) {
-                const uint32_t owner = (c % kChunk) / 8u, jj = c % 8u;
-                const float v = f16_value(en >> 16);
-                if (lane == owner) {
+            const uint32_t owner = (c % kChunk) / 8u, jj = c % 8u;
+            const float v = f16_value(en >> 16);
+            if (lane == owner) {
 #pragma unroll
-                    for (int j = 0; j < 8; ++j)
-                        if ((uint32_t)j == jj) H[j] = rt[j] + v;
-                }
+                for (int j = 0; j < 8; ++j)
+                    if ((uint32_t)j == jj) H[j] = rt[j] + v;
             }
         }
         store_xhat(xhat_row(A, row), A.xhat_bf16 != 0, (uint32_t)c0, H);
