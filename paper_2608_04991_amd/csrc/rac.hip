@@ -500,6 +500,29 @@ __device__ __forceinline__ void store_xhat(Rsrc rx, bool bf16, uint32_t c0, cons
     bstore128(rx, o1, v1);
 }
 
+// Same, for the lane's channels 8l..8l+7 of the chunk starting at channel
+// `chunk0`, with fp32 output written through the wavefront's 2 KiB LDS
+// slice `st`: lane l then stores channels 4l..4l+3 and 256+4l..256+4l+3,
+// so that each store instruction writes 1 KiB of contiguous memory (two
+// interleaved 16-byte halves per lane cost HBM efficiency).  Channels past
+// the row fall outside the section's range.
+__device__ __forceinline__ void store_xhat_t(Rsrc rx, bool bf16, uint32_t chunk0, uint32_t lane, float4* st,
+                                             const float* H) {
+    if (bf16) {
+        store_xhat(rx, true, chunk0 + lane * 8u, H);
+        return;
+    }
+    st[2 * lane] = make_float4(H[0], H[1], H[2], H[3]);
+    st[2 * lane + 1] = make_float4(H[4], H[5], H[6], H[7]);
+    wave_lds_sync();
+    const float4 lo = st[lane], hi = st[kWave + lane];
+    wave_lds_sync();  // the slice is rewritten by the next chunk
+    bstore128(rx, (chunk0 + lane * 4u) * 4u,
+              make_uint4(__float_as_uint(lo.x), __float_as_uint(lo.y), __float_as_uint(lo.z), __float_as_uint(lo.w)));
+    bstore128(rx, (chunk0 + 256u + lane * 4u) * 4u,
+              make_uint4(__float_as_uint(hi.x), __float_as_uint(hi.y), __float_as_uint(hi.z), __float_as_uint(hi.w)));
+}
+
 // Buffer resource of one row of the reconstruction (range 0 when no
 // reconstruction is wanted, which drops its stores).
 __device__ __forceinline__ Rsrc xhat_row(const Args& A, uint32_t row) {
@@ -740,6 +763,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
     // LDS state of a row, double-buffered by row parity: every row that uses
     // LDS has a workgroup barrier, so no wave is more than one row ahead.
     __shared__ RowShared SS[2];
+    __shared__ float4 XT[kMaxWaves][2 * kWave];  // per-wavefront store staging (2 KiB)
     const uint32_t lane = threadIdx.x & (kWave - 1);
     const int w = (int)(threadIdx.x / kWave);
     const int d = A.d;
@@ -914,7 +938,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
         }
         const uint32_t crb = (uint32_t)A.code_row_bytes;
         store_codes<BITS>(rsrc(A.codes, (uint64_t)row * crb, crb), w, lane, dword3, pk);
-        store_xhat(xhat_row(A, row), A.xhat_bf16 != 0, (uint32_t)c0, H);
+        store_xhat_t(xhat_row(A, row), A.xhat_bf16 != 0, (uint32_t)(w * kChunk), lane, XT[w], H);
     }
 }
 
@@ -971,6 +995,7 @@ __device__ __forceinline__ void opaque4(uint4 (&r)[kPairChunks]) {
 template <int BITS, int GA, int GQ>
 __global__ __launch_bounds__(2 * kWave) __attribute__((amdgpu_waves_per_eu(4))) void rac_encode_pair_kernel(Args A) {
     __shared__ PairShared PS[2];  // by row parity (two barriers per row)
+    __shared__ float4 XT[2][2 * kWave];  // per-wavefront store staging (2 KiB)
     const uint32_t lane = threadIdx.x & (kWave - 1);
     const int w = (int)uniform(threadIdx.x / kWave);
     const int d = A.d, k = A.k;
@@ -1235,7 +1260,7 @@ __global__ __launch_bounds__(2 * kWave) __attribute__((amdgpu_waves_per_eu(4))) 
                     if ((selm >> j) & 1u) H[j] = rt[j] + f16_value(f16_rne_sat(e[i][j]));
             }
             store_codes<BITS>(rcd, (wc0 >> 9) + i, lane, dword3, pk);
-            store_xhat(rxh, A.xhat_bf16 != 0, c0, H);
+            store_xhat_t(rxh, A.xhat_bf16 != 0, (uint32_t)(wc0 + i * kChunk), l8 >> 3, XT[w], H);
         }
     }
 }
@@ -1246,6 +1271,7 @@ __global__ __launch_bounds__(2 * kWave) __attribute__((amdgpu_waves_per_eu(4))) 
 
 template <int BITS>
 __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
+    __shared__ float4 XT[kMaxWaves][2 * kWave];  // per-wavefront store staging (2 KiB)
     const uint32_t lane = threadIdx.x & (kWave - 1);
     const int w = (int)(threadIdx.x / kWave);
     const int d = A.d, k = A.k;
@@ -1311,7 +1337,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
                     if ((uint32_t)j == jj) H[j] = rt[j] + v;
             }
         }
-        store_xhat(xhat_row(A, row), A.xhat_bf16 != 0, (uint32_t)c0, H);
+        store_xhat_t(xhat_row(A, row), A.xhat_bf16 != 0, (uint32_t)(w * kChunk), lane, XT[w], H);
     }
 }
 
