@@ -554,7 +554,7 @@ __device__ __forceinline__ uint32_t block_sum(RowShared& S, uint32_t v, int& it)
 __device__ __forceinline__ uint32_t count8(const float* e, bool act, float t) {
     uint32_t n = 0;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) n += (uint32_t)__builtin_popcountll(ballot(act && __builtin_fabsf(e[j]) >= t));
+    for (int j = 0; j < 8; ++j) n += (uint32_t)__builtin_popcountll(ballot(act & (__builtin_fabsf(e[j]) >= t)));
     return n;
 }
 
@@ -644,7 +644,7 @@ __device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S,
     {
         bool p[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) p[j] = act && __builtin_fabsf(e[j]) >= Lf;
+        for (int j = 0; j < 8; ++j) p[j] = act & (__builtin_fabsf(e[j]) >= Lf);
         append8(S, &S.cnt[0], e, p, c0, lane);
     }
     __syncthreads();
@@ -694,7 +694,7 @@ __device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S,
         const float Tf = __uint_as_float(T);
         uint32_t gtw = 0;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) gtw += (uint32_t)__builtin_popcountll(ballot(act && __builtin_fabsf(e[j]) > Tf));
+        for (int j = 0; j < 8; ++j) gtw += (uint32_t)__builtin_popcountll(ballot(act & (__builtin_fabsf(e[j]) > Tf)));
         const uint32_t gt = block_sum(S, gtw, it);
         const uint32_t ge = block_sum(S, count8(e, act, Tf), it);
         ties = ge != (uint32_t)k;
@@ -709,13 +709,14 @@ __device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S,
 #pragma unroll
                 for (int j = 0; j < 8; ++j)
                     n += (uint32_t)__builtin_popcountll(
-                        ballot(act && __builtin_fabsf(e[j]) == Tf && (uint32_t)(c0 + j) <= mid));
+                        ballot(act & (__builtin_fabsf(e[j]) == Tf) & ((uint32_t)(c0 + j) <= mid)));
                 if (block_sum(S, n, it) >= need) hi = mid;
                 else lo = mid + 1u;
             }
             cstar = lo;
         }
         // gather the k outliers; wave 0 writes them by ascending channel
+        const uint32_t cmax = ties ? cstar : 0xFFFFu;
         const int slot = 1 + it % 3;
         if (threadIdx.x == 0) S.cnt[1 + (it + 1) % 3] = 0u;
         __syncthreads();
@@ -723,7 +724,7 @@ __device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S,
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const float a = __builtin_fabsf(e[j]);
-            p[j] = act && (ties ? (a > Tf || (a == Tf && (uint32_t)(c0 + j) <= cstar)) : a >= Tf);
+            p[j] = act & ((a > Tf) | ((a == Tf) & ((uint32_t)(c0 + j) <= cmax)));
         }
         append8(S, &S.cnt[slot], e, p, c0, lane);
         __syncthreads();
@@ -737,13 +738,16 @@ __device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S,
                      ch | (f16_rne_sat(__uint_as_float(val)) << 16));
         }
     }
-    // 4. mark this lane's outliers
+    // 4. mark this lane's outliers: |E| > T, or |E| == T and channel <= c*
+    // when the cut falls inside a tie (bitwise, not short-circuit, logic:
+    // the branches of && and || cost more than the comparisons)
     const float Tf = __uint_as_float(T);
+    const uint32_t cmax = ties ? cstar : 0xFFFFu;
     uint32_t selm = 0;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         const float a = __builtin_fabsf(e[j]);
-        const bool p = act && (ties ? (a > Tf || (a == Tf && (uint32_t)(c0 + j) <= cstar)) : a >= Tf);
+        const bool p = act & ((a > Tf) | ((a == Tf) & ((uint32_t)(c0 + j) <= cmax)));
         if (p) selm |= 1u << j;
     }
     return selm;
@@ -971,7 +975,7 @@ __device__ __forceinline__ uint32_t append_chunk(uint64_t* ckey, uint32_t* cval,
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         const uint32_t eb = __float_as_uint(e[j]);
-        const bool p = act && (eb & 0x7FFFFFFFu) >= lo && (!use_key || cand_key(eb, c0 + j) >= kmin);
+        const bool p = act & ((eb & 0x7FFFFFFFu) >= lo) & (!use_key | (cand_key(eb, c0 + j) >= kmin));
         const uint64_t m = ballot(p);
         if (m) {
             const uint32_t pos = n + mbcnt64(m);
@@ -1176,6 +1180,7 @@ __global__ __launch_bounds__(2 * kWave) __attribute__((amdgpu_waves_per_eu(4))) 
         uint32_t khi = (uint32_t)(key >> 32);
         asm volatile("" : "+v"(khi));  // (a 32-bit compare; widened, it cost a spilled register)
         const bool ties = exact || __builtin_popcountll(ballot(have && khi == Tb)) > 1;
+        const uint32_t cmax = ties ? cstar : 0xFFFFu;  // outliers: |E| > T, or |E| == T and channel <= cmax
         if (w == 0) {
             // the row's outliers in ascending channel order (slot = number of
             // chosen keys of a lower channel, i.e. of a larger low word)
@@ -1217,7 +1222,7 @@ __global__ __launch_bounds__(2 * kWave) __attribute__((amdgpu_waves_per_eu(4))) 
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 const float ae = __builtin_fabsf(e[i][j]);
-                const bool sel = act && (ties ? (ae > Tf || (ae == Tf && c0 + j <= cstar)) : ae >= Tf);
+                const bool sel = act & ((ae > Tf) | ((ae == Tf) & (c0 + j <= cmax)));
                 selm |= sel ? 1u << j : 0u;
                 ed[j] = sel ? 0.0f : e[i][j];
             }
@@ -1255,9 +1260,12 @@ __global__ __launch_bounds__(2 * kWave) __attribute__((amdgpu_waves_per_eu(4))) 
                 H[j] = __builtin_fmaf(qf[j], s, rt[j]);  // q*s is exact, so this is R~ + q*s
             }
             if (selm) {
+                // (computed for all 8, then selected: cheaper than 8 branches)
 #pragma unroll
-                for (int j = 0; j < 8; ++j)
-                    if ((selm >> j) & 1u) H[j] = rt[j] + f16_value(f16_rne_sat(e[i][j]));
+                for (int j = 0; j < 8; ++j) {
+                    const float ho = rt[j] + f16_value(f16_rne_sat(e[i][j]));
+                    H[j] = ((selm >> j) & 1u) ? ho : H[j];
+                }
             }
             store_codes<BITS>(rcd, (wc0 >> 9) + i, lane, dword3, pk);
             store_xhat_t(rxh, A.xhat_bf16 != 0, (uint32_t)(wc0 + i * kChunk), l8 >> 3, XT[w], H);
