@@ -947,59 +947,74 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
 }
 
 // ---------------------------------------------------------------------------
-// Encode with per-token outliers, two wavefronts per token row.  For rows of
-// at most 4096 channels whose groups lie inside a chunk, a workgroup of two
-// wavefronts owns one token row at a time and wavefront w holds chunks
-// [4w, 4w + 4): lane l keeps E, ref (as loaded) and the coefficient pair of
-// channels [512c + 8l, 512c + 8l + 8) of its four chunks in registers.  The
-// per-token outlier choice then costs two barriers between two wavefronts and
-// its threshold search and ranking run twice per row, where the
-// one-wavefront-per-chunk kernel runs them once per chunk.
+// Encode with per-token outliers, NW wavefronts per token row.  For rows of
+// at most 4096 channels whose groups lie inside a chunk, a workgroup of NW
+// wavefronts owns one token row at a time and wavefront w holds the CPW =
+// 8 / NW chunks [CPW w, CPW w + CPW): lane l keeps E, ref (as loaded) and the
+// coefficient pair of channels [512c + 8l, 512c + 8l + 8) of its chunks in
+// registers.  The per-token outlier choice costs two barriers between NW
+// wavefronts, and its threshold search and ranking run NW times per row
+// instead of once per chunk; fewer chunks per wavefront keep more wavefronts
+// resident.
 
-constexpr int kPairChunks = 4;                      // chunks per wavefront
-constexpr int kPairMaxD = 2 * kPairChunks * kChunk;  // channels per row
+constexpr int kRowsMaxD = 8 * kChunk;  // channels per row
+constexpr int kRowsWaves = 4;          // wavefronts per row (2 chunks each)
 
-struct alignas(16) PairShared {
-    uint64_t ckey[2][kCandCap];  // candidates of each wavefront: |E| bits << 32 | (0xFFFF - channel)
-    uint32_t cval[2][kCandCap];  // their E bits
-    uint32_t smax[2][kWave];     // lane maxima of |E| of each wavefront
-    uint32_t cnt[2];             // candidate count of each wavefront
-    uint32_t xcnt[2][2];         // exact search: element counts, [slot][wavefront]
+template <int NW>
+struct alignas(16) GroupShared {
+    uint64_t ckey[kCandCap];  // candidates: |E| bits << 32 | (0xFFFF - channel)
+    uint32_t cval[kCandCap];  // their E bits
+    uint32_t smax[NW][kWave]; // lane maxima of |E| of each wavefront
+    uint32_t cnt;             // candidate count (LDS atomic)
+    uint32_t xcnt[2][NW];     // exact search: element counts, [slot][wavefront]
 };
 
 // Append this lane's elements of one chunk whose |E| pattern is >= lo (and,
-// with use_key, whose key is >= kmin) to a candidate list; entries beyond
-// kCandCap are counted but not stored.  n is the running count (uniform).
-__device__ __forceinline__ uint32_t append_chunk(uint64_t* ckey, uint32_t* cval, const float* e, bool act,
-                                                 uint32_t c0, uint32_t lo, bool use_key, uint64_t kmin, uint32_t n) {
+// with use_key, whose key is >= kmin) to the shared candidate list; one LDS
+// atomic per wavefront reserves the slots, entries beyond kCandCap are
+// counted but not stored.
+__device__ __forceinline__ void append_shared(uint64_t* ckey, uint32_t* cval, uint32_t* counter, const float* e,
+                                              bool act, uint32_t c0, uint32_t lo, bool use_key, uint64_t kmin,
+                                              uint32_t lane) {
+    bool p[8];
+    uint32_t n = 0;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         const uint32_t eb = __float_as_uint(e[j]);
-        const bool p = act & ((eb & 0x7FFFFFFFu) >= lo) & (!use_key | (cand_key(eb, c0 + j) >= kmin));
-        const uint64_t m = ballot(p);
+        p[j] = act & ((eb & 0x7FFFFFFFu) >= lo) & (!use_key | (cand_key(eb, c0 + j) >= kmin));
+        n += (uint32_t)__builtin_popcountll(ballot(p[j]));
+    }
+    if (!n) return;
+    uint32_t base = 0u;
+    if (lane == 0u) base = atomicAdd(counter, n);
+    base = uniform(base);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const uint64_t m = ballot(p[j]);
         if (m) {
-            const uint32_t pos = n + mbcnt64(m);
-            if (p && pos < (uint32_t)kCandCap) {
-                ckey[pos] = cand_key(eb, c0 + j);
-                cval[pos] = eb;
+            const uint32_t pos = base + mbcnt64(m);
+            if (p[j] & (pos < (uint32_t)kCandCap)) {
+                ckey[pos] = cand_key(__float_as_uint(e[j]), c0 + j);
+                cval[pos] = __float_as_uint(e[j]);
             }
-            n += (uint32_t)__builtin_popcountll(m);
+            base += (uint32_t)__builtin_popcountll(m);
         }
     }
-    return n;
 }
 
-// Hide the held ref values from the optimizer before they are widened again
-// (a reused widening would keep 32 more registers alive across the row).
-__device__ __forceinline__ void opaque4(uint4 (&r)[kPairChunks]) {
+// Hide held ref values from the optimizer before they are widened again (a
+// reused widening would keep 8 more registers per chunk alive across the row).
+template <int N>
+__device__ __forceinline__ void opaque_n(uint4 (&r)[N]) {
 #pragma unroll
-    for (int i = 0; i < kPairChunks; ++i) asm volatile("" : "+v"(r[i].x), "+v"(r[i].y), "+v"(r[i].z), "+v"(r[i].w));
+    for (int i = 0; i < N; ++i) asm volatile("" : "+v"(r[i].x), "+v"(r[i].y), "+v"(r[i].z), "+v"(r[i].w));
 }
 
-template <int BITS, int GA, int GQ>
-__global__ __launch_bounds__(2 * kWave) __attribute__((amdgpu_waves_per_eu(4))) void rac_encode_pair_kernel(Args A) {
-    __shared__ PairShared PS[2];  // by row parity (two barriers per row)
-    __shared__ float4 XT[2][2 * kWave];  // per-wavefront store staging (2 KiB)
+template <int BITS, int GA, int GQ, int NW>
+__global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(6))) void rac_encode_rows_kernel(Args A) {
+    constexpr int CPW = 8 / NW;  // chunks per wavefront
+    __shared__ GroupShared<NW> PS[2];   // by row parity (two barriers per row)
+    __shared__ float4 XT[NW][2 * kWave];  // per-wavefront store staging (2 KiB)
     const uint32_t lane = threadIdx.x & (kWave - 1);
     const int w = (int)uniform(threadIdx.x / kWave);
     const int d = A.d, k = A.k;
@@ -1014,21 +1029,23 @@ __global__ __launch_bounds__(2 * kWave) __attribute__((amdgpu_waves_per_eu(4))) 
     const uint32_t ngq = (uint32_t)d >> A.lg_q, nga = (uint32_t)d >> A.lg_a;
     const uint32_t row_bytes = (uint32_t)d * 2u;
     const uint32_t crb = (uint32_t)A.code_row_bytes;
-    const int wc0 = w * kPairChunks * kChunk;  // first channel of this wavefront's chunks
+    const int wc0 = w * CPW * kChunk;  // first channel of this wavefront's chunks
+    if (w == 0 && lane < 2u) PS[lane].cnt = 0u;
+    __syncthreads();
 
     uint32_t n = 0;
     for (uint32_t row = blockIdx.x; row < A.tokens; row += gridDim.x, ++n) {
-        PairShared& S = PS[n & 1];
+        GroupShared<NW>& S = PS[n & 1];
         // lane * 8, opaque inside the loop: otherwise every per-channel
-        // constant of the lane's 32 channels is hoisted out of the row loop
+        // constant of the lane's channels is hoisted out of the row loop
         uint32_t l8 = lane * 8u;
         asm volatile("" : "+v"(l8));
         const uint64_t o = (uint64_t)row * (uint64_t)d;
         const Rsrc rx = rsrc(A.x, o, row_bytes), rr = rsrc(A.ref, o, A.ref ? row_bytes : 0u);
-        uint4 xl[kPairChunks], rp[kPairChunks];
-        uint32_t cf[kPairChunks];
+        uint4 xl[CPW], rp[CPW];
+        uint32_t cf[CPW];
 #pragma unroll
-        for (int i = 0; i < kPairChunks; ++i) {
+        for (int i = 0; i < CPW; ++i) {
             const uint32_t off = ((uint32_t)(wc0 + i * kChunk) + l8) * 2u;  // past the row: reads 0
             xl[i] = bload128(rx, off);
             rp[i] = bload128(rr, off);
@@ -1037,10 +1054,10 @@ __global__ __launch_bounds__(2 * kWave) __attribute__((amdgpu_waves_per_eu(4))) 
 
         // a2-a3 per chunk: fit of the lane's group, E; lane maximum of |E|
         const Rsrc rcoef = rsrc(A.coef, (uint64_t)row * nga, nga * 4u);
-        float e[kPairChunks][8];
+        float e[CPW][8];
         float lmx = 0.0f;
 #pragma unroll
-        for (int i = 0; i < kPairChunks; ++i) {
+        for (int i = 0; i < CPW; ++i) {
 #pragma unroll
             for (int j = 0; j < 8; ++j) e[i][j] = 0.0f;
             if (wc0 + i * kChunk >= d) continue;
@@ -1069,37 +1086,40 @@ __global__ __launch_bounds__(2 * kWave) __attribute__((amdgpu_waves_per_eu(4))) 
 
         // a4: the k largest |E| of the row (ties to the lower channel).
         // Threshold L: the k-th largest of the 64 maxima of |E| over lane l
-        // of both wavefronts, cut to its top 16 bits (which can only lower
+        // of all wavefronts, cut to its top 16 bits (which can only lower
         // it); each of >= k such groups holds an element >= L, so every
         // outlier has |E| >= L.
         S.smax[w][lane] = __float_as_uint(lmx);
         __syncthreads();
-        const uint32_t v = __builtin_elementwise_max(S.smax[0][lane], S.smax[1][lane]);
+        // the other buffer was last read by the previous row, which every
+        // wavefront has left: reset its candidate count for the next row
+        if (w == 0 && lane == 0u) PS[(n + 1) & 1].cnt = 0u;
+        uint32_t v = S.smax[0][lane];
+#pragma unroll
+        for (int ww = 1; ww < NW; ++ww) v = __builtin_elementwise_max(v, S.smax[ww][lane]);
         uint32_t L = 0u;
 #pragma unroll
         for (int bit = 30; bit >= 15; --bit) {
             const uint32_t cnd = L | (1u << bit);
             if ((uint32_t)__builtin_popcountll(ballot(v >= cnd)) >= (uint32_t)k) L = cnd;
         }
-        uint32_t Cw = 0;
 #pragma unroll
-        for (int i = 0; i < kPairChunks; ++i) {
+        for (int i = 0; i < CPW; ++i) {
             if (wc0 + i * kChunk >= d) continue;
             const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
-            Cw = append_chunk(S.ckey[w], S.cval[w], e[i], c0 < (uint32_t)d, c0, L, false, 0ull, Cw);
+            append_shared(S.ckey, S.cval, &S.cnt, e[i], c0 < (uint32_t)d, c0, L, false, 0ull, lane);
         }
-        if (lane == 0u) S.cnt[w] = Cw;
         __syncthreads();
         // (values read from LDS are the same in every lane: readfirstlane
         // makes that visible, so the branches on them stay scalar)
-        uint32_t C0 = uniform(S.cnt[0]), C1 = uniform(S.cnt[1]);
-        const bool exact = C0 + C1 > (uint32_t)kCandCap;
+        uint32_t C = uniform(S.cnt);
+        const bool exact = C > (uint32_t)kCandCap;
         uint64_t kst = 0ull;  // key of the k-th largest element: the outliers are the keys >= kst
         if (exact) {
             // Heavy ties: T = the k-th largest |E| pattern by a radix search
             // over its bits, then the last tied channel by bisection; every
-            // step counts over both wavefronts (one barrier, two rotating
-            // slots).  The lists are then rebuilt from the k outliers.
+            // step counts over all wavefronts (one barrier, two rotating
+            // slots).  The list is then rebuilt from the k outliers.
             uint32_t T = 0u, lo = 0u, hi = (uint32_t)d - 1u, need = (uint32_t)k;
             int slot = 0;
 #pragma unroll 1
@@ -1117,18 +1137,21 @@ __global__ __launch_bounds__(2 * kWave) __attribute__((amdgpu_waves_per_eu(4))) 
                 }
                 uint32_t cntl = 0;
 #pragma unroll
-                for (int i = 0; i < kPairChunks; ++i) {
+                for (int i = 0; i < CPW; ++i) {
                     const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
 #pragma unroll
                     for (int j = 0; j < 8; ++j) {
                         const uint32_t a = __float_as_uint(e[i][j]) & 0x7FFFFFFFu;
-                        cntl += (c0 < (uint32_t)d && a >= plo && a <= phi && c0 + j <= pmax) ? 1u : 0u;
+                        cntl += ((c0 < (uint32_t)d) & (a >= plo) & (a <= phi) & (c0 + j <= pmax)) ? 1u : 0u;
                     }
                 }
-                const uint32_t cw = (uint32_t)lsum<6>((float)cntl, 6);  // integer counts <= 2048: exact
+                const uint32_t cw = (uint32_t)lsum<6>((float)cntl, 6);  // integer counts <= 4096: exact
                 if (lane == 0u) S.xcnt[slot][w] = cw;
                 __syncthreads();
-                const uint32_t cnt = uniform(S.xcnt[slot][0] + S.xcnt[slot][1]);
+                uint32_t cnt = 0;
+#pragma unroll
+                for (int ww = 0; ww < NW; ++ww) cnt += S.xcnt[slot][ww];
+                cnt = uniform(cnt);
                 slot ^= 1;
                 if (step < 31) {
                     if (cnt >= (uint32_t)k) T = plo;
@@ -1141,33 +1164,25 @@ __global__ __launch_bounds__(2 * kWave) __attribute__((amdgpu_waves_per_eu(4))) 
                 }
             }
             kst = ((uint64_t)T << 32) | (uint64_t)(0xFFFFu - lo);
-            Cw = 0;
-#pragma unroll
-            for (int i = 0; i < kPairChunks; ++i) {
-                const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
-                Cw = append_chunk(S.ckey[w], S.cval[w], e[i], c0 < (uint32_t)d, c0, T, true, kst, Cw);
-            }
-            if (lane == 0u) S.cnt[w] = Cw;
+            if (w == 0 && lane == 0u) S.cnt = 0u;
             __syncthreads();
-            C0 = uniform(S.cnt[0]);
-            C1 = uniform(S.cnt[1]);  // C0 + C1 == k
+#pragma unroll
+            for (int i = 0; i < CPW; ++i) {
+                const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
+                append_shared(S.ckey, S.cval, &S.cnt, e[i], c0 < (uint32_t)d, c0, T, true, kst, lane);
+            }
+            __syncthreads();
+            C = uniform(S.cnt);  // == k
         }
-        // candidate `lane` of the concatenated lists
-        const uint32_t C = C0 + C1;
         const bool have = lane < C;
-        const bool in0 = lane < C0;
-        const uint64_t key = have ? (in0 ? S.ckey[0][lane] : S.ckey[1][lane - C0]) : 0ull;
+        const uint64_t key = have ? S.ckey[lane] : 0ull;
         if (!exact) {
             // rank = number of larger keys (keys are distinct; LDS broadcast reads)
             uint32_t rank = 0;
-#pragma unroll
-            for (int li = 0; li < 2; ++li) {
-                const uint32_t cl = li ? C1 : C0;
-                for (uint32_t j = 0; j < cl; j += 2) {
-                    const ulonglong2 kk = *reinterpret_cast<const ulonglong2*>(&S.ckey[li][j]);
-                    rank += (kk.x > key) ? 1u : 0u;
-                    rank += (j + 1u < cl && kk.y > key) ? 1u : 0u;
-                }
+            for (uint32_t j = 0; j < C; j += 2) {
+                const ulonglong2 kk = *reinterpret_cast<const ulonglong2*>(&S.ckey[j]);
+                rank += (kk.x > key) ? 1u : 0u;
+                rank += (j + 1u < C && kk.y > key) ? 1u : 0u;
             }
             const uint64_t at = ballot(have && rank == (uint32_t)(k - 1));
             kst = rdlane64(key, at ? (int)__builtin_ctzll(at) : 0);
@@ -1185,28 +1200,24 @@ __global__ __launch_bounds__(2 * kWave) __attribute__((amdgpu_waves_per_eu(4))) 
             // the row's outliers in ascending channel order (slot = number of
             // chosen keys of a lower channel, i.e. of a larger low word)
             uint32_t slot = 0;
-#pragma unroll
-            for (int li = 0; li < 2; ++li) {
-                const uint32_t cl = li ? C1 : C0;
-                for (uint32_t j = 0; j < cl; j += 2) {
-                    const ulonglong2 kk = *reinterpret_cast<const ulonglong2*>(&S.ckey[li][j]);
-                    slot += (kk.x >= kst && (uint32_t)kk.x > (uint32_t)key) ? 1u : 0u;
-                    slot += (j + 1u < cl && kk.y >= kst && (uint32_t)kk.y > (uint32_t)key) ? 1u : 0u;
-                }
+            for (uint32_t j = 0; j < C; j += 2) {
+                const ulonglong2 kk = *reinterpret_cast<const ulonglong2*>(&S.ckey[j]);
+                slot += (kk.x >= kst && (uint32_t)kk.x > (uint32_t)key) ? 1u : 0u;
+                slot += (j + 1u < C && kk.y >= kst && (uint32_t)kk.y > (uint32_t)key) ? 1u : 0u;
             }
-            const uint32_t val = have ? (in0 ? S.cval[0][lane] : S.cval[1][lane - C0]) : 0u;
+            const uint32_t val = have ? S.cval[lane] : 0u;
             const Rsrc outl = rsrc(A.outl, (uint64_t)row * (uint64_t)k, (uint32_t)k * 4u);
             bstore32(outl, (have && key >= kst && slot < (uint32_t)k) ? slot * 4u : kOut,
                      key_channel(key) | (f16_rne_sat(__uint_as_float(val)) << 16));
         }
 
         // a5-a8 per chunk: scale, quantize, pack, reconstruct
-        opaque4(rp);
+        opaque_n(rp);
         const Rsrc rsc = rsrc(A.scale, (uint64_t)row * ngq, ngq * 2u);
         const Rsrc rcd = rsrc(A.codes, (uint64_t)row * crb, crb);
         const Rsrc rxh = xhat_row(A, row);
 #pragma unroll
-        for (int i = 0; i < kPairChunks; ++i) {
+        for (int i = 0; i < CPW; ++i) {
             if (wc0 + i * kChunk >= d) continue;
             const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
             const bool act = c0 < (uint32_t)d;
@@ -1489,26 +1500,26 @@ KernelFn pick_encode(const Args& A, int bits) {
 }
 
 template <int GA, int GQ>
-KernelFn pair_for(int bits) {
+KernelFn rows_for(int bits) {
     switch (bits) {
-        case 2: return rac_encode_pair_kernel<2, GA, GQ>;
-        case 3: return rac_encode_pair_kernel<3, GA, GQ>;
-        case 4: return rac_encode_pair_kernel<4, GA, GQ>;
-        default: return rac_encode_pair_kernel<8, GA, GQ>;
+        case 2: return rac_encode_rows_kernel<2, GA, GQ, kRowsWaves>;
+        case 3: return rac_encode_rows_kernel<3, GA, GQ, kRowsWaves>;
+        case 4: return rac_encode_rows_kernel<4, GA, GQ, kRowsWaves>;
+        default: return rac_encode_rows_kernel<8, GA, GQ, kRowsWaves>;
     }
 }
 
-// Rows with outliers take the two-wavefront kernel when it holds the whole
+// Rows with outliers take the NW-wavefront kernel when it holds the whole
 // row and both group sizes fit in a chunk (calibrated step tables take the
 // one-wavefront-per-chunk kernel).
-bool use_pair_kernel(const Args& A) {
-    return A.k > 0 && !A.fixed && A.d <= kPairMaxD && A.lg_cpg_a == 0 && A.lg_cpg_q == 0;
+bool use_rows_kernel(const Args& A) {
+    return A.k > 0 && !A.fixed && A.d <= kRowsMaxD && A.lg_cpg_a == 0 && A.lg_cpg_q == 0;
 }
 
-KernelFn pick_pair(const Args& A, int bits) {
-    if (A.lane_lv_a == 3 && A.lane_lv_q == 3) return pair_for<3, 3>(bits);
-    if (A.lane_lv_a == 4 && A.lane_lv_q == 4) return pair_for<4, 4>(bits);
-    return pair_for<-1, -1>(bits);
+KernelFn pick_rows(const Args& A, int bits) {
+    if (A.lane_lv_a == 3 && A.lane_lv_q == 3) return rows_for<3, 3>(bits);
+    if (A.lane_lv_a == 4 && A.lane_lv_q == 4) return rows_for<4, 4>(bits);
+    return rows_for<-1, -1>(bits);
 }
 
 KernelFn pick_decode(int bits) {
@@ -1640,7 +1651,7 @@ rac_status rac_encode(const rac_config* cfg, const void* x, const void* ref, con
     A.xhat = xhat;
     A.write_header = 1;
     fill_header(A, cfg, ref == nullptr);
-    if (use_pair_kernel(A)) return launch(pick_pair(A, cfg->bits), A, stream, 2 * kWave);
+    if (use_rows_kernel(A)) return launch(pick_rows(A, cfg->bits), A, stream, kRowsWaves * kWave);
     return launch(pick_encode(A, cfg->bits), A, stream);
 }
 
