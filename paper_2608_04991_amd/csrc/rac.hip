@@ -373,6 +373,26 @@ __device__ __forceinline__ void pack_put<8>(Packed<8>& p, int j, uint32_t c) {
     else p.hi |= (c & 255u) << (8 * (j - 4));
 }
 
+// Codes of 8 channels from their rounding patterns t + 1.5 * 2^23, whose
+// low bits are the two's-complement code: each funnel shift moves the codes
+// gathered so far down by BITS and puts the next one on top.
+template <int BITS>
+__device__ __forceinline__ Packed<BITS> pack8(const float* mg) {
+    Packed<BITS> p{};
+    if constexpr (BITS == 8) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) p.lo = __builtin_amdgcn_alignbit(__float_as_uint(mg[j]), p.lo, 8u);
+#pragma unroll
+        for (int j = 4; j < 8; ++j) p.hi = __builtin_amdgcn_alignbit(__float_as_uint(mg[j]), p.hi, 8u);
+    } else {
+        uint32_t w = 0u;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) w = __builtin_amdgcn_alignbit(__float_as_uint(mg[j]), w, (uint32_t)BITS);
+        p.w = w >> (32 - 8 * BITS);
+    }
+    return p;
+}
+
 // Store the packed codes of chunk `it` for this lane into the row's code
 // section `rc`.  Lane l's 8 channels occupy bytes [l*BITS, l*BITS + BITS) of
 // the chunk's 64*BITS bytes; lanes past the end of the row fall outside the
@@ -515,6 +535,25 @@ __device__ __forceinline__ void store_xhat_t(Rsrc rx, bool bf16, uint32_t chunk0
     st[2 * lane] = make_float4(H[0], H[1], H[2], H[3]);
     st[2 * lane + 1] = make_float4(H[4], H[5], H[6], H[7]);
     wave_lds_sync();
+    const float4 lo = st[lane], hi = st[kWave + lane];
+    wave_lds_sync();  // the slice is rewritten by the next chunk
+    bstore128(rx, (chunk0 + lane * 4u) * 4u,
+              make_uint4(__float_as_uint(lo.x), __float_as_uint(lo.y), __float_as_uint(lo.z), __float_as_uint(lo.w)));
+    bstore128(rx, (chunk0 + 256u + lane * 4u) * 4u,
+              make_uint4(__float_as_uint(hi.x), __float_as_uint(hi.y), __float_as_uint(hi.z), __float_as_uint(hi.w)));
+}
+
+// Store a chunk's reconstruction staged in the wavefront's LDS slice `st`
+// (channel c of the chunk at float c): fp32 as in store_xhat_t, bf16 with
+// lane l storing channels 8l..8l+7.
+__device__ __forceinline__ void emit_xhat(Rsrc rx, bool bf16, uint32_t chunk0, uint32_t lane, float4* st) {
+    if (bf16) {
+        const float4 a = st[2 * lane], b = st[2 * lane + 1];
+        wave_lds_sync();
+        const float H[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+        store_xhat(rx, true, chunk0 + lane * 8u, H);
+        return;
+    }
     const float4 lo = st[lane], hi = st[kWave + lane];
     wave_lds_sync();  // the slice is rewritten by the next chunk
     bstore128(rx, (chunk0 + lane * 4u) * 4u,
@@ -964,18 +1003,20 @@ template <int NW>
 struct alignas(16) GroupShared {
     uint64_t ckey[kCandCap];  // candidates: |E| bits << 32 | (0xFFFF - channel)
     uint32_t cval[kCandCap];  // their E bits
+    uint32_t crt[kCandCap];   // their R~ bits
     uint32_t smax[NW][kWave]; // lane maxima of |E| of each wavefront
     uint32_t cnt;             // candidate count (LDS atomic)
     uint32_t xcnt[2][NW];     // exact search: element counts, [slot][wavefront]
 };
 
 // Append this lane's elements of one chunk whose |E| pattern is >= lo (and,
-// with use_key, whose key is >= kmin) to the shared candidate list; one LDS
-// atomic per wavefront reserves the slots, entries beyond kCandCap are
+// with use_key, whose key is >= kmin) to the shared candidate list, with
+// their R~ (from the loaded ref pair rpk and the coefficient pair cfv); one
+// LDS atomic per wavefront reserves the slots, entries beyond kCandCap are
 // counted but not stored.
-__device__ __forceinline__ void append_shared(uint64_t* ckey, uint32_t* cval, uint32_t* counter, const float* e,
-                                              bool act, uint32_t c0, uint32_t lo, bool use_key, uint64_t kmin,
-                                              uint32_t lane) {
+__device__ __forceinline__ void append_shared(uint64_t* ckey, uint32_t* cval, uint32_t* crt, uint32_t* counter,
+                                              const float* e, const uint4& rpk, uint32_t cfv, bool act, uint32_t c0,
+                                              uint32_t lo, bool use_key, uint64_t kmin, uint32_t lane) {
     bool p[8];
     uint32_t n = 0;
 #pragma unroll
@@ -988,14 +1029,17 @@ __device__ __forceinline__ void append_shared(uint64_t* ckey, uint32_t* cval, ui
     uint32_t base = 0u;
     if (lane == 0u) base = atomicAdd(counter, n);
     base = uniform(base);
+    const uint32_t rw[4] = {rpk.x, rpk.y, rpk.z, rpk.w};
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         const uint64_t m = ballot(p[j]);
         if (m) {
             const uint32_t pos = base + mbcnt64(m);
             if (p[j] & (pos < (uint32_t)kCandCap)) {
+                const float r = (j & 1) ? bf16_hi(rw[j >> 1]) : bf16_lo(rw[j >> 1]);
                 ckey[pos] = cand_key(__float_as_uint(e[j]), c0 + j);
                 cval[pos] = __float_as_uint(e[j]);
+                crt[pos] = __float_as_uint(__builtin_fmaf(f16_value(cfv & 0xFFFFu), r, f16_value(cfv >> 16)));
             }
             base += (uint32_t)__builtin_popcountll(m);
         }
@@ -1103,11 +1147,13 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(6)))
             const uint32_t cnd = L | (1u << bit);
             if ((uint32_t)__builtin_popcountll(ballot(v >= cnd)) >= (uint32_t)k) L = cnd;
         }
+        opaque_n(rp);
 #pragma unroll
         for (int i = 0; i < CPW; ++i) {
             if (wc0 + i * kChunk >= d) continue;
             const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
-            append_shared(S.ckey, S.cval, &S.cnt, e[i], c0 < (uint32_t)d, c0, L, false, 0ull, lane);
+            append_shared(S.ckey, S.cval, S.crt, &S.cnt, e[i], rp[i], cf[i], c0 < (uint32_t)d, c0, L, false, 0ull,
+                          lane);
         }
         __syncthreads();
         // (values read from LDS are the same in every lane: readfirstlane
@@ -1169,7 +1215,8 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(6)))
 #pragma unroll
             for (int i = 0; i < CPW; ++i) {
                 const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
-                append_shared(S.ckey, S.cval, &S.cnt, e[i], c0 < (uint32_t)d, c0, T, true, kst, lane);
+                append_shared(S.ckey, S.cval, S.crt, &S.cnt, e[i], rp[i], cf[i], c0 < (uint32_t)d, c0, T, true, kst,
+                              lane);
             }
             __syncthreads();
             C = uniform(S.cnt);  // == k
@@ -1196,6 +1243,17 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(6)))
         asm volatile("" : "+v"(khi));  // (a 32-bit compare; widened, it cost a spilled register)
         const bool ties = exact || __builtin_popcountll(ballot(have && khi == Tb)) > 1;
         const uint32_t cmax = ties ? cstar : 0xFFFFu;  // outliers: |E| > T, or |E| == T and channel <= cmax
+        // Candidate lane i holds one chosen outlier (or none): its channel
+        // and its reconstruction R~ + fp16(E), which phase C writes over
+        // the staged value of that channel.
+        const bool chosen = have && key >= kst;
+        const uint32_t och = chosen ? key_channel(key) : 0xFFFFFFFFu;
+        uint32_t oval = 0u;
+        float ohat = 0.0f;
+        if (chosen) {
+            oval = f16_rne_sat(__uint_as_float(S.cval[lane]));
+            ohat = __uint_as_float(S.crt[lane]) + f16_value(oval);
+        }
         if (w == 0) {
             // the row's outliers in ascending channel order (slot = number of
             // chosen keys of a lower channel, i.e. of a larger low word)
@@ -1205,10 +1263,8 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(6)))
                 slot += (kk.x >= kst && (uint32_t)kk.x > (uint32_t)key) ? 1u : 0u;
                 slot += (j + 1u < C && kk.y >= kst && (uint32_t)kk.y > (uint32_t)key) ? 1u : 0u;
             }
-            const uint32_t val = have ? S.cval[lane] : 0u;
             const Rsrc outl = rsrc(A.outl, (uint64_t)row * (uint64_t)k, (uint32_t)k * 4u);
-            bstore32(outl, (have && key >= kst && slot < (uint32_t)k) ? slot * 4u : kOut,
-                     key_channel(key) | (f16_rne_sat(__uint_as_float(val)) << 16));
+            bstore32(outl, (chosen && slot < (uint32_t)k) ? slot * 4u : kOut, key_channel(key) | (oval << 16));
         }
 
         // a5-a8 per chunk: scale, quantize, pack, reconstruct
@@ -1219,8 +1275,8 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(6)))
 #pragma unroll
         for (int i = 0; i < CPW; ++i) {
             if (wc0 + i * kChunk >= d) continue;
-            const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
-            const bool act = c0 < (uint32_t)d;
+            const uint32_t chunk0 = (uint32_t)(wc0 + i * kChunk);
+            const uint32_t c0 = chunk0 + l8;
             float rt[8], ed[8];
             {
                 float r[8];
@@ -1229,13 +1285,16 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(6)))
 #pragma unroll
                 for (int j = 0; j < 8; ++j) rt[j] = __builtin_fmaf(a, r[j], b0);
             }
-            uint32_t selm = 0;
+            // E^d: E with the outliers set to 0 (past the row E is 0 already)
+            if (!ties) {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const float ae = __builtin_fabsf(e[i][j]);
-                const bool sel = act & ((ae > Tf) | ((ae == Tf) & (c0 + j <= cmax)));
-                selm |= sel ? 1u << j : 0u;
-                ed[j] = sel ? 0.0f : e[i][j];
+                for (int j = 0; j < 8; ++j) ed[j] = __builtin_fabsf(e[i][j]) >= Tf ? 0.0f : e[i][j];
+            } else {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const float ae = __builtin_fabsf(e[i][j]);
+                    ed[j] = ((ae > Tf) | ((ae == Tf) & (c0 + j <= cmax))) ? 0.0f : e[i][j];
+                }
             }
             float m = 0.0f;
 #pragma unroll
@@ -1245,41 +1304,37 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(6)))
             bstore16(rsc, first_q ? (c0 >> A.lg_q) * 2u : kOut, sh);
             const float s = f16_value(sh);
             const float inv = sh ? __builtin_amdgcn_rcpf(s) : 0.0f;
+            // |E^d| <= s q, so E^d * (1/s) stays below q + 1/2 unless the
+            // scale saturated; that case and quotients near a tie take the
+            // clamped, correctly rounded path
             float tc[8], mg[8], qf[8];
             float dist = 0.0f;
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
-                tc[j] = __builtin_amdgcn_fmed3f(ed[j] * inv, -q, q);
+                tc[j] = ed[j] * inv;
                 mg[j] = tc[j] + kMagic;
                 qf[j] = mg[j] - kMagic;
                 dist = __builtin_fmaxf(dist, __builtin_fabsf(tc[j] - qf[j]));
             }
-            if (dist > kNearHalf) {  // some quotient is near a tie: use the exact one
-#pragma unroll
-                for (int j = 0; j < 8; ++j)
-                    if (__builtin_fabsf(tc[j] - qf[j]) > kNearHalf) {
-                        tc[j] = __builtin_amdgcn_fmed3f(ed[j] / s, -q, q);
-                        mg[j] = tc[j] + kMagic;
-                        qf[j] = mg[j] - kMagic;
-                    }
-            }
-            Packed<BITS> pk{};
-            float H[8];
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                pack_put<BITS>(pk, j, __float_as_uint(mg[j]));
-                H[j] = __builtin_fmaf(qf[j], s, rt[j]);  // q*s is exact, so this is R~ + q*s
-            }
-            if (selm) {
-                // (computed for all 8, then selected: cheaper than 8 branches)
+            if ((dist > kNearHalf) | (sh == 0x7BFFu)) {
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    const float ho = rt[j] + f16_value(f16_rne_sat(e[i][j]));
-                    H[j] = ((selm >> j) & 1u) ? ho : H[j];
+                    const float t = __builtin_fabsf(tc[j] - qf[j]) > kNearHalf ? ed[j] / s : tc[j];
+                    mg[j] = __builtin_amdgcn_fmed3f(t, -q, q) + kMagic;
+                    qf[j] = mg[j] - kMagic;
                 }
             }
-            store_codes<BITS>(rcd, (wc0 >> 9) + i, lane, dword3, pk);
-            store_xhat_t(rxh, A.xhat_bf16 != 0, (uint32_t)(wc0 + i * kChunk), l8 >> 3, XT[w], H);
+            float H[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) H[j] = __builtin_fmaf(qf[j], s, rt[j]);  // q*s is exact: R~ + q*s
+            store_codes<BITS>(rcd, (wc0 >> 9) + i, lane, dword3, pack8<BITS>(mg));
+            float4* st = XT[w];
+            st[2 * lane] = make_float4(H[0], H[1], H[2], H[3]);
+            st[2 * lane + 1] = make_float4(H[4], H[5], H[6], H[7]);
+            wave_lds_sync();
+            if (och - chunk0 < (uint32_t)kChunk) reinterpret_cast<float*>(st)[och - chunk0] = ohat;
+            wave_lds_sync();
+            emit_xhat(rxh, A.xhat_bf16 != 0, chunk0, l8 >> 3, st);
         }
     }
 }

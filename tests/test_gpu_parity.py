@@ -70,6 +70,45 @@ def _affine(T, d, g, seed=0, **kw):
     return x, r
 
 
+def _half_integer_rows(T, d, g, with_pair, seed):
+    """Rows against a zero reference whose groups hold (v, -v) pairs of
+    half-integers below 4 and one (7, -7) pair, so each group's scale is 1
+    (b = 4) and most quotients E/s are exact ties of the rounding.  With
+    with_pair, one group of each row also holds 24 and -23 (balanced by two
+    -0.5), the two largest |E| of the row, neither tied."""
+    rng = np.random.default_rng(seed)
+    x = np.zeros((T, d), np.float32)
+    for t in range(T):
+        j0 = int(rng.integers(0, d // g))
+        for j in range(d // g):
+            v = rng.choice(np.array([0.5, 1.5, 2.5, 3.5], np.float32), g // 2)
+            v[0] = 7.0
+            grp = np.concatenate([v, -v])
+            if with_pair and j == j0:
+                grp[1], grp[g // 2 + 1] = 24.0, -23.0
+                grp[2], grp[g // 2 + 2] = -0.5, -0.5
+            rng.shuffle(grp)
+            x[t, j * g:(j + 1) * g] = grp
+    return wl.f32_to_bf16_bits(x)
+
+
+def _scaled(xb, factor):
+    """bf16 rows multiplied by a power of two (exact)."""
+    return wl.f32_to_bf16_bits(wl.bf16_bits_to_f32(xb) * np.float32(factor))
+
+
+def _signed_zero_rows(T, d, distinct):
+    """x tiny and negative, ref a negative constant: alpha = 0, beta = -0, so
+    R~ = -0 and every residual rounds to -0 in fp16; an outlier's
+    reconstruction is then -0 while quantized zeros give +0.  With distinct,
+    magnitudes grow along the row so the largest ones are not tied."""
+    c = np.arange(d)
+    mag = (np.float32(2.0) ** -100 * (1 + (c % 128) / 128) * 2.0 ** (c // 128)) if distinct \
+        else np.full(d, np.float32(2.0) ** -100)
+    x = np.tile(-mag.astype(np.float32), (T, 1))
+    return wl.f32_to_bf16_bits(x), wl.f32_to_bf16_bits(np.full((T, d), -1.0, np.float32))
+
+
 CASES = {
     "tiny_64x512_g64_b4": (cfgd(64, 512, 64, 64, 4), lambda: wl.tiny(0)[:2]),
     "uplink_37x4096_g128_b4_k8": (cfgd(37, 4096, 128, 128, 4, 8),
@@ -100,6 +139,20 @@ CASES = {
                                       lambda: (wl.f32_to_bf16_bits(_zero_sum_integer_rows(6, 512, 64, 0, 0.0, 1)), None)),
     "bf16_out_25x4096_g128_b4_k8": (cfgd(25, 4096, 128, 128, 4, 8, rac.RAC_FLAG_XHAT_BF16),
                                     lambda: wl.prefill_uplink(0, rows=(7, 32))[:2]),
+    "half_integer_quotients_8x4096_g128_b4_k2": (cfgd(8, 4096, 128, 128, 4, 2),
+                                                 lambda: (_half_integer_rows(8, 4096, 128, True, 0), None)),
+    "half_integer_quotients_8x4096_g128_b4_k0": (cfgd(8, 4096, 128, 128, 4, 0),
+                                                 lambda: (_half_integer_rows(8, 4096, 128, False, 1), None)),
+    "saturated_scales_13x4096_g128_b4_k4": (cfgd(13, 4096, 128, 128, 4, 4),
+                                            lambda: (_scaled(_affine(13, 4096, 128)[0], 2.0 ** 22), None)),
+    "saturated_scales_13x4096_g128_b4_k0": (cfgd(13, 4096, 128, 128, 4, 0),
+                                            lambda: (_scaled(_affine(13, 4096, 128)[0], 2.0 ** 22), None)),
+    "saturated_scales_ref_7x2048_g64_b8_k6": (cfgd(7, 2048, 64, 64, 8, 6),
+                                              lambda: tuple(_scaled(a, 2.0 ** 24) for a in _affine(7, 2048, 64))),
+    "signed_zero_outliers_tied_6x1024_g128_b4_k3": (cfgd(6, 1024, 128, 128, 4, 3),
+                                                    lambda: _signed_zero_rows(6, 1024, False)),
+    "signed_zero_outliers_distinct_6x1024_g128_b4_k3": (cfgd(6, 1024, 128, 128, 4, 3),
+                                                        lambda: _signed_zero_rows(6, 1024, True)),
 }
 
 
