@@ -543,6 +543,18 @@ __device__ __forceinline__ void store_xhat_t(Rsrc rx, bool bf16, uint32_t chunk0
               make_uint4(__float_as_uint(hi.x), __float_as_uint(hi.y), __float_as_uint(hi.z), __float_as_uint(hi.w)));
 }
 
+// Lane l's 8 channels at floats 8l..8l+7 of a wavefront's LDS slice.
+__device__ __forceinline__ void put8(float4* st, uint32_t lane, const float* v) {
+    st[2 * lane] = make_float4(v[0], v[1], v[2], v[3]);
+    st[2 * lane + 1] = make_float4(v[4], v[5], v[6], v[7]);
+}
+
+__device__ __forceinline__ void get8(const float4* st, uint32_t lane, float* v) {
+    const float4 a = st[2 * lane], b = st[2 * lane + 1];
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+
 // Store a chunk's reconstruction staged in the wavefront's LDS slice `st`
 // (channel c of the chunk at float c): fp32 as in store_xhat_t, bf16 with
 // lane l storing channels 8l..8l+7.
@@ -989,12 +1001,14 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
 // Encode with per-token outliers, NW wavefronts per token row.  For rows of
 // at most 4096 channels whose groups lie inside a chunk, a workgroup of NW
 // wavefronts owns one token row at a time and wavefront w holds the CPW =
-// 8 / NW chunks [CPW w, CPW w + CPW): lane l keeps E, ref (as loaded) and the
+// 8 / NW chunks [CPW w, CPW w + CPW): lane l keeps ref (as loaded) and the
 // coefficient pair of channels [512c + 8l, 512c + 8l + 8) of its chunks in
-// registers.  The per-token outlier choice costs two barriers between NW
-// wavefronts, and its threshold search and ranking run NW times per row
-// instead of once per chunk; fewer chunks per wavefront keep more wavefronts
-// resident.
+// registers and their E in LDS, where the chunk's reconstruction is later
+// staged for the store.  Keeping E out of registers leaves room to prefetch
+// the next row (x once the fit is done, each ref chunk once its R~ is
+// formed) at seven wavefronts per SIMD.  The per-token outlier choice costs
+// two barriers between NW wavefronts, and its threshold search and ranking
+// run NW times per row instead of once per chunk.
 
 constexpr int kRowsMaxD = 8 * kChunk;  // channels per row
 constexpr int kRowsWaves = 4;          // wavefronts per row (2 chunks each)
@@ -1003,7 +1017,8 @@ template <int NW>
 struct alignas(16) GroupShared {
     uint64_t ckey[kCandCap];  // candidates: |E| bits << 32 | (0xFFFF - channel)
     uint32_t cval[kCandCap];  // their E bits
-    uint32_t crt[kCandCap];   // their R~ bits
+    uint32_t crw[kCandCap];   // their ref word (the bf16 pair holding the channel)
+    uint32_t ccf[kCandCap];   // their group's coefficient pair
     uint32_t smax[NW][kWave]; // lane maxima of |E| of each wavefront
     uint32_t cnt;             // candidate count (LDS atomic)
     uint32_t xcnt[2][NW];     // exact search: element counts, [slot][wavefront]
@@ -1011,10 +1026,11 @@ struct alignas(16) GroupShared {
 
 // Append this lane's elements of one chunk whose |E| pattern is >= lo (and,
 // with use_key, whose key is >= kmin) to the shared candidate list, with
-// their R~ (from the loaded ref pair rpk and the coefficient pair cfv); one
-// LDS atomic per wavefront reserves the slots, entries beyond kCandCap are
-// counted but not stored.
-__device__ __forceinline__ void append_shared(uint64_t* ckey, uint32_t* cval, uint32_t* crt, uint32_t* counter,
+// what R~ is formed from (the loaded ref word and the coefficient pair
+// cfv); one LDS atomic per wavefront reserves the slots, entries beyond
+// kCandCap are counted but not stored.
+template <class G>
+__device__ __forceinline__ void append_shared(G& S,
                                               const float* e, const uint4& rpk, uint32_t cfv, bool act, uint32_t c0,
                                               uint32_t lo, bool use_key, uint64_t kmin, uint32_t lane) {
     bool p[8];
@@ -1027,7 +1043,7 @@ __device__ __forceinline__ void append_shared(uint64_t* ckey, uint32_t* cval, ui
     }
     if (!n) return;
     uint32_t base = 0u;
-    if (lane == 0u) base = atomicAdd(counter, n);
+    if (lane == 0u) base = atomicAdd(&S.cnt, n);
     base = uniform(base);
     const uint32_t rw[4] = {rpk.x, rpk.y, rpk.z, rpk.w};
 #pragma unroll
@@ -1036,10 +1052,10 @@ __device__ __forceinline__ void append_shared(uint64_t* ckey, uint32_t* cval, ui
         if (m) {
             const uint32_t pos = base + mbcnt64(m);
             if (p[j] & (pos < (uint32_t)kCandCap)) {
-                const float r = (j & 1) ? bf16_hi(rw[j >> 1]) : bf16_lo(rw[j >> 1]);
-                ckey[pos] = cand_key(__float_as_uint(e[j]), c0 + j);
-                cval[pos] = __float_as_uint(e[j]);
-                crt[pos] = __float_as_uint(__builtin_fmaf(f16_value(cfv & 0xFFFFu), r, f16_value(cfv >> 16)));
+                S.ckey[pos] = cand_key(__float_as_uint(e[j]), c0 + j);
+                S.cval[pos] = __float_as_uint(e[j]);
+                S.crw[pos] = rw[j >> 1];
+                S.ccf[pos] = cfv;
             }
             base += (uint32_t)__builtin_popcountll(m);
         }
@@ -1055,10 +1071,12 @@ __device__ __forceinline__ void opaque_n(uint4 (&r)[N]) {
 }
 
 template <int BITS, int GA, int GQ, int NW>
-__global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(6))) void rac_encode_rows_kernel(Args A) {
+__global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7))) void rac_encode_rows_kernel(Args A) {
     constexpr int CPW = 8 / NW;  // chunks per wavefront
     __shared__ GroupShared<NW> PS[2];   // by row parity (two barriers per row)
-    __shared__ float4 XT[NW][2 * kWave];  // per-wavefront store staging (2 KiB)
+    // E of each wavefront's chunks (lane l's channels at floats 8l..8l+7 of
+    // its chunk), later the staging of the chunk's reconstruction
+    __shared__ float4 EL[NW][CPW][2 * kWave];
     const uint32_t lane = threadIdx.x & (kWave - 1);
     const int w = (int)uniform(threadIdx.x / kWave);
     const int d = A.d, k = A.k;
@@ -1077,6 +1095,23 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(6)))
     if (w == 0 && lane < 2u) PS[lane].cnt = 0u;
     __syncthreads();
 
+    // x and ref of the block's first row; later rows are prefetched into
+    // the same registers as they fall free (x after the fit, each ref chunk
+    // after its R~ is formed), ahead of the current row's stores
+    uint4 xl[CPW], rp[CPW];
+    {
+        const uint32_t row = blockIdx.x;
+        const bool any = row < A.tokens;
+        const uint64_t o = (uint64_t)row * (uint64_t)d;
+        const Rsrc rx = rsrc(A.x, o, any ? row_bytes : 0u), rr = rsrc(A.ref, o, (A.ref && any) ? row_bytes : 0u);
+#pragma unroll
+        for (int i = 0; i < CPW; ++i) {
+            const uint32_t off = ((uint32_t)(wc0 + i * kChunk) + lane * 8u) * 2u;  // past the row: reads 0
+            xl[i] = bload128(rx, off);
+            rp[i] = bload128(rr, off);
+        }
+    }
+
     uint32_t n = 0;
     for (uint32_t row = blockIdx.x; row < A.tokens; row += gridDim.x, ++n) {
         GroupShared<NW>& S = PS[n & 1];
@@ -1084,26 +1119,19 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(6)))
         // constant of the lane's channels is hoisted out of the row loop
         uint32_t l8 = lane * 8u;
         asm volatile("" : "+v"(l8));
-        const uint64_t o = (uint64_t)row * (uint64_t)d;
-        const Rsrc rx = rsrc(A.x, o, row_bytes), rr = rsrc(A.ref, o, A.ref ? row_bytes : 0u);
-        uint4 xl[CPW], rp[CPW];
+        const uint32_t nrow = row + gridDim.x;
+        const bool more = nrow < A.tokens;
+        const uint64_t on = (uint64_t)nrow * (uint64_t)d;
+        const Rsrc nx = rsrc(A.x, on, more ? row_bytes : 0u), nr = rsrc(A.ref, on, (A.ref && more) ? row_bytes : 0u);
         uint32_t cf[CPW];
 #pragma unroll
-        for (int i = 0; i < CPW; ++i) {
-            const uint32_t off = ((uint32_t)(wc0 + i * kChunk) + l8) * 2u;  // past the row: reads 0
-            xl[i] = bload128(rx, off);
-            rp[i] = bload128(rr, off);
-            cf[i] = 0u;
-        }
+        for (int i = 0; i < CPW; ++i) cf[i] = 0u;
 
         // a2-a3 per chunk: fit of the lane's group, E; lane maximum of |E|
         const Rsrc rcoef = rsrc(A.coef, (uint64_t)row * nga, nga * 4u);
-        float e[CPW][8];
         float lmx = 0.0f;
 #pragma unroll
         for (int i = 0; i < CPW; ++i) {
-#pragma unroll
-            for (int j = 0; j < 8; ++j) e[i][j] = 0.0f;
             if (wc0 + i * kChunk >= d) continue;
             const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
             float r[8], x[8], uu[8], uv[8];
@@ -1121,12 +1149,17 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(6)))
             cf[i] = fit_coef(crr, crx, mr, mx);
             bstore32(rcoef, first_a ? (c0 >> A.lg_a) * 4u : kOut, cf[i]);
             const float a = f16_value(cf[i] & 0xFFFFu), b0 = f16_value(cf[i] >> 16);
+            float e[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j) {  // E = 0 past the row
-                e[i][j] = x[j] - __builtin_fmaf(a, r[j], b0);
-                lmx = __builtin_fmaxf(lmx, __builtin_fabsf(e[i][j]));
+                e[j] = x[j] - __builtin_fmaf(a, r[j], b0);
+                lmx = __builtin_fmaxf(lmx, __builtin_fabsf(e[j]));
             }
+            put8(EL[w][i], lane, e);
         }
+
+#pragma unroll
+        for (int i = 0; i < CPW; ++i) xl[i] = bload128(nx, ((uint32_t)(wc0 + i * kChunk) + l8) * 2u);
 
         // a4: the k largest |E| of the row (ties to the lower channel).
         // Threshold L: the k-th largest of the 64 maxima of |E| over lane l
@@ -1152,8 +1185,9 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(6)))
         for (int i = 0; i < CPW; ++i) {
             if (wc0 + i * kChunk >= d) continue;
             const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
-            append_shared(S.ckey, S.cval, S.crt, &S.cnt, e[i], rp[i], cf[i], c0 < (uint32_t)d, c0, L, false, 0ull,
-                          lane);
+            float e[8];
+            get8(EL[w][i], lane, e);
+            append_shared(S, e, rp[i], cf[i], c0 < (uint32_t)d, c0, L, false, 0ull, lane);
         }
         __syncthreads();
         // (values read from LDS are the same in every lane: readfirstlane
@@ -1185,9 +1219,11 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(6)))
 #pragma unroll
                 for (int i = 0; i < CPW; ++i) {
                     const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
+                    float e[8];
+                    get8(EL[w][i], lane, e);
 #pragma unroll
                     for (int j = 0; j < 8; ++j) {
-                        const uint32_t a = __float_as_uint(e[i][j]) & 0x7FFFFFFFu;
+                        const uint32_t a = __float_as_uint(e[j]) & 0x7FFFFFFFu;
                         cntl += ((c0 < (uint32_t)d) & (a >= plo) & (a <= phi) & (c0 + j <= pmax)) ? 1u : 0u;
                     }
                 }
@@ -1215,8 +1251,9 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(6)))
 #pragma unroll
             for (int i = 0; i < CPW; ++i) {
                 const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
-                append_shared(S.ckey, S.cval, S.crt, &S.cnt, e[i], rp[i], cf[i], c0 < (uint32_t)d, c0, T, true, kst,
-                              lane);
+                float e[8];
+                get8(EL[w][i], lane, e);
+                append_shared(S, e, rp[i], cf[i], c0 < (uint32_t)d, c0, T, true, kst, lane);
             }
             __syncthreads();
             C = uniform(S.cnt);  // == k
@@ -1252,7 +1289,9 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(6)))
         float ohat = 0.0f;
         if (chosen) {
             oval = f16_rne_sat(__uint_as_float(S.cval[lane]));
-            ohat = __uint_as_float(S.crt[lane]) + f16_value(oval);
+            const uint32_t rw = S.crw[lane], cfc = S.ccf[lane];
+            const float r = (och & 1u) ? bf16_hi(rw) : bf16_lo(rw);
+            ohat = __builtin_fmaf(f16_value(cfc & 0xFFFFu), r, f16_value(cfc >> 16)) + f16_value(oval);
         }
         if (w == 0) {
             // the row's outliers in ascending channel order (slot = number of
@@ -1277,23 +1316,21 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(6)))
             if (wc0 + i * kChunk >= d) continue;
             const uint32_t chunk0 = (uint32_t)(wc0 + i * kChunk);
             const uint32_t c0 = chunk0 + l8;
-            float rt[8], ed[8];
+            float ed[8];
+            float4* st = EL[w][i];
             {
-                float r[8];
-                widen8(rp[i], r);
-                const float a = f16_value(cf[i] & 0xFFFFu), b0 = f16_value(cf[i] >> 16);
+                float e[8];
+                get8(st, lane, e);
+                // E^d: E with the outliers set to 0 (past the row E is 0 already)
+                if (!ties) {
 #pragma unroll
-                for (int j = 0; j < 8; ++j) rt[j] = __builtin_fmaf(a, r[j], b0);
-            }
-            // E^d: E with the outliers set to 0 (past the row E is 0 already)
-            if (!ties) {
+                    for (int j = 0; j < 8; ++j) ed[j] = __builtin_fabsf(e[j]) >= Tf ? 0.0f : e[j];
+                } else {
 #pragma unroll
-                for (int j = 0; j < 8; ++j) ed[j] = __builtin_fabsf(e[i][j]) >= Tf ? 0.0f : e[i][j];
-            } else {
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const float ae = __builtin_fabsf(e[i][j]);
-                    ed[j] = ((ae > Tf) | ((ae == Tf) & (c0 + j <= cmax))) ? 0.0f : e[i][j];
+                    for (int j = 0; j < 8; ++j) {
+                        const float ae = __builtin_fabsf(e[j]);
+                        ed[j] = ((ae > Tf) | ((ae == Tf) & (c0 + j <= cmax))) ? 0.0f : e[j];
+                    }
                 }
             }
             float m = 0.0f;
@@ -1307,30 +1344,37 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(6)))
             // |E^d| <= s q, so E^d * (1/s) stays below q + 1/2 unless the
             // scale saturated; that case and quotients near a tie take the
             // clamped, correctly rounded path
-            float tc[8], mg[8], qf[8];
+            float mg[8], qf[8];
             float dist = 0.0f;
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
-                tc[j] = ed[j] * inv;
-                mg[j] = tc[j] + kMagic;
+                const float t = ed[j] * inv;
+                mg[j] = t + kMagic;
                 qf[j] = mg[j] - kMagic;
-                dist = __builtin_fmaxf(dist, __builtin_fabsf(tc[j] - qf[j]));
+                dist = __builtin_fmaxf(dist, __builtin_fabsf(t - qf[j]));
             }
             if ((dist > kNearHalf) | (sh == 0x7BFFu)) {
+                float inv2 = inv;
+                asm volatile("" : "+v"(inv2));  // recomputed here rather than kept live
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    const float t = __builtin_fabsf(tc[j] - qf[j]) > kNearHalf ? ed[j] / s : tc[j];
+                    const float t0 = ed[j] * inv2;
+                    const float t = __builtin_fabsf(t0 - qf[j]) > kNearHalf ? ed[j] / s : t0;
                     mg[j] = __builtin_amdgcn_fmed3f(t, -q, q) + kMagic;
                     qf[j] = mg[j] - kMagic;
                 }
             }
             float H[8];
+            {
+                float r[8];
+                widen8(rp[i], r);
+                const float a = f16_value(cf[i] & 0xFFFFu), b0 = f16_value(cf[i] >> 16);
 #pragma unroll
-            for (int j = 0; j < 8; ++j) H[j] = __builtin_fmaf(qf[j], s, rt[j]);  // q*s is exact: R~ + q*s
+                for (int j = 0; j < 8; ++j) H[j] = __builtin_fmaf(qf[j], s, __builtin_fmaf(a, r[j], b0));  // R~ + q*s (q*s exact)
+            }
+            rp[i] = bload128(nr, c0 * 2u);
             store_codes<BITS>(rcd, (wc0 >> 9) + i, lane, dword3, pack8<BITS>(mg));
-            float4* st = XT[w];
-            st[2 * lane] = make_float4(H[0], H[1], H[2], H[3]);
-            st[2 * lane + 1] = make_float4(H[4], H[5], H[6], H[7]);
+            put8(st, lane, H);
             wave_lds_sync();
             if (och - chunk0 < (uint32_t)kChunk) reinterpret_cast<float*>(st)[och - chunk0] = ohat;
             wave_lds_sync();
