@@ -1020,7 +1020,7 @@ struct alignas(16) GroupShared {
     uint32_t crw[kCandCap];   // their ref word (the bf16 pair holding the channel)
     uint32_t ccf[kCandCap];   // their group's coefficient pair
     uint32_t smax[NW][kWave]; // lane maxima of |E| of each wavefront
-    uint32_t cnt;             // candidate count (LDS atomic)
+    uint32_t cnt[2];          // candidate count (LDS atomic), by row parity
     uint32_t xcnt[2][NW];     // exact search: element counts, [slot][wavefront]
 };
 
@@ -1030,7 +1030,7 @@ struct alignas(16) GroupShared {
 // cfv); one LDS atomic per wavefront reserves the slots, entries beyond
 // kCandCap are counted but not stored.
 template <class G>
-__device__ __forceinline__ void append_shared(G& S,
+__device__ __forceinline__ void append_shared(G& S, uint32_t* counter,
                                               const float* e, const uint4& rpk, uint32_t cfv, bool act, uint32_t c0,
                                               uint32_t lo, bool use_key, uint64_t kmin, uint32_t lane) {
     bool p[8];
@@ -1043,7 +1043,7 @@ __device__ __forceinline__ void append_shared(G& S,
     }
     if (!n) return;
     uint32_t base = 0u;
-    if (lane == 0u) base = atomicAdd(&S.cnt, n);
+    if (lane == 0u) base = atomicAdd(counter, n);
     base = uniform(base);
     const uint32_t rw[4] = {rpk.x, rpk.y, rpk.z, rpk.w};
 #pragma unroll
@@ -1073,7 +1073,9 @@ __device__ __forceinline__ void opaque_n(uint4 (&r)[N]) {
 template <int BITS, int GA, int GQ, int NW>
 __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7))) void rac_encode_rows_kernel(Args A) {
     constexpr int CPW = 8 / NW;  // chunks per wavefront
-    __shared__ GroupShared<NW> PS[2];   // by row parity (two barriers per row)
+    // (a row's lists are read before the next row's first barrier and
+    // written after it; only the count is reset early, so it alternates)
+    __shared__ GroupShared<NW> S;
     // E of each wavefront's chunks (lane l's channels at floats 8l..8l+7 of
     // its chunk), later the staging of the chunk's reconstruction
     __shared__ float4 EL[NW][CPW][2 * kWave];
@@ -1086,13 +1088,11 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
     const bool dword3 = (d & 31) == 0;
     const int lv_a = GA >= 0 ? GA : A.lane_lv_a;
     const int lv_q = GQ >= 0 ? GQ : A.lane_lv_q;
-    const bool first_a = (lane & ((1u << lv_a) - 1u)) == 0u;
-    const bool first_q = (lane & ((1u << lv_q) - 1u)) == 0u;
     const uint32_t ngq = (uint32_t)d >> A.lg_q, nga = (uint32_t)d >> A.lg_a;
     const uint32_t row_bytes = (uint32_t)d * 2u;
     const uint32_t crb = (uint32_t)A.code_row_bytes;
     const int wc0 = w * CPW * kChunk;  // first channel of this wavefront's chunks
-    if (w == 0 && lane < 2u) PS[lane].cnt = 0u;
+    if (w == 0 && lane < 2u) S.cnt[lane] = 0u;
     __syncthreads();
 
     // x and ref of the block's first row; later rows are prefetched into
@@ -1114,11 +1114,18 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
 
     uint32_t n = 0;
     for (uint32_t row = blockIdx.x; row < A.tokens; row += gridDim.x, ++n) {
-        GroupShared<NW>& S = PS[n & 1];
+        uint32_t* const cnt = &S.cnt[n & 1];
         // lane * 8, opaque inside the loop: otherwise every per-channel
         // constant of the lane's channels is hoisted out of the row loop
-        uint32_t l8 = lane * 8u;
-        asm volatile("" : "+v"(l8));
+        // (the lane id is recomputed, not kept live across the loop)
+        uint32_t l8;
+        asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0\n\tv_lshlrev_b32 %0, 3, %0"
+                     : "=v"(l8));
+        const uint32_t lane = l8 >> 3;  // (likewise every lane offset below)
+        const bool first_a = (lane & ((1u << lv_a) - 1u)) == 0u;
+        const bool first_q = (lane & ((1u << lv_q) - 1u)) == 0u;
+        int d = A.d;  // (per row as well: tests on it stay scalar instead of being kept in registers)
+        asm volatile("" : "+s"(d));
         const uint32_t nrow = row + gridDim.x;
         const bool more = nrow < A.tokens;
         const uint64_t on = (uint64_t)nrow * (uint64_t)d;
@@ -1170,7 +1177,7 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
         __syncthreads();
         // the other buffer was last read by the previous row, which every
         // wavefront has left: reset its candidate count for the next row
-        if (w == 0 && lane == 0u) PS[(n + 1) & 1].cnt = 0u;
+        if (w == 0 && lane == 0u) S.cnt[(n + 1) & 1] = 0u;
         uint32_t v = S.smax[0][lane];
 #pragma unroll
         for (int ww = 1; ww < NW; ++ww) v = __builtin_elementwise_max(v, S.smax[ww][lane]);
@@ -1187,12 +1194,12 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
             const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
             float e[8];
             get8(EL[w][i], lane, e);
-            append_shared(S, e, rp[i], cf[i], c0 < (uint32_t)d, c0, L, false, 0ull, lane);
+            append_shared(S, cnt, e, rp[i], cf[i], c0 < (uint32_t)d, c0, L, false, 0ull, lane);
         }
         __syncthreads();
         // (values read from LDS are the same in every lane: readfirstlane
         // makes that visible, so the branches on them stay scalar)
-        uint32_t C = uniform(S.cnt);
+        uint32_t C = uniform(*cnt);
         const bool exact = C > (uint32_t)kCandCap;
         uint64_t kst = 0ull;  // key of the k-th largest element: the outliers are the keys >= kst
         if (exact) {
@@ -1246,17 +1253,17 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
                 }
             }
             kst = ((uint64_t)T << 32) | (uint64_t)(0xFFFFu - lo);
-            if (w == 0 && lane == 0u) S.cnt = 0u;
+            if (w == 0 && lane == 0u) *cnt = 0u;
             __syncthreads();
 #pragma unroll
             for (int i = 0; i < CPW; ++i) {
                 const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
                 float e[8];
                 get8(EL[w][i], lane, e);
-                append_shared(S, e, rp[i], cf[i], c0 < (uint32_t)d, c0, T, true, kst, lane);
+                append_shared(S, cnt, e, rp[i], cf[i], c0 < (uint32_t)d, c0, T, true, kst, lane);
             }
             __syncthreads();
-            C = uniform(S.cnt);  // == k
+            C = uniform(*cnt);  // == k
         }
         const bool have = lane < C;
         const uint64_t key = have ? S.ckey[lane] : 0ull;
