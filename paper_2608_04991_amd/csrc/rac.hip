@@ -520,58 +520,62 @@ __device__ __forceinline__ void store_xhat(Rsrc rx, bool bf16, uint32_t c0, cons
     bstore128(rx, o1, v1);
 }
 
-// Same, for the lane's channels 8l..8l+7 of the chunk starting at channel
-// `chunk0`, with fp32 output written through the wavefront's 2 KiB LDS
-// slice `st`: lane l then stores channels 4l..4l+3 and 256+4l..256+4l+3,
-// so that each store instruction writes 1 KiB of contiguous memory (two
-// interleaved 16-byte halves per lane cost HBM efficiency).  Channels past
-// the row fall outside the section's range.
+// A wavefront's LDS slice of one 512-channel chunk: lane l's channels
+// 8l..8l+3 at float4 l and 8l+4..8l+7 at float4 kPlane + l.  Each access
+// by the 64 lanes covers 1 KiB of consecutive float4s, and the 8-float4 gap
+// puts the two planes in different banks for the transposed read below.
+constexpr int kPlane = kWave + 8;
+constexpr int kSlice = 2 * kPlane;  // float4 per slice
+
+__device__ __forceinline__ void put8(float4* st, uint32_t lane, const float* v) {
+    st[lane] = make_float4(v[0], v[1], v[2], v[3]);
+    st[kPlane + lane] = make_float4(v[4], v[5], v[6], v[7]);
+}
+
+__device__ __forceinline__ void get8(const float4* st, uint32_t lane, float* v) {
+    const float4 a = st[lane], b = st[kPlane + lane];
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+
+// Float offset of chunk channel c in a slice.
+__device__ __forceinline__ uint32_t slice_float(uint32_t c) {
+    return ((c & 4u) ? 4u * kPlane : 0u) + ((c >> 3) << 2) + (c & 3u);
+}
+
+// Store a chunk's reconstruction staged in the wavefront's slice `st`.  For
+// fp32, lane m stores channels 4m..4m+3 and 256+4m..256+4m+3, so that each
+// store instruction writes 1 KiB of contiguous memory (two interleaved
+// 16-byte halves per lane cost HBM efficiency); bf16 lanes store their own 8
+// channels.  Channels past the row fall outside the section's range.
+__device__ __forceinline__ void emit_xhat(Rsrc rx, bool bf16, uint32_t chunk0, uint32_t lane, float4* st) {
+    if (bf16) {
+        float H[8];
+        get8(st, lane, H);
+        wave_lds_sync();
+        store_xhat(rx, true, chunk0 + lane * 8u, H);
+        return;
+    }
+    const uint32_t t = (lane & 1u) * kPlane + (lane >> 1);
+    const float4 lo = st[t], hi = st[t + 32u];
+    wave_lds_sync();  // the slice is rewritten by the next chunk
+    bstore128(rx, (chunk0 + lane * 4u) * 4u,
+              make_uint4(__float_as_uint(lo.x), __float_as_uint(lo.y), __float_as_uint(lo.z), __float_as_uint(lo.w)));
+    bstore128(rx, (chunk0 + 256u + lane * 4u) * 4u,
+              make_uint4(__float_as_uint(hi.x), __float_as_uint(hi.y), __float_as_uint(hi.z), __float_as_uint(hi.w)));
+}
+
+// Stage and store the lane's 8 reconstructed channels (the lane's channels
+// 8l..8l+7 of the chunk starting at `chunk0`).
 __device__ __forceinline__ void store_xhat_t(Rsrc rx, bool bf16, uint32_t chunk0, uint32_t lane, float4* st,
                                              const float* H) {
     if (bf16) {
         store_xhat(rx, true, chunk0 + lane * 8u, H);
         return;
     }
-    st[2 * lane] = make_float4(H[0], H[1], H[2], H[3]);
-    st[2 * lane + 1] = make_float4(H[4], H[5], H[6], H[7]);
+    put8(st, lane, H);
     wave_lds_sync();
-    const float4 lo = st[lane], hi = st[kWave + lane];
-    wave_lds_sync();  // the slice is rewritten by the next chunk
-    bstore128(rx, (chunk0 + lane * 4u) * 4u,
-              make_uint4(__float_as_uint(lo.x), __float_as_uint(lo.y), __float_as_uint(lo.z), __float_as_uint(lo.w)));
-    bstore128(rx, (chunk0 + 256u + lane * 4u) * 4u,
-              make_uint4(__float_as_uint(hi.x), __float_as_uint(hi.y), __float_as_uint(hi.z), __float_as_uint(hi.w)));
-}
-
-// Lane l's 8 channels at floats 8l..8l+7 of a wavefront's LDS slice.
-__device__ __forceinline__ void put8(float4* st, uint32_t lane, const float* v) {
-    st[2 * lane] = make_float4(v[0], v[1], v[2], v[3]);
-    st[2 * lane + 1] = make_float4(v[4], v[5], v[6], v[7]);
-}
-
-__device__ __forceinline__ void get8(const float4* st, uint32_t lane, float* v) {
-    const float4 a = st[2 * lane], b = st[2 * lane + 1];
-    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
-}
-
-// Store a chunk's reconstruction staged in the wavefront's LDS slice `st`
-// (channel c of the chunk at float c): fp32 as in store_xhat_t, bf16 with
-// lane l storing channels 8l..8l+7.
-__device__ __forceinline__ void emit_xhat(Rsrc rx, bool bf16, uint32_t chunk0, uint32_t lane, float4* st) {
-    if (bf16) {
-        const float4 a = st[2 * lane], b = st[2 * lane + 1];
-        wave_lds_sync();
-        const float H[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-        store_xhat(rx, true, chunk0 + lane * 8u, H);
-        return;
-    }
-    const float4 lo = st[lane], hi = st[kWave + lane];
-    wave_lds_sync();  // the slice is rewritten by the next chunk
-    bstore128(rx, (chunk0 + lane * 4u) * 4u,
-              make_uint4(__float_as_uint(lo.x), __float_as_uint(lo.y), __float_as_uint(lo.z), __float_as_uint(lo.w)));
-    bstore128(rx, (chunk0 + 256u + lane * 4u) * 4u,
-              make_uint4(__float_as_uint(hi.x), __float_as_uint(hi.y), __float_as_uint(hi.z), __float_as_uint(hi.w)));
+    emit_xhat(rx, false, chunk0, lane, st);
 }
 
 // Buffer resource of one row of the reconstruction (range 0 when no
@@ -818,7 +822,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
     // LDS state of a row, double-buffered by row parity: every row that uses
     // LDS has a workgroup barrier, so no wave is more than one row ahead.
     __shared__ RowShared SS[2];
-    __shared__ float4 XT[kMaxWaves][2 * kWave];  // per-wavefront store staging (2 KiB)
+    extern __shared__ float4 XT[];  // per-wavefront store staging, kSlice each (sized at launch)
     const uint32_t lane = threadIdx.x & (kWave - 1);
     const int w = (int)(threadIdx.x / kWave);
     const int d = A.d;
@@ -993,7 +997,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
         }
         const uint32_t crb = (uint32_t)A.code_row_bytes;
         store_codes<BITS>(rsrc(A.codes, (uint64_t)row * crb, crb), w, lane, dword3, pk);
-        store_xhat_t(xhat_row(A, row), A.xhat_bf16 != 0, (uint32_t)(w * kChunk), lane, XT[w], H);
+        store_xhat_t(xhat_row(A, row), A.xhat_bf16 != 0, (uint32_t)(w * kChunk), lane, XT + w * kSlice, H);
     }
 }
 
@@ -1076,9 +1080,9 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
     // (a row's lists are read before the next row's first barrier and
     // written after it; only the count is reset early, so it alternates)
     __shared__ GroupShared<NW> S;
-    // E of each wavefront's chunks (lane l's channels at floats 8l..8l+7 of
-    // its chunk), later the staging of the chunk's reconstruction
-    __shared__ float4 EL[NW][CPW][2 * kWave];
+    // E of each wavefront's chunks (one slice per chunk), later the staging
+    // of the chunk's reconstruction
+    __shared__ float4 EL[NW][CPW][kSlice];
     const uint32_t lane = threadIdx.x & (kWave - 1);
     const int w = (int)uniform(threadIdx.x / kWave);
     const int d = A.d, k = A.k;
@@ -1383,7 +1387,7 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
             store_codes<BITS>(rcd, (wc0 >> 9) + i, lane, dword3, pack8<BITS>(mg));
             put8(st, lane, H);
             wave_lds_sync();
-            if (och - chunk0 < (uint32_t)kChunk) reinterpret_cast<float*>(st)[och - chunk0] = ohat;
+            if (och - chunk0 < (uint32_t)kChunk) reinterpret_cast<float*>(st)[slice_float(och - chunk0)] = ohat;
             wave_lds_sync();
             emit_xhat(rxh, A.xhat_bf16 != 0, chunk0, l8 >> 3, st);
         }
@@ -1396,7 +1400,7 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
 
 template <int BITS>
 __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
-    __shared__ float4 XT[kMaxWaves][2 * kWave];  // per-wavefront store staging (2 KiB)
+    extern __shared__ float4 XT[];  // per-wavefront store staging, kSlice each (sized at launch)
     const uint32_t lane = threadIdx.x & (kWave - 1);
     const int w = (int)(threadIdx.x / kWave);
     const int d = A.d, k = A.k;
@@ -1462,7 +1466,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
                     if ((uint32_t)j == jj) H[j] = rt[j] + v;
             }
         }
-        store_xhat_t(xhat_row(A, row), A.xhat_bf16 != 0, (uint32_t)(w * kChunk), lane, XT[w], H);
+        store_xhat_t(xhat_row(A, row), A.xhat_bf16 != 0, (uint32_t)(w * kChunk), lane, XT + w * kSlice, H);
     }
 }
 
@@ -1642,13 +1646,17 @@ KernelFn pick_decode(int bits) {
 // prefetching its next row); small counts launch one workgroup per row.
 rac_status launch(KernelFn fn, Args A, hipStream_t stream, int threads = 0) {
     const int64_t rows = A.tokens;
-    if (threads == 0) threads = A.nch * kWave;
+    // kernels launched with one wavefront per chunk stage through a
+    // dynamically sized slice per wavefront
+    const bool staged = threads == 0;
+    if (staged) threads = A.nch * kWave;
+    const size_t lds = staged ? (size_t)A.nch * kSlice * sizeof(float4) : 0;
     int64_t blocks = rows <= 0 ? 1 : rows;
     if (rows > 256) {
         int dev = 0, cus = 0, per_cu = 0;
         if (hipGetDevice(&dev) != hipSuccess ||
             hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(fn), threads, 0) !=
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(fn), threads, lds) !=
                 hipSuccess)
             return RAC_ERR_HIP;
         const int64_t resident = (int64_t)cus * (per_cu > 0 ? per_cu : 1);
@@ -1656,7 +1664,7 @@ rac_status launch(KernelFn fn, Args A, hipStream_t stream, int threads = 0) {
     }
     void* args[] = {&A};
     const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3((unsigned)blocks),
-                                         dim3((unsigned)threads), args, 0, stream);
+                                         dim3((unsigned)threads), args, lds, stream);
     return e == hipSuccess ? RAC_OK : RAC_ERR_HIP;
 }
 
