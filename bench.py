@@ -6,7 +6,9 @@ alignment/quantization group 128, 4-bit codes, top-8 outliers per token):
 rac_encode with the fused sender reconstruction, then the receiver's
 rac_decode, on one stream.  Inputs are resident in HBM before timing starts;
 batches rotate through enough buffer sets (> 1 GB) that no step finds its
-inputs in the 256 MB Infinity Cache.
+inputs in the 256 MB Infinity Cache.  Untimed steps run for --warm-ms first:
+the GPU clock climbs over the first ~20 ms of sustained load, and the timed
+steps measure the steady state.
 
 Prints ONE JSON line:
   value       bf16 activation bytes processed per second (2*T*d per step), GB/s
@@ -51,6 +53,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warm-ms", type=float, default=50.0,
+                    help="after the warmup steps, keep running untimed steps for this long: the GPU clock "
+                         "climbs for the first ~20 ms of sustained load")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -105,11 +110,18 @@ def main():
         s = sets[i % nsets]
         rac.rac_decode(cfg, s["wire"], s["ref"], None, s["xdec"], stream=stream)
 
-    log(f"[bench] warmup {args.warmup} steps ({nsets} rotating buffer sets)")
+    log(f"[bench] warmup {args.warmup} steps, then {args.warm_ms:g} ms ({nsets} rotating buffer sets)")
     for i in range(args.warmup):
         encode(i)
         decode(i)
     torch.cuda.synchronize()
+    t_warm, i = time.perf_counter(), 0
+    while (time.perf_counter() - t_warm) * 1e3 < args.warm_ms:
+        for _ in range(10):
+            encode(i)
+            decode(i)
+            i += 1
+        torch.cuda.synchronize()
     # The timed steps: encode + decode per step, back to back on one stream.
     log(f"[bench] timing {args.steps} steps")
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]

@@ -1,8 +1,11 @@
 """Summaries of rocprofv3 output for the codec kernels.
 
-  python -m paper_2608_04991_amd.rocprof_summary stats DIR OUT.txt "COMMAND"
+  python -m paper_2608_04991_amd.rocprof_summary stats DIR OUT.txt "COMMAND" [LAST]
       kernel-trace statistics (calls, average and total duration per kernel)
-      of a `rocprofv3 --kernel-trace --stats --output-format csv` run.
+      of a `rocprofv3 --kernel-trace --stats --output-format csv` run; with
+      LAST, also the average of the last LAST dispatches of each codec
+      kernel (bench.py ends with LAST back-to-back launches of each, the
+      run its per-kernel HIP-event durations come from).
 
   python -m paper_2608_04991_amd.rocprof_summary traffic KERNEL FETCH_DIR WRITE_DIR \
          COPY_FETCH_DIR COPY_WRITE_DIR COPY_BYTES OUT.json "COMMANDS"
@@ -37,7 +40,7 @@ def _one(pattern: str) -> str:
     return files[0]
 
 
-def stats(dirpath: str, out: str, command: str) -> None:
+def stats(dirpath: str, out: str, command: str, last: int = 0) -> None:
     rows = list(csv.DictReader(open(_one(os.path.join(dirpath, "**", "*kernel_stats.csv")))))
     lines = [f"# rocprofv3 kernel-trace statistics", f"# command: {command}", "",
              f"{'calls':>6} {'avg_us':>10} {'min_us':>10} {'max_us':>10} {'total_us':>12} {'pct':>6}  kernel"]
@@ -46,6 +49,16 @@ def stats(dirpath: str, out: str, command: str) -> None:
         lines.append(f"{int(r['Calls']):>6} {ns('AverageNs'):>10.2f} {ns('MinNs'):>10.2f} "
                      f"{ns('MaxNs'):>10.2f} {ns('TotalDurationNs'):>12.1f} {float(r['Percentage']):>6.2f}  "
                      f"{r['Name'][:110]}")
+    if last:
+        trace = list(csv.DictReader(open(_one(os.path.join(dirpath, "**", "*kernel_trace.csv")))))
+        lines += ["", f"# last {last} dispatches of each codec kernel (back to back)",
+                  f"{'calls':>6} {'avg_us':>10} {'span_us':>10}  kernel"]
+        names = sorted({t["Kernel_Name"] for t in trace if "rac_" in t["Kernel_Name"]})
+        for name in names:
+            ds = [t for t in trace if t["Kernel_Name"] == name][-last:]
+            dur = [(int(t["End_Timestamp"]) - int(t["Start_Timestamp"])) / 1e3 for t in ds]
+            span = (int(ds[-1]["End_Timestamp"]) - int(ds[0]["Start_Timestamp"])) / 1e3 / len(ds)
+            lines.append(f"{len(ds):>6} {sum(dur) / len(dur):>10.2f} {span:>10.2f}  {name[:110]}")
     open(out, "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
@@ -84,7 +97,7 @@ def traffic(kernel, fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_b
 
 if __name__ == "__main__":
     if sys.argv[1] == "stats":
-        stats(*sys.argv[2:5])
+        stats(*sys.argv[2:5], *(int(a) for a in sys.argv[5:6]))
     elif sys.argv[1] == "traffic":
         traffic(*sys.argv[2:10])
     else:
