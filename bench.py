@@ -212,8 +212,9 @@ def main():
 def decode_step_latency(torch, rac, wl, dev, stream):
     """µs per call of rac_encode and rac_decode for decode-phase batches
     (1 token per sequence, 4096 hidden, group 128, 4-bit, no outliers):
-    wall time per call with back-to-back launches, and kernel time from
-    HIP events."""
+    wall time per call with back-to-back launches, kernel time from HIP
+    events, and the time per encode + decode pair when 20 pairs are captured
+    in one HIP graph and replayed."""
     res = {}
     for B in (1, 16, 64, 256):
         cfg = rac.RacConfig(B, 4096, 128, 128, 4, 0)
@@ -247,10 +248,24 @@ def decode_step_latency(torch, rac, wl, dev, stream):
             torch.cuda.synchronize()
             ke.append(e[0].elapsed_time(e[1]))
             kd.append(e[1].elapsed_time(e[2]))
+        # the same pair captured in a HIP graph (20 pairs per graph), replayed
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(20):
+                rac.rac_encode(cfg, x, ref, None, wire, xh)
+                rac.rac_decode(cfg, wire, ref, None, xd)
+        g.replay()
+        torch.cuda.synchronize()
+        e[0].record(stream)
+        for _ in range(10):
+            g.replay()
+        e[1].record(stream)
+        torch.cuda.synchronize()
         res[f"B{B}"] = {"encode_us_per_call": round((t1 - t0) / n * 1e6, 2),
                         "decode_us_per_call": round((t2 - t1) / n * 1e6, 2),
                         "encode_event_us": round(float(np.median(ke)) * 1e3, 2),
-                        "decode_event_us": round(float(np.median(kd)) * 1e3, 2)}
+                        "decode_event_us": round(float(np.median(kd)) * 1e3, 2),
+                        "graph_pair_us": round(e[0].elapsed_time(e[1]) * 1e3 / 200, 2)}
     return res
 
 
