@@ -565,6 +565,22 @@ __device__ __forceinline__ void emit_xhat(Rsrc rx, bool bf16, uint32_t chunk0, u
               make_uint4(__float_as_uint(hi.x), __float_as_uint(hi.y), __float_as_uint(hi.z), __float_as_uint(hi.w)));
 }
 
+// Same as emit_xhat without a branch on the format: both forms read two
+// float4 of the slice and issue two stores (the bf16 form's second one outside
+// the range), so the memory operations of a row do not depend on the format.
+__device__ __forceinline__ void emit_xhat_flat(Rsrc rx, bool bf16, uint32_t chunk0, uint32_t lane, float4* st) {
+    const uint32_t tt = (lane & 1u) * kPlane + (lane >> 1);
+    const uint32_t t0 = bf16 ? lane : tt, t1 = bf16 ? kPlane + lane : tt + 32u;
+    const float4 lo = st[t0], hi = st[t1];
+    wave_lds_sync();  // the slice is rewritten by the next chunk
+    const uint4 pk = make_uint4(bf16_rne(lo.x) | (bf16_rne(lo.y) << 16), bf16_rne(lo.z) | (bf16_rne(lo.w) << 16),
+                                bf16_rne(hi.x) | (bf16_rne(hi.y) << 16), bf16_rne(hi.z) | (bf16_rne(hi.w) << 16));
+    const uint4 f0 = make_uint4(__float_as_uint(lo.x), __float_as_uint(lo.y), __float_as_uint(lo.z), __float_as_uint(lo.w));
+    const uint4 f1 = make_uint4(__float_as_uint(hi.x), __float_as_uint(hi.y), __float_as_uint(hi.z), __float_as_uint(hi.w));
+    bstore128(rx, bf16 ? (chunk0 + lane * 8u) * 2u : (chunk0 + lane * 4u) * 4u, bf16 ? pk : f0);
+    bstore128(rx, bf16 ? kOut : (chunk0 + 256u + lane * 4u) * 4u, f1);
+}
+
 // Stage and store the lane's 8 reconstructed channels (the lane's channels
 // 8l..8l+7 of the chunk starting at `chunk0`).
 __device__ __forceinline__ void store_xhat_t(Rsrc rx, bool bf16, uint32_t chunk0, uint32_t lane, float4* st,
@@ -1115,6 +1131,12 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
             rp[i] = bload128(rr, off);
         }
     }
+    // A store that the range check drops, so that stores are outstanding at
+    // the loop entry as they are at the end of every row: the compiler's wait
+    // analysis then keeps the memory operations in order across the loop and
+    // the fit waits for the prefetched loads, not for the previous row's
+    // stores issued after them.
+    bstore32(rsrc(A.coef, 0, 0u), kOut, 0u);
 
     uint32_t n = 0;
     for (uint32_t row = blockIdx.x; row < A.tokens; row += gridDim.x, ++n) {
@@ -1397,8 +1419,10 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
 // ---------------------------------------------------------------------------
 // Decode / reconstruct: one workgroup per token row (strided, with the next
 // row's inputs prefetched), one wavefront per chunk, no cross-wave work.
+// OUTL: the wire has outliers; BF16: the reconstruction is stored as bf16.
+// (Both are compile-time, so no branch separates a row's memory operations.)
 
-template <int BITS>
+template <int BITS, bool OUTL, bool BF16>
 __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
     extern __shared__ float4 XT[];  // per-wavefront store staging, kSlice each (sized at launch)
     const uint32_t lane = threadIdx.x & (kWave - 1);
@@ -1430,43 +1454,57 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
         in.sh = bload16(rsrc(A.scale, r * ngq, (in_range && !A.fixed) ? ngq * 2u : 0u), (uint32_t)grp_q * 2u);
         if (A.fixed) in.sh = sh_fixed;
         load_codes<BITS>(rsrc(A.codes, r * crb, in_range ? crb : 0u), w, lane, dword3, in.lo, in.hi);
-        in.ent = bload32(rsrc(A.outl, r * (uint64_t)k, in_range ? (uint32_t)k * 4u : 0u), lane * 4u);
+        in.ent = OUTL ? bload32(rsrc(A.outl, r * (uint64_t)k, in_range ? (uint32_t)k * 4u : 0u), lane * 4u) : 0u;
         return in;
     };
 
-    uint32_t row = blockIdx.x;
-    In nxt = load(row);
-    __builtin_amdgcn_s_waitcnt(kWaitVmem0);  // as in the encode kernel
-    for (; row < A.tokens; row += gridDim.x) {
-        const In in = nxt;
-        nxt = load(row + gridDim.x);
+    // One row: outliers of this chunk (lane i < k holds entry i) take R~ +
+    // value, R~ formed from the channel's ref value and coefficient pair.
+    // These are gathered first (just read by the owning lanes, so the reads
+    // hit in cache), then the next-but-one row is prefetched into `nx`, so
+    // waiting for the gathers does not wait for the prefetch.
+    auto row_body = [&](const In& in, uint32_t row, In& nx, uint32_t nrow) {
+        const uint32_t ech = in.ent & 0xFFFFu;
+        const bool pch = OUTL & (lane < (uint32_t)k) & (ech < (uint32_t)d) & ((ech >> 9) == (uint32_t)w);
+        uint32_t gref = 0u, gcf = 0u;
+        if constexpr (OUTL) {
+            gref = bload16(rsrc(A.ref, (uint64_t)row * (uint64_t)d, A.ref ? (uint32_t)d * 2u : 0u), pch ? ech * 2u : kOut);
+            gcf = bload32(rsrc(A.coef, (uint64_t)row * nga, nga * 4u), pch ? (ech >> A.lg_a) * 4u : kOut);
+        }
+        nx = load(nrow);
         const float a = f16_value(in.cf & 0xFFFFu), b0 = f16_value(in.cf >> 16);
         const float s = f16_value(in.sh);
-        float r[8], rt[8], H[8];
+        float r[8], H[8];
         widen8(in.rv, r);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            rt[j] = __builtin_fmaf(a, r[j], b0);
-            H[j] = __builtin_fmaf((float)code_at<BITS>(in.lo, in.hi, j), s, rt[j]);  // R~ + q*s, q*s exact
+        for (int j = 0; j < 8; ++j)  // R~ + q*s, q*s exact
+            H[j] = __builtin_fmaf((float)code_at<BITS>(in.lo, in.hi, j), s, __builtin_fmaf(a, r[j], b0));
+        float4* st = XT + w * kSlice;
+        put8(st, lane, H);
+        wave_lds_sync();
+        if (pch) {
+            const float rt = __builtin_fmaf(f16_value(gcf & 0xFFFFu), bf16_lo(gref), f16_value(gcf >> 16));
+            reinterpret_cast<float*>(st)[slice_float(ech & (uint32_t)(kChunk - 1))] = rt + f16_value(in.ent >> 16);
         }
-        // Outliers of this chunk replace the dense value at their channel.
-        // Lane i holds entry i; only the entries inside this wavefront's
-        // chunk are visited (about k / chunks of them).
-        const uint32_t ech = in.ent & 0xFFFFu;
-        uint64_t mine = ballot(lane < (uint32_t)k && ech < (uint32_t)d && (ech >> 9) == (uint32_t)w);
-        while (mine) {
-            const uint32_t en = rdlane(in.ent, (int)__builtin_ctzll(mine));
-            mine &= mine - 1u;
-            const uint32_t c = en & 0xFFFFu;
-            const uint32_t owner = (c % kChunk) / 8u, jj = c % 8u;
-            const float v = f16_value(en >> 16);
-            if (lane == owner) {
-#pragma unroll
-                for (int j = 0; j < 8; ++j)
-                    if ((uint32_t)j == jj) H[j] = rt[j] + v;
-            }
-        }
-        store_xhat_t(xhat_row(A, row), A.xhat_bf16 != 0, (uint32_t)(w * kChunk), lane, XT + w * kSlice, H);
+        wave_lds_sync();
+        emit_xhat_flat(xhat_row(A, row), BF16, (uint32_t)(w * kChunk), lane, st);
+    };
+
+    // Rows in strides of the grid, two per iteration through two input
+    // buffers (p holds the row being processed while q loads the next one, then
+    // the roles swap), so no prefetched register is copied and nothing waits
+    // for a prefetch before its row starts.
+    const uint32_t G = gridDim.x;
+    uint32_t row = blockIdx.x;
+    In p = load(row), q;
+    // (a store that the range check drops, so that stores are outstanding at
+    // the loop entry as at the end of every row; the compiler's wait analysis
+    // then keeps later waits exact instead of waiting for everything)
+    bstore32(rsrc(A.coef, 0, 0u), kOut, 0u);
+    for (; row < A.tokens; row += 2u * G) {
+        row_body(p, row, q, row + G);
+        if (row + G >= A.tokens) break;
+        row_body(q, row + G, p, row + 2u * G);
     }
 }
 
@@ -1632,13 +1670,20 @@ KernelFn pick_rows(const Args& A, int bits) {
     return rows_for<-1, -1>(bits);
 }
 
-KernelFn pick_decode(int bits) {
+template <bool OUTL, bool BF16>
+KernelFn decode_for(int bits) {
     switch (bits) {
-        case 2: return rac_decode_kernel<2>;
-        case 3: return rac_decode_kernel<3>;
-        case 4: return rac_decode_kernel<4>;
-        default: return rac_decode_kernel<8>;
+        case 2: return rac_decode_kernel<2, OUTL, BF16>;
+        case 3: return rac_decode_kernel<3, OUTL, BF16>;
+        case 4: return rac_decode_kernel<4, OUTL, BF16>;
+        default: return rac_decode_kernel<8, OUTL, BF16>;
     }
+}
+
+KernelFn pick_decode(const Args& A, int bits) {
+    const bool outl = A.k > 0, bf16 = A.xhat_bf16 != 0;
+    if (outl) return bf16 ? decode_for<true, true>(bits) : decode_for<true, false>(bits);
+    return bf16 ? decode_for<false, true>(bits) : decode_for<false, false>(bits);
 }
 
 // One workgroup per token row.  Large row counts use a grid of as many
@@ -1691,7 +1736,7 @@ rac_status run_decode(const rac_config* cfg, const void* wire, const void* ref, 
     A.ref = static_cast<const uint16_t*>(ref);
     A.steps = steps;
     A.xhat = xhat;
-    return launch(pick_decode(cfg->bits), A, stream);
+    return launch(pick_decode(A, cfg->bits), A, stream);
 }
 
 }  // namespace
