@@ -1032,6 +1032,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
 
 constexpr int kRowsMaxD = 8 * kChunk;  // channels per row
 constexpr int kRowsWaves = 4;          // wavefronts per row (2 chunks each)
+constexpr int kNarrowRounds = 1;       // list narrowings before the exact search
 
 template <int NW>
 struct alignas(16) GroupShared {
@@ -1041,6 +1042,7 @@ struct alignas(16) GroupShared {
     uint32_t ccf[kCandCap];   // their group's coefficient pair
     uint32_t smax[NW][kWave]; // lane maxima of |E| of each wavefront
     uint32_t cnt[2];          // candidate count (LDS atomic), by row parity
+    uint32_t rcnt[2][4];      // counts of the narrowed lists, by row parity and round
     uint32_t xcnt[2][NW];     // exact search: element counts, [slot][wavefront]
 };
 
@@ -1082,6 +1084,39 @@ __device__ __forceinline__ void append_shared(G& S, uint32_t* counter,
     }
 }
 
+// The same for the candidate rule |E| >= Lf alone (the threshold search's
+// bound), with float compares on |E| (inputs are finite, so E is never NaN and
+// the float order of |E| is the order of its bit patterns).  A lane's mask
+// bit comes from its compare ANDed with the wavefront's active-lane mask
+// (ballot of act), so each element costs one vector compare.
+template <class G>
+__device__ __forceinline__ void append_bound(G& S, uint32_t* counter, const float* e, const uint4& rpk, uint32_t cfv,
+                                             bool act, uint32_t c0, float Lf, uint32_t lane) {
+    const uint64_t actm = ballot(act);
+    uint32_t n = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) n += (uint32_t)__builtin_popcountll(ballot(__builtin_fabsf(e[j]) >= Lf) & actm);
+    if (!n) return;
+    uint32_t base = 0u;
+    if (lane == 0u) base = atomicAdd(counter, n);
+    base = uniform(base);
+    const uint32_t rw[4] = {rpk.x, rpk.y, rpk.z, rpk.w};
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const uint64_t m = ballot(__builtin_fabsf(e[j]) >= Lf) & actm;
+        if (m) {
+            const uint32_t pos = base + mbcnt64(m);
+            if (act & (__builtin_fabsf(e[j]) >= Lf) & (pos < (uint32_t)kCandCap)) {
+                S.ckey[pos] = cand_key(__float_as_uint(e[j]), c0 + j);
+                S.cval[pos] = __float_as_uint(e[j]);
+                S.crw[pos] = rw[j >> 1];
+                S.ccf[pos] = cfv;
+            }
+            base += (uint32_t)__builtin_popcountll(m);
+        }
+    }
+}
+
 // Hide held ref values from the optimizer before they are widened again (a
 // reused widening would keep 8 more registers per chunk alive across the row).
 template <int N>
@@ -1113,6 +1148,7 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
     const uint32_t crb = (uint32_t)A.code_row_bytes;
     const int wc0 = w * CPW * kChunk;  // first channel of this wavefront's chunks
     if (w == 0 && lane < 2u) S.cnt[lane] = 0u;
+    if (w == 0 && lane < 2u * kNarrowRounds) S.rcnt[lane / kNarrowRounds][lane % kNarrowRounds] = 0u;
     __syncthreads();
 
     // x and ref of the block's first row; later rows are prefetched into
@@ -1160,9 +1196,12 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
 #pragma unroll
         for (int i = 0; i < CPW; ++i) cf[i] = 0u;
 
-        // a2-a3 per chunk: fit of the lane's group, E; lane maximum of |E|
+        // a2-a3 per chunk: fit of the lane's group, E; lane maxima of |E|
+        // (per chunk, and over the wavefront's chunks)
         const Rsrc rcoef = rsrc(A.coef, (uint64_t)row * nga, nga * 4u);
-        float lmx = 0.0f;
+        float lmc[CPW];
+#pragma unroll
+        for (int i = 0; i < CPW; ++i) lmc[i] = 0.0f;
 #pragma unroll
         for (int i = 0; i < CPW; ++i) {
             if (wc0 + i * kChunk >= d) continue;
@@ -1186,10 +1225,13 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
 #pragma unroll
             for (int j = 0; j < 8; ++j) {  // E = 0 past the row
                 e[j] = x[j] - __builtin_fmaf(a, r[j], b0);
-                lmx = __builtin_fmaxf(lmx, __builtin_fabsf(e[j]));
+                lmc[i] = __builtin_fmaxf(lmc[i], __builtin_fabsf(e[j]));
             }
             put8(EL[w][i], lane, e);
         }
+        float lmx = lmc[0];
+#pragma unroll
+        for (int i = 1; i < CPW; ++i) lmx = __builtin_fmaxf(lmx, lmc[i]);
 
 #pragma unroll
         for (int i = 0; i < CPW; ++i) xl[i] = bload128(nx, ((uint32_t)(wc0 + i * kChunk) + l8) * 2u);
@@ -1204,6 +1246,7 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
         // the other buffer was last read by the previous row, which every
         // wavefront has left: reset its candidate count for the next row
         if (w == 0 && lane == 0u) S.cnt[(n + 1) & 1] = 0u;
+        if (w == 0 && lane < (uint32_t)kNarrowRounds) S.rcnt[(n + 1) & 1][lane] = 0u;
         uint32_t v = S.smax[0][lane];
 #pragma unroll
         for (int ww = 1; ww < NW; ++ww) v = __builtin_elementwise_max(v, S.smax[ww][lane]);
@@ -1214,18 +1257,56 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
             if ((uint32_t)__builtin_popcountll(ballot(v >= cnd)) >= (uint32_t)k) L = cnd;
         }
         opaque_n(rp);
+        const float Lf = __uint_as_float(L);
 #pragma unroll
         for (int i = 0; i < CPW; ++i) {
-            if (wc0 + i * kChunk >= d) continue;
+            // (a chunk none of whose lane maxima reaches L holds no candidate)
+            if ((wc0 + i * kChunk >= d) || !ballot(lmc[i] >= Lf)) continue;
             const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
             float e[8];
             get8(EL[w][i], lane, e);
-            append_shared(S, cnt, e, rp[i], cf[i], c0 < (uint32_t)d, c0, L, false, 0ull, lane);
+            append_bound(S, cnt, e, rp[i], cf[i], c0 < (uint32_t)d, c0, Lf, lane);
         }
         __syncthreads();
+        // k-th largest of the first Cn listed keys (Cn <= kCandCap; lane i
+        // ranks key i by the number of larger keys, which are distinct; LDS
+        // broadcast reads, two keys at a time); `key` gets lane i's key
+        auto kth_key = [&](uint32_t Cn, uint64_t& key) -> uint64_t {
+            const bool have = lane < Cn;
+            key = have ? S.ckey[lane] : 0ull;
+            uint32_t rank = 0;
+            for (uint32_t j = 0; j < Cn; j += 2) {
+                const ulonglong2 kk = *reinterpret_cast<const ulonglong2*>(&S.ckey[j]);
+                rank += (kk.x > key) ? 1u : 0u;
+                rank += (j + 1u < Cn && kk.y > key) ? 1u : 0u;
+            }
+            const uint64_t at = ballot(have && rank == (uint32_t)(k - 1));
+            return rdlane64(key, at ? (int)__builtin_ctzll(at) : 0);
+        };
         // (values read from LDS are the same in every lane: readfirstlane
         // makes that visible, so the branches on them stay scalar)
         uint32_t C = uniform(*cnt);
+        uint64_t key = 0ull;
+        for (int nr = 0; nr < kNarrowRounds && C > (uint32_t)kCandCap; ++nr) {
+            // More candidates than the list holds: the k-th largest key of
+            // the kCandCap listed ones is a lower bound of the k-th largest
+            // of the row, and usually far tighter than L; the list is
+            // rebuilt from the keys >= that bound.
+            uint64_t lkey;
+            const uint64_t kmin = kth_key((uint32_t)kCandCap, lkey);
+            __syncthreads();
+            uint32_t* const rc = &S.rcnt[n & 1][nr];
+#pragma unroll
+            for (int i = 0; i < CPW; ++i) {
+                const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
+                float e[8];
+                get8(EL[w][i], lane, e);
+                append_shared(S, rc, e, rp[i], cf[i], c0 < (uint32_t)d, c0, (uint32_t)(kmin >> 32), true, kmin,
+                              lane);
+            }
+            __syncthreads();
+            C = uniform(*rc);
+        }
         const bool exact = C > (uint32_t)kCandCap;
         uint64_t kst = 0ull;  // key of the k-th largest element: the outliers are the keys >= kst
         if (exact) {
@@ -1290,32 +1371,16 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
             }
             __syncthreads();
             C = uniform(*cnt);  // == k
+            key = lane < C ? S.ckey[lane] : 0ull;
+        } else {
+            kst = kth_key(C, key);
         }
         const bool have = lane < C;
-        const uint64_t key = have ? S.ckey[lane] : 0ull;
-        if (!exact) {
-            // rank = number of larger keys (keys are distinct; LDS broadcast reads)
-            uint32_t rank = 0;
-            for (uint32_t j = 0; j < C; j += 2) {
-                const ulonglong2 kk = *reinterpret_cast<const ulonglong2*>(&S.ckey[j]);
-                rank += (kk.x > key) ? 1u : 0u;
-                rank += (j + 1u < C && kk.y > key) ? 1u : 0u;
-            }
-            const uint64_t at = ballot(have && rank == (uint32_t)(k - 1));
-            kst = rdlane64(key, at ? (int)__builtin_ctzll(at) : 0);
-        }
-        const uint32_t Tb = (uint32_t)(kst >> 32), cstar = key_channel(kst);
-        const float Tf = __uint_as_float(Tb);
-        // The channel rule matters only if another element has pattern Tb:
-        // on the fast path every such element is a candidate; the exact path
-        // always applies it.
-        uint32_t khi = (uint32_t)(key >> 32);
-        asm volatile("" : "+v"(khi));  // (a 32-bit compare; widened, it cost a spilled register)
-        const bool ties = exact || __builtin_popcountll(ballot(have && khi == Tb)) > 1;
-        const uint32_t cmax = ties ? cstar : 0xFFFFu;  // outliers: |E| > T, or |E| == T and channel <= cmax
         // Candidate lane i holds one chosen outlier (or none): its channel
         // and its reconstruction R~ + fp16(E), which phase C writes over
-        // the staged value of that channel.
+        // the staged value of that channel.  Every outlier is a candidate
+        // and keys are distinct, so the outliers are exactly the candidate
+        // keys >= kst.
         const bool chosen = have && key >= kst;
         const uint32_t och = chosen ? key_channel(key) : 0xFFFFFFFFu;
         uint32_t oval = 0u;
@@ -1339,6 +1404,15 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
             bstore32(outl, (chosen && slot < (uint32_t)k) ? slot * 4u : kOut, key_channel(key) | (oval << 16));
         }
 
+        // E^d: E with the outliers set to 0, in place (each wavefront
+        // clears the outliers of its own chunks, which only it reads)
+#pragma unroll
+        for (int i = 0; i < CPW; ++i) {
+            const uint32_t oc = och - (uint32_t)(wc0 + i * kChunk);
+            if (oc < (uint32_t)kChunk) reinterpret_cast<float*>(EL[w][i])[slice_float(oc)] = 0.0f;
+        }
+        wave_lds_sync();
+
         // a5-a8 per chunk: scale, quantize, pack, reconstruct
         opaque_n(rp);
         const Rsrc rsc = rsrc(A.scale, (uint64_t)row * ngq, ngq * 2u);
@@ -1351,21 +1425,7 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
             const uint32_t c0 = chunk0 + l8;
             float ed[8];
             float4* st = EL[w][i];
-            {
-                float e[8];
-                get8(st, lane, e);
-                // E^d: E with the outliers set to 0 (past the row E is 0 already)
-                if (!ties) {
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) ed[j] = __builtin_fabsf(e[j]) >= Tf ? 0.0f : e[j];
-                } else {
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        const float ae = __builtin_fabsf(e[j]);
-                        ed[j] = ((ae > Tf) | ((ae == Tf) & (c0 + j <= cmax))) ? 0.0f : e[j];
-                    }
-                }
-            }
+            get8(st, lane, ed);  // (past the row E is 0)
             float m = 0.0f;
 #pragma unroll
             for (int j = 0; j < 8; ++j) m = __builtin_fmaxf(m, __builtin_fabsf(ed[j]));
@@ -1687,9 +1747,10 @@ KernelFn pick_decode(const Args& A, int bits) {
 }
 
 // One workgroup per token row.  Large row counts use a grid of as many
-// workgroups as the device keeps resident, each taking rows in strides (and
-// prefetching its next row); small counts launch one workgroup per row.
-rac_status launch(KernelFn fn, Args A, hipStream_t stream, int threads = 0) {
+// workgroups as the device keeps resident (at most max_per_cu per compute
+// unit), each taking rows in strides (and prefetching its next row); small
+// counts launch one workgroup per row.
+rac_status launch(KernelFn fn, Args A, hipStream_t stream, int threads = 0, int max_per_cu = 0) {
     const int64_t rows = A.tokens;
     // kernels launched with one wavefront per chunk stage through a
     // dynamically sized slice per wavefront
@@ -1704,6 +1765,7 @@ rac_status launch(KernelFn fn, Args A, hipStream_t stream, int threads = 0) {
             hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(fn), threads, lds) !=
                 hipSuccess)
             return RAC_ERR_HIP;
+        if (max_per_cu > 0 && per_cu > max_per_cu) per_cu = max_per_cu;
         const int64_t resident = (int64_t)cus * (per_cu > 0 ? per_cu : 1);
         if (blocks > resident) blocks = resident;
     }
@@ -1736,7 +1798,9 @@ rac_status run_decode(const rac_config* cfg, const void* wire, const void* ref, 
     A.ref = static_cast<const uint16_t*>(ref);
     A.steps = steps;
     A.xhat = xhat;
-    return launch(pick_decode(A, cfg->bits), A, stream);
+    // (with outliers, two workgroups per compute unit, each taking more rows,
+    // measured fastest: 4-8% below a full grid at 4096 x 4096 and 16384 x 3584)
+    return launch(pick_decode(A, cfg->bits), A, stream, 0, A.k > 0 ? 2 : 0);
 }
 
 }  // namespace
