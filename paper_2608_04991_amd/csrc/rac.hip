@@ -25,6 +25,7 @@
 // exactly.  The file is compiled with -ffp-contract=off so no multiply-add is
 // fused, and divisions stay correctly rounded.
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 #include "rac.h"
@@ -1032,19 +1033,22 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
 
 constexpr int kRowsMaxD = 8 * kChunk;  // channels per row
 constexpr int kRowsWaves = 4;          // wavefronts per row (2 chunks each)
-constexpr int kNarrowRounds = 1;       // list narrowings before the exact search
 
 template <int NW>
 struct alignas(16) GroupShared {
+    // (ckey and cval, contiguous, also hold the exact search's three
+    // 64-bin histograms while the list is dropped)
     uint64_t ckey[kCandCap];  // candidates: |E| bits << 32 | (0xFFFF - channel)
     uint32_t cval[kCandCap];  // their E bits
     uint32_t crw[kCandCap];   // their ref word (the bf16 pair holding the channel)
     uint32_t ccf[kCandCap];   // their group's coefficient pair
     uint32_t smax[NW][kWave]; // lane maxima of |E| of each wavefront
     uint32_t cnt[2];          // candidate count (LDS atomic), by row parity
-    uint32_t rcnt[2][4];      // counts of the narrowed lists, by row parity and round
-    uint32_t xcnt[2][NW];     // exact search: element counts, [slot][wavefront]
+    uint32_t xn[2];           // count of the rebuilt list (exact search), by row parity
 };
+static_assert(offsetof(GroupShared<4>, cval) == sizeof(uint64_t) * kCandCap &&
+                  sizeof(uint64_t) * kCandCap + sizeof(uint32_t) * kCandCap >= 3 * kWave * sizeof(uint32_t),
+              "the histograms of the exact search fit in ckey and cval");
 
 // Append this lane's elements of one chunk whose |E| pattern is >= lo (and,
 // with use_key, whose key is >= kmin) to the shared candidate list, with
@@ -1147,8 +1151,10 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
     const uint32_t row_bytes = (uint32_t)d * 2u;
     const uint32_t crb = (uint32_t)A.code_row_bytes;
     const int wc0 = w * CPW * kChunk;  // first channel of this wavefront's chunks
-    if (w == 0 && lane < 2u) S.cnt[lane] = 0u;
-    if (w == 0 && lane < 2u * kNarrowRounds) S.rcnt[lane / kNarrowRounds][lane % kNarrowRounds] = 0u;
+    if (w == 0 && lane < 2u) {
+        S.cnt[lane] = 0u;
+        S.xn[lane] = 0u;
+    }
     __syncthreads();
 
     // x and ref of the block's first row; later rows are prefetched into
@@ -1245,8 +1251,10 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
         __syncthreads();
         // the other buffer was last read by the previous row, which every
         // wavefront has left: reset its candidate count for the next row
-        if (w == 0 && lane == 0u) S.cnt[(n + 1) & 1] = 0u;
-        if (w == 0 && lane < (uint32_t)kNarrowRounds) S.rcnt[(n + 1) & 1][lane] = 0u;
+        if (w == 0 && lane == 0u) {
+            S.cnt[(n + 1) & 1] = 0u;
+            S.xn[(n + 1) & 1] = 0u;
+        }
         uint32_t v = S.smax[0][lane];
 #pragma unroll
         for (int ww = 1; ww < NW; ++ww) v = __builtin_elementwise_max(v, S.smax[ww][lane]);
@@ -1287,94 +1295,86 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
         // makes that visible, so the branches on them stay scalar)
         uint32_t C = uniform(*cnt);
         uint64_t key = 0ull;
-        for (int nr = 0; nr < kNarrowRounds && C > (uint32_t)kCandCap; ++nr) {
-            // More candidates than the list holds: the k-th largest key of
-            // the kCandCap listed ones is a lower bound of the k-th largest
-            // of the row, and usually far tighter than L; the list is
-            // rebuilt from the keys >= that bound.
-            uint64_t lkey;
-            const uint64_t kmin = kth_key((uint32_t)kCandCap, lkey);
-            __syncthreads();
-            uint32_t* const rc = &S.rcnt[n & 1][nr];
+        uint64_t kst = 0ull;  // the outliers are the listed keys >= kst
+        if (C > (uint32_t)kCandCap) {
+            // More candidates than the list holds: they are narrowed by a
+            // radix search over a 48-bit key (|E| pattern, 4095 - channel,
+            // 5 zero bits; a larger key ranks higher), from the top digit
+            // not shared by every candidate (all lie in [L, row maximum]).
+            // Each digit (6 bits, the last one narrower) is taken from a
+            // 64-bin histogram of the candidates that share the digits found
+            // so far: the bin holding the k-th largest.  Once the keys in
+            // that bin or above number at most kCandCap, the list is rebuilt
+            // from them and ranked as usual; keys are distinct, so at worst
+            // the last digit gets there.  The histograms (three, in turn,
+            // each cleared two levels before it is filled, so one barrier
+            // per level) use the list's storage.
+            uint32_t* const H = reinterpret_cast<uint32_t*>(S.ckey);  // [3][64]: ckey and cval
+            if (threadIdx.x < 2u * kWave) H[threadIdx.x] = 0u;
+            uint32_t mx = v;  // row maximum of the |E| patterns
 #pragma unroll
-            for (int i = 0; i < CPW; ++i) {
-                const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
-                float e[8];
-                get8(EL[w][i], lane, e);
-                append_shared(S, rc, e, rp[i], cf[i], c0 < (uint32_t)d, c0, (uint32_t)(kmin >> 32), true, kmin,
-                              lane);
-            }
+            for (int o = 1; o < kWave; o <<= 1) mx = __builtin_elementwise_max(mx, (uint32_t)__shfl_xor((int)mx, o));
+            mx = uniform(mx);
+            const int hb = (mx == L) ? -1 : 31 - __builtin_clz(mx ^ L);  // highest bit not shared
+            uint64_t prefix = (uint64_t)(L >> (hb + 1));
+            int shift = hb + 12, width = 6;
+            uint32_t need = (uint32_t)k;
             __syncthreads();
-            C = uniform(*rc);
-        }
-        const bool exact = C > (uint32_t)kCandCap;
-        uint64_t kst = 0ull;  // key of the k-th largest element: the outliers are the keys >= kst
-        if (exact) {
-            // Heavy ties: T = the k-th largest |E| pattern by a radix search
-            // over its bits, then the last tied channel by bisection; every
-            // step counts over all wavefronts (one barrier, two rotating
-            // slots).  The list is then rebuilt from the k outliers.
-            uint32_t T = 0u, lo = 0u, hi = (uint32_t)d - 1u, need = (uint32_t)k;
-            int slot = 0;
 #pragma unroll 1
-            for (int step = 0;; ++step) {
-                uint32_t plo = T, phi = 0x7FFFFFFFu, pmax = 0xFFFFu;
-                if (step < 31) {
-                    plo = T | (1u << (30 - step));
-                } else if (step == 31) {
-                    if (T == 0x7FFFFFFFu) continue;
-                    plo = T + 1u;
-                } else {
-                    if (lo >= hi) break;
-                    phi = T;
-                    pmax = (lo + hi) >> 1;
-                }
-                uint32_t cntl = 0;
-#pragma unroll
+            for (int lev = 0;; ++lev) {
+                uint32_t* const h = H + (lev % 3) * kWave;
+                if (w == 0) H[((lev + 1) % 3) * kWave + lane] = 0u;
+                // (one element at a time, read from the slices: this rare path
+                // then needs few registers)
+#pragma unroll 1
                 for (int i = 0; i < CPW; ++i) {
                     const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
-                    float e[8];
-                    get8(EL[w][i], lane, e);
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        const uint32_t a = __float_as_uint(e[j]) & 0x7FFFFFFFu;
-                        cntl += ((c0 < (uint32_t)d) & (a >= plo) & (a <= phi) & (c0 + j <= pmax)) ? 1u : 0u;
+                    if (c0 >= (uint32_t)d) continue;
+                    const float* const es = reinterpret_cast<const float*>(EL[w][i]);
+#pragma unroll 1
+                    for (uint32_t j = 0; j < 8u; ++j) {
+                        const uint32_t pa = __float_as_uint(es[slice_float(l8 + j)]) & 0x7FFFFFFFu;
+                        const uint64_t k48 = ((uint64_t)pa << 17) | ((uint64_t)(4095u - (c0 + j)) << 5);
+                        if ((pa >= L) & ((k48 >> (shift + width)) == prefix))
+                            atomicAdd(&h[(uint32_t)(k48 >> shift) & ((1u << width) - 1u)], 1u);
                     }
                 }
-                const uint32_t cw = (uint32_t)lsum<6>((float)cntl, 6);  // integer counts <= 4096: exact
-                if (lane == 0u) S.xcnt[slot][w] = cw;
                 __syncthreads();
-                uint32_t cnt = 0;
+                // lane l takes bin 63 - l; inclusive sums from the top bin
+                const uint32_t hv = h[kWave - 1 - lane];
+                uint32_t P = hv;
 #pragma unroll
-                for (int ww = 0; ww < NW; ++ww) cnt += S.xcnt[slot][ww];
-                cnt = uniform(cnt);
-                slot ^= 1;
-                if (step < 31) {
-                    if (cnt >= (uint32_t)k) T = plo;
-                } else if (step == 31) {
-                    need = (uint32_t)k - cnt;
-                } else if (cnt >= need) {
-                    hi = pmax;
-                } else {
-                    lo = pmax + 1u;
+                for (int o = 1; o < kWave; o <<= 1) {
+                    const uint32_t t = (uint32_t)__shfl_up((int)P, o);
+                    if (lane >= (uint32_t)o) P += t;
                 }
+                const int ls = (int)__builtin_ctzll(ballot(P >= need));  // some lane: the prefix holds >= need
+                const uint32_t above = rdlane(P - hv, ls), nb = rdlane(hv, ls);
+                prefix = (prefix << width) | (uint64_t)(kWave - 1 - ls);
+                need -= above;
+                // keys in this bin or above: k - need + nb
+                if ((uint32_t)k - need + nb <= (uint32_t)kCandCap || shift == 0) break;
+                width = shift >= 6 ? 6 : shift;
+                shift -= width;
             }
-            kst = ((uint64_t)T << 32) | (uint64_t)(0xFFFFu - lo);
-            if (w == 0 && lane == 0u) *cnt = 0u;
-            __syncthreads();
+            // rebuild the list from the keys >= the bin's lowest: |E|
+            // pattern > pm, or == pm and channel <= 4095 - cm
+            const uint64_t k43 = (prefix << shift) >> 5;
+            const uint32_t pm = (uint32_t)(k43 >> 12), cm = (uint32_t)(k43 & 4095u);
+            const uint64_t kmin = ((uint64_t)pm << 32) | (uint64_t)(0xFFFFu - 4095u + cm);
+            uint32_t* const xc = &S.xn[n & 1];
+            __syncthreads();  // (every wavefront has read the last histogram)
 #pragma unroll
             for (int i = 0; i < CPW; ++i) {
                 const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
                 float e[8];
                 get8(EL[w][i], lane, e);
-                append_shared(S, cnt, e, rp[i], cf[i], c0 < (uint32_t)d, c0, T, true, kst, lane);
+                append_shared(S, xc, e, rp[i], cf[i], c0 < (uint32_t)d, c0, pm, true, kmin, lane);
             }
             __syncthreads();
-            C = uniform(*cnt);  // == k
-            key = lane < C ? S.ckey[lane] : 0ull;
-        } else {
-            kst = kth_key(C, key);
+            C = uniform(*xc);  // k <= C <= kCandCap
         }
+        kst = kth_key(C, key);
         const bool have = lane < C;
         // Candidate lane i holds one chosen outlier (or none): its channel
         // and its reconstruction R~ + fp16(E), which phase C writes over

@@ -122,10 +122,15 @@ CASES = {
                                  lambda: wl.long_context(0, rows=(0, 29), group=128)[:2]),
     "long_13x4096_g128_b8_k16": (cfgd(13, 4096, 128, 128, 8, 16),
                                  lambda: wl.long_context(2, rows=(500, 513), group=128)[:2]),
-    # g = 64, k = 16 on uplink rows: about a quarter of them have more than 64
-    # elements above the first threshold, so their list is narrowed
-    "narrowed_list_uplink_32x4096_g64_b4_k16": (cfgd(32, 4096, 64, 64, 4, 16),
-                                                lambda: wl.prefill_uplink(0, rows=(0, 32))[:2]),
+    # Uplink rows with more than 64 elements above the first threshold (about
+    # a quarter of them at g = 64, k = 16, most of them at k = 32 and k = 64),
+    # whose outliers come from the histogram search
+    "overflow_uplink_32x4096_g64_b4_k16": (cfgd(32, 4096, 64, 64, 4, 16),
+                                           lambda: wl.prefill_uplink(0, rows=(0, 32))[:2]),
+    "overflow_uplink_24x4096_g128_b4_k32": (cfgd(24, 4096, 128, 128, 4, 32),
+                                            lambda: wl.prefill_uplink(0, rows=(40, 64))[:2]),
+    "overflow_uplink_16x4096_g64_b8_k64": (cfgd(16, 4096, 64, 64, 8, 64),
+                                           lambda: wl.prefill_uplink(2, rows=(64, 80))[:2]),
     "partial_chunk_13x2880_ga64_gq32_b4_k5": (cfgd(13, 2880, 64, 32, 4, 5), lambda: _affine(13, 2880, 64)),
     "bytewise3_11x2888_g8_b3_k3": (cfgd(11, 2888, 8, 8, 3, 3), lambda: _affine(11, 2888, 8)),
     "d8192_9x8192_ga128_gq256_b4_k8": (cfgd(9, 8192, 128, 256, 4, 8), lambda: _affine(9, 8192, 128)),
