@@ -131,6 +131,12 @@ CASES = {
                                             lambda: wl.prefill_uplink(0, rows=(40, 64))[:2]),
     "overflow_uplink_16x4096_g64_b8_k64": (cfgd(16, 4096, 64, 64, 8, 64),
                                            lambda: wl.prefill_uplink(2, rows=(64, 80))[:2]),
+    # rows of 4097..8192 channels (the one-wavefront-per-chunk kernel)
+    "wide_uplink_12x8192_g128_b4_k16": (cfgd(12, 8192, 128, 128, 4, 16),
+                                        lambda: wl.prefill_uplink(0, rows=(0, 12), hidden=8192)[:2]),
+    "wide_overflow_8x8192_g64_b4_k64": (cfgd(8, 8192, 64, 64, 4, 64),
+                                        lambda: wl.prefill_uplink(3, rows=(20, 28), hidden=8192)[:2]),
+    "wide_partial_chunk_7x4864_g256_b3_k6": (cfgd(7, 4864, 256, 256, 3, 6), lambda: _affine(7, 4864, 256)),
     "partial_chunk_13x2880_ga64_gq32_b4_k5": (cfgd(13, 2880, 64, 32, 4, 5), lambda: _affine(13, 2880, 64)),
     "bytewise3_11x2888_g8_b3_k3": (cfgd(11, 2888, 8, 8, 3, 3), lambda: _affine(11, 2888, 8)),
     "d8192_9x8192_ga128_gq256_b4_k8": (cfgd(9, 8192, 128, 256, 4, 8), lambda: _affine(9, 8192, 128)),
