@@ -1020,19 +1020,21 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
 
 // ---------------------------------------------------------------------------
 // Encode with per-token outliers, NW wavefronts per token row.  For rows of
-// at most 4096 channels whose groups lie inside a chunk, a workgroup of NW
-// wavefronts owns one token row at a time and wavefront w holds the CPW =
-// 8 / NW chunks [CPW w, CPW w + CPW): lane l keeps ref (as loaded) and the
+// at most NW * CPW * 512 channels whose groups lie inside a chunk, a
+// workgroup of NW wavefronts owns one token row at a time and wavefront w
+// holds the CPW chunks [CPW w, CPW w + CPW): lane l keeps ref (as loaded) and the
 // coefficient pair of channels [512c + 8l, 512c + 8l + 8) of its chunks in
 // registers and their E in LDS, where the chunk's reconstruction is later
 // staged for the store.  Keeping E out of registers leaves room to prefetch
 // the next row (x once the fit is done, each ref chunk once its R~ is
-// formed) at seven wavefronts per SIMD.  The per-token outlier choice costs
+// formed) at seven (CPW = 2) or five (CPW = 4) wavefronts per SIMD.  The
+// per-token outlier choice costs
 // two barriers between NW wavefronts, and its threshold search and ranking
 // run NW times per row instead of once per chunk.
 
-constexpr int kRowsMaxD = 8 * kChunk;  // channels per row
-constexpr int kRowsWaves = 4;          // wavefronts per row (2 chunks each)
+constexpr int kRowsWaves = 4;               // wavefronts per row
+constexpr int kRowsMaxD = 16 * kChunk;       // channels per row (4 chunks per wavefront)
+constexpr int kKeyChBits = 13;               // channel bits of the exact search's key (d <= 8192)
 
 template <int NW>
 struct alignas(16) GroupShared {
@@ -1129,9 +1131,9 @@ __device__ __forceinline__ void opaque_n(uint4 (&r)[N]) {
     for (int i = 0; i < N; ++i) asm volatile("" : "+v"(r[i].x), "+v"(r[i].y), "+v"(r[i].z), "+v"(r[i].w));
 }
 
-template <int BITS, int GA, int GQ, int NW>
-__global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7))) void rac_encode_rows_kernel(Args A) {
-    constexpr int CPW = 8 / NW;  // chunks per wavefront
+template <int BITS, int GA, int GQ, int NW, int CPW>
+__global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(CPW == 2 ? 7 : 5)))
+void rac_encode_rows_kernel(Args A) {
     // (a row's lists are read before the next row's first barrier and
     // written after it; only the count is reset early, so it alternates)
     __shared__ GroupShared<NW> S;
@@ -1298,7 +1300,7 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
         uint64_t kst = 0ull;  // the outliers are the listed keys >= kst
         if (C > (uint32_t)kCandCap) {
             // More candidates than the list holds: they are narrowed by a
-            // radix search over a 48-bit key (|E| pattern, 4095 - channel,
+            // radix search over a 49-bit key (|E| pattern, 8191 - channel,
             // 5 zero bits; a larger key ranks higher), from the top digit
             // not shared by every candidate (all lie in [L, row maximum]).
             // Each digit (6 bits, the last one narrower) is taken from a
@@ -1317,7 +1319,8 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
             mx = uniform(mx);
             const int hb = (mx == L) ? -1 : 31 - __builtin_clz(mx ^ L);  // highest bit not shared
             uint64_t prefix = (uint64_t)(L >> (hb + 1));
-            int shift = hb + 12, width = 6;
+            constexpr uint32_t kChMax = (1u << kKeyChBits) - 1u;
+            int shift = hb + kKeyChBits, width = 6;  // the digit just below the shared bits
             uint32_t need = (uint32_t)k;
             __syncthreads();
 #pragma unroll 1
@@ -1334,9 +1337,9 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
 #pragma unroll 1
                     for (uint32_t j = 0; j < 8u; ++j) {
                         const uint32_t pa = __float_as_uint(es[slice_float(l8 + j)]) & 0x7FFFFFFFu;
-                        const uint64_t k48 = ((uint64_t)pa << 17) | ((uint64_t)(4095u - (c0 + j)) << 5);
-                        if ((pa >= L) & ((k48 >> (shift + width)) == prefix))
-                            atomicAdd(&h[(uint32_t)(k48 >> shift) & ((1u << width) - 1u)], 1u);
+                        const uint64_t key = ((uint64_t)pa << (kKeyChBits + 5)) | ((uint64_t)(kChMax - (c0 + j)) << 5);
+                        if ((pa >= L) & ((key >> (shift + width)) == prefix))
+                            atomicAdd(&h[(uint32_t)(key >> shift) & ((1u << width) - 1u)], 1u);
                     }
                 }
                 __syncthreads();
@@ -1358,10 +1361,10 @@ __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(7)))
                 shift -= width;
             }
             // rebuild the list from the keys >= the bin's lowest: |E|
-            // pattern > pm, or == pm and channel <= 4095 - cm
-            const uint64_t k43 = (prefix << shift) >> 5;
-            const uint32_t pm = (uint32_t)(k43 >> 12), cm = (uint32_t)(k43 & 4095u);
-            const uint64_t kmin = ((uint64_t)pm << 32) | (uint64_t)(0xFFFFu - 4095u + cm);
+            // pattern > pm, or == pm and channel <= kChMax - cm
+            const uint64_t kl = (prefix << shift) >> 5;
+            const uint32_t pm = (uint32_t)(kl >> kKeyChBits), cm = (uint32_t)(kl & kChMax);
+            const uint64_t kmin = ((uint64_t)pm << 32) | (uint64_t)(0xFFFFu - kChMax + cm);
             uint32_t* const xc = &S.xn[n & 1];
             __syncthreads();  // (every wavefront has read the last histogram)
 #pragma unroll
@@ -1707,14 +1710,20 @@ KernelFn pick_encode(const Args& A, int bits) {
     return encode_for<-1, -1>(bits, outl);
 }
 
-template <int GA, int GQ>
-KernelFn rows_for(int bits) {
+template <int GA, int GQ, int CPW>
+KernelFn rows_for_bits(int bits) {
     switch (bits) {
-        case 2: return rac_encode_rows_kernel<2, GA, GQ, kRowsWaves>;
-        case 3: return rac_encode_rows_kernel<3, GA, GQ, kRowsWaves>;
-        case 4: return rac_encode_rows_kernel<4, GA, GQ, kRowsWaves>;
-        default: return rac_encode_rows_kernel<8, GA, GQ, kRowsWaves>;
+        case 2: return rac_encode_rows_kernel<2, GA, GQ, kRowsWaves, CPW>;
+        case 3: return rac_encode_rows_kernel<3, GA, GQ, kRowsWaves, CPW>;
+        case 4: return rac_encode_rows_kernel<4, GA, GQ, kRowsWaves, CPW>;
+        default: return rac_encode_rows_kernel<8, GA, GQ, kRowsWaves, CPW>;
     }
+}
+
+// Rows of up to 4096 channels: two chunks per wavefront; up to 8192: four.
+template <int GA, int GQ>
+KernelFn rows_for(int bits, int d) {
+    return d <= kRowsWaves * 2 * kChunk ? rows_for_bits<GA, GQ, 2>(bits) : rows_for_bits<GA, GQ, 4>(bits);
 }
 
 // Rows with outliers take the NW-wavefront kernel when it holds the whole
@@ -1725,9 +1734,9 @@ bool use_rows_kernel(const Args& A) {
 }
 
 KernelFn pick_rows(const Args& A, int bits) {
-    if (A.lane_lv_a == 3 && A.lane_lv_q == 3) return rows_for<3, 3>(bits);
-    if (A.lane_lv_a == 4 && A.lane_lv_q == 4) return rows_for<4, 4>(bits);
-    return rows_for<-1, -1>(bits);
+    if (A.lane_lv_a == 3 && A.lane_lv_q == 3) return rows_for<3, 3>(bits, A.d);
+    if (A.lane_lv_a == 4 && A.lane_lv_q == 4) return rows_for<4, 4>(bits, A.d);
+    return rows_for<-1, -1>(bits, A.d);
 }
 
 template <bool OUTL, bool BF16>
