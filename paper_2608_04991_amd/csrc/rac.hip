@@ -1022,7 +1022,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
 // Encode with per-token outliers, NW wavefronts per token row.  For rows of
 // at most NW * CPW * 512 channels whose groups lie inside a chunk, a
 // workgroup of NW wavefronts owns one token row at a time and wavefront w
-// holds the CPW chunks [CPW w, CPW w + CPW): lane l keeps ref (as loaded) and the
+// holds the CPW chunks w, w + NW, ...: lane l keeps ref (as loaded) and the
 // coefficient pair of channels [512c + 8l, 512c + 8l + 8) of its chunks in
 // registers and their E in LDS, where the chunk's reconstruction is later
 // staged for the store.  Keeping E out of registers leaves room to prefetch
@@ -1132,7 +1132,7 @@ __device__ __forceinline__ void opaque_n(uint4 (&r)[N]) {
 }
 
 template <int BITS, int GA, int GQ, int NW, int CPW>
-__global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(CPW == 2 ? 7 : 5)))
+__global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(CPW == 2 ? 7 : 4)))
 void rac_encode_rows_kernel(Args A) {
     // (a row's lists are read before the next row's first barrier and
     // written after it; only the count is reset early, so it alternates)
@@ -1152,7 +1152,9 @@ void rac_encode_rows_kernel(Args A) {
     const uint32_t ngq = (uint32_t)d >> A.lg_q, nga = (uint32_t)d >> A.lg_a;
     const uint32_t row_bytes = (uint32_t)d * 2u;
     const uint32_t crb = (uint32_t)A.code_row_bytes;
-    const int wc0 = w * CPW * kChunk;  // first channel of this wavefront's chunks
+    // first channel of the wavefront's i-th chunk: chunks are dealt round the
+    // wavefronts, so a row of fewer than NW * CPW chunks stays balanced
+    auto chunk_at = [&](int i) { return (w + i * NW) * kChunk; };
     if (w == 0 && lane < 2u) {
         S.cnt[lane] = 0u;
         S.xn[lane] = 0u;
@@ -1170,7 +1172,7 @@ void rac_encode_rows_kernel(Args A) {
         const Rsrc rx = rsrc(A.x, o, any ? row_bytes : 0u), rr = rsrc(A.ref, o, (A.ref && any) ? row_bytes : 0u);
 #pragma unroll
         for (int i = 0; i < CPW; ++i) {
-            const uint32_t off = ((uint32_t)(wc0 + i * kChunk) + lane * 8u) * 2u;  // past the row: reads 0
+            const uint32_t off = ((uint32_t)(chunk_at(i)) + lane * 8u) * 2u;  // past the row: reads 0
             xl[i] = bload128(rx, off);
             rp[i] = bload128(rr, off);
         }
@@ -1212,8 +1214,8 @@ void rac_encode_rows_kernel(Args A) {
         for (int i = 0; i < CPW; ++i) lmc[i] = 0.0f;
 #pragma unroll
         for (int i = 0; i < CPW; ++i) {
-            if (wc0 + i * kChunk >= d) continue;
-            const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
+            if (chunk_at(i) >= d) continue;
+            const uint32_t c0 = (uint32_t)(chunk_at(i)) + l8;
             float r[8], x[8], uu[8], uv[8];
             widen8(rp[i], r);
             widen8(xl[i], x);
@@ -1242,7 +1244,7 @@ void rac_encode_rows_kernel(Args A) {
         for (int i = 1; i < CPW; ++i) lmx = __builtin_fmaxf(lmx, lmc[i]);
 
 #pragma unroll
-        for (int i = 0; i < CPW; ++i) xl[i] = bload128(nx, ((uint32_t)(wc0 + i * kChunk) + l8) * 2u);
+        for (int i = 0; i < CPW; ++i) xl[i] = bload128(nx, ((uint32_t)(chunk_at(i)) + l8) * 2u);
 
         // a4: the k largest |E| of the row (ties to the lower channel).
         // Threshold L: the k-th largest of the 64 maxima of |E| over lane l
@@ -1271,8 +1273,8 @@ void rac_encode_rows_kernel(Args A) {
 #pragma unroll
         for (int i = 0; i < CPW; ++i) {
             // (a chunk none of whose lane maxima reaches L holds no candidate)
-            if ((wc0 + i * kChunk >= d) || !ballot(lmc[i] >= Lf)) continue;
-            const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
+            if ((chunk_at(i) >= d) || !ballot(lmc[i] >= Lf)) continue;
+            const uint32_t c0 = (uint32_t)(chunk_at(i)) + l8;
             float e[8];
             get8(EL[w][i], lane, e);
             append_bound(S, cnt, e, rp[i], cf[i], c0 < (uint32_t)d, c0, Lf, lane);
@@ -1331,7 +1333,7 @@ void rac_encode_rows_kernel(Args A) {
                 // then needs few registers)
 #pragma unroll 1
                 for (int i = 0; i < CPW; ++i) {
-                    const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
+                    const uint32_t c0 = (uint32_t)(chunk_at(i)) + l8;
                     if (c0 >= (uint32_t)d) continue;
                     const float* const es = reinterpret_cast<const float*>(EL[w][i]);
 #pragma unroll 1
@@ -1369,7 +1371,7 @@ void rac_encode_rows_kernel(Args A) {
             __syncthreads();  // (every wavefront has read the last histogram)
 #pragma unroll
             for (int i = 0; i < CPW; ++i) {
-                const uint32_t c0 = (uint32_t)(wc0 + i * kChunk) + l8;
+                const uint32_t c0 = (uint32_t)(chunk_at(i)) + l8;
                 float e[8];
                 get8(EL[w][i], lane, e);
                 append_shared(S, xc, e, rp[i], cf[i], c0 < (uint32_t)d, c0, pm, true, kmin, lane);
@@ -1411,7 +1413,7 @@ void rac_encode_rows_kernel(Args A) {
         // clears the outliers of its own chunks, which only it reads)
 #pragma unroll
         for (int i = 0; i < CPW; ++i) {
-            const uint32_t oc = och - (uint32_t)(wc0 + i * kChunk);
+            const uint32_t oc = och - (uint32_t)(chunk_at(i));
             if (oc < (uint32_t)kChunk) reinterpret_cast<float*>(EL[w][i])[slice_float(oc)] = 0.0f;
         }
         wave_lds_sync();
@@ -1423,8 +1425,8 @@ void rac_encode_rows_kernel(Args A) {
         const Rsrc rxh = xhat_row(A, row);
 #pragma unroll
         for (int i = 0; i < CPW; ++i) {
-            if (wc0 + i * kChunk >= d) continue;
-            const uint32_t chunk0 = (uint32_t)(wc0 + i * kChunk);
+            if (chunk_at(i) >= d) continue;
+            const uint32_t chunk0 = (uint32_t)(chunk_at(i));
             const uint32_t c0 = chunk0 + l8;
             float ed[8];
             float4* st = EL[w][i];
@@ -1469,7 +1471,7 @@ void rac_encode_rows_kernel(Args A) {
                 for (int j = 0; j < 8; ++j) H[j] = __builtin_fmaf(qf[j], s, __builtin_fmaf(a, r[j], b0));  // R~ + q*s (q*s exact)
             }
             rp[i] = bload128(nr, c0 * 2u);
-            store_codes<BITS>(rcd, (wc0 >> 9) + i, lane, dword3, pack8<BITS>(mg));
+            store_codes<BITS>(rcd, w + i * NW, lane, dword3, pack8<BITS>(mg));
             put8(st, lane, H);
             wave_lds_sync();
             if (och - chunk0 < (uint32_t)kChunk) reinterpret_cast<float*>(st)[slice_float(och - chunk0)] = ohat;
