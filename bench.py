@@ -202,6 +202,11 @@ def main():
     }
     if not args.no_extras:
         extras["decode_step"] = decode_step_latency(torch, rac, wl, dev, stream)
+        # graph-replayed encode + decode pair, µs, across the bit widths and
+        # with one scale per token row (quantization group = hidden)
+        extras["decode_step_graph_pair_us"] = {
+            f"b{bits}_gq{gq}": decode_step_latency(torch, rac, wl, dev, stream, bits, gq, detail=False)
+            for bits, gq in ((2, 128), (8, 128), (4, 4096))}
     out["extras"] = extras
 
     if not args.no_cpu_baseline:
@@ -209,15 +214,15 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-def decode_step_latency(torch, rac, wl, dev, stream):
+def decode_step_latency(torch, rac, wl, dev, stream, bits=4, gq=128, detail=True):
     """µs per call of rac_encode and rac_decode for decode-phase batches
-    (1 token per sequence, 4096 hidden, group 128, 4-bit, no outliers):
-    wall time per call with back-to-back launches, kernel time from HIP
-    events, and the time per encode + decode pair when 20 pairs are captured
-    in one HIP graph and replayed."""
+    (1 token per sequence, 4096 hidden, alignment group 128, quantization
+    group gq, no outliers): wall time per call with back-to-back launches,
+    kernel time from HIP events (with detail), and the time per encode +
+    decode pair when 20 pairs are captured in one HIP graph and replayed."""
     res = {}
     for B in (1, 16, 64, 256):
-        cfg = rac.RacConfig(B, 4096, 128, 128, 4, 0)
+        cfg = rac.RacConfig(B, 4096, 128, gq, bits, 0)
         xb, rb = wl.decode_step(B)
         x, ref = dev(xb), dev(rb)
         wire = torch.empty(rac.rac_wire_size(cfg), dtype=torch.uint8, device="cuda")
@@ -227,7 +232,7 @@ def decode_step_latency(torch, rac, wl, dev, stream):
             rac.rac_encode(cfg, x, ref, None, wire, xh, stream=stream)
             rac.rac_decode(cfg, wire, ref, None, xd, stream=stream)
         torch.cuda.synchronize()
-        n = 200
+        n = 200 if detail else 20
         t0 = time.perf_counter()
         for _ in range(n):
             rac.rac_encode(cfg, x, ref, None, wire, xh, stream=stream)
@@ -239,7 +244,7 @@ def decode_step_latency(torch, rac, wl, dev, stream):
         t2 = time.perf_counter()
         e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
         ke, kd = [], []
-        for _ in range(20):
+        for _ in range(20 if detail else 0):
             e[0].record(stream)
             rac.rac_encode(cfg, x, ref, None, wire, xh, stream=stream)
             e[1].record(stream)
@@ -261,11 +266,15 @@ def decode_step_latency(torch, rac, wl, dev, stream):
             g.replay()
         e[1].record(stream)
         torch.cuda.synchronize()
+        pair = round(e[0].elapsed_time(e[1]) * 1e3 / 200, 2)
+        if not detail:
+            res[f"B{B}"] = pair
+            continue
         res[f"B{B}"] = {"encode_us_per_call": round((t1 - t0) / n * 1e6, 2),
                         "decode_us_per_call": round((t2 - t1) / n * 1e6, 2),
                         "encode_event_us": round(float(np.median(ke)) * 1e3, 2),
                         "decode_event_us": round(float(np.median(kd)) * 1e3, 2),
-                        "graph_pair_us": round(e[0].elapsed_time(e[1]) * 1e3 / 200, 2)}
+                        "graph_pair_us": pair}
     return res
 
 
