@@ -21,6 +21,7 @@ LIB_PATH = os.path.join(_HERE, "librac_oracle.so")
 ORC_OK, ORC_ERR_INVALID, ORC_ERR_CAPACITY, ORC_ERR_FORMAT, ORC_ERR_NONFINITE = 0, 1, 3, 5, 6
 FLAG_FIXED_STEP = 1
 FLAG_XHAT_BF16 = 2
+FLAG_GROUP_OUTLIERS = 4
 
 
 def build(verbose: bool = False) -> str:
@@ -44,7 +45,7 @@ class _Cfg(ctypes.Structure):
 class _Layout(ctypes.Structure):
     _fields_ = [("off_coef", ctypes.c_uint64), ("off_scale", ctypes.c_uint64),
                 ("off_codes", ctypes.c_uint64), ("off_outl", ctypes.c_uint64),
-                ("total", ctypes.c_uint64)]
+                ("total", ctypes.c_uint64), ("off_ooff", ctypes.c_uint64)]
 
 
 _lib = None

@@ -28,6 +28,10 @@
  *   - codes are q-bit two's complement, packed LSB-first per token row;
  *   - outliers are the k largest |E| per token row, ties to the lower channel,
  *     emitted in ascending channel order with fp16 values;
+ *   - in the per-group outlier mode (the outlier paragraph's own scope) each
+ *     quantization group gives up its k_g largest |E|, ties to the lower
+ *     channel, listed group by group in ascending in-group offset, the
+ *     offsets as u8 and the values as fp16 in two separate arrays;
  *   - q in {2,3} use the same formula as {4,8} (Qmax = 1 and 3).
  */
 #include "rac_oracle.h"
@@ -236,8 +240,15 @@ static int orc_valid(const orc_config* c) {
         c->hidden % c->group_quant != 0)
         return 0;
     if (c->bits != 2 && c->bits != 3 && c->bits != 4 && c->bits != 8) return 0;
-    if (c->outlier_k < 0 || c->outlier_k > 64 || c->outlier_k > c->hidden) return 0;
-    if (c->flags & ~(uint32_t)(ORC_FLAG_FIXED_STEP | ORC_FLAG_XHAT_BF16)) return 0;
+    if (c->flags & ~(uint32_t)(ORC_FLAG_FIXED_STEP | ORC_FLAG_XHAT_BF16 | ORC_FLAG_GROUP_OUTLIERS))
+        return 0;
+    if (c->flags & ORC_FLAG_GROUP_OUTLIERS) {
+        /* u8 in-group offsets, and at most a quarter of a group set aside */
+        if (c->group_quant > 256) return 0;
+        if (c->outlier_k < 1 || c->outlier_k > 16 || c->outlier_k > c->group_quant / 4) return 0;
+    } else if (c->outlier_k < 0 || c->outlier_k > 64 || c->outlier_k > c->hidden) {
+        return 0;
+    }
     return 1;
 }
 
@@ -250,12 +261,19 @@ int orc_layout_of(const orc_config* cfg, orc_layout* out) {
     const uint64_t scale =
         (cfg->flags & ORC_FLAG_FIXED_STEP) ? 0u : T * (d / (uint64_t)cfg->group_quant) * 2u;
     const uint64_t codes = T * d * (uint64_t)cfg->bits / 8u;
-    const uint64_t outl = T * (uint64_t)cfg->outlier_k * 4u;
     out->off_coef = ORC_HDR;
     out->off_scale = up256(out->off_coef + coef);
     out->off_codes = up256(out->off_scale + scale);
     out->off_outl = up256(out->off_codes + codes);
-    out->total = up256(out->off_outl + outl);
+    if (cfg->flags & ORC_FLAG_GROUP_OUTLIERS) {
+        /* fp16 values [T][d/g_q][k_g], then u8 offsets [T][d/g_q][k_g] */
+        const uint64_t n = T * (d / (uint64_t)cfg->group_quant) * (uint64_t)cfg->outlier_k;
+        out->off_ooff = up256(out->off_outl + 2u * n);
+        out->total = up256(out->off_ooff + n);
+    } else {
+        out->off_ooff = 0;
+        out->total = up256(out->off_outl + T * (uint64_t)cfg->outlier_k * 4u);
+    }
     return ORC_OK;
 }
 
@@ -281,9 +299,11 @@ static uint64_t get64(const uint8_t* p) {
 
 static uint16_t orc_wire_flags(const orc_config* cfg, int zero_ref) {
     uint16_t f = 0;
-    if (cfg->outlier_k > 0) f |= 1u;
+    const int grouped = (cfg->flags & ORC_FLAG_GROUP_OUTLIERS) != 0;
+    if (cfg->outlier_k > 0 && !grouped) f |= 1u;
     if (cfg->flags & ORC_FLAG_FIXED_STEP) f |= 2u;
     if (zero_ref) f |= 4u;
+    if (grouped) f |= 8u;
     return f;
 }
 
@@ -299,13 +319,16 @@ static void orc_write_header(const orc_config* cfg, const orc_layout* L, int zer
     w[24] = (uint8_t)cfg->bits;
     w[25] = 1; /* coefficients: fp16 (alpha, beta) pairs */
     w[26] = (cfg->flags & ORC_FLAG_FIXED_STEP) ? 0 : 1; /* scales: fp16 or absent */
-    w[27] = cfg->outlier_k > 0 ? 1 : 0; /* outliers: u16 channel | fp16 value */
+    /* outliers: 1 = u32 (u16 channel | fp16 value) per token, 2 = fp16 values
+     * and u8 in-group offsets per quantization group */
+    w[27] = (cfg->flags & ORC_FLAG_GROUP_OUTLIERS) ? 2 : (cfg->outlier_k > 0 ? 1 : 0);
     put16(w + 28, (uint16_t)cfg->outlier_k);
     put64(w + 32, L->off_coef);
     put64(w + 40, L->off_scale);
     put64(w + 48, L->off_codes);
     put64(w + 56, L->off_outl);
     put64(w + 64, L->total);
+    put64(w + 72, L->off_ooff);
 }
 
 /* q-bit two's complement code of channel c goes to bits [c*q, c*q+q) of the
@@ -352,6 +375,7 @@ int orc_encode(const orc_config* cfg, const uint16_t* x, const uint16_t* ref,
     const int32_t bits = cfg->bits, k = cfg->outlier_k;
     const int32_t qmax = (1 << (bits - 1)) - 1; /* Eq. residual-quantization */
     const int fixed = (cfg->flags & ORC_FLAG_FIXED_STEP) != 0;
+    const int grouped = (cfg->flags & ORC_FLAG_GROUP_OUTLIERS) != 0;
 
     for (int64_t i = 0; i < T * d; ++i) {
         if (!isfinite(orc_bf16_to_f32(x[i]))) return ORC_ERR_NONFINITE;
@@ -395,7 +419,24 @@ int orc_encode(const orc_config* cfg, const uint16_t* x, const uint16_t* ref,
         /* step 3: dense / outlier split (mask M over the k largest |E|) */
         memset(is_out, 0, (size_t)d);
         for (int32_t c = 0; c < d; ++c) ed[c] = e[c];
-        if (k > 0) {
+        if (grouped) {
+            /* the k_g largest |E| of every quantization group (the outlier
+             * paragraph's mask M_j per fixed group) */
+            const uint64_t n = (uint64_t)(d / gq) * (uint64_t)k;
+            uint8_t* vrow = wire + L.off_outl + (uint64_t)t * n * 2u;
+            uint8_t* orow = wire + L.off_ooff + (uint64_t)t * n;
+            for (int32_t g = 0; g < d / gq; ++g) {
+                orc_topk_row(e + g * gq, gq, k, sel); /* ascending in-group offsets */
+                for (int32_t i = 0; i < k; ++i) {
+                    const int32_t c = g * gq + sel[i];
+                    oval[c] = orc_f16_rne_sat(e[c]);
+                    is_out[c] = 1;
+                    ed[c] = 0.0f;
+                    put16(vrow + 2 * ((uint64_t)g * k + i), oval[c]);
+                    orow[(uint64_t)g * k + i] = (uint8_t)sel[i];
+                }
+            }
+        } else if (k > 0) {
             orc_topk_row(e, d, k, sel);
             uint8_t* ol = wire + L.off_outl + (uint64_t)t * (uint64_t)k * 4u;
             for (int32_t i = 0; i < k; ++i) {
@@ -458,19 +499,21 @@ int orc_decode(const orc_config* cfg, const uint8_t* wire, const uint16_t* ref,
     /* the header must describe exactly this configuration */
     if (get32(wire + 0) != ORC_MAGIC || get16(wire + 4) != ORC_VERSION) return ORC_ERR_FORMAT;
     const uint16_t wf = get16(wire + 6);
-    if ((wf & 3u) != (orc_wire_flags(cfg, 0) & 3u)) return ORC_ERR_FORMAT;
+    if ((wf & 11u) != (orc_wire_flags(cfg, 0) & 11u)) return ORC_ERR_FORMAT;
     if (get32(wire + 8) != (uint32_t)cfg->tokens || get32(wire + 12) != (uint32_t)cfg->hidden ||
         get32(wire + 16) != (uint32_t)cfg->group_align ||
         get32(wire + 20) != (uint32_t)cfg->group_quant || wire[24] != (uint8_t)cfg->bits ||
         get16(wire + 28) != (uint16_t)cfg->outlier_k || get64(wire + 32) != L.off_coef ||
         get64(wire + 40) != L.off_scale || get64(wire + 48) != L.off_codes ||
-        get64(wire + 56) != L.off_outl || get64(wire + 64) != L.total)
+        get64(wire + 56) != L.off_outl || get64(wire + 64) != L.total ||
+        get64(wire + 72) != L.off_ooff)
         return ORC_ERR_FORMAT;
 
     const int64_t T = cfg->tokens;
     const int32_t d = cfg->hidden, ga = cfg->group_align, gq = cfg->group_quant;
     const int32_t bits = cfg->bits, k = cfg->outlier_k;
     const int fixed = (cfg->flags & ORC_FLAG_FIXED_STEP) != 0;
+    const int grouped = (cfg->flags & ORC_FLAG_GROUP_OUTLIERS) != 0;
     float* eh = (float*)malloc(sizeof(float) * (size_t)d);
     for (int64_t t = 0; t < T; ++t) {
         const uint8_t* crow = wire + L.off_codes + (uint64_t)t * (uint64_t)d * (uint64_t)bits / 8u;
@@ -484,7 +527,21 @@ int orc_decode(const orc_config* cfg, const uint8_t* wire, const uint16_t* ref,
                 eh[c] = (float)orc_get_code(crow, c, bits) * s;
         }
         /* restore the outliers at their channels */
-        if (k > 0) {
+        if (grouped) {
+            const uint64_t n = (uint64_t)(d / gq) * (uint64_t)k;
+            const uint8_t* vrow = wire + L.off_outl + (uint64_t)t * n * 2u;
+            const uint8_t* orow = wire + L.off_ooff + (uint64_t)t * n;
+            for (int32_t g = 0; g < d / gq; ++g) {
+                for (int32_t i = 0; i < k; ++i) {
+                    const uint32_t o = orow[(uint64_t)g * k + i];
+                    if (o >= (uint32_t)gq) {
+                        free(eh);
+                        return ORC_ERR_FORMAT;
+                    }
+                    eh[g * gq + (int32_t)o] = orc_f16_to_f32(get16(vrow + 2 * ((uint64_t)g * k + i)));
+                }
+            }
+        } else if (k > 0) {
             const uint8_t* ol = wire + L.off_outl + (uint64_t)t * (uint64_t)k * 4u;
             for (int32_t i = 0; i < k; ++i) {
                 const uint32_t w = get32(ol + 4 * i);

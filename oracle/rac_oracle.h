@@ -34,7 +34,9 @@ enum {
 
 enum {
     ORC_FLAG_FIXED_STEP = 1u << 0, /* calibrated per-channel-group step table */
-    ORC_FLAG_XHAT_BF16 = 1u << 1   /* reconstruction written as bf16 (RNE)    */
+    ORC_FLAG_XHAT_BF16 = 1u << 1,  /* reconstruction written as bf16 (RNE)    */
+    ORC_FLAG_GROUP_OUTLIERS = 1u << 2 /* outlier_k = k_g per quantization group,
+                                         sent as u8 in-group offsets + fp16 */
 };
 
 typedef struct {
@@ -43,13 +45,17 @@ typedef struct {
     int32_t group_align;  /* g_a, power of two, divides d                  */
     int32_t group_quant;  /* g_q, power of two, divides d                  */
     int32_t bits;         /* q in {2,3,4,8}                                */
-    int32_t outlier_k;    /* outliers per token row, 0..min(64,d)          */
+    int32_t outlier_k;    /* outliers per token row, 0..min(64,d); with
+                             ORC_FLAG_GROUP_OUTLIERS the k_g per group,
+                             1..min(16, g_q/4), g_q <= 256                 */
     uint32_t flags;       /* ORC_FLAG_*                                    */
 } orc_config;
 
-/* Byte offsets of the wire sections (all 256-byte aligned). */
+/* Byte offsets of the wire sections (all 256-byte aligned).  off_ooff is the
+ * in-group offset array of the per-group outlier mode (0 otherwise); off_outl
+ * then holds the fp16 values. */
 typedef struct {
-    uint64_t off_coef, off_scale, off_codes, off_outl, total;
+    uint64_t off_coef, off_scale, off_codes, off_outl, total, off_ooff;
 } orc_layout;
 
 int orc_layout_of(const orc_config* cfg, orc_layout* out);

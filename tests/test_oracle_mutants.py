@@ -14,6 +14,7 @@ import subprocess
 import pytest
 
 import oracle
+from tests import test_oracle_group_outliers as gpins
 from tests import test_oracle_pins as pins
 
 # (name, text in rac_oracle.c, replacement)
@@ -31,13 +32,22 @@ MUTANTS = [
      "row[pos / 8] |= (uint8_t)(1u << (7 - pos % 8));"),
     ("outlier_ties_to_higher", "return (a->idx < b->idx) ? -1 : (a->idx > b->idx);",
      "return (a->idx > b->idx) ? -1 : (a->idx < b->idx);"),
-    ("outlier_left_in_dense", "                ed[c] = 0.0f;\n", "\n"),
+    ("outlier_left_in_dense", "is_out[c] = 1;\n                ed[c] = 0.0f;\n", "is_out[c] = 1;\n"),
     ("aligned_ref_drops_beta", "                rt[c] = fmaf(a, r[c], b0);", "                rt[c] = a * r[c];"),
     ("decoder_drops_outliers", "eh[c] = orc_f16_to_f32((uint16_t)(w >> 16));", "(void)c;"),
     ("alpha_beta_swapped", "put16(coef + 4 * j, ah);", "put16(coef + 4 * j, bh);"),
     ("outlier_value_unrounded_recon", "? orc_f16_to_f32(oval[c]) :", "? e[c] :"),
     ("f16_ties_up", "p = (lo & 1u) ? lo + 1 : lo; /* tie: even fraction */",
      "p = lo + 1; /* tie: even fraction */"),
+    ("group_offset_absolute", "orow[(uint64_t)g * k + i] = (uint8_t)sel[i];",
+     "orow[(uint64_t)g * k + i] = (uint8_t)c;"),
+    ("group_selects_from_first_group", "orc_topk_row(e + g * gq, gq, k, sel);",
+     "orc_topk_row(e, gq, k, sel);"),
+    ("group_outlier_left_in_dense", "is_out[c] = 1;\n                    ed[c] = 0.0f;\n",
+     "is_out[c] = 1;\n"),
+    ("group_decoder_ignores_group", "eh[g * gq + (int32_t)o] =", "eh[(int32_t)o] ="),
+    ("group_values_in_reverse", "put16(vrow + 2 * ((uint64_t)g * k + i), oval[c]);",
+     "put16(vrow + 2 * ((uint64_t)g * k + (k - 1 - i)), oval[c]);"),
 ]
 
 PINS = [
@@ -53,6 +63,9 @@ PINS = [
     pins.test_zero_reference_is_textbook_grouped_absmax_quantization,
     lambda: pins.test_error_bound_and_equivalence_on_uplink_rows(4, 8),
     pins.test_sender_reconstruction_equals_receiver_decode_bitwise,
+    lambda: gpins.test_group_outliers_match_brute_force_on_uplink_rows(128, 2, 4),
+    gpins.test_group_outliers_ties_go_to_the_lower_offset,
+    lambda: gpins.test_group_mode_sender_equals_receiver_bitwise(0),
 ]
 
 
