@@ -12,7 +12,10 @@
  *   2. aligned residual (Eq. aligned-residual): E = H - (alpha R + beta).
  *   3. outliers (paragraph "Outlier Metadata and Calibration"): optionally the
  *      k largest |E| of each token row leave the dense base and travel as
- *      (channel, fp16 value); ties go to the lower channel.
+ *      (channel, fp16 value); ties go to the lower channel.  With
+ *      RAC_FLAG_GROUP_OUTLIERS the scope is the paragraph's own: the k_g
+ *      largest |E| of every quantization group, sent as u8 in-group offsets
+ *      and fp16 values.
  *   4. grouped symmetric quantization (Eq. residual-quantization): per group of
  *      g_q channels, Qmax = 2^(q-1)-1, the scale is the smallest fp16 s with
  *      s*Qmax >= max|E^d| (rounded up, so nothing clips), codes are
@@ -45,13 +48,16 @@
  *     detect in the wire.
  *
  * Wire format (little-endian, self-describing, all padding zero):
- *   header (256 B): u32 magic 'RAC1', u16 version 1, u16 flags (1 outliers,
- *     2 fixed step, 4 encoded against a zero reference), u32 tokens,
+ *   header (256 B): u32 magic 'RAC1', u16 version 1, u16 flags (1 per-token
+ *     outliers, 2 fixed step, 4 encoded against a zero reference, 8 per-group
+ *     outliers), u32 tokens,
  *     u32 hidden, u32 g_a, u32 g_q, u8 bits, u8 coef fmt (1 = fp16 pair),
  *     u8 scale fmt (1 = fp16, 0 = absent), u8 outlier fmt (1 = u16 channel in
- *     the low half and fp16 value in the high half of a u32, 0 = absent),
- *     u16 k, u16 0, then u64 offsets of the coef, scale, code and outlier
- *     sections and the total size; sections start at 256-byte boundaries.
+ *     the low half and fp16 value in the high half of a u32, 2 = per-group
+ *     fp16 values and u8 offsets, 0 = absent), u16 k, u16 0, then u64 offsets
+ *     of the coef, scale, code and outlier sections, the total size and the
+ *     offset of the per-group offset array (0 without per-group outliers);
+ *     sections start at 256-byte boundaries.
  *   coef   : fp16 [tokens][hidden/g_a][2]   (alpha, beta)
  *   scale  : fp16 [tokens][hidden/g_q]      (absent with RAC_FLAG_FIXED_STEP)
  *   codes  : u8   [tokens][hidden*bits/8]   channel c of a row occupies bits
@@ -59,6 +65,10 @@
  *            bits-wide two's complement (INT4: two values per byte, even
  *            channel in the low nibble)
  *   outl   : u32  [tokens][k]               ascending channel per row
+ *   per-group outliers instead (k = k_g):
+ *   oval   : fp16 [tokens][hidden/g_q][k_g] at the outlier offset
+ *   ooff   : u8   [tokens][hidden/g_q][k_g] in-group offsets, ascending within
+ *            each group, aligned with oval
  */
 #ifndef RAC_H
 #define RAC_H
@@ -90,7 +100,11 @@ enum {
     RAC_FLAG_FIXED_STEP = 1u << 0,
     /* Write the reconstruction as bf16 (round to nearest even of the fp32
      * value) instead of fp32. */
-    RAC_FLAG_XHAT_BF16 = 1u << 1
+    RAC_FLAG_XHAT_BF16 = 1u << 1,
+    /* Outliers per quantization group (the outlier paragraph's mask M_j):
+     * outlier_k is k_g, the number taken from every group of g_q channels
+     * (ties to the lower channel), 1 <= k_g <= min(16, g_q/4), g_q <= 256. */
+    RAC_FLAG_GROUP_OUTLIERS = 1u << 2
 };
 
 typedef struct {
@@ -99,12 +113,14 @@ typedef struct {
     int32_t group_align; /* g_a: power of two, 8 <= g_a <= d, divides d           */
     int32_t group_quant; /* g_q: power of two, 8 <= g_q <= d, divides d           */
     int32_t bits;        /* q in {2, 3, 4, 8}; Qmax = 2^(q-1) - 1                  */
-    int32_t outlier_k;   /* outliers per token row, 0 <= k <= min(64, d)          */
+    int32_t outlier_k;   /* outliers per token row, 0 <= k <= min(64, d); with   */
+                         /* RAC_FLAG_GROUP_OUTLIERS the k_g per group             */
     uint32_t flags;      /* RAC_FLAG_*                                            */
 } rac_config;
 
 typedef struct {
     uint64_t off_coef, off_scale, off_codes, off_outl, total; /* bytes */
+    uint64_t off_ooff; /* per-group outlier offsets (0 without that mode) */
 } rac_layout;
 
 /* Host-only, pure.  Section offsets and total wire size for `cfg`.
@@ -116,7 +132,7 @@ size_t rac_wire_size(const rac_config* cfg);
 
 /* Host-only, pure.  Parse a wire header the caller has copied to HOST memory
  * (at least 256 bytes) into `out` (flags gets RAC_FLAG_FIXED_STEP when the
- * wire carries no scales).  Checks magic, version, field ranges and that the
+ * wire carries no scales and RAC_FLAG_GROUP_OUTLIERS for per-group outliers).  Checks magic, version, field ranges and that the
  * recorded offsets match the layout of the parsed configuration; returns
  * RAC_ERR_FORMAT otherwise.  `zero_ref` (may be NULL) receives 1 when the
  * wire was encoded against a zero reference. */
@@ -153,7 +169,8 @@ rac_status rac_reconstruct(const rac_config* cfg, const void* wire, const void* 
  *   ref         : bf16 [T][d], or NULL for a zero reference
  *   fixed_steps : fp32 [d/g_q] with RAC_FLAG_FIXED_STEP, else ignored
  *   xhat        : fp32 [T][d] (bf16 with RAC_FLAG_XHAT_BF16)
- * Outlier entries whose channel is >= d are ignored.  One kernel launch. */
+ * Outlier entries whose channel is >= d (per-group entries: whose in-group
+ * offset is >= g_q) are ignored.  One kernel launch. */
 rac_status rac_decode(const rac_config* cfg, const void* wire, const void* ref,
                       const float* fixed_steps, void* xhat, rac_stream_t stream);
 

@@ -19,13 +19,15 @@ import os
 from dataclasses import dataclass
 
 __all__ = [
-    "RacConfig", "RacError", "RAC_FLAG_FIXED_STEP", "RAC_FLAG_XHAT_BF16", "STATUS",
+    "RacConfig", "RacError", "RAC_FLAG_FIXED_STEP", "RAC_FLAG_XHAT_BF16", "RAC_FLAG_GROUP_OUTLIERS",
+    "STATUS",
     "library", "library_path", "rac_wire_layout", "rac_wire_size", "rac_parse_header",
     "rac_encode", "rac_reconstruct", "rac_decode", "rac_status_string",
 ]
 
 RAC_FLAG_FIXED_STEP = 1
 RAC_FLAG_XHAT_BF16 = 2
+RAC_FLAG_GROUP_OUTLIERS = 4
 STATUS = {0: "RAC_OK", 1: "RAC_ERR_INVALID", 2: "RAC_ERR_ALIGN", 3: "RAC_ERR_CAPACITY",
           4: "RAC_ERR_HIP", 5: "RAC_ERR_FORMAT", 6: "RAC_ERR_UNSUPPORTED"}
 
@@ -52,7 +54,7 @@ class _Config(ctypes.Structure):
 class _Layout(ctypes.Structure):
     _fields_ = [("off_coef", ctypes.c_uint64), ("off_scale", ctypes.c_uint64),
                 ("off_codes", ctypes.c_uint64), ("off_outl", ctypes.c_uint64),
-                ("total", ctypes.c_uint64)]
+                ("total", ctypes.c_uint64), ("off_ooff", ctypes.c_uint64)]
 
 
 @dataclass(frozen=True)

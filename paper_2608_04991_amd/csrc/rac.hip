@@ -50,7 +50,9 @@ struct alignas(8) Args {
     uint32_t* coef;     // wire sections
     uint16_t* scale;
     uint8_t* codes;
-    uint32_t* outl;
+    uint32_t* outl;     // per-token outliers, or the fp16 values of per-group ones
+    uint16_t* gval;     // per-group outliers: fp16 values [T][d/g_q][k_g] (= outl)
+    uint8_t* goff;      //                     u8 in-group offsets [T][d/g_q][k_g]
     void* xhat;
     uint32_t tokens;    // < 2^31, so row + gridDim.x never wraps
     int32_t d;
@@ -61,15 +63,16 @@ struct alignas(8) Args {
     int32_t lane_lv_q;
     int32_t lg_cpg_a;   // log2 chunks per group (0 when a group fits in a chunk)
     int32_t lg_cpg_q;
-    int32_t k;
+    int32_t k;          // outliers per row, or per group with gout
+    int32_t gout;       // per-group outlier mode
     int32_t fixed;
     int32_t xhat_bf16;
     float inv_ga;       // 1 / g_a (exact, power of two)
     // header and padding (written once, by the first wavefront)
     int32_t write_header;
     uint8_t* wire;
-    uint64_t off_scale, off_codes, off_outl, total;
-    uint64_t end_coef, end_scale, end_codes, end_outl;  // first byte after each section
+    uint64_t off_scale, off_codes, off_outl, off_ooff, total;
+    uint64_t end_coef, end_scale, end_codes, end_outl, end_ooff;  // first byte after each section
     uint32_t hdr[24];   // first 96 bytes of the header; the rest is zero
 };
 
@@ -342,7 +345,8 @@ __device__ __forceinline__ void write_header(const Args& A, uint32_t lane) {
     zero_bytes(A.wire, A.end_coef, A.off_scale, lane);
     zero_bytes(A.wire, A.end_scale, A.off_codes, lane);
     zero_bytes(A.wire, A.end_codes, A.off_outl, lane);
-    zero_bytes(A.wire, A.end_outl, A.total, lane);
+    zero_bytes(A.wire, A.end_outl, A.off_ooff, lane);
+    zero_bytes(A.wire, A.end_ooff, A.total, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -666,6 +670,90 @@ __device__ __forceinline__ void append8(RowShared& S, uint32_t* counter, const f
 }
 
 // ---------------------------------------------------------------------------
+// Per-group outlier choice (the outlier paragraph's own scope: the mask of
+// every fixed quantization group keeps its k_g largest magnitudes, and the
+// packet carries in-group offsets and fp16 values).  A group of g_q <= 256
+// channels is 2^lv lanes of one wavefront, so the choice is wave-local.
+
+// Unsigned max over the 2^lv lanes of an aligned block.
+template <int LV>
+__device__ __forceinline__ uint32_t umax_lanes(uint32_t v, int lv) {
+    const int L = LV >= 0 ? LV : lv;
+    if (L > 0) v = __builtin_elementwise_max(v, dpp_u<0xB1>(v));
+    if (L > 1) v = __builtin_elementwise_max(v, dpp_u<0x4E>(v));
+    if (L > 2) v = __builtin_elementwise_max(v, dpp_u<0x141>(v));
+    if (L > 3) v = __builtin_elementwise_max(v, dpp_u<0x140>(v));
+    if (L > 4) {
+        auto p = __builtin_amdgcn_permlane16_swap((int)v, (int)v, false, false);
+        v = __builtin_elementwise_max((uint32_t)p[0], (uint32_t)p[1]);
+    }
+    return v;
+}
+
+// Chooses the k_g outliers of the lane's group and returns the lane's mask of
+// chosen channels (bit j = channel c0 + j).  k_g rounds, each taking the
+// group's largest remaining key and, among lanes holding it, the lowest
+// channel.  A key is the |E| pattern plus one, so a zero residual still
+// outranks a chosen element (key 0); k_g < g_q leaves every round a
+// candidate.  The entries, (fp16 value | in-group offset << 16), go to `st`
+// at their position in the chunk's part of the row: group by group, ascending
+// offset inside a group.
+template <int LV>
+__device__ __forceinline__ uint32_t select_group_outliers(const float* e, int lv, int kg, uint32_t lane,
+                                                          uint32_t* st) {
+    uint32_t key[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) key[j] = (__float_as_uint(e[j]) & 0x7FFFFFFFu) + 1u;
+    const uint32_t g0 = lane & ~((1u << lv) - 1u);  // first lane of the group
+    const uint32_t gmask = (uint32_t)((1ull << (1u << lv)) - 1ull);  // groups span at most 32 lanes
+    uint32_t selm = 0u;
+    for (int i = 0; i < kg; ++i) {
+        uint32_t lb = 0u;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) lb = __builtin_elementwise_max(lb, key[j]);
+        const uint32_t m = umax_lanes<LV>(lb, lv);
+        uint32_t hit = 0u;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) hit |= (uint32_t)(key[j] == m) << j;
+        const uint32_t holders = (uint32_t)(ballot(hit != 0u) >> g0) & gmask;
+        const uint32_t pick = (lane - g0 == (uint32_t)__builtin_ctz(holders)) ? (hit & (0u - hit)) : 0u;
+        selm |= pick;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) key[j] = ((pick >> j) & 1u) ? 0u : key[j];
+    }
+    // slot of the lane's first entry: chosen channels of the group's lower
+    // lanes (counts <= 8 summed bit by bit over ballots)
+    const uint32_t cnt = (uint32_t)__builtin_popcount(selm);
+    const uint64_t below = ((1ull << lane) - 1ull) & ~((1ull << g0) - 1ull);
+    uint32_t slot = (lane >> lv) * (uint32_t)kg;
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+        slot += (uint32_t)__builtin_popcountll(ballot((cnt >> b) & 1u) & below) << b;
+    if (selm) {
+        const uint32_t o0 = (lane - g0) * 8u;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if ((selm >> j) & 1u) st[slot++] = f16_rne_sat(e[j]) | ((o0 + (uint32_t)j) << 16);
+    }
+    return selm;
+}
+
+// Store the chunk's staged per-group entries (at most 128: k_g <= g_q / 4):
+// lane l writes entries l and l + 64 of the chunk, fp16 values to `rv` and u8
+// offsets to `ro` (the row's two arrays); `first` is the chunk's first entry
+// in the row and `n` its entry count.  Four stores per lane whatever n is.
+__device__ __forceinline__ void store_group_outliers(Rsrc rv, Rsrc ro, uint32_t first, uint32_t n, uint32_t lane,
+                                                     const uint32_t* st) {
+    const uint32_t v0 = st[lane], v1 = st[lane + kWave];
+    wave_lds_sync();  // the slice is reused for the reconstruction
+    const bool in0 = lane < n, in1 = lane + kWave < n;
+    bstore16(rv, in0 ? (first + lane) * 2u : kOut, v0);
+    bstore16(rv, in1 ? (first + lane + kWave) * 2u : kOut, v1);
+    bstore8(ro, in0 ? first + lane : kOut, v0 >> 16);
+    bstore8(ro, in1 ? first + lane + kWave : kOut, v1 >> 16);
+}
+
+// ---------------------------------------------------------------------------
 // Per-token outlier choice: the k largest |E| of the row, ties to the lower
 // channel.  Called by every wavefront of the workgroup with its 8 residuals
 // per lane; returns the per-lane mask of chosen channels (bit j = channel
@@ -833,8 +921,9 @@ __device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S,
 
 // GA / GQ select the group shape at compile time: 0..6 = groups inside one
 // chunk with that many butterfly levels, 7 = groups spanning chunks, -1 =
-// read from the arguments at run time.
-template <int BITS, int GA, int GQ, bool OUTL>
+// read from the arguments at run time.  OM is the outlier mode: 0 none, 1 the
+// k largest |E| per token row, 2 the k_g largest per quantization group.
+template <int BITS, int GA, int GQ, int OM>
 __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
     // LDS state of a row, double-buffered by row parity: every row that uses
     // LDS has a workgroup barrier, so no wave is more than one row ahead.
@@ -859,8 +948,12 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
     const bool first_q = !multi_q ? (lane & ((1u << lv_q) - 1u)) == 0u : (lane == 0u && (w & (cpg_q - 1)) == 0);
     const uint32_t sh_fixed = (A.fixed && act) ? step_roundup(A.steps[grp_q]) : 0u;
     const uint32_t ngq = (uint32_t)d >> A.lg_q, nga = (uint32_t)d >> A.lg_a;
+    // per-group outliers: entries per row, this chunk's first entry and count
+    const uint32_t gent = (uint32_t)A.k * ngq;
+    const uint32_t gfirst = ((uint32_t)(w * kChunk) >> A.lg_q) * (uint32_t)A.k;
+    const uint32_t gcount = ((uint32_t)__builtin_elementwise_min(kChunk, d - w * kChunk) >> A.lg_q) * (uint32_t)A.k;
 
-    if (OUTL) {
+    if (OM == 1) {
         if (w == 0) {
             SS[0].smax[lane] = 0u;
             SS[1].smax[lane] = 0u;
@@ -949,7 +1042,14 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
 
         // a4: outliers
         uint32_t selm = 0;
-        if constexpr (OUTL) selm = select_outliers(A, S, SS[(n + 1) & 1], e, act, c0, lane, w, row);
+        if constexpr (OM == 1) selm = select_outliers(A, S, SS[(n + 1) & 1], e, act, c0, lane, w, row);
+        if constexpr (OM == 2) {
+            uint32_t* st = reinterpret_cast<uint32_t*>(XT + w * kSlice);
+            selm = select_group_outliers<GQ>(e, lv_q, A.k, lane, st);
+            wave_lds_sync();
+            store_group_outliers(rsrc(A.gval, (uint64_t)row * gent, gent * 2u), rsrc(A.goff, (uint64_t)row * gent, gent),
+                                 gfirst, gcount, lane, st);
+        }
         float ed[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) ed[j] = e[j];
@@ -1484,10 +1584,11 @@ void rac_encode_rows_kernel(Args A) {
 // ---------------------------------------------------------------------------
 // Decode / reconstruct: one workgroup per token row (strided, with the next
 // row's inputs prefetched), one wavefront per chunk, no cross-wave work.
-// OUTL: the wire has outliers; BF16: the reconstruction is stored as bf16.
-// (Both are compile-time, so no branch separates a row's memory operations.)
+// OM: the wire's outlier mode (0 none, 1 per token row, 2 per quantization
+// group); BF16: the reconstruction is stored as bf16.  (Both are compile-time,
+// so no branch separates a row's memory operations.)
 
-template <int BITS, bool OUTL, bool BF16>
+template <int BITS, int OM, bool BF16>
 __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
     extern __shared__ float4 XT[];  // per-wavefront store staging, kSlice each (sized at launch)
     const uint32_t lane = threadIdx.x & (kWave - 1);
@@ -1499,12 +1600,18 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
     const int grp_a = c0 >> A.lg_a, grp_q = c0 >> A.lg_q;
     const uint32_t ngq = (uint32_t)d >> A.lg_q, nga = (uint32_t)d >> A.lg_a;
     const uint32_t sh_fixed = (A.fixed && act) ? step_roundup(A.steps[grp_q]) : 0u;
+    constexpr bool OUTL = OM == 1;
+    // per-group outliers: entries per row, this chunk's first entry and count
+    const uint32_t gent = (uint32_t)k * ngq;
+    const uint32_t gfirst = ((uint32_t)(w * kChunk) >> A.lg_q) * (uint32_t)k;
+    const uint32_t gcount = ((uint32_t)__builtin_elementwise_min(kChunk, d - w * kChunk) >> A.lg_q) * (uint32_t)k;
 
     // inputs of one row for this lane: ref words, packed codes, coefficient
-    // pair, scale, and (lanes < k) one outlier entry
+    // pair, scale, and either (lanes < k) one per-token outlier entry or
+    // entries l and l + 64 of the chunk's per-group outliers
     struct In {
         uint4 rv;
-        uint32_t lo, hi, cf, sh, ent;
+        uint32_t lo, hi, cf, sh, ent, ent2;
     };
     // (zeros past the last row and past the end of the row; entries of lanes
     // >= k are never read)
@@ -1520,6 +1627,15 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
         if (A.fixed) in.sh = sh_fixed;
         load_codes<BITS>(rsrc(A.codes, r * crb, in_range ? crb : 0u), w, lane, dword3, in.lo, in.hi);
         in.ent = OUTL ? bload32(rsrc(A.outl, r * (uint64_t)k, in_range ? (uint32_t)k * 4u : 0u), lane * 4u) : 0u;
+        in.ent2 = 0u;
+        if constexpr (OM == 2) {
+            const Rsrc rv = rsrc(A.gval, r * gent, in_range ? gent * 2u : 0u);
+            const Rsrc ro = rsrc(A.goff, r * gent, in_range ? gent : 0u);
+            const bool in0 = lane < gcount, in1 = lane + kWave < gcount;
+            in.ent = bload16(rv, in0 ? (gfirst + lane) * 2u : kOut) | (bload8(ro, in0 ? gfirst + lane : kOut) << 16);
+            in.ent2 = bload16(rv, in1 ? (gfirst + lane + kWave) * 2u : kOut) |
+                      (bload8(ro, in1 ? gfirst + lane + kWave : kOut) << 16);
+        }
         return in;
     };
 
@@ -1539,11 +1655,32 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
         nx = load(nrow);
         const float a = f16_value(in.cf & 0xFFFFu), b0 = f16_value(in.cf >> 16);
         const float s = f16_value(in.sh);
-        float r[8], H[8];
+        float r[8], rt[8], H[8];
         widen8(in.rv, r);
 #pragma unroll
-        for (int j = 0; j < 8; ++j)  // R~ + q*s, q*s exact
-            H[j] = __builtin_fmaf((float)code_at<BITS>(in.lo, in.hi, j), s, __builtin_fmaf(a, r[j], b0));
+        for (int j = 0; j < 8; ++j) {  // R~ + q*s, q*s exact
+            rt[j] = __builtin_fmaf(a, r[j], b0);
+            H[j] = __builtin_fmaf((float)code_at<BITS>(in.lo, in.hi, j), s, rt[j]);
+        }
+        if constexpr (OM == 2) {
+            // the k_g entries of this lane's group, pulled from the lanes that
+            // loaded them; an entry whose offset falls in this lane's 8
+            // channels replaces that channel by R~ + value
+            const uint32_t lv = (uint32_t)A.lane_lv_q;
+            const uint32_t mine = lane & ((1u << lv) - 1u), gbase = (lane >> lv) * (uint32_t)k;
+            for (int i = 0; i < k; ++i) {
+                const uint32_t src = gbase + (uint32_t)i;
+                const int addr = (int)((src & (kWave - 1u)) << 2);
+                const uint32_t e0 = (uint32_t)__builtin_amdgcn_ds_bpermute(addr, (int)in.ent);
+                const uint32_t e1 = (uint32_t)__builtin_amdgcn_ds_bpermute(addr, (int)in.ent2);
+                const uint32_t ent = src < (uint32_t)kWave ? e0 : e1;
+                const uint32_t off = (ent >> 16) & 0xFFu;
+                const float v = f16_value(ent & 0xFFFFu);
+                const bool here = (off >> 3) == mine;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) H[j] = (here & ((off & 7u) == (uint32_t)j)) ? rt[j] + v : H[j];
+            }
+        }
         float4* st = XT + w * kSlice;
         put8(st, lane, H);
         wave_lds_sync();
@@ -1591,14 +1728,21 @@ bool config_valid(const rac_config* c) {
         c->hidden % c->group_quant != 0)
         return false;
     if (c->bits != 2 && c->bits != 3 && c->bits != 4 && c->bits != 8) return false;
-    if (c->outlier_k < 0 || c->outlier_k > 64 || c->outlier_k > c->hidden) return false;
-    if (c->flags & ~uint32_t(RAC_FLAG_FIXED_STEP | RAC_FLAG_XHAT_BF16)) return false;
+    if (c->flags & ~uint32_t(RAC_FLAG_FIXED_STEP | RAC_FLAG_XHAT_BF16 | RAC_FLAG_GROUP_OUTLIERS)) return false;
+    if (c->flags & RAC_FLAG_GROUP_OUTLIERS) {
+        if (c->group_quant > 256) return false;  // u8 in-group offsets
+        if (c->outlier_k < 1 || c->outlier_k > 16 || c->outlier_k > c->group_quant / 4) return false;
+    } else if (c->outlier_k < 0 || c->outlier_k > 64 || c->outlier_k > c->hidden) {
+        return false;
+    }
     return true;
 }
 
+bool grouped(const rac_config* c) { return (c->flags & RAC_FLAG_GROUP_OUTLIERS) != 0; }
+
 struct Sizes {
     rac_layout L;
-    uint64_t coef, scale, codes, outl;
+    uint64_t coef, scale, codes, outl, ooff;
 };
 
 Sizes sizes_of(const rac_config* c) {
@@ -1607,12 +1751,15 @@ Sizes sizes_of(const rac_config* c) {
     s.coef = T * (d / (uint64_t)c->group_align) * 4u;
     s.scale = (c->flags & RAC_FLAG_FIXED_STEP) ? 0u : T * (d / (uint64_t)c->group_quant) * 2u;
     s.codes = T * d * (uint64_t)c->bits / 8u;
-    s.outl = T * (uint64_t)c->outlier_k * 4u;
+    const uint64_t gent = T * (d / (uint64_t)c->group_quant) * (uint64_t)c->outlier_k;
+    s.outl = grouped(c) ? gent * 2u : T * (uint64_t)c->outlier_k * 4u;
+    s.ooff = grouped(c) ? gent : 0u;
     s.L.off_coef = 256;
     s.L.off_scale = up256(s.L.off_coef + s.coef);
     s.L.off_codes = up256(s.L.off_scale + s.scale);
     s.L.off_outl = up256(s.L.off_codes + s.codes);
-    s.L.total = up256(s.L.off_outl + s.outl);
+    s.L.off_ooff = grouped(c) ? up256(s.L.off_outl + s.outl) : 0u;
+    s.L.total = grouped(c) ? up256(s.L.off_ooff + s.ooff) : up256(s.L.off_outl + s.outl);
     return s;
 }
 
@@ -1624,6 +1771,9 @@ Args make_args(const rac_config* c, const Sizes& S) {
     A.off_codes = S.L.off_codes;
     A.off_outl = S.L.off_outl;
     A.total = S.L.total;
+    // without per-group outliers the offset array is empty, at the end
+    A.off_ooff = grouped(c) ? S.L.off_ooff : S.L.total;
+    A.end_ooff = A.off_ooff + S.ooff;
     A.end_coef = S.L.off_coef + S.coef;
     A.end_scale = S.L.off_scale + S.scale;
     A.end_codes = S.L.off_codes + S.codes;
@@ -1639,6 +1789,7 @@ Args make_args(const rac_config* c, const Sizes& S) {
     A.lg_cpg_a = c->group_align > kChunk ? ilog2(c->group_align / kChunk) : 0;
     A.lg_cpg_q = c->group_quant > kChunk ? ilog2(c->group_quant / kChunk) : 0;
     A.k = c->outlier_k;
+    A.gout = grouped(c) ? 1 : 0;
     A.fixed = (c->flags & RAC_FLAG_FIXED_STEP) ? 1 : 0;
     A.xhat_bf16 = (c->flags & RAC_FLAG_XHAT_BF16) ? 1 : 0;
     A.inv_ga = 1.0f / (float)c->group_align;
@@ -1650,6 +1801,8 @@ void set_sections(Args& A, const Sizes& S) {
     A.scale = reinterpret_cast<uint16_t*>(A.wire + S.L.off_scale);
     A.codes = A.wire + S.L.off_codes;
     A.outl = reinterpret_cast<uint32_t*>(A.wire + S.L.off_outl);
+    A.gval = reinterpret_cast<uint16_t*>(A.wire + S.L.off_outl);
+    A.goff = A.wire + (A.gout ? S.L.off_ooff : S.L.total);
 }
 
 void fill_header(Args& A, const rac_config* c, bool zero_ref) {
@@ -1658,9 +1811,10 @@ void fill_header(Args& A, const rac_config* c, bool zero_ref) {
     auto put32 = [&](int o, uint32_t v) { for (int i = 0; i < 4; ++i) h[o + i] = (uint8_t)(v >> (8 * i)); };
     auto put64 = [&](int o, uint64_t v) { for (int i = 0; i < 8; ++i) h[o + i] = (uint8_t)(v >> (8 * i)); };
     uint32_t flags = 0;
-    if (c->outlier_k > 0) flags |= 1u;
+    if (c->outlier_k > 0 && !grouped(c)) flags |= 1u;
     if (c->flags & RAC_FLAG_FIXED_STEP) flags |= 2u;
     if (zero_ref) flags |= 4u;
+    if (grouped(c)) flags |= 8u;
     put32(0, 0x31434152u);
     put16(4, 1u);
     put16(6, flags);
@@ -1671,13 +1825,14 @@ void fill_header(Args& A, const rac_config* c, bool zero_ref) {
     h[24] = (uint8_t)c->bits;
     h[25] = 1;
     h[26] = (c->flags & RAC_FLAG_FIXED_STEP) ? 0 : 1;
-    h[27] = c->outlier_k > 0 ? 1 : 0;
+    h[27] = grouped(c) ? 2 : (c->outlier_k > 0 ? 1 : 0);
     put16(28, (uint32_t)c->outlier_k);
     put64(32, (uint64_t)256);
     put64(40, A.off_scale);
     put64(48, A.off_codes);
     put64(56, A.off_outl);
     put64(64, A.total);
+    put64(72, grouped(c) ? A.off_ooff : 0u);
     for (int i = 0; i < 24; ++i)
         A.hdr[i] = (uint32_t)h[4 * i] | ((uint32_t)h[4 * i + 1] << 8) | ((uint32_t)h[4 * i + 2] << 16) |
                    ((uint32_t)h[4 * i + 3] << 24);
@@ -1685,31 +1840,38 @@ void fill_header(Args& A, const rac_config* c, bool zero_ref) {
 
 using KernelFn = void (*)(Args);
 
-template <int GA, int GQ, bool OUTL>
+template <int GA, int GQ, int OM>
 KernelFn encode_for_bits(int bits) {
     switch (bits) {
-        case 2: return rac_encode_kernel<2, GA, GQ, OUTL>;
-        case 3: return rac_encode_kernel<3, GA, GQ, OUTL>;
-        case 4: return rac_encode_kernel<4, GA, GQ, OUTL>;
-        default: return rac_encode_kernel<8, GA, GQ, OUTL>;
+        case 2: return rac_encode_kernel<2, GA, GQ, OM>;
+        case 3: return rac_encode_kernel<3, GA, GQ, OM>;
+        case 4: return rac_encode_kernel<4, GA, GQ, OM>;
+        default: return rac_encode_kernel<8, GA, GQ, OM>;
     }
 }
 
+// (groups spanning chunks, GQ = 7, exceed the 256 channels of per-group
+// outliers, so that form has no mode 2)
 template <int GA, int GQ>
-KernelFn encode_for(int bits, bool outl) {
-    return outl ? encode_for_bits<GA, GQ, true>(bits) : encode_for_bits<GA, GQ, false>(bits);
+KernelFn encode_for(int bits, int om) {
+    if constexpr (GQ != 7) {
+        if (om == 2) return encode_for_bits<GA, GQ, 2>(bits);
+    }
+    return om == 1 ? encode_for_bits<GA, GQ, 1>(bits) : encode_for_bits<GA, GQ, 0>(bits);
 }
+
+int outlier_mode(const Args& A) { return A.gout ? 2 : (A.k > 0 ? 1 : 0); }
 
 // Specialized group shapes: 64/64, 128/128 and 128 with one scale per row
 // of up to 8192 channels; anything else takes the generic kernel.
 KernelFn pick_encode(const Args& A, int bits) {
     const int ga = A.lg_cpg_a > 0 ? 7 : A.lane_lv_a;
     const int gq = A.lg_cpg_q > 0 ? 7 : A.lane_lv_q;
-    const bool outl = A.k > 0;
-    if (ga == 3 && gq == 3) return encode_for<3, 3>(bits, outl);
-    if (ga == 4 && gq == 4) return encode_for<4, 4>(bits, outl);
-    if (ga == 4 && gq == 7) return encode_for<4, 7>(bits, outl);
-    return encode_for<-1, -1>(bits, outl);
+    const int om = outlier_mode(A);
+    if (ga == 3 && gq == 3) return encode_for<3, 3>(bits, om);
+    if (ga == 4 && gq == 4) return encode_for<4, 4>(bits, om);
+    if (ga == 4 && gq == 7) return encode_for<4, 7>(bits, om);
+    return encode_for<-1, -1>(bits, om);
 }
 
 template <int GA, int GQ, int CPW>
@@ -1732,7 +1894,7 @@ KernelFn rows_for(int bits, int d) {
 // row and both group sizes fit in a chunk (calibrated step tables take the
 // one-wavefront-per-chunk kernel).
 bool use_rows_kernel(const Args& A) {
-    return A.k > 0 && !A.fixed && A.d <= kRowsMaxD && A.lg_cpg_a == 0 && A.lg_cpg_q == 0;
+    return outlier_mode(A) == 1 && !A.fixed && A.d <= kRowsMaxD && A.lg_cpg_a == 0 && A.lg_cpg_q == 0;
 }
 
 KernelFn pick_rows(const Args& A, int bits) {
@@ -1741,20 +1903,23 @@ KernelFn pick_rows(const Args& A, int bits) {
     return rows_for<-1, -1>(bits, A.d);
 }
 
-template <bool OUTL, bool BF16>
+template <int OM, bool BF16>
 KernelFn decode_for(int bits) {
     switch (bits) {
-        case 2: return rac_decode_kernel<2, OUTL, BF16>;
-        case 3: return rac_decode_kernel<3, OUTL, BF16>;
-        case 4: return rac_decode_kernel<4, OUTL, BF16>;
-        default: return rac_decode_kernel<8, OUTL, BF16>;
+        case 2: return rac_decode_kernel<2, OM, BF16>;
+        case 3: return rac_decode_kernel<3, OM, BF16>;
+        case 4: return rac_decode_kernel<4, OM, BF16>;
+        default: return rac_decode_kernel<8, OM, BF16>;
     }
 }
 
 KernelFn pick_decode(const Args& A, int bits) {
-    const bool outl = A.k > 0, bf16 = A.xhat_bf16 != 0;
-    if (outl) return bf16 ? decode_for<true, true>(bits) : decode_for<true, false>(bits);
-    return bf16 ? decode_for<false, true>(bits) : decode_for<false, false>(bits);
+    const bool bf16 = A.xhat_bf16 != 0;
+    switch (outlier_mode(A)) {
+        case 1: return bf16 ? decode_for<1, true>(bits) : decode_for<1, false>(bits);
+        case 2: return bf16 ? decode_for<2, true>(bits) : decode_for<2, false>(bits);
+        default: return bf16 ? decode_for<0, true>(bits) : decode_for<0, false>(bits);
+    }
 }
 
 // One workgroup per token row.  Large row counts use a grid of as many
@@ -1811,7 +1976,7 @@ rac_status run_decode(const rac_config* cfg, const void* wire, const void* ref, 
     A.xhat = xhat;
     // (with outliers, two workgroups per compute unit, each taking more rows,
     // measured fastest: 4-8% below a full grid at 4096 x 4096 and 16384 x 3584)
-    return launch(pick_decode(A, cfg->bits), A, stream, 0, A.k > 0 ? 2 : 0);
+    return launch(pick_decode(A, cfg->bits), A, stream, 0, outlier_mode(A) == 1 ? 2 : 0);
 }
 
 }  // namespace
@@ -1838,7 +2003,8 @@ rac_status rac_parse_header(const void* header_host, size_t len, rac_config* out
     auto g64 = [&](int o) { uint64_t v = 0; for (int i = 7; i >= 0; --i) v = (v << 8) | h[o + i]; return v; };
     if (g32(0) != 0x31434152u || g16(4) != 1u) return RAC_ERR_FORMAT;
     const uint32_t flags = g16(6);
-    if (flags & ~7u) return RAC_ERR_FORMAT;
+    if (flags & ~15u) return RAC_ERR_FORMAT;
+    if ((flags & 1u) && (flags & 8u)) return RAC_ERR_FORMAT;
     rac_config c{};
     c.tokens = g32(8);
     c.hidden = (int32_t)g32(12);
@@ -1846,19 +2012,19 @@ rac_status rac_parse_header(const void* header_host, size_t len, rac_config* out
     c.group_quant = (int32_t)g32(20);
     c.bits = h[24];
     c.outlier_k = (int32_t)g16(28);
-    c.flags = (flags & 2u) ? RAC_FLAG_FIXED_STEP : 0u;
+    c.flags = ((flags & 2u) ? RAC_FLAG_FIXED_STEP : 0u) | ((flags & 8u) ? RAC_FLAG_GROUP_OUTLIERS : 0u);
     if (g32(12) > 65535u || g32(16) > 65535u || g32(20) > 65535u) return RAC_ERR_FORMAT;
     if (!config_valid(&c)) return RAC_ERR_FORMAT;
-    if (((flags & 1u) != 0) != (c.outlier_k > 0)) return RAC_ERR_FORMAT;
-    if (h[25] != 1 || h[26] != ((flags & 2u) ? 0 : 1) || h[27] != (c.outlier_k > 0 ? 1 : 0))
-        return RAC_ERR_FORMAT;
+    if (!(flags & 8u) && ((flags & 1u) != 0) != (c.outlier_k > 0)) return RAC_ERR_FORMAT;
+    const uint32_t ofmt = (flags & 8u) ? 2u : (c.outlier_k > 0 ? 1u : 0u);
+    if (h[25] != 1 || h[26] != ((flags & 2u) ? 0 : 1) || h[27] != ofmt) return RAC_ERR_FORMAT;
     const Sizes S = sizes_of(&c);
     if (g64(32) != S.L.off_coef || g64(40) != S.L.off_scale || g64(48) != S.L.off_codes ||
-        g64(56) != S.L.off_outl || g64(64) != S.L.total)
+        g64(56) != S.L.off_outl || g64(64) != S.L.total || g64(72) != S.L.off_ooff)
         return RAC_ERR_FORMAT;
     for (int i = 30; i < 32; ++i)
         if (h[i]) return RAC_ERR_FORMAT;
-    for (int i = 72; i < 256; ++i)
+    for (int i = 80; i < 256; ++i)
         if (h[i]) return RAC_ERR_FORMAT;
     *out = c;
     if (zero_ref) *zero_ref = (flags & 4u) ? 1 : 0;

@@ -72,7 +72,7 @@ def oracle_run(c, xb, rb, steps=None):
 def row_sections(wire: np.ndarray, rows) -> dict:
     s = wirefmt.sections(wire)
     out = {}
-    for k in ("coef", "scale", "codes", "outl"):
+    for k in ("coef", "scale", "codes", "outl", "gval", "goff"):
         out[k] = None if s[k] is None else s[k][rows]
     return out
 
@@ -102,7 +102,14 @@ def assert_parity(c, g_wire, g_xhat, o_wire, o_xhat, g_rows=None, o_rows=None, s
     if os_["scale"] is not None:
         assert np.array_equal(gs["scale"], os_["scale"]), \
             f"scales differ at {np.argwhere(gs['scale'] != os_['scale'])[:5].tolist()}"
-    assert np.array_equal(gs["outl"], os_["outl"]), "outliers differ"
+    assert (gs["outl"] is None) == (os_["outl"] is None) and (gs["gval"] is None) == (os_["gval"] is None)
+    if os_["outl"] is not None:
+        assert np.array_equal(gs["outl"], os_["outl"]), "outliers differ"
+    if os_["gval"] is not None:
+        assert np.array_equal(gs["goff"], os_["goff"]), \
+            f"group outlier offsets differ at {np.argwhere(gs['goff'] != os_['goff'])[:5].tolist()}"
+        assert np.array_equal(gs["gval"], os_["gval"]), \
+            f"group outlier values differ at {np.argwhere(gs['gval'] != os_['gval'])[:5].tolist()}"
     gc = wirefmt.unpack_codes(gs["codes"], d, b)
     oc = wirefmt.unpack_codes(os_["codes"], d, b)
     diff = gc != oc

@@ -19,6 +19,7 @@ from tests import wirefmt
 from tests.gpu_util import assert_parity, cfgd, gpu_run, oracle_run, say
 
 pytestmark = pytest.mark.gpu
+GRP = rac.RAC_FLAG_GROUP_OUTLIERS
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -168,6 +169,29 @@ CASES = {
                                                     lambda: _signed_zero_rows(6, 1024, False)),
     "signed_zero_outliers_distinct_6x1024_g128_b4_k3": (cfgd(6, 1024, 128, 128, 4, 3),
                                                         lambda: _signed_zero_rows(6, 1024, True)),
+    # per-group outliers (k_g per quantization group, u8 in-group offsets)
+    "group_uplink_37x4096_g128_b4_kg1": (cfgd(37, 4096, 128, 128, 4, 1, GRP),
+                                         lambda: wl.prefill_uplink(0, rows=(0, 37))[:2]),
+    "group_uplink_21x4096_ga64_gq128_b8_kg4": (cfgd(21, 4096, 64, 128, 8, 4, GRP),
+                                               lambda: wl.prefill_uplink(1, rows=(100, 121))[:2]),
+    "group_long_29x4096_g64_b3_kg2": (cfgd(29, 4096, 64, 64, 3, 2, GRP),
+                                      lambda: wl.long_context(0, rows=(0, 29), group=64)[:2]),
+    "group_long_13x4096_g128_b2_kg16": (cfgd(13, 4096, 128, 128, 2, 16, GRP),
+                                        lambda: wl.long_context(2, rows=(500, 513), group=128)[:2]),
+    "group_partial_chunk_7x4864_g256_b2_kg8": (cfgd(7, 4864, 256, 256, 2, 8, GRP), lambda: _affine(7, 4864, 256)),
+    "group_g8_partial_chunk_11x2888_b3_kg2": (cfgd(11, 2888, 8, 8, 3, 2, GRP), lambda: _affine(11, 2888, 8)),
+    "group_g32_full_lanes_13x2880_ga64_b4_kg8": (cfgd(13, 2880, 64, 32, 4, 8, GRP), lambda: _affine(13, 2880, 64)),
+    "group_wide_9x8192_ga128_gq256_b4_kg4": (cfgd(9, 8192, 128, 256, 4, 4, GRP), lambda: _affine(9, 8192, 128)),
+    "group_ties_zero_ref_6x512_g64_kg16": (cfgd(6, 512, 64, 64, 4, 16, GRP),
+                                           lambda: (wl.f32_to_bf16_bits(_zero_sum_integer_rows(6, 512, 64, 0, 0.0, 1)), None)),
+    "group_ties_exact_affine_7x1024_ga64_gq32_kg5": (cfgd(7, 1024, 64, 32, 4, 5, GRP), lambda: _dyadic_exact_rows(7, 1024, 3)),
+    "group_bf16_out_25x4096_g128_b4_kg2": (cfgd(25, 4096, 128, 128, 4, 2, GRP | rac.RAC_FLAG_XHAT_BF16),
+                                           lambda: wl.prefill_uplink(0, rows=(7, 32))[:2]),
+    "group_saturated_scales_13x4096_g128_b4_kg3": (cfgd(13, 4096, 128, 128, 4, 3, GRP),
+                                                   lambda: (_scaled(_affine(13, 4096, 128)[0], 2.0 ** 22), None)),
+    "group_signed_zero_6x1024_g128_b4_kg3": (cfgd(6, 1024, 128, 128, 4, 3, GRP),
+                                             lambda: _signed_zero_rows(6, 1024, False)),
+    "group_smallest_5x8_b4_kg2": (cfgd(5, 8, 8, 8, 4, 2, GRP), lambda: _affine(5, 8, 8)),
 }
 
 
@@ -203,6 +227,18 @@ def test_fixed_step_tiny():
     steps = _fixed_steps(512, 64)
     xb, rb, _ = wl.tiny(0)
     say(f"[gpu] fixed step tiny: steps[:3]={steps[:3]}")
+    rc, ow, ox = oracle.encode(xb, rb, steps, **c)
+    assert rc == 0
+    gw, gx, gd, gr = gpu_run(c, xb, rb, steps)
+    assert_parity(c, gw, gx, ow, ox)
+    assert np.array_equal(gx, gd) and np.array_equal(gx, gr)
+
+
+def test_fixed_step_tiny_with_group_outliers():
+    c = cfgd(64, 512, 64, 64, 4, 2, rac.RAC_FLAG_FIXED_STEP | GRP)
+    steps = _fixed_steps(512, 64)
+    xb, rb, _ = wl.tiny(0)
+    say("[gpu] fixed step tiny, two outliers per group")
     rc, ow, ox = oracle.encode(xb, rb, steps, **c)
     assert rc == 0
     gw, gx, gd, gr = gpu_run(c, xb, rb, steps)
@@ -305,6 +341,18 @@ def test_full_prefill_uplink_4096x4096_sampled():
     n = assert_parity(c, gw, gx, ow, ox, g_rows=rows, o_rows=slice(None))
     assert n == rows.size
     assert wirefmt.padding_is_zero(gw) and wirefmt.header(gw)["tokens"] == 4096
+
+
+def test_full_prefill_uplink_4096x4096_group_outliers_sampled():
+    c = cfgd(4096, 4096, 128, 128, 4, 1, GRP)
+    say("[gpu] full prefill uplink 4096x4096, one outlier per group: generating")
+    xb, rb, _ = wl.prefill_uplink(0)
+    gw, gx, gd, _ = gpu_run(c, xb, rb)
+    assert np.array_equal(gx, gd)
+    rows = _sample(4096, 48, seed=3)
+    ow, ox = oracle_run(dict(c, tokens=rows.size), xb[rows], rb[rows])
+    assert_parity(c, gw, gx, ow, ox, g_rows=rows, o_rows=slice(None))
+    assert wirefmt.padding_is_zero(gw) and wirefmt.header(gw)["off_ooff"] > 0
 
 
 def test_full_long_context_32768x4096_g128_b4_sampled():
