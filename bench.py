@@ -16,7 +16,9 @@ Prints ONE JSON line:
               launch / its average HIP-event duration, against 8 TB/s
   cpu_baseline the CPU oracle (single thread) on the same step
   extras      encode-only and decode-only rates, decode-phase µs per call at
-              batch 1/16/64/256 (GLM-4-9B-shaped, 4096 hidden)
+              batch 1/16/64/256 (GLM-4-9B-shaped, 4096 hidden), and the same
+              4096 x 4096 inputs coded with k_g outliers per quantization
+              group instead of per token (and with none, for comparison)
 """
 from __future__ import annotations
 
@@ -207,11 +209,64 @@ def main():
         extras["decode_step_graph_pair_us"] = {
             f"b{bits}_gq{gq}": decode_step_latency(torch, rac, wl, dev, stream, bits, gq, detail=False)
             for bits, gq in ((2, 128), (8, 128), (4, 4096))}
+        extras["outlier_modes_4096x4096_g128_b4"] = outlier_mode_rates(
+            torch, rac, sets, nsets, stream, args.steps)
     out["extras"] = extras
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(xb, rb, cfg)
     print(json.dumps(out), flush=True)
+
+
+def outlier_mode_rates(torch, rac, sets, nsets, stream, steps):
+    """Average launch time (HIP events around `steps` back-to-back launches
+    over the rotating buffer sets) of rac_encode and of rac_decode on the
+    benchmark inputs with other outlier settings: k_g = 1, 2, 4 outliers per
+    quantization group (u8 offsets), and none.  Each entry gives µs, the
+    fraction of 8 TB/s by algorithmic bytes, and the wire size relative to
+    the bf16 tensor."""
+    res = {}
+    variants = {"none": (0, 0), "per_group_kg1": (1, rac.RAC_FLAG_GROUP_OUTLIERS),
+                "per_group_kg2": (2, rac.RAC_FLAG_GROUP_OUTLIERS),
+                "per_group_kg4": (4, rac.RAC_FLAG_GROUP_OUTLIERS)}
+    T, d = 4096, 4096
+    for name, (k, flags) in variants.items():
+        cfg = rac.RacConfig(T, d, 128, 128, 4, k, flags)
+        wb = rac.rac_wire_size(cfg)
+        wires = [torch.empty(wb, dtype=torch.uint8, device="cuda") for _ in range(nsets)]
+
+        def enc(i):
+            s = sets[i % nsets]
+            rac.rac_encode(cfg, s["x"], s["ref"], None, wires[i % nsets], s["xhat"], stream=stream)
+
+        def dec(i):
+            s = sets[i % nsets]
+            rac.rac_decode(cfg, wires[i % nsets], s["ref"], None, s["xdec"], stream=stream)
+
+        for i in range(2 * nsets):
+            enc(i)
+            dec(i)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for i in range(steps):
+            enc(i)
+        ev[1].record(stream)
+        for i in range(steps):
+            dec(i)
+        ev[2].record(stream)
+        torch.cuda.synchronize()
+        assert torch.equal(sets[0]["xhat"], sets[0]["xdec"]), name
+        e_us = ev[0].elapsed_time(ev[1]) / steps * 1e3
+        d_us = ev[1].elapsed_time(ev[2]) / steps * 1e3
+        res[name] = {"encode_us": round(e_us, 2),
+                     "encode_hbm_frac": round(algorithmic_bytes(T, d, wb) / e_us / 1e3 / HBM_PEAK_GBPS, 4),
+                     "decode_us": round(d_us, 2),
+                     "decode_hbm_frac": round(algorithmic_bytes(T, d, wb, encode=False) / d_us / 1e3
+                                              / HBM_PEAK_GBPS, 4),
+                     "wire_over_bf16": round(wb / (T * d * 2), 4)}
+        del wires
+    return res
 
 
 def decode_step_latency(torch, rac, wl, dev, stream, bits=4, gq=128, detail=True):

@@ -675,65 +675,108 @@ __device__ __forceinline__ void append8(RowShared& S, uint32_t* counter, const f
 // packet carries in-group offsets and fp16 values).  A group of g_q <= 256
 // channels is 2^lv lanes of one wavefront, so the choice is wave-local.
 
-// Unsigned max over the 2^lv lanes of an aligned block.
+// Signed max over the 2^lv lanes of an aligned block.
 template <int LV>
-__device__ __forceinline__ uint32_t umax_lanes(uint32_t v, int lv) {
+__device__ __forceinline__ int32_t imax_lanes(int32_t v, int lv) {
     const int L = LV >= 0 ? LV : lv;
-    if (L > 0) v = __builtin_elementwise_max(v, dpp_u<0xB1>(v));
-    if (L > 1) v = __builtin_elementwise_max(v, dpp_u<0x4E>(v));
-    if (L > 2) v = __builtin_elementwise_max(v, dpp_u<0x141>(v));
-    if (L > 3) v = __builtin_elementwise_max(v, dpp_u<0x140>(v));
+    auto dmax = [](int32_t a, int32_t b) { return a > b ? a : b; };
+    if (L > 0) v = dmax(v, __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false));
+    if (L > 1) v = dmax(v, __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false));
+    if (L > 2) v = dmax(v, __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false));
+    if (L > 3) v = dmax(v, __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false));
     if (L > 4) {
-        auto p = __builtin_amdgcn_permlane16_swap((int)v, (int)v, false, false);
-        v = __builtin_elementwise_max((uint32_t)p[0], (uint32_t)p[1]);
+        auto p = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+        v = dmax((int32_t)p[0], (int32_t)p[1]);
     }
     return v;
 }
 
+// One bit at the first lane of every aligned block of 2^lv lanes.
+__device__ __forceinline__ uint64_t block_starts(int lv) {
+    switch (lv) {
+        case 0: return ~0ull;
+        case 1: return 0x5555555555555555ull;
+        case 2: return 0x1111111111111111ull;
+        case 3: return 0x0101010101010101ull;
+        case 4: return 0x0001000100010001ull;
+        default: return 0x0000000100000001ull;
+    }
+}
+
+// The lowest set bit of every aligned block of 2^lv bits of a lane mask
+// (scalar work: an OR-prefix inside the blocks, then the bits with nothing
+// set below them in their block).
+__device__ __forceinline__ uint64_t block_firsts(uint64_t x, int lv, uint64_t starts) {
+    uint64_t p = x;
+    for (int s = 1; s < (1 << lv); s <<= 1) p |= (p << s) & ~(starts * ((1ull << s) - 1ull));
+    return x & ~((p << 1) & ~starts);
+}
+
 // Chooses the k_g outliers of the lane's group and returns the lane's mask of
 // chosen channels (bit j = channel c0 + j).  k_g rounds, each taking the
-// group's largest remaining key and, among lanes holding it, the lowest
-// channel.  A key is the |E| pattern plus one, so a zero residual still
-// outranks a chosen element (key 0); k_g < g_q leaves every round a
-// candidate.  The entries, (fp16 value | in-group offset << 16), go to `st`
-// at their position in the chunk's part of the row: group by group, ascending
-// offset inside a group.
+// group's largest remaining |E| and, among the channels holding it, the
+// lowest.  Magnitudes are compared as the integer patterns of |E|, a chosen
+// channel drops to -1, so a zero residual still outranks it, and k_g < g_q
+// leaves every round a candidate.  The tie-break is scalar work on the
+// wave-wide masks of lanes whose channel j holds the group maximum.  The
+// entries, (fp16 value | in-group offset << 16), go to `st` at their position
+// in the chunk's part of the row: group by group, ascending offset inside a
+// group.
 template <int LV>
 __device__ __forceinline__ uint32_t select_group_outliers(const float* e, int lv, int kg, uint32_t lane,
                                                           uint32_t* st) {
-    uint32_t key[8];
+    const int L = LV >= 0 ? LV : lv;
+    int32_t a[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) key[j] = (__float_as_uint(e[j]) & 0x7FFFFFFFu) + 1u;
-    const uint32_t g0 = lane & ~((1u << lv) - 1u);  // first lane of the group
-    const uint32_t gmask = (uint32_t)((1ull << (1u << lv)) - 1ull);  // groups span at most 32 lanes
-    uint32_t selm = 0u;
+    for (int j = 0; j < 8; ++j) a[j] = (int32_t)(__float_as_uint(e[j]) & 0x7FFFFFFFu);
+    const uint64_t starts = block_starts(L);
+    uint64_t sel[8], pick[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sel[j] = pick[j] = 0ull;
     for (int i = 0; i < kg; ++i) {
-        uint32_t lb = 0u;
+        if (i > 0) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) lb = __builtin_elementwise_max(lb, key[j]);
-        const uint32_t m = umax_lanes<LV>(lb, lv);
-        uint32_t hit = 0u;
+            for (int j = 0; j < 8; ++j) a[j] = __builtin_amdgcn_inverse_ballot_w64(pick[j]) ? -1 : a[j];
+        }
+        int32_t lb = a[0];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) hit |= (uint32_t)(key[j] == m) << j;
-        const uint32_t holders = (uint32_t)(ballot(hit != 0u) >> g0) & gmask;
-        const uint32_t pick = (lane - g0 == (uint32_t)__builtin_ctz(holders)) ? (hit & (0u - hit)) : 0u;
-        selm |= pick;
+        for (int j = 1; j < 8; ++j) lb = lb > a[j] ? lb : a[j];
+        const int32_t m = imax_lanes<LV>(lb, L);
+        uint64_t hit[8], any = 0ull;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) key[j] = ((pick >> j) & 1u) ? 0u : key[j];
+        for (int j = 0; j < 8; ++j) {
+            hit[j] = ballot(a[j] == m);
+            any |= hit[j];
+        }
+        uint64_t free_lanes = block_firsts(any, L, starts);  // one lane per group
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            pick[j] = hit[j] & free_lanes;
+            free_lanes &= ~pick[j];
+            sel[j] |= pick[j];
+        }
     }
+    uint32_t selm = 0u;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) selm |= __builtin_amdgcn_inverse_ballot_w64(sel[j]) ? (1u << j) : 0u;
     // slot of the lane's first entry: chosen channels of the group's lower
-    // lanes (counts <= 8 summed bit by bit over ballots)
-    const uint32_t cnt = (uint32_t)__builtin_popcount(selm);
-    const uint64_t below = ((1ull << lane) - 1ull) & ~((1ull << g0) - 1ull);
-    uint32_t slot = (lane >> lv) * (uint32_t)kg;
+    // lanes, summed bit by bit over ballots of the per-lane counts (k_g = 1:
+    // the group's one entry)
+    uint32_t slot = (lane >> L) * (uint32_t)kg;
+    if (kg > 1) {
+        const uint32_t cnt = (uint32_t)__builtin_popcount(selm);
+        const uint32_t g0 = lane & ~((1u << L) - 1u);
+        const uint64_t below = ((1ull << lane) - 1ull) & ~((1ull << g0) - 1ull);
+        const int nb = kg >= 8 ? 4 : (kg >= 4 ? 3 : 2);
+        for (int b = 0; b < nb; ++b)
+            slot += (uint32_t)__builtin_popcountll(ballot((cnt >> b) & 1u) & below) << b;
+    }
+    const uint32_t o0 = (lane & ((1u << L) - 1u)) * 8u;
 #pragma unroll
-    for (int b = 0; b < 4; ++b)
-        slot += (uint32_t)__builtin_popcountll(ballot((cnt >> b) & 1u) & below) << b;
-    if (selm) {
-        const uint32_t o0 = (lane - g0) * 8u;
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-            if ((selm >> j) & 1u) st[slot++] = f16_rne_sat(e[j]) | ((o0 + (uint32_t)j) << 16);
+    for (int j = 0; j < 8; ++j) {
+        if (sel[j] != 0ull && __builtin_amdgcn_inverse_ballot_w64(sel[j]))
+            st[slot] = f16_rne_sat(e[j]) | ((o0 + (uint32_t)j) << 16);
+        slot += (selm >> j) & 1u;
     }
     return selm;
 }
@@ -924,7 +967,8 @@ __device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S,
 // read from the arguments at run time.  OM is the outlier mode: 0 none, 1 the
 // k largest |E| per token row, 2 the k_g largest per quantization group.
 template <int BITS, int GA, int GQ, int OM>
-__global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
+__global__ __launch_bounds__(kWave * kMaxWaves) __attribute__((amdgpu_waves_per_eu(OM == 2 && GQ >= 0 ? 6 : 1)))
+void rac_encode_kernel(Args A) {
     // LDS state of a row, double-buffered by row parity: every row that uses
     // LDS has a workgroup barrier, so no wave is more than one row ahead.
     __shared__ RowShared SS[2];
@@ -1056,7 +1100,12 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
         if (selm) {
 #pragma unroll
             for (int j = 0; j < 8; ++j)
-                if ((selm >> j) & 1u) ed[j] = 0.0f;
+                if ((selm >> j) & 1u) {
+                    ed[j] = 0.0f;
+                    // per-group mode: R~ of a chosen channel becomes its
+                    // reconstruction R~ + O-hat now, so E is dead from here on
+                    if constexpr (OM == 2) rt[j] = rt[j] + f16_value(f16_rne_sat(e[j]));
+                }
         }
 
         // a5: scale of the quantization group
@@ -1110,7 +1159,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_encode_kernel(Args A) {
         if (selm) {
 #pragma unroll
             for (int j = 0; j < 8; ++j)
-                if ((selm >> j) & 1u) H[j] = rt[j] + f16_value(f16_rne_sat(e[j]));
+                if ((selm >> j) & 1u) H[j] = OM == 2 ? rt[j] : rt[j] + f16_value(f16_rne_sat(e[j]));
         }
         const uint32_t crb = (uint32_t)A.code_row_bytes;
         store_codes<BITS>(rsrc(A.codes, (uint64_t)row * crb, crb), w, lane, dword3, pk);

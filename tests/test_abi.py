@@ -54,6 +54,12 @@ CFGS = [
     dict(tokens=0, hidden=512, group_align=64, group_quant=64, bits=8),
     dict(tokens=7, hidden=520, group_align=8, group_quant=8, bits=3, outlier_k=64,
          flags=rac.RAC_FLAG_FIXED_STEP),
+    dict(tokens=4096, hidden=4096, group_align=128, group_quant=128, bits=4, outlier_k=1,
+         flags=rac.RAC_FLAG_GROUP_OUTLIERS),
+    dict(tokens=9, hidden=4864, group_align=256, group_quant=256, bits=2, outlier_k=16,
+         flags=rac.RAC_FLAG_GROUP_OUTLIERS | rac.RAC_FLAG_FIXED_STEP),
+    dict(tokens=5, hidden=2888, group_align=8, group_quant=8, bits=3, outlier_k=2,
+         flags=rac.RAC_FLAG_GROUP_OUTLIERS),
 ]
 
 
@@ -93,10 +99,47 @@ def test_parse_header_reads_oracle_headers(lib):
             rc, wire, _ = oracle.encode(xb, ref, steps, want_xhat=False, **small)
             assert rc == 0
             cfg, zero_ref = rac.rac_parse_header(wire[:256].tobytes())
-            want = dict(small, flags=small.get("flags", 0) & rac.RAC_FLAG_FIXED_STEP)
+            want = dict(small, flags=small.get("flags", 0) & (rac.RAC_FLAG_FIXED_STEP |
+                                                              rac.RAC_FLAG_GROUP_OUTLIERS))
             want.setdefault("outlier_k", 0)
             assert cfg == rac.RacConfig(**want)
             assert zero_ref == (ref is None)
+
+
+def test_group_outlier_configs_outside_the_domain_are_rejected(lib):
+    G = rac.RAC_FLAG_GROUP_OUTLIERS
+    base = dict(tokens=4, hidden=512, group_align=64, group_quant=64, bits=4, outlier_k=2, flags=G)
+    assert rac.rac_wire_size(rac.RacConfig(**base)) > 0
+    for bad in [dict(group_quant=512), dict(outlier_k=0), dict(outlier_k=17), dict(outlier_k=17, group_quant=256),
+                dict(group_quant=16, outlier_k=5), dict(group_quant=8, outlier_k=3)]:
+        cfg = rac.RacConfig(**dict(base, **bad))
+        assert rac.rac_wire_size(cfg) == 0, bad
+        assert _encode(cfg) == 1 and _decode(cfg) == 1
+
+
+def test_group_outlier_payload_of_the_prefill_uplink_shape(lib):
+    cfg = rac.RacConfig(4096, 4096, 128, 128, 4, 1, rac.RAC_FLAG_GROUP_OUTLIERS)
+    ratio = rac.rac_wire_size(cfg) / (4096 * 4096 * 2)
+    # 4-bit codes + fp16 scale/coef + one (u8 offset, fp16 value) per group of 128
+    assert abs(ratio - (0.25 + 6 / 256 + 3 / 256)) < 1e-5
+
+
+def test_parse_header_rejects_corruption_of_group_outlier_headers(lib):
+    c = dict(tokens=2, hidden=256, group_align=64, group_quant=64, bits=4, outlier_k=2,
+             flags=rac.RAC_FLAG_GROUP_OUTLIERS)
+    xb = wl.f32_to_bf16_bits(np.random.default_rng(0).standard_normal((2, 256)))
+    rc, wire, _ = oracle.encode(xb, None, want_xhat=False, **c)
+    good = wire[:256].tobytes()
+    cfg, _ = rac.rac_parse_header(good)
+    assert cfg == rac.RacConfig(**c)
+    # flags 9 (both outlier kinds), format 1 with flag 8, a moved offset array,
+    # k_g above a quarter of the group, a byte past the fields
+    for off, val in [(6, 9), (27, 1), (73, 0), (28, 17), (80, 1)]:
+        bad = bytearray(good)
+        bad[off] = val
+        with pytest.raises(rac.RacError) as e:
+            rac.rac_parse_header(bytes(bad))
+        assert e.value.status == 5, off
 
 
 def test_parse_header_rejects_corruption(lib):
