@@ -211,6 +211,7 @@ def main():
             for bits, gq in ((2, 128), (8, 128), (4, 4096))}
         extras["outlier_modes_4096x4096_g128_b4"] = outlier_mode_rates(
             torch, rac, sets, nsets, stream, args.steps)
+        extras["gathered_reference"] = gather_rates(torch, rac, cfg, rb, sets, nsets, stream, args.steps)
     out["extras"] = extras
 
     if not args.no_cpu_baseline:
@@ -267,6 +268,54 @@ def outlier_mode_rates(torch, rac, sets, nsets, stream, steps):
                      "wire_over_bf16": round(wb / (T * d * 2), 4)}
         del wires
     return res
+
+
+def gather_rates(torch, rac, cfg, rb, sets, nsets, stream, steps):
+    """rac_encode_gather / rac_decode_gather on the benchmark configuration:
+    each row's reference sits at a random row of an 8192-row bf16 store of
+    earlier rows (one store per buffer set), a fifth of the rows name no row
+    (zero reference).  Average launch time over `steps` back-to-back launches,
+    next to the same calls with the reference materialized."""
+    T, d = cfg.tokens, cfg.hidden
+    rng = np.random.default_rng(11)
+    pos = rng.permutation(2 * T)[:T].astype(np.int32)
+    pos[rng.random(T) < 0.2] = -1
+    idx = torch.from_numpy(pos).cuda()
+    stores = []
+    for i in range(nsets):
+        st = torch.zeros(2 * T, d, dtype=torch.int16, device="cuda")
+        ok = idx >= 0
+        st[idx[ok].long()] = sets[i]["ref"][ok]
+        stores.append(st)
+    wb = rac.rac_wire_size(cfg)
+    wires = [torch.empty(wb, dtype=torch.uint8, device="cuda") for _ in range(nsets)]
+
+    def enc(i):
+        s = sets[i % nsets]
+        rac.rac_encode_gather(cfg, s["x"], stores[i % nsets], idx, None, wires[i % nsets], s["xhat"], stream=stream)
+
+    def dec(i):
+        s = sets[i % nsets]
+        rac.rac_decode_gather(cfg, wires[i % nsets], stores[i % nsets], idx, None, s["xdec"], stream=stream)
+
+    for i in range(2 * nsets):
+        enc(i)
+        dec(i)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    for i in range(steps):
+        enc(i)
+    ev[1].record(stream)
+    for i in range(steps):
+        dec(i)
+    ev[2].record(stream)
+    torch.cuda.synchronize()
+    assert torch.equal(sets[0]["xhat"], sets[0]["xdec"])
+    del stores, wires
+    return {"store_rows": 2 * T, "miss_fraction": round(float((pos < 0).mean()), 4),
+            "encode_us": round(ev[0].elapsed_time(ev[1]) / steps * 1e3, 2),
+            "decode_us": round(ev[1].elapsed_time(ev[2]) / steps * 1e3, 2)}
 
 
 def decode_step_latency(torch, rac, wl, dev, stream, bits=4, gq=128, detail=True):

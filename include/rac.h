@@ -174,6 +174,33 @@ rac_status rac_reconstruct(const rac_config* cfg, const void* wire, const void* 
 rac_status rac_decode(const rac_config* cfg, const void* wire, const void* ref,
                       const float* fixed_steps, void* xhat, rac_stream_t stream);
 
+/* Encode against a gathered reference (the prefill uplink's retrieved spans):
+ * the reference of token row t is row ref_rows[t] of `ref_store`, a
+ * device-resident store of earlier reconstructions kept as bf16 (for example
+ * the XHAT_BF16 output of earlier calls, which sender and receiver hold
+ * bit-identical).  The reference rows are read from the store inside the
+ * encode kernel, so the [T][d] reference is never materialized.  Everything
+ * else is rac_encode: same wire, same reconstruction as rac_encode with a
+ * reference whose row t is that store row.
+ *   ref_store  : bf16 [store_rows][d], 16-byte aligned, or NULL for a zero
+ *                reference on every row (then ref_rows is ignored)
+ *   store_rows : 0 <= store_rows < 2^31
+ *   ref_rows   : int32 [T] device array, 4-byte aligned, required with a
+ *                store.  A negative index, or one >= store_rows, gives that
+ *                token a zero reference row (no span hit); the kernels never
+ *                read outside the store.
+ * Errors as rac_encode, plus RAC_ERR_INVALID for a store without ref_rows or
+ * store_rows out of range.  One kernel launch. */
+rac_status rac_encode_gather(const rac_config* cfg, const void* x, const void* ref_store, int64_t store_rows,
+                             const int32_t* ref_rows, const float* fixed_steps, void* wire, size_t wire_cap,
+                             void* xhat, rac_stream_t stream);
+
+/* Receiver side of rac_encode_gather: rac_decode with the reference of token
+ * row t taken from row ref_rows[t] of the receiver's own store (arguments as
+ * in rac_encode_gather; the result equals rac_decode with that reference). */
+rac_status rac_decode_gather(const rac_config* cfg, const void* wire, const void* ref_store, int64_t store_rows,
+                             const int32_t* ref_rows, const float* fixed_steps, void* xhat, rac_stream_t stream);
+
 /* Static string naming a status code. */
 const char* rac_status_string(rac_status s);
 

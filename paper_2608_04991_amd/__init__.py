@@ -22,7 +22,8 @@ __all__ = [
     "RacConfig", "RacError", "RAC_FLAG_FIXED_STEP", "RAC_FLAG_XHAT_BF16", "RAC_FLAG_GROUP_OUTLIERS",
     "STATUS",
     "library", "library_path", "rac_wire_layout", "rac_wire_size", "rac_parse_header",
-    "rac_encode", "rac_reconstruct", "rac_decode", "rac_status_string",
+    "rac_encode", "rac_reconstruct", "rac_decode", "rac_encode_gather", "rac_decode_gather",
+    "rac_status_string",
 ]
 
 RAC_FLAG_FIXED_STEP = 1
@@ -97,6 +98,10 @@ def library():
         L.rac_reconstruct.restype = ctypes.c_int
         L.rac_decode.argtypes = [cp, vp, vp, vp, vp, vp]
         L.rac_decode.restype = ctypes.c_int
+        L.rac_encode_gather.argtypes = [cp, vp, vp, ctypes.c_int64, vp, vp, vp, ctypes.c_size_t, vp, vp]
+        L.rac_encode_gather.restype = ctypes.c_int
+        L.rac_decode_gather.argtypes = [cp, vp, vp, ctypes.c_int64, vp, vp, vp, vp]
+        L.rac_decode_gather.restype = ctypes.c_int
         L.rac_status_string.argtypes = [ctypes.c_int]
         L.rac_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -174,3 +179,27 @@ def rac_decode(cfg: RacConfig, wire, ref, fixed_steps, xhat, stream=None) -> Non
     """Receiver-side reconstruction from a wire and the receiver's reference."""
     _check(library().rac_decode(ctypes.byref(cfg._c()), _ptr(wire), _ptr(ref),
                                 _ptr(fixed_steps), _ptr(xhat), _stream(stream)), "rac_decode")
+
+
+def _rows(store, store_rows):
+    if store_rows is not None:
+        return int(store_rows)
+    return 0 if store is None or isinstance(store, int) else int(store.shape[0])
+
+
+def rac_encode_gather(cfg: RacConfig, x, store, ref_rows, fixed_steps, wire, xhat=None, stream=None,
+                      store_rows: int | None = None, wire_cap: int | None = None) -> None:
+    """Encode x against the store rows that ref_rows names (int32 [T]; an index
+    outside the store means a zero reference row)."""
+    cap = wire_cap if wire_cap is not None else (_nbytes(wire) if not isinstance(wire, int) else 0)
+    _check(library().rac_encode_gather(ctypes.byref(cfg._c()), _ptr(x), _ptr(store), _rows(store, store_rows),
+                                       _ptr(ref_rows), _ptr(fixed_steps), _ptr(wire), cap, _ptr(xhat),
+                                       _stream(stream)), "rac_encode_gather")
+
+
+def rac_decode_gather(cfg: RacConfig, wire, store, ref_rows, fixed_steps, xhat, stream=None,
+                      store_rows: int | None = None) -> None:
+    """Receiver-side reconstruction with the reference gathered from a store."""
+    _check(library().rac_decode_gather(ctypes.byref(cfg._c()), _ptr(wire), _ptr(store), _rows(store, store_rows),
+                                       _ptr(ref_rows), _ptr(fixed_steps), _ptr(xhat), _stream(stream)),
+           "rac_decode_gather")

@@ -45,7 +45,9 @@ constexpr float kNearHalf = 0.5f - 0x1p-14f;
 struct alignas(8) Args {
     // hot-path fields
     const uint16_t* x;
-    const uint16_t* ref;
+    const uint16_t* ref;      // the reference, or with ref_rows the store its rows come from
+    const int32_t* ref_rows;  // per token row: the store row of its reference (NULL: row t of ref)
+    uint32_t store_rows;
     const float* steps;
     uint32_t* coef;     // wire sections
     uint16_t* scale;
@@ -607,6 +609,46 @@ __device__ __forceinline__ Rsrc xhat_row(const Args& A, uint32_t row) {
                 A.xhat ? (uint32_t)A.d * es : 0u);
 }
 
+// Store-row indices of the rows a workgroup takes, 64 rows at a time in LDS:
+// slot i holds the index of the workgroup's row n0 + i, that is token row
+// blockIdx.x + (n0 + i) * gridDim.x (-1 past the last token).  Every
+// wavefront of the workgroup calls this at the same row counts (n0 a multiple
+// of 64), and the barriers keep the previous 64 in place until all have read
+// them.  Nothing happens without a row index array.
+__device__ __forceinline__ void fill_ref_rows(const Args& A, int32_t* rix, uint32_t n0) {
+    if (!A.ref_rows) return;
+    __syncthreads();
+    if (threadIdx.x < (uint32_t)kWave) {
+        const uint64_t r = (uint64_t)blockIdx.x + (uint64_t)(n0 + threadIdx.x) * gridDim.x;
+        rix[threadIdx.x] = r < A.tokens ? A.ref_rows[r] : -1;
+    }
+    __syncthreads();
+}
+
+__device__ __forceinline__ int32_t ref_index(const Args& A, const int32_t* rix, uint32_t n) {
+    return A.ref_rows ? rix[n & (uint32_t)(kWave - 1)] : 0;
+}
+
+// The index of the workgroup's first row, read directly (a scalar load), so
+// that the first row's loads need not wait for the LDS copy.
+__device__ __forceinline__ int32_t first_ref_index(const Args& A) {
+    return (A.ref_rows && blockIdx.x < A.tokens) ? A.ref_rows[blockIdx.x] : 0;
+}
+
+// Buffer resource of token row `row`'s reference: row `row` of ref, or, with
+// a row index array, store row `ix`.  A missing reference, a row past the
+// last token (`in` false) and an index outside the store give an empty range,
+// which reads as a zero reference row.
+__device__ __forceinline__ Rsrc ref_row(const Args& A, uint32_t row, bool in, int32_t ix) {
+    uint32_t r = row;
+    bool ok = in && A.ref != nullptr;
+    if (A.ref_rows) {
+        ok = ok && ix >= 0 && (uint32_t)ix < A.store_rows;
+        r = ok ? (uint32_t)ix : 0u;
+    }
+    return rsrc(A.ref, (uint64_t)r * (uint64_t)A.d, ok ? (uint32_t)A.d * 2u : 0u);
+}
+
 // Workgroup-shared state of one row.
 struct alignas(16) RowShared {
     uint32_t smax[kWave];           // max |E| bits over lane l of every wave (threshold search)
@@ -972,6 +1014,7 @@ void rac_encode_kernel(Args A) {
     // LDS state of a row, double-buffered by row parity: every row that uses
     // LDS has a workgroup barrier, so no wave is more than one row ahead.
     __shared__ RowShared SS[2];
+    __shared__ int32_t RIX[kWave];  // store rows of the reference (gathered references only)
     extern __shared__ float4 XT[];  // per-wavefront store staging, kSlice each (sized at launch)
     const uint32_t lane = threadIdx.x & (kWave - 1);
     const int w = (int)(threadIdx.x / kWave);
@@ -1011,23 +1054,26 @@ void rac_encode_kernel(Args A) {
     // x and ref of row `rw` for this lane (zeros past the last row, past the
     // end of the row and for a zero reference)
     const uint32_t row_bytes = (uint32_t)d * 2u;
-    auto load_row = [&](uint32_t rw, uint4& vx, uint4& vr) {
+    // (nn: the row's position among the workgroup's rows)
+    auto load_row = [&](uint32_t rw, int32_t ix, uint4& vx, uint4& vr) {
         const bool in = rw < A.tokens;
         const uint64_t o = (uint64_t)(in ? rw : 0) * (uint64_t)d;
         vx = bload128(rsrc(A.x, o, in ? row_bytes : 0u), (uint32_t)c0 * 2u);
-        vr = bload128(rsrc(A.ref, o, (in && A.ref) ? row_bytes : 0u), (uint32_t)c0 * 2u);
+        vr = bload128(ref_row(A, rw, in, ix), (uint32_t)c0 * 2u);
     };
     uint32_t row = blockIdx.x;
     uint4 nx, nr;
-    load_row(row, nx, nr);
+    load_row(row, first_ref_index(A), nx, nr);
     // Let the first row land before the loop: then the loop head holds no
     // wait, and inside the loop only the prefetched loads are waited for
     // (never the stores of the row before).
     __builtin_amdgcn_s_waitcnt(kWaitVmem0);
+    fill_ref_rows(A, RIX, 0u);
     for (uint32_t n = 0; row < A.tokens; row += gridDim.x, ++n) {
         RowShared& S = SS[n & 1];
         const uint4 xv = nx, rv = nr;
-        load_row(row + gridDim.x, nx, nr);
+        if (((n + 1u) & (uint32_t)(kWave - 1)) == 0u) fill_ref_rows(A, RIX, n + 1u);
+        load_row(row + gridDim.x, ref_index(A, RIX, n + 1u), nx, nr);
         float r[8], x[8];
         widen8(rv, r);
         widen8(xv, x);
@@ -1304,6 +1350,7 @@ void rac_encode_rows_kernel(Args A) {
     // first channel of the wavefront's i-th chunk: chunks are dealt round the
     // wavefronts, so a row of fewer than NW * CPW chunks stays balanced
     auto chunk_at = [&](int i) { return (w + i * NW) * kChunk; };
+    __shared__ int32_t RIX[kWave];  // store rows of the reference (gathered references only)
     if (w == 0 && lane < 2u) {
         S.cnt[lane] = 0u;
         S.xn[lane] = 0u;
@@ -1318,7 +1365,7 @@ void rac_encode_rows_kernel(Args A) {
         const uint32_t row = blockIdx.x;
         const bool any = row < A.tokens;
         const uint64_t o = (uint64_t)row * (uint64_t)d;
-        const Rsrc rx = rsrc(A.x, o, any ? row_bytes : 0u), rr = rsrc(A.ref, o, (A.ref && any) ? row_bytes : 0u);
+        const Rsrc rx = rsrc(A.x, o, any ? row_bytes : 0u), rr = ref_row(A, row, any, first_ref_index(A));
 #pragma unroll
         for (int i = 0; i < CPW; ++i) {
             const uint32_t off = ((uint32_t)(chunk_at(i)) + lane * 8u) * 2u;  // past the row: reads 0
@@ -1326,6 +1373,7 @@ void rac_encode_rows_kernel(Args A) {
             rp[i] = bload128(rr, off);
         }
     }
+    fill_ref_rows(A, RIX, 0u);
     // A store that the range check drops, so that stores are outstanding at
     // the loop entry as they are at the end of every row: the compiler's wait
     // analysis then keeps the memory operations in order across the loop and
@@ -1350,7 +1398,8 @@ void rac_encode_rows_kernel(Args A) {
         const uint32_t nrow = row + gridDim.x;
         const bool more = nrow < A.tokens;
         const uint64_t on = (uint64_t)nrow * (uint64_t)d;
-        const Rsrc nx = rsrc(A.x, on, more ? row_bytes : 0u), nr = rsrc(A.ref, on, (A.ref && more) ? row_bytes : 0u);
+        if (((n + 1u) & (uint32_t)(kWave - 1)) == 0u) fill_ref_rows(A, RIX, n + 1u);
+        const Rsrc nx = rsrc(A.x, on, more ? row_bytes : 0u), nr = ref_row(A, nrow, more, ref_index(A, RIX, n + 1u));
         uint32_t cf[CPW];
 #pragma unroll
         for (int i = 0; i < CPW; ++i) cf[i] = 0u;
@@ -1639,6 +1688,7 @@ void rac_encode_rows_kernel(Args A) {
 
 template <int BITS, int OM, bool BF16>
 __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
+    __shared__ int32_t RIX[kWave];  // store rows of the reference (gathered references only)
     extern __shared__ float4 XT[];  // per-wavefront store staging, kSlice each (sized at launch)
     const uint32_t lane = threadIdx.x & (kWave - 1);
     const int w = (int)(threadIdx.x / kWave);
@@ -1665,12 +1715,11 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
     // (zeros past the last row and past the end of the row; entries of lanes
     // >= k are never read)
     const uint32_t crb = (uint32_t)A.code_row_bytes;
-    auto load = [&](uint32_t rw) {
+    auto load = [&](uint32_t rw, int32_t ix) {
         const bool in_range = rw < A.tokens;
         const uint64_t r = (uint64_t)(in_range ? rw : 0);
         In in;
-        in.rv = bload128(rsrc(A.ref, r * (uint64_t)d, (in_range && A.ref) ? (uint32_t)d * 2u : 0u),
-                         (uint32_t)c0 * 2u);
+        in.rv = bload128(ref_row(A, rw, in_range, ix), (uint32_t)c0 * 2u);
         in.cf = bload32(rsrc(A.coef, r * nga, in_range ? nga * 4u : 0u), (uint32_t)grp_a * 4u);
         in.sh = bload16(rsrc(A.scale, r * ngq, (in_range && !A.fixed) ? ngq * 2u : 0u), (uint32_t)grp_q * 2u);
         if (A.fixed) in.sh = sh_fixed;
@@ -1693,15 +1742,16 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
     // These are gathered first (just read by the owning lanes, so the reads
     // hit in cache), then the next-but-one row is prefetched into `nx`, so
     // waiting for the gathers does not wait for the prefetch.
-    auto row_body = [&](const In& in, uint32_t row, In& nx, uint32_t nrow) {
+    auto row_body = [&](const In& in, uint32_t row, uint32_t n, In& nx, uint32_t nrow) {
         const uint32_t ech = in.ent & 0xFFFFu;
         const bool pch = OUTL & (lane < (uint32_t)k) & (ech < (uint32_t)d) & ((ech >> 9) == (uint32_t)w);
         uint32_t gref = 0u, gcf = 0u;
         if constexpr (OUTL) {
-            gref = bload16(rsrc(A.ref, (uint64_t)row * (uint64_t)d, A.ref ? (uint32_t)d * 2u : 0u), pch ? ech * 2u : kOut);
+            gref = bload16(ref_row(A, row, true, ref_index(A, RIX, n)), pch ? ech * 2u : kOut);
             gcf = bload32(rsrc(A.coef, (uint64_t)row * nga, nga * 4u), pch ? (ech >> A.lg_a) * 4u : kOut);
         }
-        nx = load(nrow);
+        if (((n + 1u) & (uint32_t)(kWave - 1)) == 0u) fill_ref_rows(A, RIX, n + 1u);
+        nx = load(nrow, ref_index(A, RIX, n + 1u));
         const float a = f16_value(in.cf & 0xFFFFu), b0 = f16_value(in.cf >> 16);
         const float s = f16_value(in.sh);
         float r[8], rt[8], H[8];
@@ -1747,15 +1797,16 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
     // for a prefetch before its row starts.
     const uint32_t G = gridDim.x;
     uint32_t row = blockIdx.x;
-    In p = load(row), q;
+    In p = load(row, first_ref_index(A)), q;
+    fill_ref_rows(A, RIX, 0u);
     // (a store that the range check drops, so that stores are outstanding at
     // the loop entry as at the end of every row; the compiler's wait analysis
     // then keeps later waits exact instead of waiting for everything)
     bstore32(rsrc(A.coef, 0, 0u), kOut, 0u);
-    for (; row < A.tokens; row += 2u * G) {
-        row_body(p, row, q, row + G);
+    for (uint32_t n = 0; row < A.tokens; row += 2u * G, n += 2u) {
+        row_body(p, row, n, q, row + G);
         if (row + G >= A.tokens) break;
-        row_body(q, row + G, p, row + 2u * G);
+        row_body(q, row + G, n + 1u, p, row + 2u * G);
     }
 }
 
@@ -2006,12 +2057,24 @@ rac_status common_checks(const rac_config* cfg) {
     return RAC_OK;
 }
 
+// A gathered reference: a store of store_rows rows and one int32 index per
+// token row (NULL ref_rows: the reference is ref itself, one row per token).
+rac_status check_gather(const void* store, int64_t store_rows, const int32_t* ref_rows, bool gather) {
+    if (!gather) return RAC_OK;
+    if (store_rows < 0 || store_rows > 0x7FFFFFFFll) return RAC_ERR_INVALID;
+    if (store && !ref_rows) return RAC_ERR_INVALID;
+    if (ref_rows && !aligned(ref_rows, 4)) return RAC_ERR_ALIGN;
+    return RAC_OK;
+}
+
 rac_status run_decode(const rac_config* cfg, const void* wire, const void* ref, const float* steps,
-                      void* xhat, hipStream_t stream) {
+                      void* xhat, hipStream_t stream, bool gather = false, int64_t store_rows = 0,
+                      const int32_t* ref_rows = nullptr) {
     rac_status st = common_checks(cfg);
     if (st != RAC_OK) return st;
     if (!wire || (cfg->tokens > 0 && !xhat)) return RAC_ERR_INVALID;
     if ((cfg->flags & RAC_FLAG_FIXED_STEP) && !steps) return RAC_ERR_INVALID;
+    if ((st = check_gather(ref, store_rows, ref_rows, gather)) != RAC_OK) return st;
     if (!aligned(wire, 256) || !aligned(xhat, 16) || (ref && !aligned(ref, 16)) ||
         (steps && !aligned(steps, 4)))
         return RAC_ERR_ALIGN;
@@ -2021,6 +2084,8 @@ rac_status run_decode(const rac_config* cfg, const void* wire, const void* ref, 
     A.wire = const_cast<uint8_t*>(static_cast<const uint8_t*>(wire));
     set_sections(A, S);
     A.ref = static_cast<const uint16_t*>(ref);
+    A.ref_rows = (gather && ref) ? ref_rows : nullptr;
+    A.store_rows = (uint32_t)store_rows;
     A.steps = steps;
     A.xhat = xhat;
     // (with outliers, two workgroups per compute unit, each taking more rows,
@@ -2080,12 +2145,18 @@ rac_status rac_parse_header(const void* header_host, size_t len, rac_config* out
     return RAC_OK;
 }
 
-rac_status rac_encode(const rac_config* cfg, const void* x, const void* ref, const float* fixed_steps,
-                      void* wire, size_t wire_cap, void* xhat, rac_stream_t stream) {
+}  // extern "C"
+
+namespace {
+
+rac_status run_encode(const rac_config* cfg, const void* x, const void* ref, const float* fixed_steps,
+                      void* wire, size_t wire_cap, void* xhat, hipStream_t stream, bool gather,
+                      int64_t store_rows, const int32_t* ref_rows) {
     rac_status st = common_checks(cfg);
     if (st != RAC_OK) return st;
     if (!wire || (cfg->tokens > 0 && !x)) return RAC_ERR_INVALID;
     if ((cfg->flags & RAC_FLAG_FIXED_STEP) && !fixed_steps) return RAC_ERR_INVALID;
+    if ((st = check_gather(ref, store_rows, ref_rows, gather)) != RAC_OK) return st;
     if (!aligned(wire, 256) || !aligned(x, 16) || (ref && !aligned(ref, 16)) ||
         (xhat && !aligned(xhat, 16)) || (fixed_steps && !aligned(fixed_steps, 4)))
         return RAC_ERR_ALIGN;
@@ -2094,6 +2165,8 @@ rac_status rac_encode(const rac_config* cfg, const void* x, const void* ref, con
     Args A = make_args(cfg, S);
     A.x = static_cast<const uint16_t*>(x);
     A.ref = static_cast<const uint16_t*>(ref);
+    A.ref_rows = (gather && ref) ? ref_rows : nullptr;
+    A.store_rows = (uint32_t)store_rows;
     A.steps = (cfg->flags & RAC_FLAG_FIXED_STEP) ? fixed_steps : nullptr;
     A.wire = static_cast<uint8_t*>(wire);
     set_sections(A, S);
@@ -2102,6 +2175,26 @@ rac_status rac_encode(const rac_config* cfg, const void* x, const void* ref, con
     fill_header(A, cfg, ref == nullptr);
     if (use_rows_kernel(A)) return launch(pick_rows(A, cfg->bits), A, stream, kRowsWaves * kWave);
     return launch(pick_encode(A, cfg->bits), A, stream);
+}
+
+}  // namespace
+
+extern "C" {
+
+rac_status rac_encode(const rac_config* cfg, const void* x, const void* ref, const float* fixed_steps,
+                      void* wire, size_t wire_cap, void* xhat, rac_stream_t stream) {
+    return run_encode(cfg, x, ref, fixed_steps, wire, wire_cap, xhat, stream, false, 0, nullptr);
+}
+
+rac_status rac_encode_gather(const rac_config* cfg, const void* x, const void* ref_store, int64_t store_rows,
+                             const int32_t* ref_rows, const float* fixed_steps, void* wire, size_t wire_cap,
+                             void* xhat, rac_stream_t stream) {
+    return run_encode(cfg, x, ref_store, fixed_steps, wire, wire_cap, xhat, stream, true, store_rows, ref_rows);
+}
+
+rac_status rac_decode_gather(const rac_config* cfg, const void* wire, const void* ref_store, int64_t store_rows,
+                             const int32_t* ref_rows, const float* fixed_steps, void* xhat, rac_stream_t stream) {
+    return run_decode(cfg, wire, ref_store, fixed_steps, xhat, stream, true, store_rows, ref_rows);
 }
 
 rac_status rac_reconstruct(const rac_config* cfg, const void* wire, const void* ref,

@@ -35,7 +35,8 @@ def lib():
 def test_exports_every_declared_symbol(lib):
     names = _declared_functions()
     assert set(names) == {"rac_wire_layout", "rac_wire_size", "rac_parse_header", "rac_encode",
-                          "rac_reconstruct", "rac_decode", "rac_status_string"}
+                          "rac_reconstruct", "rac_decode", "rac_encode_gather", "rac_decode_gather",
+                          "rac_status_string"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -188,3 +189,20 @@ def test_argument_errors_are_synchronous(lib):
     assert _decode(good, wire=FAKE + 128) == 2
     assert _decode(good, xhat=None) == 1
     assert rac.library().rac_reconstruct(ctypes.byref(good._c()), FAKE, FAKE, None, FAKE + 1, 0) == 2
+
+
+def test_gather_argument_errors_are_synchronous(lib):
+    good = rac.RacConfig(64, 512, 64, 64, 4)
+    L = rac.library()
+    enc = lambda store=FAKE, rows=64, idx=FAKE, x=FAKE: L.rac_encode_gather(
+        ctypes.byref(good._c()), x, store, rows, idx, None, FAKE, 1 << 40, FAKE, 0)
+    dec = lambda store=FAKE, rows=64, idx=FAKE, xhat=FAKE: L.rac_decode_gather(
+        ctypes.byref(good._c()), FAKE, store, rows, idx, None, xhat, 0)
+    assert enc(idx=None) == 1                   # a store needs its row indices
+    assert enc(rows=-1) == 1 and enc(rows=2 ** 31) == 1
+    assert enc(idx=FAKE + 2) == 2               # indices are int32
+    assert enc(store=FAKE + 8) == 2             # store rows are read 16 bytes at a time
+    assert enc(x=None) == 1
+    assert dec(idx=None) == 1 and dec(rows=-5) == 1 and dec(idx=FAKE + 1) == 2 and dec(xhat=None) == 1
+    big = rac.RacConfig(4, 16384, 128, 128, 4)
+    assert L.rac_encode_gather(ctypes.byref(big._c()), FAKE, FAKE, 4, FAKE, None, FAKE, 1 << 40, FAKE, 0) == 6

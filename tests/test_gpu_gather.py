@@ -1,0 +1,142 @@
+"""GPU parity of the gathered-reference entry points (rac_encode_gather,
+rac_decode_gather), through the C ABI.
+
+The expected result is the plain definition: the reference of token row t is
+row ref_rows[t] of the store, or a zero row when the index is negative or
+past the store.  That reference is gathered on the host and handed to the
+oracle's encode and decode; the GPU must match them bit for bit, and must also
+equal rac_encode / rac_decode given the materialized reference.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+import paper_2608_04991_amd as rac
+from paper_2608_04991_amd import workloads as wl
+from tests.gpu_util import assert_parity, cfgd, gpu_run, oracle_run, say, to_dev
+
+pytestmark = pytest.mark.gpu
+GRP = rac.RAC_FLAG_GROUP_OUTLIERS
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    rac.library()
+
+
+def _gathered(store, idx):
+    ref = np.zeros((idx.size, store.shape[1]), np.uint16)
+    ok = (idx >= 0) & (idx < store.shape[0])
+    ref[ok] = store[idx[ok]]
+    return ref
+
+
+def _history(xb, rb, extra, seed):
+    """A store holding each row's reference at a random position among
+    `extra` unrelated rows, and per row its index; a fifth of the rows get an
+    index outside the store (negative or past the end) and so no reference."""
+    rng = np.random.default_rng(seed)
+    T, d = xb.shape
+    S = T + extra
+    store = wl.f32_to_bf16_bits(rng.standard_normal((S, d)).astype(np.float32))
+    pos = rng.permutation(S)[:T]
+    store[pos] = rb
+    idx = pos.astype(np.int32)
+    miss = rng.random(T) < 0.2
+    idx[miss] = rng.choice(np.array([-1, -7, S, S + 3, 2 ** 31 - 1], np.int64), miss.sum()).astype(np.int32)
+    return store, idx
+
+
+def _gpu_gather(c, xb, store, idx, steps=None):
+    import torch
+    cfg = rac.RacConfig(**c)
+    T, d = c["tokens"], c["hidden"]
+    assert xb.shape == (T, d) and idx.shape == (T,) and idx.dtype == np.int32
+    assert store is None or store.shape[1] == d
+    x = to_dev(xb)
+    st = to_dev(store) if store is not None else None
+    ix = torch.from_numpy(idx).cuda()
+    stp = torch.from_numpy(np.asarray(steps, np.float32)).cuda() if steps is not None else None
+    wire = torch.full((rac.rac_wire_size(cfg),), 0xAB, dtype=torch.uint8, device="cuda")
+    bf16 = bool(c["flags"] & rac.RAC_FLAG_XHAT_BF16)
+    dt = torch.int16 if bf16 else torch.float32
+    xh = torch.full((T, d), -1, dtype=dt, device="cuda")
+    xd = torch.full((T, d), -1, dtype=dt, device="cuda")
+    rows = 0 if store is None else store.shape[0]
+    rac.rac_encode_gather(cfg, x, st, ix, stp, wire, xh, store_rows=rows)
+    rac.rac_decode_gather(cfg, wire, st, ix, stp, xd, store_rows=rows)
+    torch.cuda.synchronize()
+    view = (lambda a: a.view(np.uint16)) if bf16 else (lambda a: a)
+    return wire.cpu().numpy(), view(xh.cpu().numpy()), view(xd.cpu().numpy())
+
+
+CASES = {
+    "uplink_37x4096_g128_b4_k8": (cfgd(37, 4096, 128, 128, 4, 8), lambda: wl.prefill_uplink(0, rows=(0, 37))[:2]),
+    "tiny_64x512_g64_b4": (cfgd(64, 512, 64, 64, 4), lambda: wl.tiny(0)[:2]),
+    "group_21x4096_ga64_gq128_b8_kg2": (cfgd(21, 4096, 64, 128, 8, 2, GRP),
+                                        lambda: wl.prefill_uplink(1, rows=(100, 121))[:2]),
+    "wide_9x8192_g128_b4_k16": (cfgd(9, 8192, 128, 128, 4, 16),
+                                lambda: wl.prefill_uplink(0, rows=(0, 9), hidden=8192)[:2]),
+    "long_13x4096_g64_b3_k16": (cfgd(13, 4096, 64, 64, 3, 16), lambda: wl.long_context(0, rows=(0, 13), group=64)[:2]),
+    "decode_step_16x4096_gq4096_b2": (cfgd(16, 4096, 128, 4096, 2), lambda: wl.decode_step(16)),
+    "bf16_out_25x4096_g128_b4_k8": (cfgd(25, 4096, 128, 128, 4, 8, rac.RAC_FLAG_XHAT_BF16),
+                                    lambda: wl.prefill_uplink(0, rows=(7, 32))[:2]),
+}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_gather_parity(name):
+    c, gen = CASES[name]
+    xb, rb = gen()
+    store, idx = _history(xb, rb, 40, seed=len(name))
+    say(f"[gpu] gather {name}: store {store.shape[0]} rows, {int(((idx < 0) | (idx >= store.shape[0])).sum())} misses")
+    ref = _gathered(store, idx)
+    ow, ox = oracle_run(c, xb, ref)
+    gw, gx, gd = _gpu_gather(c, xb, store, idx)
+    assert_parity(c, gw, gx, ow, ox)
+    assert np.array_equal(gx.view(np.uint8), gd.view(np.uint8))
+    # the same call with the reference materialized gives the same bytes
+    mw, mx, md, _ = gpu_run(c, xb, ref)
+    assert np.array_equal(mw, gw) and np.array_equal(mx.view(np.uint8), gx.view(np.uint8))
+
+
+def test_gather_without_a_store_is_a_zero_reference():
+    c = cfgd(19, 1024, 128, 64, 4, 4)
+    xb, _, _ = wl.prefill_uplink(2, rows=(0, 19), hidden=1024)
+    say("[gpu] gather without a store")
+    gw, gx, gd = _gpu_gather(c, xb, None, np.zeros(19, np.int32))
+    ow, ox = oracle_run(c, xb, None)
+    assert_parity(c, gw, gx, ow, ox)
+    assert np.array_equal(gx, gd)
+
+
+def test_gather_from_an_empty_store_and_all_misses():
+    c = cfgd(11, 4096, 128, 128, 4, 8)
+    xb, rb, _ = wl.prefill_uplink(4, rows=(0, 11))
+    idx = np.full(11, -1, np.int32)
+    say("[gpu] gather, every index a miss")
+    gw, gx, gd = _gpu_gather(c, xb, rb, idx)
+    ow, ox = oracle_run(c, xb, np.zeros_like(rb))   # a zero reference, but not a missing one
+    assert_parity(c, gw, gx, ow, ox)
+    assert np.array_equal(gx, gd)
+
+
+def test_full_prefill_uplink_4096x4096_gathered_sampled():
+    """The benchmark shape with its reference in an 8192-row history store:
+    the span-hit rows name their store row, the other fifth name none."""
+    import torch
+    c = cfgd(4096, 4096, 128, 128, 4, 8)
+    say("[gpu] full prefill uplink 4096x4096 from an 8192-row store: generating")
+    xb, rb, _ = wl.prefill_uplink(0)
+    store, idx = _history(xb, rb, 4096, seed=9)
+    gw, gx, gd = _gpu_gather(c, xb, store, idx)
+    assert np.array_equal(gx, gd)
+    rng = np.random.default_rng(5)
+    rows = np.unique(np.concatenate([[0, 1, 4094, 4095], rng.choice(4096, 48, replace=False)]))
+    ow, ox = oracle_run(dict(c, tokens=rows.size), xb[rows], _gathered(store, idx[rows]))
+    assert_parity(c, gw, gx, ow, ox, g_rows=rows, o_rows=slice(None))
+    torch.cuda.empty_cache()
