@@ -60,6 +60,10 @@ def main():
                          "climbs for the first ~20 ms of sustained load")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true")
+    ap.add_argument("--all-configs", action="store_true",
+                    help="also time every other workload at full size (tiny 64 x 512; prefill downlink "
+                         "65536 x 3584; long context 32768 x 4096 at groups 64 and 128 and 2/3/4/8 bits) "
+                         "into extras.all_configs; adds about a minute")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run plain device copies of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
@@ -212,6 +216,10 @@ def main():
         extras["outlier_modes_4096x4096_g128_b4"] = outlier_mode_rates(
             torch, rac, sets, nsets, stream, args.steps)
         extras["gathered_reference"] = gather_rates(torch, rac, cfg, rb, sets, nsets, stream, args.steps)
+    if args.all_configs:
+        del sets
+        torch.cuda.empty_cache()
+        extras["all_configs"] = all_config_rates(torch, rac, wl, dev, stream)
     out["extras"] = extras
 
     if not args.no_cpu_baseline:
@@ -268,6 +276,104 @@ def outlier_mode_rates(torch, rac, sets, nsets, stream, steps):
                      "wire_over_bf16": round(wb / (T * d * 2), 4)}
         del wires
     return res
+
+
+def time_pair(torch, rac, cfg, sets, stream, iters=20):
+    """Average µs of rac_encode (fused fp32 reconstruction), of rac_decode,
+    and of encode + decode on one stream, each over `iters` back-to-back
+    launches rotating over `sets` (inputs and outputs per set), after at
+    least 60 ms of untimed launches."""
+    n = len(sets)
+
+    def enc(i):
+        s = sets[i % n]
+        rac.rac_encode(cfg, s["x"], s["ref"], None, s["wire"], s["xhat"], stream=stream)
+
+    def dec(i):
+        s = sets[i % n]
+        rac.rac_decode(cfg, s["wire"], s["ref"], None, s["xdec"], stream=stream)
+
+    # untimed launches for at least 60 ms first: the data of each workload is
+    # generated on the host while the GPU idles, and its clock drops meanwhile
+    t0, i = time.perf_counter(), 0
+    while (time.perf_counter() - t0) < 0.06 or i < 2 * n:
+        enc(i)
+        dec(i)
+        i += 1
+        if i % 4 == 0:
+            torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    for i in range(iters):
+        enc(i)
+    ev[1].record(stream)
+    for i in range(iters):
+        dec(i)
+    ev[2].record(stream)
+    for i in range(iters):
+        enc(i)
+        dec(i)
+    ev[3].record(stream)
+    torch.cuda.synchronize()
+    assert torch.equal(sets[0]["xhat"], sets[0]["xdec"])
+    return [ev[j].elapsed_time(ev[j + 1]) / iters * 1e3 for j in range(3)]
+
+
+def all_config_rates(torch, rac, wl, dev, stream):
+    """Every other workload at its full size, on its own synthetic data: µs
+    per call of encode, decode and the encode + decode round trip on one
+    stream, with the fraction of 8 TB/s by algorithmic bytes (the tiny case
+    is launch-bound and reports µs only).  Two buffer sets rotate (each set of
+    the large shapes is far above the 256 MB last-level cache; the tiny case
+    uses 64)."""
+    out = {}
+
+    def run(name, cfg, xb, rb, nsets, report_frac=True):
+        T, d = cfg.tokens, cfg.hidden
+        wb = rac.rac_wire_size(cfg)
+        x, r = dev(xb), dev(rb)
+        sets = [dict(x=x if i == 0 else x.clone(), ref=r if i == 0 else r.clone(),
+                     wire=torch.empty(wb, dtype=torch.uint8, device="cuda"),
+                     xhat=torch.empty(T, d, dtype=torch.float32, device="cuda"),
+                     xdec=torch.empty(T, d, dtype=torch.float32, device="cuda")) for i in range(nsets)]
+        e, dcd, rt = time_pair(torch, rac, cfg, sets, stream)
+        res = {"encode_us": round(e, 2), "decode_us": round(dcd, 2), "round_trip_us": round(rt, 2),
+               "wire_over_bf16": round(wb / (T * d * 2), 4)}
+        if report_frac:
+            res["encode_hbm_frac"] = round(algorithmic_bytes(T, d, wb) / e / 1e3 / HBM_PEAK_GBPS, 4)
+            res["decode_hbm_frac"] = round(algorithmic_bytes(T, d, wb, encode=False) / dcd / 1e3 / HBM_PEAK_GBPS, 4)
+            res["activation_GBps_round_trip"] = round(T * d * 2 / rt / 1e3, 1)
+        out[name] = res
+        log(f"[bench] {name}: {res}")
+        del sets
+        torch.cuda.empty_cache()
+
+    xb, rb, _ = wl.tiny(0)
+    run("tiny_64x512_g64_b4", rac.RacConfig(64, 512, 64, 64, 4, 0), xb, rb, 64, report_frac=False)
+    # prefill downlink: the reference is the sender reconstruction (bf16) of a
+    # synthetic uplink, made here by the GPU encode (bit-identical to the
+    # oracle's, which the GPU tests check on sampled rows)
+    T, d = 65536, 3584
+    cfg = rac.RacConfig(T, d, 128, 128, 4, 4)
+    log("[bench] generating the prefill-downlink workload")
+    xu, ru, _ = wl.prefill_downlink_uplink(0)
+    xh = torch.empty(T, d, dtype=torch.float32, device="cuda")
+    w = torch.empty(rac.rac_wire_size(cfg), dtype=torch.uint8, device="cuda")
+    rac.rac_encode(cfg, dev(xu), dev(ru), None, w, xh, stream=stream)
+    torch.cuda.synchronize()
+    ref = wl.f32_to_bf16_bits(xh.cpu().numpy())
+    del xh, w, xu, ru
+    torch.cuda.empty_cache()
+    xd = wl.prefill_downlink(ref, 0)
+    run("prefill_downlink_65536x3584_g128_b4_k4", cfg, xd, ref, 2)
+    del xd, ref
+    for g in (64, 128):
+        log(f"[bench] generating the long-context workload, group {g}")
+        xb, rb, _ = wl.long_context(0, group=g)
+        for bits in (2, 3, 4, 8):
+            run(f"long_context_32768x4096_g{g}_b{bits}_k16", rac.RacConfig(32768, 4096, g, g, bits, 16), xb, rb, 2)
+    return out
 
 
 def gather_rates(torch, rac, cfg, rb, sets, nsets, stream, steps):
