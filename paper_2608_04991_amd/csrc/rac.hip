@@ -1962,14 +1962,17 @@ KernelFn encode_for(int bits, int om) {
 
 int outlier_mode(const Args& A) { return A.gout ? 2 : (A.k > 0 ? 1 : 0); }
 
-// Specialized group shapes: 64/64, 128/128 and 128 with one scale per row
-// of up to 8192 channels; anything else takes the generic kernel.
+// Specialized group shapes: 64/64, 128/128, the mixed 64/128 and 128/64, and
+// 128 with one scale per row of up to 8192 channels; anything else takes the
+// generic kernel.
 KernelFn pick_encode(const Args& A, int bits) {
     const int ga = A.lg_cpg_a > 0 ? 7 : A.lane_lv_a;
     const int gq = A.lg_cpg_q > 0 ? 7 : A.lane_lv_q;
     const int om = outlier_mode(A);
     if (ga == 3 && gq == 3) return encode_for<3, 3>(bits, om);
     if (ga == 4 && gq == 4) return encode_for<4, 4>(bits, om);
+    if (ga == 3 && gq == 4) return encode_for<3, 4>(bits, om);
+    if (ga == 4 && gq == 3) return encode_for<4, 3>(bits, om);
     if (ga == 4 && gq == 7) return encode_for<4, 7>(bits, om);
     return encode_for<-1, -1>(bits, om);
 }
@@ -2000,6 +2003,8 @@ bool use_rows_kernel(const Args& A) {
 KernelFn pick_rows(const Args& A, int bits) {
     if (A.lane_lv_a == 3 && A.lane_lv_q == 3) return rows_for<3, 3>(bits, A.d);
     if (A.lane_lv_a == 4 && A.lane_lv_q == 4) return rows_for<4, 4>(bits, A.d);
+    if (A.lane_lv_a == 3 && A.lane_lv_q == 4) return rows_for<3, 4>(bits, A.d);
+    if (A.lane_lv_a == 4 && A.lane_lv_q == 3) return rows_for<4, 3>(bits, A.d);
     return rows_for<-1, -1>(bits, A.d);
 }
 

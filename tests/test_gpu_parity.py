@@ -144,6 +144,12 @@ CASES = {
     "large_groups_10x4096_ga1024_gq2048_b4_k8": (cfgd(10, 4096, 1024, 2048, 4, 8),
                                                  lambda: _affine(10, 4096, 1024)),
     "gq_eq_d_16x4096_b4": (cfgd(16, 4096, 128, 4096, 4), lambda: wl.decode_step(16)),
+    "mixed_groups_17x4096_ga64_gq128_b4_k0": (cfgd(17, 4096, 64, 128, 4), lambda: wl.prefill_uplink(0, rows=(50, 67))[:2]),
+    "mixed_groups_15x4096_ga128_gq64_b2_k0": (cfgd(15, 4096, 128, 64, 2), lambda: wl.prefill_uplink(1, rows=(9, 24))[:2]),
+    "mixed_groups_11x8192_ga128_gq64_b4_k8": (cfgd(11, 8192, 128, 64, 4, 8),
+                                              lambda: wl.prefill_uplink(2, rows=(0, 11), hidden=8192)[:2]),
+    "mixed_groups_group_outliers_9x4096_ga64_gq128_b8_kg2": (cfgd(9, 4096, 64, 128, 8, 2, GRP),
+                                                             lambda: wl.prefill_uplink(3, rows=(0, 9))[:2]),
     "all_outliers_12x64_ga8_gq16_k64": (cfgd(12, 64, 8, 16, 4, 64), lambda: _affine(12, 64, 8)),
     "smallest_5x8_b4_k2": (cfgd(5, 8, 8, 8, 4, 2), lambda: _affine(5, 8, 8)),
     "zero_reference_19x1024_b4_k4": (cfgd(19, 1024, 128, 64, 4, 4),
