@@ -89,8 +89,9 @@ typedef enum {
     RAC_ERR_CAPACITY = 3,    /* wire buffer smaller than rac_wire_size()         */
     RAC_ERR_HIP = 4,         /* the HIP runtime refused the kernel launch        */
     RAC_ERR_FORMAT = 5,      /* a wire header does not parse                     */
-    RAC_ERR_UNSUPPORTED = 6  /* valid codec configuration the kernels do not
+    RAC_ERR_UNSUPPORTED = 6, /* valid codec configuration the kernels do not
                                 implement (hidden above 8192)                   */
+    RAC_ERR_NOMEM = 7        /* host memory exhausted (span index only)          */
 } rac_status;
 
 enum {
@@ -200,6 +201,52 @@ rac_status rac_encode_gather(const rac_config* cfg, const void* x, const void* r
  * in rac_encode_gather; the result equals rac_decode with that reference). */
 rac_status rac_decode_gather(const rac_config* cfg, const void* wire, const void* ref_store, int64_t store_rows,
                              const int32_t* ref_rows, const float* fixed_steps, void* xhat, rac_stream_t stream);
+
+/* ---- Reference selection for the prefill uplink (host only) ------------
+ * Subsection "Historical References for Prefill Uplinks",
+ * Eq. prefill-reference-selection.  A span index holds the token streams of
+ * earlier requests and the store row of each of their tokens' activations;
+ * rac_span_select turns the current prompt into the ref_rows array of
+ * rac_encode_gather / rac_decode_gather.  Both ends can run it, since it
+ * depends only on tokens.
+ *
+ * The index is a host object with an explicit lifetime (the one exception to
+ * "the library allocates nothing": it holds host memory only, never device
+ * memory).  Calls on one index must not overlap with rac_span_index_add on
+ * the same index; concurrent rac_span_select calls are fine.
+ *
+ * Rule (every part of it is the paper's, the grouping of hash buckets by
+ * window content is this library's reading):
+ *   - every `window`-token window of the added requests is indexed; each
+ *     distinct window content keeps its eight most recent occurrences
+ *     (recency = request order, then position);
+ *   - at prompt position i, each kept occurrence of the window starting at i
+ *     extends forward to its longest exact match L >= window; the
+ *     lexicographic maximum of (L, recency) is chosen and the scan moves to
+ *     i + L (to i + 1 without a candidate);
+ *   - the chosen span's positions i + o reference store row
+ *     store_row0(request) + start + o; uncovered positions get -1 (no
+ *     reference: rac_encode_gather codes them against zero). */
+typedef struct rac_span_index rac_span_index;
+
+/* New empty index over `window`-token windows, 1 <= window <= 4096.  NULL for
+ * an invalid window or when host memory is exhausted. */
+rac_span_index* rac_span_index_create(int32_t window);
+
+/* Free an index (NULL is ignored). */
+void rac_span_index_destroy(rac_span_index* index);
+
+/* Add a request: host tokens[n]; the activation of token p is store row
+ * store_row0 + p (store_row0 + n <= 2^31 - 1).  RAC_ERR_INVALID for bad
+ * arguments, RAC_ERR_NOMEM if host memory runs out (the index may then hold
+ * part of the request). */
+rac_status rac_span_index_add(rac_span_index* index, const int32_t* tokens, int64_t n, int64_t store_row0);
+
+/* Select the reference rows of a prompt: host tokens[n] -> host ref_rows[n]
+ * (store row or -1).  `covered` (may be NULL) receives the number of
+ * positions with a reference. */
+rac_status rac_span_select(const rac_span_index* index, const int32_t* tokens, int64_t n, int32_t* ref_rows,
+                           int64_t* covered);
 
 /* Static string naming a status code. */
 const char* rac_status_string(rac_status s);

@@ -23,14 +23,14 @@ __all__ = [
     "STATUS",
     "library", "library_path", "rac_wire_layout", "rac_wire_size", "rac_parse_header",
     "rac_encode", "rac_reconstruct", "rac_decode", "rac_encode_gather", "rac_decode_gather",
-    "rac_status_string",
+    "rac_status_string", "SpanIndex",
 ]
 
 RAC_FLAG_FIXED_STEP = 1
 RAC_FLAG_XHAT_BF16 = 2
 RAC_FLAG_GROUP_OUTLIERS = 4
 STATUS = {0: "RAC_OK", 1: "RAC_ERR_INVALID", 2: "RAC_ERR_ALIGN", 3: "RAC_ERR_CAPACITY",
-          4: "RAC_ERR_HIP", 5: "RAC_ERR_FORMAT", 6: "RAC_ERR_UNSUPPORTED"}
+          4: "RAC_ERR_HIP", 5: "RAC_ERR_FORMAT", 6: "RAC_ERR_UNSUPPORTED", 7: "RAC_ERR_NOMEM"}
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 
@@ -102,6 +102,14 @@ def library():
         L.rac_encode_gather.restype = ctypes.c_int
         L.rac_decode_gather.argtypes = [cp, vp, vp, ctypes.c_int64, vp, vp, vp, vp]
         L.rac_decode_gather.restype = ctypes.c_int
+        L.rac_span_index_create.argtypes = [ctypes.c_int32]
+        L.rac_span_index_create.restype = vp
+        L.rac_span_index_destroy.argtypes = [vp]
+        L.rac_span_index_destroy.restype = None
+        L.rac_span_index_add.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int64]
+        L.rac_span_index_add.restype = ctypes.c_int
+        L.rac_span_select.argtypes = [vp, vp, ctypes.c_int64, vp, ctypes.POINTER(ctypes.c_int64)]
+        L.rac_span_select.restype = ctypes.c_int
         L.rac_status_string.argtypes = [ctypes.c_int]
         L.rac_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -203,3 +211,39 @@ def rac_decode_gather(cfg: RacConfig, wire, store, ref_rows, fixed_steps, xhat, 
     _check(library().rac_decode_gather(ctypes.byref(cfg._c()), _ptr(wire), _ptr(store), _rows(store, store_rows),
                                        _ptr(ref_rows), _ptr(fixed_steps), _ptr(xhat), _stream(stream)),
            "rac_decode_gather")
+
+
+class SpanIndex:
+    """Host-side index of earlier requests for the prefill-uplink reference
+    selection (rac_span_index_* / rac_span_select); tokens are int32 arrays."""
+
+    def __init__(self, window: int):
+        import numpy as np
+        self._np = np
+        self._h = library().rac_span_index_create(int(window))
+        if not self._h:
+            raise RacError(1, "rac_span_index_create")
+
+    def add(self, tokens, store_row0: int) -> None:
+        t = self._np.ascontiguousarray(tokens, dtype=self._np.int32)
+        _check(library().rac_span_index_add(self._h, t.ctypes.data, t.size, int(store_row0)), "rac_span_index_add")
+
+    def select(self, tokens):
+        """Returns (ref_rows int32[n], covered positions)."""
+        t = self._np.ascontiguousarray(tokens, dtype=self._np.int32)
+        out = self._np.empty(t.size, dtype=self._np.int32)
+        cov = ctypes.c_int64(0)
+        _check(library().rac_span_select(self._h, t.ctypes.data, t.size, out.ctypes.data, ctypes.byref(cov)),
+               "rac_span_select")
+        return out, int(cov.value)
+
+    def close(self) -> None:
+        if self._h:
+            library().rac_span_index_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

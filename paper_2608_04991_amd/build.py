@@ -21,6 +21,7 @@ except ImportError:  # run as a script
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SRC = os.path.join(HERE, "csrc", "rac.hip")
+HOST_SRC = os.path.join(HERE, "csrc", "spans.cpp")   # host-only C++ (reference selection)
 INC = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "lib", "librac.so")
 
@@ -33,7 +34,7 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
 def build(verbose: bool = True) -> str:
     os.makedirs(os.path.dirname(LIB), exist_ok=True)
     tmp = LIB + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-I", INC, "-o", tmp, SRC]
+    cmd = [HIPCC, *FLAGS, "-I", INC, "-o", tmp, SRC, HOST_SRC]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

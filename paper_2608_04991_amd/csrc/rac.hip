@@ -2221,6 +2221,7 @@ const char* rac_status_string(rac_status s) {
         case RAC_ERR_HIP: return "HIP kernel launch failed";
         case RAC_ERR_FORMAT: return "malformed wire header";
         case RAC_ERR_UNSUPPORTED: return "configuration not supported by the kernels";
+        case RAC_ERR_NOMEM: return "host memory exhausted";
     }
     return "unknown status";
 }

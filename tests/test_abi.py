@@ -36,13 +36,14 @@ def test_exports_every_declared_symbol(lib):
     names = _declared_functions()
     assert set(names) == {"rac_wire_layout", "rac_wire_size", "rac_parse_header", "rac_encode",
                           "rac_reconstruct", "rac_decode", "rac_encode_gather", "rac_decode_gather",
-                          "rac_status_string"}
+                          "rac_status_string", "rac_span_index_create", "rac_span_index_destroy",
+                          "rac_span_index_add", "rac_span_select"}
     for n in names:
         assert hasattr(lib, n), n
 
 
 def test_status_strings(lib):
-    for s in range(7):
+    for s in range(8):
         assert rac.rac_status_string(s) != "unknown status"
     assert rac.rac_status_string(99) == "unknown status"
 
