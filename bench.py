@@ -216,6 +216,7 @@ def main():
         extras["outlier_modes_4096x4096_g128_b4"] = outlier_mode_rates(
             torch, rac, sets, nsets, stream, args.steps)
         extras["gathered_reference"] = gather_rates(torch, rac, cfg, rb, sets, nsets, stream, args.steps)
+        extras["span_selection"] = span_selection_cost(rac, T)
     if args.all_configs:
         del sets
         torch.cuda.empty_cache()
@@ -374,6 +375,42 @@ def all_config_rates(torch, rac, wl, dev, stream):
         for bits in (2, 3, 4, 8):
             run(f"long_context_32768x4096_g{g}_b{bits}_k16", rac.RacConfig(32768, 4096, g, g, bits, 16), xb, rb, 2)
     return out
+
+
+def span_selection_cost(rac, T, window=16, n_hist=7):
+    """Host cost of the reference selection (librac's span index, one CPU
+    thread) for a T-token prompt against n_hist earlier T-token requests of a
+    synthetic agent session: a shared system prompt, stretches copied from
+    earlier requests, fresh tokens.  Index build time for the history, then
+    the selection time for the prompt, and the fraction of positions
+    covered."""
+    rng = np.random.default_rng(3)
+    system = rng.integers(0, 32000, T // 4).tolist()
+    reqs = []
+    for _ in range(n_hist + 1):
+        r = list(system)
+        while len(r) < T:
+            if reqs and rng.random() < 0.6:
+                src = reqs[rng.integers(0, len(reqs))]
+                a = int(rng.integers(0, len(src)))
+                r += src[a:a + int(rng.integers(16, 400))]
+            else:
+                r += rng.integers(0, 32000, int(rng.integers(1, 64))).tolist()
+        reqs.append(r[:T])
+    reqs = [np.asarray(r, np.int32) for r in reqs]
+    t0 = time.perf_counter()
+    ix = rac.SpanIndex(window)
+    for i in range(n_hist):
+        ix.add(reqs[i], i * T)
+    t1 = time.perf_counter()
+    reps = 20
+    for _ in range(reps):
+        idx, cov = ix.select(reqs[n_hist])
+    t2 = time.perf_counter()
+    ix.close()
+    return {"window": window, "history_tokens": n_hist * T, "prompt_tokens": T,
+            "index_build_ms": round((t1 - t0) * 1e3, 2), "select_us": round((t2 - t1) / reps * 1e6, 1),
+            "covered_fraction": round(cov / T, 4)}
 
 
 def gather_rates(torch, rac, cfg, rb, sets, nsets, stream, steps):

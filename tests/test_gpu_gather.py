@@ -140,3 +140,43 @@ def test_full_prefill_uplink_4096x4096_gathered_sampled():
     ow, ox = oracle_run(dict(c, tokens=rows.size), xb[rows], _gathered(store, idx[rows]))
     assert_parity(c, gw, gx, ow, ox, g_rows=rows, o_rows=slice(None))
     torch.cuda.empty_cache()
+
+
+def test_selected_spans_end_to_end():
+    """Prompt tokens -> native span selection -> gathered encode and decode
+    on the GPU, against the selection oracle -> host gather -> codec oracle.
+    The store holds one activation row per token of the earlier requests."""
+    from oracle.spans import select_spans
+    rng = np.random.default_rng(21)
+    d, w = 1024, 4
+    system = rng.integers(0, 500, 64).tolist()
+    reqs = []
+    for _ in range(4):
+        r = list(system)
+        while len(r) < 160:
+            if reqs and rng.random() < 0.6:
+                src = reqs[rng.integers(0, len(reqs))]
+                a = int(rng.integers(0, len(src)))
+                r += src[a:a + 30]
+            else:
+                r += rng.integers(0, 500, 8).tolist()
+        reqs.append(r[:160])
+    hist = [(reqs[i], 160 * i) for i in range(3)]
+    prompt = reqs[3]
+    want, _ = select_spans(hist, prompt, w)
+    ix = rac.SpanIndex(w)
+    for tr, base in hist:
+        ix.add(np.asarray(tr, np.int32), base)
+    idx, cov = ix.select(np.asarray(prompt, np.int32))
+    ix.close()
+    assert idx.tolist() == want and cov > 64
+    store = wl.f32_to_bf16_bits(rng.standard_normal((480, d)).astype(np.float32))
+    T = len(prompt)
+    xb = wl.f32_to_bf16_bits((wl.bf16_bits_to_f32(_gathered(store, idx)) * np.float32(1.1)
+                              + rng.standard_normal((T, d)).astype(np.float32) * np.float32(0.05)))
+    c = cfgd(T, d, 128, 128, 4, 8)
+    say(f"[gpu] selected spans end to end: {cov} of {T} positions covered")
+    ow, ox = oracle_run(c, xb, _gathered(store, np.asarray(want, np.int32)))
+    gw, gx, gd = _gpu_gather(c, xb, store, idx)
+    assert_parity(c, gw, gx, ow, ox)
+    assert np.array_equal(gx, gd)
