@@ -207,3 +207,16 @@ def test_gather_argument_errors_are_synchronous(lib):
     assert dec(idx=None) == 1 and dec(rows=-5) == 1 and dec(idx=FAKE + 1) == 2 and dec(xhat=None) == 1
     big = rac.RacConfig(4, 16384, 128, 128, 4)
     assert L.rac_encode_gather(ctypes.byref(big._c()), FAKE, FAKE, 4, FAKE, None, FAKE, 1 << 40, FAKE, 0) == 6
+
+
+def test_binding_raises_without_the_library(monkeypatch):
+    """No fallback: with librac.so absent every call raises instead of
+    computing anything elsewhere."""
+    monkeypatch.setattr(rac, "_lib", None)
+    monkeypatch.setattr(rac, "library_path", lambda: "/nonexistent/librac.so")
+    with pytest.raises(RuntimeError, match="missing"):
+        rac.rac_wire_size(rac.RacConfig(4, 512, 64, 64, 4))
+    with pytest.raises(RuntimeError, match="missing"):
+        rac.rac_encode(rac.RacConfig(4, 512, 64, 64, 4), FAKE, FAKE, None, FAKE, FAKE, stream=0, wire_cap=1)
+    with pytest.raises(RuntimeError, match="missing"):
+        rac.SpanIndex(8)
