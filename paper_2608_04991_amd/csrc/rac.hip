@@ -36,6 +36,7 @@ constexpr int kWave = 64;
 constexpr int kChunk = 512;       // channels per wavefront (8 per lane)
 constexpr int kMaxWaves = 16;     // rows up to 8192 channels
 constexpr int kCandCap = 64;      // outlier candidates ranked by one wavefront
+constexpr int kMaxGatherRows = 64; // rows per workgroup with a gathered reference
 constexpr float kMagic = 12582912.0f;  // 1.5 * 2^23: adding it rounds to an integer (RNE)
 // Quotients t' = E * (1/s) within this distance of a half-integer are
 // recomputed with the correctly rounded division E / s.  |t' - E/s| is below
@@ -609,17 +610,18 @@ __device__ __forceinline__ Rsrc xhat_row(const Args& A, uint32_t row) {
                 A.xhat ? (uint32_t)A.d * es : 0u);
 }
 
-// Store-row indices of the rows a workgroup takes, 64 rows at a time in LDS:
-// slot i holds the index of the workgroup's row n0 + i, that is token row
-// blockIdx.x + (n0 + i) * gridDim.x (-1 past the last token).  Every
-// wavefront of the workgroup calls this at the same row counts (n0 a multiple
-// of 64), and the barriers keep the previous 64 in place until all have read
-// them.  Nothing happens without a row index array.
-__device__ __forceinline__ void fill_ref_rows(const Args& A, int32_t* rix, uint32_t n0) {
+// Store-row indices of the rows a workgroup takes.  With a gathered reference
+// the launch gives every workgroup at most kMaxGatherRows rows, so all of
+// them are loaded once, before the row loop (a load inside the loop would
+// make the compiler's wait counts conservative for the prefetched rows).
+//
+// LDS copy (the outlier kernel): slot i holds the index of the workgroup's
+// row i, that is token row blockIdx.x + i * gridDim.x (-1 past the last
+// token); filled by the first wavefront before a barrier.
+__device__ __forceinline__ void fill_ref_rows(const Args& A, int32_t* rix) {
     if (!A.ref_rows) return;
-    __syncthreads();
     if (threadIdx.x < (uint32_t)kWave) {
-        const uint64_t r = (uint64_t)blockIdx.x + (uint64_t)(n0 + threadIdx.x) * gridDim.x;
+        const uint64_t r = (uint64_t)blockIdx.x + (uint64_t)threadIdx.x * gridDim.x;
         rix[threadIdx.x] = r < A.tokens ? A.ref_rows[r] : -1;
     }
     __syncthreads();
@@ -627,6 +629,18 @@ __device__ __forceinline__ void fill_ref_rows(const Args& A, int32_t* rix, uint3
 
 __device__ __forceinline__ int32_t ref_index(const Args& A, const int32_t* rix, uint32_t n) {
     return A.ref_rows ? rix[n & (uint32_t)(kWave - 1)] : 0;
+}
+
+// Register copy (the other kernels): each wavefront holds the same indices in
+// one register, lane i for row i; reading one is a lane read, with no memory
+// wait and no barrier.
+__device__ __forceinline__ int32_t load_ref_rows_v(const Args& A, uint32_t lane) {
+    const uint64_t r = (uint64_t)blockIdx.x + (uint64_t)lane * gridDim.x;
+    return (A.ref_rows && r < A.tokens) ? A.ref_rows[r] : -1;
+}
+
+__device__ __forceinline__ int32_t ref_index_v(const Args& A, int32_t cache, uint32_t n) {
+    return A.ref_rows ? __builtin_amdgcn_readlane(cache, (int)(n & (uint32_t)(kWave - 1))) : 0;
 }
 
 // The index of the workgroup's first row, read directly (a scalar load), so
@@ -1014,7 +1028,6 @@ void rac_encode_kernel(Args A) {
     // LDS state of a row, double-buffered by row parity: every row that uses
     // LDS has a workgroup barrier, so no wave is more than one row ahead.
     __shared__ RowShared SS[2];
-    __shared__ int32_t RIX[kWave];  // store rows of the reference (gathered references only)
     extern __shared__ float4 XT[];  // per-wavefront store staging, kSlice each (sized at launch)
     const uint32_t lane = threadIdx.x & (kWave - 1);
     const int w = (int)(threadIdx.x / kWave);
@@ -1063,17 +1076,16 @@ void rac_encode_kernel(Args A) {
     };
     uint32_t row = blockIdx.x;
     uint4 nx, nr;
+    const int32_t rix = load_ref_rows_v(A, lane);  // store rows of the gathered reference
     load_row(row, first_ref_index(A), nx, nr);
     // Let the first row land before the loop: then the loop head holds no
     // wait, and inside the loop only the prefetched loads are waited for
     // (never the stores of the row before).
     __builtin_amdgcn_s_waitcnt(kWaitVmem0);
-    fill_ref_rows(A, RIX, 0u);
     for (uint32_t n = 0; row < A.tokens; row += gridDim.x, ++n) {
         RowShared& S = SS[n & 1];
         const uint4 xv = nx, rv = nr;
-        if (((n + 1u) & (uint32_t)(kWave - 1)) == 0u) fill_ref_rows(A, RIX, n + 1u);
-        load_row(row + gridDim.x, ref_index(A, RIX, n + 1u), nx, nr);
+        load_row(row + gridDim.x, ref_index_v(A, rix, n + 1u), nx, nr);
         float r[8], x[8];
         widen8(rv, r);
         widen8(xv, x);
@@ -1373,7 +1385,7 @@ void rac_encode_rows_kernel(Args A) {
             rp[i] = bload128(rr, off);
         }
     }
-    fill_ref_rows(A, RIX, 0u);
+    fill_ref_rows(A, RIX);
     // A store that the range check drops, so that stores are outstanding at
     // the loop entry as they are at the end of every row: the compiler's wait
     // analysis then keeps the memory operations in order across the loop and
@@ -1398,7 +1410,6 @@ void rac_encode_rows_kernel(Args A) {
         const uint32_t nrow = row + gridDim.x;
         const bool more = nrow < A.tokens;
         const uint64_t on = (uint64_t)nrow * (uint64_t)d;
-        if (((n + 1u) & (uint32_t)(kWave - 1)) == 0u) fill_ref_rows(A, RIX, n + 1u);
         const Rsrc nx = rsrc(A.x, on, more ? row_bytes : 0u), nr = ref_row(A, nrow, more, ref_index(A, RIX, n + 1u));
         uint32_t cf[CPW];
 #pragma unroll
@@ -1688,7 +1699,6 @@ void rac_encode_rows_kernel(Args A) {
 
 template <int BITS, int OM, bool BF16>
 __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
-    __shared__ int32_t RIX[kWave];  // store rows of the reference (gathered references only)
     extern __shared__ float4 XT[];  // per-wavefront store staging, kSlice each (sized at launch)
     const uint32_t lane = threadIdx.x & (kWave - 1);
     const int w = (int)(threadIdx.x / kWave);
@@ -1700,6 +1710,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
     const uint32_t ngq = (uint32_t)d >> A.lg_q, nga = (uint32_t)d >> A.lg_a;
     const uint32_t sh_fixed = (A.fixed && act) ? step_roundup(A.steps[grp_q]) : 0u;
     constexpr bool OUTL = OM == 1;
+    const int32_t rix = load_ref_rows_v(A, lane);  // store rows of the gathered reference
     // per-group outliers: entries per row, this chunk's first entry and count
     const uint32_t gent = (uint32_t)k * ngq;
     const uint32_t gfirst = ((uint32_t)(w * kChunk) >> A.lg_q) * (uint32_t)k;
@@ -1747,11 +1758,10 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
         const bool pch = OUTL & (lane < (uint32_t)k) & (ech < (uint32_t)d) & ((ech >> 9) == (uint32_t)w);
         uint32_t gref = 0u, gcf = 0u;
         if constexpr (OUTL) {
-            gref = bload16(ref_row(A, row, true, ref_index(A, RIX, n)), pch ? ech * 2u : kOut);
+            gref = bload16(ref_row(A, row, true, ref_index_v(A, rix, n)), pch ? ech * 2u : kOut);
             gcf = bload32(rsrc(A.coef, (uint64_t)row * nga, nga * 4u), pch ? (ech >> A.lg_a) * 4u : kOut);
         }
-        if (((n + 1u) & (uint32_t)(kWave - 1)) == 0u) fill_ref_rows(A, RIX, n + 1u);
-        nx = load(nrow, ref_index(A, RIX, n + 1u));
+        nx = load(nrow, ref_index_v(A, rix, n + 1u));
         const float a = f16_value(in.cf & 0xFFFFu), b0 = f16_value(in.cf >> 16);
         const float s = f16_value(in.sh);
         float r[8], rt[8], H[8];
@@ -1798,7 +1808,6 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
     const uint32_t G = gridDim.x;
     uint32_t row = blockIdx.x;
     In p = load(row, first_ref_index(A)), q;
-    fill_ref_rows(A, RIX, 0u);
     // (a store that the range check drops, so that stores are outstanding at
     // the loop entry as at the end of every row; the compiler's wait analysis
     // then keeps later waits exact instead of waiting for everything)
@@ -2047,7 +2056,11 @@ rac_status launch(KernelFn fn, Args A, hipStream_t stream, int threads = 0, int 
                 hipSuccess)
             return RAC_ERR_HIP;
         if (max_per_cu > 0 && per_cu > max_per_cu) per_cu = max_per_cu;
-        const int64_t resident = (int64_t)cus * (per_cu > 0 ? per_cu : 1);
+        int64_t resident = (int64_t)cus * (per_cu > 0 ? per_cu : 1);
+        // a gathered reference: at most kMaxGatherRows rows per workgroup,
+        // whose indices are loaded once up front
+        const int64_t gather_min = (rows + kMaxGatherRows - 1) / kMaxGatherRows;
+        if (A.ref_rows && resident < gather_min) resident = gather_min;
         if (blocks > resident) blocks = resident;
     }
     void* args[] = {&A};
