@@ -12,6 +12,7 @@ from __future__ import annotations
 import numpy as np
 import pytest
 
+import oracle
 import paper_2608_04991_amd as rac
 from paper_2608_04991_amd import workloads as wl
 from tests.gpu_util import assert_parity, cfgd, gpu_run, oracle_run, say, to_dev
@@ -178,5 +179,19 @@ def test_selected_spans_end_to_end():
     say(f"[gpu] selected spans end to end: {cov} of {T} positions covered")
     ow, ox = oracle_run(c, xb, _gathered(store, np.asarray(want, np.int32)))
     gw, gx, gd = _gpu_gather(c, xb, store, idx)
+    assert_parity(c, gw, gx, ow, ox)
+    assert np.array_equal(gx, gd)
+
+
+def test_gather_with_fixed_steps():
+    c = cfgd(64, 512, 64, 64, 4, 2, rac.RAC_FLAG_FIXED_STEP | GRP)
+    xb, rb, _ = wl.tiny(0)
+    steps = np.linspace(0.02, 0.2, 512 // 64).astype(np.float32)
+    store, idx = _history(xb, rb, 30, seed=77)
+    say("[gpu] gather with a calibrated step table and per-group outliers")
+    ref = _gathered(store, idx)
+    rc, ow, ox = oracle.encode(xb, ref, steps, **c)
+    assert rc == 0
+    gw, gx, gd = _gpu_gather(c, xb, store, idx, steps)
     assert_parity(c, gw, gx, ow, ox)
     assert np.array_equal(gx, gd)
