@@ -48,6 +48,11 @@ class _Layout(ctypes.Structure):
                 ("total", ctypes.c_uint64), ("off_ooff", ctypes.c_uint64)]
 
 
+class Moments(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_float), ("mr", ctypes.c_float), ("mx", ctypes.c_float),
+                ("crr", ctypes.c_float), ("crx", ctypes.c_float)]
+
+
 _lib = None
 
 
@@ -74,6 +79,11 @@ def _load(path: str):
     L.orc_fit_group.argtypes = [f32p, f32p, ctypes.c_int32, ctypes.POINTER(ctypes.c_float),
                                 ctypes.POINTER(ctypes.c_float)]
     L.orc_topk_row.argtypes = [f32p, ctypes.c_int32, ctypes.c_int32, vp]
+    L.orc_encode_pooled.argtypes = [ctypes.POINTER(_Cfg), u16p, u16p, ctypes.c_int64, vp, f32p, vp,
+                                    ctypes.c_size_t, vp]
+    L.orc_moments_row.argtypes = [f32p, f32p, ctypes.c_int32, ctypes.POINTER(Moments)]
+    L.orc_moments_merge.argtypes = [ctypes.POINTER(Moments), ctypes.POINTER(Moments), ctypes.POINTER(Moments)]
+    L.orc_moments_pool.argtypes = [vp, ctypes.c_int64, ctypes.POINTER(Moments)]
     return L
 
 
@@ -196,3 +206,37 @@ def topk_row(e, k: int):
     idx = np.zeros(max(int(k), 1), dtype=np.uint16)
     lib().orc_topk_row(_ptr(e), int(e.size), int(k), _ptr(idx))
     return idx[:k].copy()
+
+
+def encode_pooled(x, ref, seg_start, steps=None, *, want_xhat=True, **cfg):
+    """Encode with the fit pooled over segments (seg_start: [S+1] row starts).
+    Returns (status, wire, xhat)."""
+    c = _cfg(**cfg)
+    lay = layout(**cfg)
+    x = np.ascontiguousarray(x, dtype=np.uint16)
+    ref = None if ref is None else np.ascontiguousarray(ref, dtype=np.uint16)
+    steps = None if steps is None else np.ascontiguousarray(steps, dtype=np.float32)
+    seg = np.ascontiguousarray(seg_start, dtype=np.int32)
+    wire = np.zeros(max(lay["total"], 1), dtype=np.uint8)
+    xhat = None
+    if want_xhat:
+        dt = np.uint16 if (c.flags & FLAG_XHAT_BF16) else np.float32
+        xhat = np.zeros((c.tokens, c.hidden), dtype=dt)
+    rc = lib().orc_encode_pooled(ctypes.byref(c), _ptr(x), _ptr(ref), seg.size - 1, _ptr(seg), _ptr(steps),
+                                 _ptr(wire), lay["total"], _ptr(xhat))
+    return rc, wire[:lay["total"]], xhat
+
+
+def moments_row(r, x) -> Moments:
+    r = np.ascontiguousarray(r, dtype=np.float32)
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    m = Moments()
+    lib().orc_moments_row(_ptr(r), _ptr(x), int(r.size), ctypes.byref(m))
+    return m
+
+
+def moments_pool(rows) -> Moments:
+    arr = (Moments * len(rows))(*rows)
+    m = Moments()
+    lib().orc_moments_pool(ctypes.cast(arr, ctypes.c_void_p), len(rows), ctypes.byref(m))
+    return m

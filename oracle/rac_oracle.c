@@ -362,8 +362,11 @@ static void orc_store_xhat(const orc_config* cfg, void* xhat, int64_t i, float v
 }
 
 /* ------------------------------------------------------------------------ */
-int orc_encode(const orc_config* cfg, const uint16_t* x, const uint16_t* ref,
-               const float* steps, uint8_t* wire, size_t wire_cap, void* xhat) {
+/* pooled: NULL for the per-token fit, else [T][d/g_a][2] unrounded (alpha*,
+ * beta*) of each row's segment; pooled_flag marks the header. */
+static int orc_encode_impl(const orc_config* cfg, const uint16_t* x, const uint16_t* ref,
+                           const float* steps, uint8_t* wire, size_t wire_cap, void* xhat,
+                           const float* pooled) {
     orc_layout L;
     if (orc_layout_of(cfg, &L) != ORC_OK || !wire) return ORC_ERR_INVALID;
     if ((cfg->flags & ORC_FLAG_FIXED_STEP) && !steps) return ORC_ERR_INVALID;
@@ -384,6 +387,7 @@ int orc_encode(const orc_config* cfg, const uint16_t* x, const uint16_t* ref,
 
     memset(wire, 0, L.total);
     orc_write_header(cfg, &L, ref == NULL, wire);
+    if (pooled) put16(wire + 6, (uint16_t)(get16(wire + 6) | 16u)); /* coefficients pooled over segments */
 
     float* r = (float*)malloc(sizeof(float) * (size_t)d);
     float* xv = (float*)malloc(sizeof(float) * (size_t)d);
@@ -406,7 +410,12 @@ int orc_encode(const orc_config* cfg, const uint16_t* x, const uint16_t* ref,
         uint8_t* coef = wire + L.off_coef + (uint64_t)t * (uint64_t)(d / ga) * 4u;
         for (int32_t j = 0; j < d / ga; ++j) {
             float as, bs;
-            orc_fit_group(r + j * ga, xv + j * ga, ga, &as, &bs);
+            if (pooled) {
+                as = pooled[((uint64_t)t * (uint64_t)(d / ga) + (uint64_t)j) * 2u];
+                bs = pooled[((uint64_t)t * (uint64_t)(d / ga) + (uint64_t)j) * 2u + 1u];
+            } else {
+                orc_fit_group(r + j * ga, xv + j * ga, ga, &as, &bs);
+            }
             const uint16_t ah = orc_f16_rne_sat(as), bh = orc_f16_rne_sat(bs);
             put16(coef + 4 * j, ah);
             put16(coef + 4 * j + 2, bh);
@@ -488,6 +497,125 @@ int orc_encode(const orc_config* cfg, const uint16_t* x, const uint16_t* ref,
     free(oval);
     free(is_out);
     return ORC_OK;
+}
+
+int orc_encode(const orc_config* cfg, const uint16_t* x, const uint16_t* ref,
+               const float* steps, uint8_t* wire, size_t wire_cap, void* xhat) {
+    return orc_encode_impl(cfg, x, ref, steps, wire, wire_cap, xhat, NULL);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Fit pooled over segments of rows (the affine-fit equation over all fitting
+ * positions of a segment, for example one retrieved span).  Each (row, group)
+ * gives its two-pass centred moments exactly as the per-token fit does; the
+ * rows of a segment are combined by the pairwise merge of centred moments
+ * (Chan, Golub and LeVeque) over the binary-decomposition tree: a range of n
+ * rows splits into its first p rows, p the largest power of two below n, and
+ * the rest.  A one-row segment is the per-token fit, bit for bit. */
+
+void orc_moments_row(const float* r, const float* x, int32_t g, orc_moments* m) {
+    float* uu = (float*)malloc(sizeof(float) * (size_t)g);
+    float* uv = (float*)malloc(sizeof(float) * (size_t)g);
+    m->n = (float)g;
+    m->mr = orc_tsum(r, g) / (float)g;
+    m->mx = orc_tsum(x, g) / (float)g;
+    for (int32_t c = 0; c < g; ++c) {
+        const float u = r[c] - m->mr;
+        const float v = x[c] - m->mx;
+        uu[c] = u * u;
+        uv[c] = u * v;
+    }
+    m->crr = orc_tsum(uu, g);
+    m->crx = orc_tsum(uv, g);
+    free(uu);
+    free(uv);
+}
+
+void orc_moments_merge(const orc_moments* a, const orc_moments* b, orc_moments* o) {
+    const float n = a->n + b->n;
+    const float dr = b->mr - a->mr;
+    const float dx = b->mx - a->mx;
+    const float fb = b->n / n;
+    const float w = (a->n * b->n) / n;
+    orc_moments m;
+    m.n = n;
+    m.mr = a->mr + dr * fb;
+    m.mx = a->mx + dx * fb;
+    m.crr = (a->crr + b->crr) + (dr * dr) * w;
+    m.crx = (a->crx + b->crx) + (dr * dx) * w;
+    *o = m;
+}
+
+static void orc_pool_range(const orc_moments* rows, int64_t n, orc_moments* out) {
+    if (n == 1) {
+        *out = rows[0];
+        return;
+    }
+    int64_t p = 1;
+    while (p * 2 < n) p *= 2;
+    orc_moments a, b;
+    orc_pool_range(rows, p, &a);
+    orc_pool_range(rows + p, n - p, &b);
+    orc_moments_merge(&a, &b, out);
+}
+
+void orc_moments_pool(const orc_moments* rows, int64_t n, orc_moments* out) { orc_pool_range(rows, n, out); }
+
+int orc_encode_pooled(const orc_config* cfg, const uint16_t* x, const uint16_t* ref, int64_t segments,
+                      const int32_t* seg_start, const float* steps, uint8_t* wire, size_t wire_cap,
+                      void* xhat) {
+    orc_layout L;
+    if (orc_layout_of(cfg, &L) != ORC_OK || !seg_start) return ORC_ERR_INVALID;
+    const int64_t T = cfg->tokens;
+    const int32_t d = cfg->hidden, ga = cfg->group_align, G = d / ga;
+    if (segments < 1 || segments > T || seg_start[0] != 0 || seg_start[segments] != T) return ORC_ERR_INVALID;
+    for (int64_t s = 0; s < segments; ++s)
+        if (seg_start[s + 1] <= seg_start[s]) return ORC_ERR_INVALID;
+    if (!x) return ORC_ERR_INVALID;
+    for (int64_t i = 0; i < T * d; ++i) {
+        if (!isfinite(orc_bf16_to_f32(x[i]))) return ORC_ERR_NONFINITE;
+        if (ref && !isfinite(orc_bf16_to_f32(ref[i]))) return ORC_ERR_NONFINITE;
+    }
+    orc_moments* mom = (orc_moments*)malloc(sizeof(orc_moments) * (size_t)(T * G));
+    float* pooled = (float*)malloc(sizeof(float) * 2u * (size_t)(T * G));
+    float* r = (float*)malloc(sizeof(float) * (size_t)ga);
+    float* xv = (float*)malloc(sizeof(float) * (size_t)ga);
+    orc_moments* seg = (orc_moments*)malloc(sizeof(orc_moments) * (size_t)T);
+    for (int64_t t = 0; t < T; ++t)
+        for (int32_t j = 0; j < G; ++j) {
+            for (int32_t c = 0; c < ga; ++c) {
+                xv[c] = orc_bf16_to_f32(x[t * d + j * ga + c]);
+                r[c] = ref ? orc_bf16_to_f32(ref[t * d + j * ga + c]) : 0.0f;
+            }
+            orc_moments_row(r, xv, ga, &mom[t * G + j]);
+        }
+    for (int64_t s = 0; s < segments; ++s) {
+        const int64_t lo = seg_start[s], n = seg_start[s + 1] - seg_start[s];
+        for (int32_t j = 0; j < G; ++j) {
+            for (int64_t i = 0; i < n; ++i) seg[i] = mom[(lo + i) * G + j];
+            orc_moments m;
+            orc_moments_pool(seg, n, &m);
+            float a, b;
+            if (m.crr == 0.0f) { /* zero-variance reference: (0, mean x) */
+                a = 0.0f;
+                b = m.mx;
+            } else {
+                a = m.crx / m.crr;
+                b = m.mx - a * m.mr;
+            }
+            for (int64_t i = 0; i < n; ++i) {
+                pooled[((lo + i) * G + j) * 2] = a;
+                pooled[((lo + i) * G + j) * 2 + 1] = b;
+            }
+        }
+    }
+    const int rc = orc_encode_impl(cfg, x, ref, steps, wire, wire_cap, xhat, pooled);
+    free(mom);
+    free(pooled);
+    free(r);
+    free(xv);
+    free(seg);
+    return rc;
 }
 
 int orc_decode(const orc_config* cfg, const uint8_t* wire, const uint16_t* ref,

@@ -66,6 +66,15 @@ int orc_layout_of(const orc_config* cfg, orc_layout* out);
 int orc_encode(const orc_config* cfg, const uint16_t* x, const uint16_t* ref,
                const float* steps, uint8_t* wire, size_t wire_cap, void* xhat);
 
+/* Encode with the affine fit pooled over segments of rows: segment s covers
+ * rows [seg_start[s], seg_start[s+1]), 0 = seg_start[0] < ... <
+ * seg_start[segments] = T (host array).  Every row of a segment carries the
+ * segment's (alpha, beta); the wire is otherwise that of orc_encode, with
+ * header flag 16 set.  orc_decode reads it unchanged. */
+int orc_encode_pooled(const orc_config* cfg, const uint16_t* x, const uint16_t* ref, int64_t segments,
+                      const int32_t* seg_start, const float* steps, uint8_t* wire, size_t wire_cap,
+                      void* xhat);
+
 /* Receiver reconstruction from a wire and the receiver's own reference. */
 int orc_decode(const orc_config* cfg, const uint8_t* wire, const uint16_t* ref,
                const float* steps, void* xhat);
@@ -91,6 +100,16 @@ float orc_tsum(const float* v, int32_t n);
 /* Affine fit of one group before wire rounding: alpha*, beta*. */
 void orc_fit_group(const float* r, const float* x, int32_t g, float* alpha_star,
                    float* beta_star);
+/* Centred moments of one group: n, means, C_rr, C_rx. */
+typedef struct {
+    float n, mr, mx, crr, crx;
+} orc_moments;
+/* Moments of one row's group (two-pass, pairwise sums, as the fit). */
+void orc_moments_row(const float* r, const float* x, int32_t g, orc_moments* m);
+/* Pairwise merge of two disjoint sets' moments. */
+void orc_moments_merge(const orc_moments* a, const orc_moments* b, orc_moments* o);
+/* Moments of n consecutive rows merged over the binary-decomposition tree. */
+void orc_moments_pool(const orc_moments* rows, int64_t n, orc_moments* out);
 /* Per-token outlier choice: the k channels with the largest |e| (ties to the
  * lower channel), written ascending into idx[k]. */
 void orc_topk_row(const float* e, int32_t d, int32_t k, uint16_t* idx);

@@ -15,6 +15,7 @@ import pytest
 
 import oracle
 from tests import test_oracle_group_outliers as gpins
+from tests import test_oracle_pooled as ppins
 from tests import test_oracle_pins as pins
 
 # (name, text in rac_oracle.c, replacement)
@@ -46,6 +47,11 @@ MUTANTS = [
     ("group_outlier_left_in_dense", "is_out[c] = 1;\n                    ed[c] = 0.0f;\n",
      "is_out[c] = 1;\n"),
     ("group_decoder_ignores_group", "eh[g * gq + (int32_t)o] =", "eh[(int32_t)o] ="),
+    ("pool_drops_between_term", "m.crr = (a->crr + b->crr) + (dr * dr) * w;", "m.crr = a->crr + b->crr;"),
+    ("pool_weight_of_wrong_side", "const float fb = b->n / n;", "const float fb = a->n / n;"),
+    ("pool_crx_uses_dr_twice", "m.crx = (a->crx + b->crx) + (dr * dx) * w;",
+     "m.crx = (a->crx + b->crx) + (dr * dr) * w;"),
+    ("pool_repeats_the_first_row", "seg[i] = mom[(lo + i) * G + j];", "seg[i] = mom[lo * G + j];"),
     ("group_values_in_reverse", "put16(vrow + 2 * ((uint64_t)g * k + i), oval[c]);",
      "put16(vrow + 2 * ((uint64_t)g * k + (k - 1 - i)), oval[c]);"),
 ]
@@ -66,6 +72,9 @@ PINS = [
     lambda: gpins.test_group_outliers_match_brute_force_on_uplink_rows(128, 2, 4),
     gpins.test_group_outliers_ties_go_to_the_lower_offset,
     lambda: gpins.test_group_mode_sender_equals_receiver_bitwise(0),
+    lambda: ppins.test_pooled_fit_matches_exact_rational_least_squares(0),
+    ppins.test_pooled_moments_match_float64,
+    ppins.test_constant_reference_over_a_segment_gives_alpha_zero_and_the_pooled_mean,
 ]
 
 
