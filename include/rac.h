@@ -50,7 +50,7 @@
  * Wire format (little-endian, self-describing, all padding zero):
  *   header (256 B): u32 magic 'RAC1', u16 version 1, u16 flags (1 per-token
  *     outliers, 2 fixed step, 4 encoded against a zero reference, 8 per-group
- *     outliers), u32 tokens,
+ *     outliers, 16 coefficients pooled over segments), u32 tokens,
  *     u32 hidden, u32 g_a, u32 g_q, u8 bits, u8 coef fmt (1 = fp16 pair),
  *     u8 scale fmt (1 = fp16, 0 = absent), u8 outlier fmt (1 = u16 channel in
  *     the low half and fp16 value in the high half of a u32, 2 = per-group
@@ -201,6 +201,29 @@ rac_status rac_encode_gather(const rac_config* cfg, const void* x, const void* r
  * in rac_encode_gather; the result equals rac_decode with that reference). */
 rac_status rac_decode_gather(const rac_config* cfg, const void* wire, const void* ref_store, int64_t store_rows,
                              const int32_t* ref_rows, const float* fixed_steps, void* xhat, rac_stream_t stream);
+
+/* Encode with the affine fit pooled over segments of rows: the affine-fit
+ * equation over all fitting positions of a segment (for example one retrieved
+ * span) instead of one row.  Segment s covers token rows
+ * [seg_start[s], seg_start[s+1]); seg_start is a device int32 array of
+ * segments + 1 entries with 0 = seg_start[0] < ... < seg_start[segments] = T
+ * (bounds outside [0, T] are clamped on the device; other broken segmentations
+ * give unspecified coefficients, never an access outside the buffers).  Per
+ * (row, group) the centred moments are those of the per-token fit; the rows
+ * of a segment are combined by the pairwise merge of centred moments over the
+ * binary-decomposition tree (n rows split into the first p, p the largest
+ * power of two below n, and the rest), so a one-row segment is exactly the
+ * per-token fit.  Every row of a segment carries the segment's (alpha, beta),
+ * the wire is otherwise the one of rac_encode (header flag 16 marks the
+ * pooled fit) and rac_decode / rac_reconstruct read it unchanged.  Element
+ * counts of a segment are exact in binary32 up to 2^24 (g_a * rows).
+ * Requires g_a <= 512 and g_a * bits >= 128 (the row moments are staged in
+ * the wire's code section before the codes overwrite them), else
+ * RAC_ERR_UNSUPPORTED.  Three kernel launches on `stream`.  Other arguments
+ * and errors as rac_encode. */
+rac_status rac_encode_pooled(const rac_config* cfg, const void* x, const void* ref, int64_t segments,
+                             const int32_t* seg_start, const float* fixed_steps, void* wire, size_t wire_cap,
+                             void* xhat, rac_stream_t stream);
 
 /* ---- Reference selection for the prefill uplink (host only) ------------
  * Subsection "Historical References for Prefill Uplinks",

@@ -23,7 +23,7 @@ __all__ = [
     "STATUS",
     "library", "library_path", "rac_wire_layout", "rac_wire_size", "rac_parse_header",
     "rac_encode", "rac_reconstruct", "rac_decode", "rac_encode_gather", "rac_decode_gather",
-    "rac_status_string", "SpanIndex",
+    "rac_status_string", "SpanIndex", "rac_encode_pooled",
 ]
 
 RAC_FLAG_FIXED_STEP = 1
@@ -102,6 +102,8 @@ def library():
         L.rac_encode_gather.restype = ctypes.c_int
         L.rac_decode_gather.argtypes = [cp, vp, vp, ctypes.c_int64, vp, vp, vp, vp]
         L.rac_decode_gather.restype = ctypes.c_int
+        L.rac_encode_pooled.argtypes = [cp, vp, vp, ctypes.c_int64, vp, vp, vp, ctypes.c_size_t, vp, vp]
+        L.rac_encode_pooled.restype = ctypes.c_int
         L.rac_span_index_create.argtypes = [ctypes.c_int32]
         L.rac_span_index_create.restype = vp
         L.rac_span_index_destroy.argtypes = [vp]
@@ -247,3 +249,14 @@ class SpanIndex:
             self.close()
         except Exception:
             pass
+
+
+def rac_encode_pooled(cfg: RacConfig, x, ref, seg_start, fixed_steps, wire, xhat=None, stream=None,
+                      segments: int | None = None, wire_cap: int | None = None) -> None:
+    """Encode with the fit pooled over segments of rows (seg_start: device
+    int32 [segments + 1] row starts)."""
+    cap = wire_cap if wire_cap is not None else (_nbytes(wire) if not isinstance(wire, int) else 0)
+    nseg = int(segments) if segments is not None else int(seg_start.numel()) - 1
+    _check(library().rac_encode_pooled(ctypes.byref(cfg._c()), _ptr(x), _ptr(ref), nseg, _ptr(seg_start),
+                                       _ptr(fixed_steps), _ptr(wire), cap, _ptr(xhat), _stream(stream)),
+           "rac_encode_pooled")

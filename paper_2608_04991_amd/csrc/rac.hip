@@ -68,6 +68,9 @@ struct alignas(8) Args {
     int32_t lg_cpg_q;
     int32_t k;          // outliers per row, or per group with gout
     int32_t gout;       // per-group outlier mode
+    int32_t cf_given;   // the wire already holds every row's (alpha, beta) (pooled fit)
+    int32_t segments;   // pooled fit: segment count and row starts [segments + 1]
+    const int32_t* seg_start;
     int32_t fixed;
     int32_t xhat_bf16;
     float inv_ga;       // 1 / g_a (exact, power of two)
@@ -1130,8 +1133,9 @@ void rac_encode_kernel(Args A) {
             crr = tree_n(&S.part[2][g0], cpg_a);
             crx = tree_n(&S.part[3][g0], cpg_a);
         }
-        const uint32_t cf = fit_coef(crr, crx, mr, mx);
-        bstore32(rsrc(A.coef, (uint64_t)row * nga, nga * 4u), first_a ? (uint32_t)grp_a * 4u : kOut, cf);
+        const uint32_t cf = A.cf_given ? bload32(rsrc(A.coef, (uint64_t)row * nga, nga * 4u), (uint32_t)grp_a * 4u)
+                                       : fit_coef(crr, crx, mr, mx);
+        bstore32(rsrc(A.coef, (uint64_t)row * nga, nga * 4u), (first_a && !A.cf_given) ? (uint32_t)grp_a * 4u : kOut, cf);
 
         // a3: aligned reference R~ = fma(alpha, r, beta) and residual E = x - R~
         const float a = f16_value(cf & 0xFFFFu), b0 = f16_value(cf >> 16);
@@ -1820,6 +1824,131 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
 }
 
 // ---------------------------------------------------------------------------
+// Fit pooled over segments of rows (the affine-fit equation over all fitting
+// positions of a segment).  Three launches: the per-(row, group) centred
+// moments, their merge over each segment, then the encode with the merged
+// pair of every row given.
+
+struct Mom {
+    float n, mr, mx, crr, crx;
+};
+
+// Pairwise merge of the centred moments of two disjoint sets (Chan, Golub and
+// LeVeque), each step one rounded operation in a fixed order.
+__device__ __forceinline__ Mom mom_merge(const Mom& a, const Mom& b) {
+    const float n = a.n + b.n;
+    const float dr = b.mr - a.mr, dx = b.mx - a.mx;
+    const float fb = b.n / n;
+    const float w = (a.n * b.n) / n;
+    Mom m;
+    m.n = n;
+    m.mr = a.mr + dr * fb;
+    m.mx = a.mx + dx * fb;
+    m.crr = (a.crr + b.crr) + (dr * dr) * w;
+    m.crx = (a.crx + b.crx) + (dr * dx) * w;
+    return m;
+}
+
+// Moments of every (row, alignment group), as the per-token fit computes
+// them: one workgroup per row (strided), one wavefront per 512-channel chunk,
+// groups inside a chunk.  Written as float4 (m_r, m_x, C_rr, C_rx) to `mom`
+// [T][d/g_a] (the wire's code section, which the encode overwrites later).
+template <int GA>
+__global__ __launch_bounds__(kWave * kMaxWaves) void rac_moments_kernel(Args A, float4* mom) {
+    const uint32_t lane = threadIdx.x & (kWave - 1);
+    const int w = (int)(threadIdx.x / kWave);
+    const int d = A.d;
+    const int c0 = w * kChunk + (int)lane * 8;
+    const int lv_a = GA >= 0 ? GA : A.lane_lv_a;
+    const bool first_a = (lane & ((1u << lv_a) - 1u)) == 0u;
+    const uint32_t nga = (uint32_t)d >> A.lg_a, grp_a = (uint32_t)c0 >> A.lg_a;
+    const uint32_t row_bytes = (uint32_t)d * 2u;
+    for (uint32_t row = blockIdx.x; row < A.tokens; row += gridDim.x) {
+        const uint64_t o = (uint64_t)row * (uint64_t)d;
+        const uint4 xv = bload128(rsrc(A.x, o, row_bytes), (uint32_t)c0 * 2u);
+        const uint4 rv = bload128(rsrc(A.ref, o, A.ref ? row_bytes : 0u), (uint32_t)c0 * 2u);
+        float r[8], x[8], uu[8], uv[8];
+        widen8(rv, r);
+        widen8(xv, x);
+        const float mr = lsum<GA>(tree8(r), lv_a) * A.inv_ga;
+        const float mx = lsum<GA>(tree8(x), lv_a) * A.inv_ga;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const float u = r[j] - mr, v = x[j] - mx;
+            uu[j] = u * u;
+            uv[j] = u * v;
+        }
+        const float crr = lsum<GA>(tree8(uu), lv_a);
+        const float crx = lsum<GA>(tree8(uv), lv_a);
+        if (first_a && c0 < d) mom[(uint64_t)row * nga + grp_a] = make_float4(mr, mx, crr, crx);
+    }
+}
+
+// One wavefront per (segment, alignment group): merges the segment's row
+// moments over the binary-decomposition tree (a range of n rows splits into
+// its first p rows, p the largest power of two below n, and the rest).  Rows
+// are taken 64 at a time: inside a block, a bottom-up tree across lanes (an
+// unpaired last element passes up), which is that tree for the block; the
+// block results go on a stack of power-of-two sizes, merged whenever the top
+// two are equal, and the stack is merged from the top down at the end.  The
+// fp16 pair is then written to the coefficient slot of every row of the
+// segment.  Segment bounds are clamped to [0, T], so no access leaves the
+// buffers whatever the starts hold.
+__global__ __launch_bounds__(kWave) void rac_pool_kernel(Args A, const float4* mom) {
+    __shared__ Mom stk[40];
+    __shared__ uint32_t ssz[40];
+    const uint32_t lane = threadIdx.x;
+    const uint32_t nga = (uint32_t)A.d >> A.lg_a;
+    const uint32_t s = blockIdx.x / nga, j = blockIdx.x % nga;
+    const int64_t T = (int64_t)A.tokens;
+    int64_t lo = A.seg_start[s], hi = A.seg_start[s + 1];
+    lo = lo < 0 ? 0 : (lo > T ? T : lo);
+    hi = hi < lo ? lo : (hi > T ? T : hi);
+    const float gn = (float)(1 << A.lg_a);
+    int top = 0;
+    for (int64_t b0 = lo; b0 < hi; b0 += kWave) {
+        const uint32_t m = (uint32_t)((hi - b0) < kWave ? (hi - b0) : kWave);
+        Mom v{0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+        if (lane < m) {
+            const float4 f = mom[(uint64_t)(b0 + lane) * nga + j];
+            v = Mom{gn, f.x, f.y, f.z, f.w};
+        }
+#pragma unroll
+        for (int k = 0; k < 6; ++k) {
+            const uint32_t off = 1u << k;
+            const int addr = (int)(((lane + off) & (kWave - 1)) << 2);
+            Mom p;
+            p.n = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(v.n)));
+            p.mr = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(v.mr)));
+            p.mx = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(v.mx)));
+            p.crr = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(v.crr)));
+            p.crx = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(v.crx)));
+            if ((lane & (2u * off - 1u)) == 0u && lane + off < m) v = mom_merge(v, p);
+        }
+        if (lane == 0u) {
+            stk[top] = v;
+            ssz[top] = m;
+            ++top;
+            while (top >= 2 && ssz[top - 1] == ssz[top - 2]) {
+                stk[top - 2] = mom_merge(stk[top - 2], stk[top - 1]);
+                ssz[top - 2] *= 2u;
+                --top;
+            }
+        }
+        top = __builtin_amdgcn_readfirstlane(top);
+    }
+    uint32_t cf = 0u;
+    if (lane == 0u && top > 0) {
+        Mom r = stk[top - 1];
+        for (int i = top - 2; i >= 0; --i) r = mom_merge(stk[i], r);
+        cf = fit_coef(r.crr, r.crx, r.mr, r.mx);
+    }
+    cf = (uint32_t)__builtin_amdgcn_readfirstlane((int)cf);
+    for (int64_t t = lo + lane; t < hi; t += kWave)
+        bstore32(rsrc(A.coef, (uint64_t)t * nga, nga * 4u), j * 4u, cf);
+}
+
+// ---------------------------------------------------------------------------
 // Host side
 
 bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
@@ -1914,7 +2043,7 @@ void set_sections(Args& A, const Sizes& S) {
     A.goff = A.wire + (A.gout ? S.L.off_ooff : S.L.total);
 }
 
-void fill_header(Args& A, const rac_config* c, bool zero_ref) {
+void fill_header(Args& A, const rac_config* c, bool zero_ref, bool pooled = false) {
     uint8_t h[96] = {0};
     auto put16 = [&](int o, uint32_t v) { h[o] = (uint8_t)v; h[o + 1] = (uint8_t)(v >> 8); };
     auto put32 = [&](int o, uint32_t v) { for (int i = 0; i < 4; ++i) h[o + i] = (uint8_t)(v >> (8 * i)); };
@@ -1924,6 +2053,7 @@ void fill_header(Args& A, const rac_config* c, bool zero_ref) {
     if (c->flags & RAC_FLAG_FIXED_STEP) flags |= 2u;
     if (zero_ref) flags |= 4u;
     if (grouped(c)) flags |= 8u;
+    if (pooled) flags |= 16u;
     put32(0, 0x31434152u);
     put16(4, 1u);
     put16(6, flags);
@@ -2135,7 +2265,7 @@ rac_status rac_parse_header(const void* header_host, size_t len, rac_config* out
     auto g64 = [&](int o) { uint64_t v = 0; for (int i = 7; i >= 0; --i) v = (v << 8) | h[o + i]; return v; };
     if (g32(0) != 0x31434152u || g16(4) != 1u) return RAC_ERR_FORMAT;
     const uint32_t flags = g16(6);
-    if (flags & ~15u) return RAC_ERR_FORMAT;
+    if (flags & ~31u) return RAC_ERR_FORMAT;
     if ((flags & 1u) && (flags & 8u)) return RAC_ERR_FORMAT;
     rac_config c{};
     c.tokens = g32(8);
@@ -2213,6 +2343,60 @@ rac_status rac_encode_gather(const rac_config* cfg, const void* x, const void* r
 rac_status rac_decode_gather(const rac_config* cfg, const void* wire, const void* ref_store, int64_t store_rows,
                              const int32_t* ref_rows, const float* fixed_steps, void* xhat, rac_stream_t stream) {
     return run_decode(cfg, wire, ref_store, fixed_steps, xhat, stream, true, store_rows, ref_rows);
+}
+
+rac_status rac_encode_pooled(const rac_config* cfg, const void* x, const void* ref, int64_t segments,
+                             const int32_t* seg_start, const float* fixed_steps, void* wire, size_t wire_cap,
+                             void* xhat, rac_stream_t stream) {
+    rac_status st = common_checks(cfg);
+    if (st != RAC_OK) return st;
+    if (!wire || !x || cfg->tokens < 1 || !seg_start || segments < 1 || segments > cfg->tokens)
+        return RAC_ERR_INVALID;
+    if ((cfg->flags & RAC_FLAG_FIXED_STEP) && !fixed_steps) return RAC_ERR_INVALID;
+    // groups inside a chunk; the row moments (16 B per row and group) fit in
+    // the code section they are staged in
+    if (cfg->group_align > kChunk || (int64_t)cfg->group_align * cfg->bits < 128) return RAC_ERR_UNSUPPORTED;
+    if (!aligned(wire, 256) || !aligned(x, 16) || (ref && !aligned(ref, 16)) || (xhat && !aligned(xhat, 16)) ||
+        (fixed_steps && !aligned(fixed_steps, 4)) || !aligned(seg_start, 4))
+        return RAC_ERR_ALIGN;
+    const Sizes S = sizes_of(cfg);
+    if (wire_cap < S.L.total) return RAC_ERR_CAPACITY;
+    Args A = make_args(cfg, S);
+    A.x = static_cast<const uint16_t*>(x);
+    A.ref = static_cast<const uint16_t*>(ref);
+    A.steps = (cfg->flags & RAC_FLAG_FIXED_STEP) ? fixed_steps : nullptr;
+    A.wire = static_cast<uint8_t*>(wire);
+    set_sections(A, S);
+    A.xhat = xhat;
+    A.segments = (int32_t)segments;
+    A.seg_start = seg_start;
+    float4* mom = reinterpret_cast<float4*>(A.codes);
+    // 1. row moments
+    const int threads = A.nch * kWave;
+    void* margs[] = {&A, &mom};
+    const void* mfn = A.lane_lv_a == 3 ? reinterpret_cast<const void*>(rac_moments_kernel<3>)
+                    : A.lane_lv_a == 4 ? reinterpret_cast<const void*>(rac_moments_kernel<4>)
+                                       : reinterpret_cast<const void*>(rac_moments_kernel<-1>);
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return RAC_ERR_HIP;
+    const int64_t mblocks = cfg->tokens < (int64_t)cus * 4 ? cfg->tokens : (int64_t)cus * 4;
+    if (hipLaunchKernel(mfn, dim3((unsigned)mblocks), dim3((unsigned)threads), margs, 0, stream) != hipSuccess)
+        return RAC_ERR_HIP;
+    // 2. merge per (segment, group) into every row's coefficient slot
+    const uint64_t nga = (uint64_t)(cfg->hidden / cfg->group_align);
+    const uint64_t pblocks = (uint64_t)segments * nga;
+    if (pblocks > 0x7FFFFFFFull) return RAC_ERR_UNSUPPORTED;
+    void* pargs[] = {&A, &mom};
+    if (hipLaunchKernel(reinterpret_cast<const void*>(rac_pool_kernel), dim3((unsigned)pblocks), dim3(kWave), pargs, 0,
+                        stream) != hipSuccess)
+        return RAC_ERR_HIP;
+    // 3. the encode with the pairs given (one-wavefront-per-chunk kernel)
+    A.cf_given = 1;
+    A.write_header = 1;
+    fill_header(A, cfg, ref == nullptr, true);
+    return launch(pick_encode(A, cfg->bits), A, stream);
 }
 
 rac_status rac_reconstruct(const rac_config* cfg, const void* wire, const void* ref,

@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == {"rac_wire_layout", "rac_wire_size", "rac_parse_header", "rac_encode",
                           "rac_reconstruct", "rac_decode", "rac_encode_gather", "rac_decode_gather",
                           "rac_status_string", "rac_span_index_create", "rac_span_index_destroy",
-                          "rac_span_index_add", "rac_span_select"}
+                          "rac_span_index_add", "rac_span_select", "rac_encode_pooled"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -220,3 +220,15 @@ def test_binding_raises_without_the_library(monkeypatch):
         rac.rac_encode(rac.RacConfig(4, 512, 64, 64, 4), FAKE, FAKE, None, FAKE, FAKE, stream=0, wire_cap=1)
     with pytest.raises(RuntimeError, match="missing"):
         rac.SpanIndex(8)
+
+
+def test_pooled_argument_errors_are_synchronous(lib):
+    L = rac.library()
+    enc = lambda cfg, segs=4, starts=FAKE, x=FAKE: L.rac_encode_pooled(
+        ctypes.byref(cfg._c()), x, FAKE, segs, starts, None, FAKE, 1 << 40, FAKE, 0)
+    good = rac.RacConfig(64, 512, 64, 64, 4)
+    assert enc(good, starts=None) == 1 and enc(good, segs=0) == 1 and enc(good, segs=65) == 1
+    assert enc(good, x=None) == 1 and enc(good, starts=FAKE + 2) == 2
+    assert enc(rac.RacConfig(64, 2048, 1024, 64, 4)) == 6        # groups wider than a chunk
+    assert enc(rac.RacConfig(64, 512, 32, 64, 2)) == 6           # moments do not fit the code section
+    assert enc(rac.RacConfig(0, 512, 64, 64, 4), segs=1) == 1    # no rows to pool
