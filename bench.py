@@ -217,6 +217,7 @@ def main():
             torch, rac, sets, nsets, stream, args.steps)
         extras["gathered_reference"] = gather_rates(torch, rac, cfg, rb, sets, nsets, stream, args.steps)
         extras["span_selection"] = span_selection_cost(rac, T)
+        extras["pooled_fit"] = pooled_rates(torch, rac, cfg, sets, nsets, stream, args.steps)
     if args.all_configs:
         del sets
         torch.cuda.empty_cache()
@@ -375,6 +376,38 @@ def all_config_rates(torch, rac, wl, dev, stream):
         for bits in (2, 3, 4, 8):
             run(f"long_context_32768x4096_g{g}_b{bits}_k16", rac.RacConfig(32768, 4096, g, g, bits, 16), xb, rb, 2)
     return out
+
+
+def pooled_rates(torch, rac, cfg, sets, nsets, stream, steps):
+    """rac_encode_pooled on the benchmark inputs, with segments standing for
+    retrieved spans (random lengths of 1 to 600 rows): average time of the
+    whole call (its three launches) over `steps` back-to-back calls, and the
+    fraction of 8 TB/s by the per-token encode's algorithmic bytes (the
+    pooled call also reads x and ref a second time for the moments)."""
+    T, d = cfg.tokens, cfg.hidden
+    rng = np.random.default_rng(12)
+    cuts = np.unique(np.concatenate([[0, T], np.cumsum(rng.integers(1, 600, 40))]))
+    seg = torch.from_numpy(cuts[cuts <= T].astype(np.int32)).cuda()
+    wb = rac.rac_wire_size(cfg)
+    wires = [torch.empty(wb, dtype=torch.uint8, device="cuda") for _ in range(nsets)]
+
+    def enc(i):
+        s = sets[i % nsets]
+        rac.rac_encode_pooled(cfg, s["x"], s["ref"], seg, None, wires[i % nsets], s["xhat"], stream=stream)
+
+    for i in range(2 * nsets):
+        enc(i)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    for i in range(steps):
+        enc(i)
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    us = ev[0].elapsed_time(ev[1]) / steps * 1e3
+    del wires
+    return {"segments": int(seg.numel()) - 1, "encode_us": round(us, 2),
+            "hbm_frac_by_encode_bytes": round(algorithmic_bytes(T, d, wb) / us / 1e3 / HBM_PEAK_GBPS, 4)}
 
 
 def span_selection_cost(rac, T, window=16, n_hist=7):

@@ -1441,8 +1441,12 @@ void rac_encode_rows_kernel(Args A) {
                 uv[j] = u * v;
             }
             const float crr = lsum<GA>(tree8(uu), lv_a), crx = lsum<GA>(tree8(uv), lv_a);
-            cf[i] = fit_coef(crr, crx, mr, mx);
-            bstore32(rcoef, first_a ? (c0 >> A.lg_a) * 4u : kOut, cf[i]);
+            // (a pooled fit gives every row's pair in the wire: read, not fitted;
+            // the load is issued in both cases, out of range unless given, so the
+            // row's memory operations do not depend on the mode)
+            const uint32_t given = bload32(rcoef, A.cf_given ? (c0 >> A.lg_a) * 4u : kOut);
+            cf[i] = A.cf_given ? given : fit_coef(crr, crx, mr, mx);
+            bstore32(rcoef, (first_a && !A.cf_given) ? (c0 >> A.lg_a) * 4u : kOut, cf[i]);
             const float a = f16_value(cf[i] & 0xFFFFu), b0 = f16_value(cf[i] >> 16);
             float e[8];
 #pragma unroll
@@ -1884,20 +1888,26 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_moments_kernel(Args A, 
     }
 }
 
-// One wavefront per (segment, alignment group): merges the segment's row
-// moments over the binary-decomposition tree (a range of n rows splits into
-// its first p rows, p the largest power of two below n, and the rest).  Rows
-// are taken 64 at a time: inside a block, a bottom-up tree across lanes (an
-// unpaired last element passes up), which is that tree for the block; the
-// block results go on a stack of power-of-two sizes, merged whenever the top
-// two are equal, and the stack is merged from the top down at the end.  The
-// fp16 pair is then written to the coefficient slot of every row of the
-// segment.  Segment bounds are clamped to [0, T], so no access leaves the
-// buffers whatever the starts hold.
-__global__ __launch_bounds__(kWave) void rac_pool_kernel(Args A, const float4* mom) {
+// One workgroup of kPoolWaves wavefronts per (segment, alignment group):
+// merges the segment's row moments over the binary-decomposition tree (a
+// range of n rows splits into its first p rows, p the largest power of two
+// below n, and the rest).  Rows are taken in blocks of 64, one block per
+// wavefront at a time: inside a block, a bottom-up tree across lanes (an
+// unpaired last element passes up), which is that tree for the block.  One
+// thread then takes the block results in row order onto a stack of
+// power-of-two sizes, merging whenever the top two are equal, and merges the
+// stack from the top down at the end.  The fp16 pair goes to the coefficient
+// slot of every row of the segment.  Segment bounds are clamped to [0, T], so
+// no access leaves the buffers whatever the starts hold.
+constexpr int kPoolWaves = 16;
+
+__global__ __launch_bounds__(kWave * kPoolWaves) void rac_pool_kernel(Args A, const float4* mom) {
+    __shared__ Mom blk[kPoolWaves];
+    __shared__ uint32_t bsz[kPoolWaves];
     __shared__ Mom stk[40];
     __shared__ uint32_t ssz[40];
-    const uint32_t lane = threadIdx.x;
+    __shared__ uint32_t cf_shared;
+    const uint32_t lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
     const uint32_t nga = (uint32_t)A.d >> A.lg_a;
     const uint32_t s = blockIdx.x / nga, j = blockIdx.x % nga;
     const int64_t T = (int64_t)A.tokens;
@@ -1905,9 +1915,11 @@ __global__ __launch_bounds__(kWave) void rac_pool_kernel(Args A, const float4* m
     lo = lo < 0 ? 0 : (lo > T ? T : lo);
     hi = hi < lo ? lo : (hi > T ? T : hi);
     const float gn = (float)(1 << A.lg_a);
-    int top = 0;
-    for (int64_t b0 = lo; b0 < hi; b0 += kWave) {
-        const uint32_t m = (uint32_t)((hi - b0) < kWave ? (hi - b0) : kWave);
+    int top = 0;  // (thread 0's)
+    for (int64_t p0 = lo; p0 < hi; p0 += (int64_t)kWave * kPoolWaves) {
+        const int64_t b0 = p0 + (int64_t)wv * kWave;
+        const int64_t left = hi - b0;
+        const uint32_t m = left <= 0 ? 0u : (left < kWave ? (uint32_t)left : (uint32_t)kWave);
         Mom v{0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
         if (lane < m) {
             const float4 f = mom[(uint64_t)(b0 + lane) * nga + j];
@@ -1926,25 +1938,36 @@ __global__ __launch_bounds__(kWave) void rac_pool_kernel(Args A, const float4* m
             if ((lane & (2u * off - 1u)) == 0u && lane + off < m) v = mom_merge(v, p);
         }
         if (lane == 0u) {
-            stk[top] = v;
-            ssz[top] = m;
-            ++top;
-            while (top >= 2 && ssz[top - 1] == ssz[top - 2]) {
-                stk[top - 2] = mom_merge(stk[top - 2], stk[top - 1]);
-                ssz[top - 2] *= 2u;
-                --top;
+            blk[wv] = v;
+            bsz[wv] = m;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0u) {
+            for (int b = 0; b < kPoolWaves && bsz[b] != 0u; ++b) {
+                stk[top] = blk[b];
+                ssz[top] = bsz[b];
+                ++top;
+                while (top >= 2 && ssz[top - 1] == ssz[top - 2]) {
+                    stk[top - 2] = mom_merge(stk[top - 2], stk[top - 1]);
+                    ssz[top - 2] *= 2u;
+                    --top;
+                }
             }
         }
-        top = __builtin_amdgcn_readfirstlane(top);
+        __syncthreads();
     }
-    uint32_t cf = 0u;
-    if (lane == 0u && top > 0) {
-        Mom r = stk[top - 1];
-        for (int i = top - 2; i >= 0; --i) r = mom_merge(stk[i], r);
-        cf = fit_coef(r.crr, r.crx, r.mr, r.mx);
+    if (threadIdx.x == 0u) {
+        uint32_t cf = 0u;
+        if (top > 0) {
+            Mom r = stk[top - 1];
+            for (int i = top - 2; i >= 0; --i) r = mom_merge(stk[i], r);
+            cf = fit_coef(r.crr, r.crx, r.mr, r.mx);
+        }
+        cf_shared = cf;
     }
-    cf = (uint32_t)__builtin_amdgcn_readfirstlane((int)cf);
-    for (int64_t t = lo + lane; t < hi; t += kWave)
+    __syncthreads();
+    const uint32_t cf = cf_shared;
+    for (int64_t t = lo + threadIdx.x; t < hi; t += (int64_t)kWave * kPoolWaves)
         bstore32(rsrc(A.coef, (uint64_t)t * nga, nga * 4u), j * 4u, cf);
 }
 
@@ -2389,13 +2412,14 @@ rac_status rac_encode_pooled(const rac_config* cfg, const void* x, const void* r
     const uint64_t pblocks = (uint64_t)segments * nga;
     if (pblocks > 0x7FFFFFFFull) return RAC_ERR_UNSUPPORTED;
     void* pargs[] = {&A, &mom};
-    if (hipLaunchKernel(reinterpret_cast<const void*>(rac_pool_kernel), dim3((unsigned)pblocks), dim3(kWave), pargs, 0,
-                        stream) != hipSuccess)
+    if (hipLaunchKernel(reinterpret_cast<const void*>(rac_pool_kernel), dim3((unsigned)pblocks),
+                        dim3(kWave * kPoolWaves), pargs, 0, stream) != hipSuccess)
         return RAC_ERR_HIP;
-    // 3. the encode with the pairs given (one-wavefront-per-chunk kernel)
+    // 3. the encode with the pairs given
     A.cf_given = 1;
     A.write_header = 1;
     fill_header(A, cfg, ref == nullptr, true);
+    if (use_rows_kernel(A)) return launch(pick_rows(A, cfg->bits), A, stream, kRowsWaves * kWave);
     return launch(pick_encode(A, cfg->bits), A, stream);
 }
 
