@@ -1893,8 +1893,10 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_moments_kernel(Args A, 
 // range of n rows splits into its first p rows, p the largest power of two
 // below n, and the rest).  Rows are taken in blocks of 64, one block per
 // wavefront at a time: inside a block, a bottom-up tree across lanes (an
-// unpaired last element passes up), which is that tree for the block.  One
-// thread then takes the block results in row order onto a stack of
+// unpaired last element passes up), which is that tree for the block.  The
+// pass's blocks (all whole but possibly the last) are merged the same way by
+// the lanes of the first wavefront, which is again that tree over their rows.
+// One thread takes the pass results in row order onto a stack of
 // power-of-two sizes, merging whenever the top two are equal, and merges the
 // stack from the top down at the end.  The fp16 pair goes to the coefficient
 // slot of every row of the segment.  Segment bounds are clamped to [0, T], so
@@ -1915,18 +1917,9 @@ __global__ __launch_bounds__(kWave * kPoolWaves) void rac_pool_kernel(Args A, co
     lo = lo < 0 ? 0 : (lo > T ? T : lo);
     hi = hi < lo ? lo : (hi > T ? T : hi);
     const float gn = (float)(1 << A.lg_a);
-    int top = 0;  // (thread 0's)
-    for (int64_t p0 = lo; p0 < hi; p0 += (int64_t)kWave * kPoolWaves) {
-        const int64_t b0 = p0 + (int64_t)wv * kWave;
-        const int64_t left = hi - b0;
-        const uint32_t m = left <= 0 ? 0u : (left < kWave ? (uint32_t)left : (uint32_t)kWave);
-        Mom v{0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
-        if (lane < m) {
-            const float4 f = mom[(uint64_t)(b0 + lane) * nga + j];
-            v = Mom{gn, f.x, f.y, f.z, f.w};
-        }
-#pragma unroll
-        for (int k = 0; k < 6; ++k) {
+    // bottom-up tree over the first m lanes' moments (result in lane 0)
+    auto lane_tree = [&](Mom v, uint32_t m, int levels) {
+        for (int k = 0; k < levels; ++k) {
             const uint32_t off = 1u << k;
             const int addr = (int)(((lane + off) & (kWave - 1)) << 2);
             Mom p;
@@ -1937,15 +1930,37 @@ __global__ __launch_bounds__(kWave * kPoolWaves) void rac_pool_kernel(Args A, co
             p.crx = __int_as_float(__builtin_amdgcn_ds_bpermute(addr, __float_as_int(v.crx)));
             if ((lane & (2u * off - 1u)) == 0u && lane + off < m) v = mom_merge(v, p);
         }
+        return v;
+    };
+    int top = 0;  // (thread 0's)
+    for (int64_t p0 = lo; p0 < hi; p0 += (int64_t)kWave * kPoolWaves) {
+        const int64_t b0 = p0 + (int64_t)wv * kWave;
+        const int64_t left = hi - b0;
+        const uint32_t m = left <= 0 ? 0u : (left < kWave ? (uint32_t)left : (uint32_t)kWave);
+        Mom v{0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+        if (lane < m) {
+            const float4 f = mom[(uint64_t)(b0 + lane) * nga + j];
+            v = Mom{gn, f.x, f.y, f.z, f.w};
+        }
+        v = lane_tree(v, m, 6);
         if (lane == 0u) {
             blk[wv] = v;
             bsz[wv] = m;
         }
         __syncthreads();
-        if (threadIdx.x == 0u) {
-            for (int b = 0; b < kPoolWaves && bsz[b] != 0u; ++b) {
-                stk[top] = blk[b];
-                ssz[top] = bsz[b];
+        if (wv == 0u) {
+            // the pass's blocks: whole 64-row blocks, possibly a partial last one
+            uint32_t nb = 0u, rows = 0u;
+            for (int b = 0; b < kPoolWaves; ++b) {
+                nb += bsz[b] != 0u ? 1u : 0u;
+                rows += bsz[b];
+            }
+            Mom u{0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+            if (lane < nb) u = blk[lane];
+            u = lane_tree(u, nb, 4);
+            if (lane == 0u) {
+                stk[top] = u;
+                ssz[top] = rows;
                 ++top;
                 while (top >= 2 && ssz[top - 1] == ssz[top - 2]) {
                     stk[top - 2] = mom_merge(stk[top - 2], stk[top - 1]);
