@@ -192,7 +192,7 @@ def main():
                                "reconstruction, fp32) + rac_decode",
                    "tokens": T, "hidden": d, "group": g, "bits": b, "outlier_k": k,
                    "wire_bytes": wbytes, "rotating_buffer_sets": nsets},
-        "roofline": {"kernel": "rac_encode_rows_kernel<4,4,4,4,2>", "bound": "hbm",
+        "roofline": {"kernel": "rac_encode_rows_kernel<4,4,4,4,2,false>", "bound": "hbm",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "algorithmic_bytes_per_launch": enc_alg,

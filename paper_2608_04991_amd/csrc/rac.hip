@@ -1342,7 +1342,9 @@ __device__ __forceinline__ void opaque_n(uint4 (&r)[N]) {
     for (int i = 0; i < N; ++i) asm volatile("" : "+v"(r[i].x), "+v"(r[i].y), "+v"(r[i].z), "+v"(r[i].w));
 }
 
-template <int BITS, int GA, int GQ, int NW, int CPW>
+// GIVEN: the wire already holds every row's (alpha, beta) (pooled fit), which
+// is read instead of fitted.
+template <int BITS, int GA, int GQ, int NW, int CPW, bool GIVEN>
 __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(CPW == 2 ? 7 : 4)))
 void rac_encode_rows_kernel(Args A) {
     // (a row's lists are read before the next row's first barrier and
@@ -1441,12 +1443,12 @@ void rac_encode_rows_kernel(Args A) {
                 uv[j] = u * v;
             }
             const float crr = lsum<GA>(tree8(uu), lv_a), crx = lsum<GA>(tree8(uv), lv_a);
-            // (a pooled fit gives every row's pair in the wire: read, not fitted;
-            // the load is issued in both cases, out of range unless given, so the
-            // row's memory operations do not depend on the mode)
-            const uint32_t given = bload32(rcoef, A.cf_given ? (c0 >> A.lg_a) * 4u : kOut);
-            cf[i] = A.cf_given ? given : fit_coef(crr, crx, mr, mx);
-            bstore32(rcoef, (first_a && !A.cf_given) ? (c0 >> A.lg_a) * 4u : kOut, cf[i]);
+            if constexpr (GIVEN) {
+                cf[i] = bload32(rcoef, (c0 >> A.lg_a) * 4u);
+            } else {
+                cf[i] = fit_coef(crr, crx, mr, mx);
+                bstore32(rcoef, first_a ? (c0 >> A.lg_a) * 4u : kOut, cf[i]);
+            }
             const float a = f16_value(cf[i] & 0xFFFFu), b0 = f16_value(cf[i] >> 16);
             float e[8];
 #pragma unroll
@@ -2154,20 +2156,20 @@ KernelFn pick_encode(const Args& A, int bits) {
     return encode_for<-1, -1>(bits, om);
 }
 
-template <int GA, int GQ, int CPW>
+template <int GA, int GQ, int CPW, bool GIVEN>
 KernelFn rows_for_bits(int bits) {
     switch (bits) {
-        case 2: return rac_encode_rows_kernel<2, GA, GQ, kRowsWaves, CPW>;
-        case 3: return rac_encode_rows_kernel<3, GA, GQ, kRowsWaves, CPW>;
-        case 4: return rac_encode_rows_kernel<4, GA, GQ, kRowsWaves, CPW>;
-        default: return rac_encode_rows_kernel<8, GA, GQ, kRowsWaves, CPW>;
+        case 2: return rac_encode_rows_kernel<2, GA, GQ, kRowsWaves, CPW, GIVEN>;
+        case 3: return rac_encode_rows_kernel<3, GA, GQ, kRowsWaves, CPW, GIVEN>;
+        case 4: return rac_encode_rows_kernel<4, GA, GQ, kRowsWaves, CPW, GIVEN>;
+        default: return rac_encode_rows_kernel<8, GA, GQ, kRowsWaves, CPW, GIVEN>;
     }
 }
 
 // Rows of up to 4096 channels: two chunks per wavefront; up to 8192: four.
-template <int GA, int GQ>
+template <int GA, int GQ, bool GIVEN = false>
 KernelFn rows_for(int bits, int d) {
-    return d <= kRowsWaves * 2 * kChunk ? rows_for_bits<GA, GQ, 2>(bits) : rows_for_bits<GA, GQ, 4>(bits);
+    return d <= kRowsWaves * 2 * kChunk ? rows_for_bits<GA, GQ, 2, GIVEN>(bits) : rows_for_bits<GA, GQ, 4, GIVEN>(bits);
 }
 
 // Rows with outliers take the NW-wavefront kernel when it holds the whole
@@ -2178,6 +2180,12 @@ bool use_rows_kernel(const Args& A) {
 }
 
 KernelFn pick_rows(const Args& A, int bits) {
+    // given pairs (pooled fit): the fixed 128 and 64 shapes and the generic one
+    if (A.cf_given) {
+        if (A.lane_lv_a == 4 && A.lane_lv_q == 4) return rows_for<4, 4, true>(bits, A.d);
+        if (A.lane_lv_a == 3 && A.lane_lv_q == 3) return rows_for<3, 3, true>(bits, A.d);
+        return rows_for<-1, -1, true>(bits, A.d);
+    }
     if (A.lane_lv_a == 3 && A.lane_lv_q == 3) return rows_for<3, 3>(bits, A.d);
     if (A.lane_lv_a == 4 && A.lane_lv_q == 4) return rows_for<4, 4>(bits, A.d);
     if (A.lane_lv_a == 3 && A.lane_lv_q == 4) return rows_for<3, 4>(bits, A.d);
