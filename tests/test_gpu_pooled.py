@@ -110,3 +110,25 @@ def test_full_prefill_uplink_4096x4096_pooled_over_spans():
     ow, ox = _oracle_pooled(c, xb, rb, seg)
     assert_parity(c, gw, gx, ow, ox)
     torch.cuda.empty_cache()
+
+
+def test_pooled_with_fixed_steps_and_group_outliers():
+    import torch
+    c = cfgd(64, 512, 64, 64, 4, 2, rac.RAC_FLAG_FIXED_STEP | GRP)
+    xb, rb, _ = wl.tiny(0)
+    steps = np.linspace(0.02, 0.2, 512 // 64).astype(np.float32)
+    seg = np.array([0, 10, 11, 40, 64], np.int32)
+    say("[gpu] pooled with a calibrated step table and per-group outliers")
+    rc, ow, ox = oracle.encode_pooled(xb, rb, seg, steps, **c)
+    assert rc == 0
+    cfg = rac.RacConfig(**c)
+    x, ref = to_dev(xb), to_dev(rb)
+    st = torch.from_numpy(steps).cuda()
+    wire = torch.full((rac.rac_wire_size(cfg),), 0xAB, dtype=torch.uint8, device="cuda")
+    xh = torch.full((64, 512), -1.0, dtype=torch.float32, device="cuda")
+    xd = torch.full((64, 512), -1.0, dtype=torch.float32, device="cuda")
+    rac.rac_encode_pooled(cfg, x, ref, torch.from_numpy(seg).cuda(), st, wire, xh)
+    rac.rac_decode(cfg, wire, ref, st, xd)
+    torch.cuda.synchronize()
+    assert_parity(c, wire.cpu().numpy(), xh.cpu().numpy(), ow, ox)
+    assert torch.equal(xh, xd)
