@@ -226,7 +226,7 @@ rac_status rac_encode_pooled(const rac_config* cfg, const void* x, const void* r
                              void* xhat, rac_stream_t stream);
 
 /* ---- Reference selection for the prefill uplink (host only) ------------
- * Subsection "Historical References for Prefill Uplinks",
+ * Subsection "Repeated-Span Retrieval for Prefill Uplinks",
  * Eq. prefill-reference-selection.  A span index holds the token streams of
  * earlier requests and the store row of each of their tokens' activations;
  * rac_span_select turns the current prompt into the ref_rows array of

@@ -1,5 +1,5 @@
 """Plain reference of the prefill-uplink reference selection (subsection
-"Historical References for Prefill Uplinks", Eq. prefill-reference-selection).
+"Repeated-Span Retrieval for Prefill Uplinks", Eq. prefill-reference-selection).
 
 TEST INFRASTRUCTURE ONLY: the test suite is the only caller; the product
 library never imports it and it imports nothing from the product.

@@ -1,5 +1,5 @@
 // spans.cpp - host-side selection of the prefill-uplink reference rows
-// (subsection "Historical References for Prefill Uplinks",
+// (subsection "Repeated-Span Retrieval for Prefill Uplinks",
 // Eq. prefill-reference-selection).  Produces, for every position of the
 // current prompt, the row of the activation store that rac_encode_gather and
 // rac_decode_gather read as its reference.
