@@ -1,24 +1,39 @@
 """Benchmark of the RAC codec hot path on one MI355X.
 
-One step = one pass of the whole hot path over one batch of the prefill-uplink
-workload (Llama-3-8B-shaped boundary state: 4096 tokens x 4096 hidden bf16,
-alignment/quantization group 128, 4-bit codes, top-8 outliers per token):
-rac_encode with the fused sender reconstruction, then the receiver's
-rac_decode, on one stream.  Inputs are resident in HBM before timing starts;
-batches rotate through enough buffer sets (> 1 GB) that no step finds its
-inputs in the 256 MB Infinity Cache.  Untimed steps run for --warm-ms first:
-the GPU clock climbs over the first ~20 ms of sustained load, and the timed
-steps measure the steady state.
+One step = one pass of the whole hot path over one batch of the prefill
+downlink workload, the largest one-GPU configuration (Qwen2-7B-shaped boundary
+state: 8 sequences x 8192 tokens = 65536 tokens x 3584 hidden bf16, group 128,
+4-bit codes, top-4 outliers per token; the reference is the bf16 sender
+reconstruction of a synthetic uplink state): rac_encode with the fused fp32
+sender reconstruction of one batch, and rac_decode of the batch encoded in the
+step before, on one stream.  Three buffer sets of 2.9 GB rotate, so no launch
+reads what the launch just before it touched: the decode reads a wire and
+reference that the previous step wrote, with 3 GB of other traffic since, and
+the encode reads inputs no launch has touched for two steps.  Nothing is served
+from the 256 MB Infinity Cache.
+Inputs are resident in HBM before timing starts.  Untimed steps run for
+--warm-ms first: the GPU clock climbs over the first ~20 ms of sustained load.
 
 Prints ONE JSON line:
-  value       bf16 activation bytes processed per second (2*T*d per step), GB/s
-  roofline    the encode kernel (the dominant one): algorithmic bytes per
-              launch / its average HIP-event duration, against 8 TB/s
-  cpu_baseline the CPU oracle (single thread) on the same step
-  extras      encode-only and decode-only rates, decode-phase µs per call at
-              batch 1/16/64/256 (GLM-4-9B-shaped, 4096 hidden), and the same
-              4096 x 4096 inputs coded with k_g outliers per quantization
-              group instead of per token (and with none, for comparison)
+  value        bf16 activation bytes processed per second (2*T*d per step), GB/s
+  roofline     the encode kernel (the dominant one): algorithmic bytes per
+               launch / its average duration from HIP events around each encode
+               of the timed steps, against 8 TB/s; traffic from the committed
+               rocprofv3 counter runs (null once the kernel source changed)
+  cpu_baseline the CPU oracle, one thread pinned to one core, on a row sample
+               of the same workload
+  extras       encode-only and decode-only rates of the headline workload; the
+               prefill uplink (4096 x 4096, k = 8), the long context
+               (32768 x 4096 at groups 64/128 and 2/3/4/8 bits, k = 16) and the
+               tiny case, each with its fraction of 8 TB/s; decode-phase
+               microseconds per call at batch 1/16/64/256; the per-group
+               outlier modes, gathered reference, span selection and pooled fit
+               on the uplink inputs.
+
+--profile WORKLOAD runs only that workload's launches (back-to-back encodes,
+then back-to-back decodes, over rotating buffers) and prints their event
+timings: the command the rocprofv3 kernel traces and counter runs under
+profiles/ were taken with.
 """
 from __future__ import annotations
 
@@ -34,7 +49,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "rac_encode_prefill_uplink_4096x4096_traffic.json")
+PROFILES = os.path.join(ROOT, "profiles")
+# calibrated HBM traffic per launch of the headline encode, from rocprofv3
+# FETCH_SIZE / WRITE_SIZE runs (see paper_2608_04991_amd/rocprof_summary.py)
+TRAFFIC_FILE = os.path.join(PROFILES, "rac_encode_prefill_downlink_65536x3584_traffic.json")
+HEADLINE_KERNEL = "rac_encode_rows_kernel<4, 4, 4, 4, 2, false>"
 
 
 def log(msg):
@@ -50,20 +69,121 @@ def algorithmic_bytes(T, d, wire_bytes, xhat_bytes_per_elem=4, encode=True):
     return wire_bytes + elems * 2 + elems * xhat_bytes_per_elem
 
 
+def frac(nbytes, us):
+    return round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
+
+
+class Codec:
+    """Buffer sets of one configuration and its encode / decode calls."""
+
+    def __init__(self, torch, rac, cfg, x, ref, nsets, stream):
+        self.torch, self.rac, self.cfg, self.stream = torch, rac, cfg, stream
+        T, d = cfg.tokens, cfg.hidden
+        self.wbytes = rac.rac_wire_size(cfg)
+        self.sets = [dict(x=x if i == 0 else x.clone(), ref=ref if i == 0 else ref.clone(),
+                          wire=torch.empty(self.wbytes, dtype=torch.uint8, device="cuda"),
+                          xhat=torch.empty(T, d, dtype=torch.float32, device="cuda"),
+                          xdec=torch.empty(T, d, dtype=torch.float32, device="cuda"))
+                     for i in range(nsets)]
+        self.n = nsets
+
+    def enc(self, i):
+        s = self.sets[i % self.n]
+        self.rac.rac_encode(self.cfg, s["x"], s["ref"], None, s["wire"], s["xhat"], stream=self.stream)
+
+    def dec(self, i):
+        s = self.sets[i % self.n]
+        self.rac.rac_decode(self.cfg, s["wire"], s["ref"], None, s["xdec"], stream=self.stream)
+
+    def alg(self, encode=True):
+        return algorithmic_bytes(self.cfg.tokens, self.cfg.hidden, self.wbytes, encode=encode)
+
+    def warm(self, ms=60.0):
+        """Untimed encode + decode pairs for at least `ms` (and every set
+        encoded twice): the GPU clock drops while the host generates data."""
+        t0, i = time.perf_counter(), 0
+        while (time.perf_counter() - t0) * 1e3 < ms or i < 2 * self.n:
+            self.enc(i)
+            self.dec(i)
+            i += 1
+            if i % 4 == 0:
+                self.torch.cuda.synchronize()
+        self.torch.cuda.synchronize()
+
+    def back_to_back(self, iters):
+        """Average µs of `iters` back-to-back encodes, then of as many
+        decodes, rotating over the sets (HIP events on the launch stream)."""
+        torch = self.torch
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        torch.cuda.synchronize()
+        ev[0].record(self.stream)
+        for i in range(iters):
+            self.enc(i)
+        ev[1].record(self.stream)
+        for i in range(iters):
+            self.dec(i)
+        ev[2].record(self.stream)
+        torch.cuda.synchronize()
+        s0 = self.sets[(iters - 1) % self.n]
+        assert torch.equal(s0["xhat"], s0["xdec"]), "sender and receiver reconstructions differ"
+        return [ev[j].elapsed_time(ev[j + 1]) / iters * 1e3 for j in range(2)]
+
+    def round_trip(self, iters):
+        """Average µs of an encode followed by the decode of the same set."""
+        torch = self.torch
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        ev[0].record(self.stream)
+        for i in range(iters):
+            self.enc(i)
+            self.dec(i)
+        ev[1].record(self.stream)
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / iters * 1e3
+
+    def free(self):
+        del self.sets
+        self.torch.cuda.empty_cache()
+
+
+def to_dev(torch, a):
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda()
+
+
+def downlink_workload(torch, rac, wl, stream):
+    """Prefill downlink inputs on the device: the reference is the bf16 sender
+    reconstruction of a synthetic uplink (made by the GPU encode, which the
+    GPU tests check bit for bit against the oracle on sampled rows); x is
+    drawn from it on the host.  Returns (cfg, x_dev, ref_dev, x_bits, ref_bits)."""
+    T, d = 65536, 3584
+    cfg = rac.RacConfig(T, d, 128, 128, 4, 4)
+    log("[bench] generating the prefill-downlink workload (uplink state)")
+    xu, ru, _ = wl.prefill_downlink_uplink(0)
+    xh = torch.empty(T, d, dtype=torch.float32, device="cuda")
+    w = torch.empty(rac.rac_wire_size(cfg), dtype=torch.uint8, device="cuda")
+    rac.rac_encode(cfg, to_dev(torch, xu), to_dev(torch, ru), None, w, xh, stream=stream)
+    torch.cuda.synchronize()
+    ref = wl.f32_to_bf16_bits(xh.cpu().numpy())
+    del xh, w, xu, ru
+    torch.cuda.empty_cache()
+    log("[bench] generating the prefill-downlink workload (downlink state)")
+    xd = wl.prefill_downlink(ref, 0)
+    return cfg, to_dev(torch, xd), to_dev(torch, ref), xd, ref
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--warm-ms", type=float, default=50.0,
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=4)
+    ap.add_argument("--warm-ms", type=float, default=60.0,
                     help="after the warmup steps, keep running untimed steps for this long: the GPU clock "
                          "climbs for the first ~20 ms of sustained load")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true")
-    ap.add_argument("--all-configs", action="store_true",
-                    help="also time every other workload at full size (tiny 64 x 512; prefill downlink "
-                         "65536 x 3584; long context 32768 x 4096 at groups 64 and 128 and 2/3/4/8 bits) "
-                         "into extras.all_configs; adds about a minute")
+    ap.add_argument("--profile", choices=["downlink", "uplink", "long_context", "decode_step", "tiny"],
+                    help="run only this workload's back-to-back encodes and decodes and print their timings")
+    ap.add_argument("--iters", type=int, default=20, help="back-to-back launches per kernel in --profile runs")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run plain device copies of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
@@ -90,85 +210,62 @@ def main():
         log(f"[bench] copied {n} bytes 5 times")
         return
     rac.library()
-    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda()
-
-    T, d, g, b, k = 4096, 4096, 128, 4, 8
-    cfg = rac.RacConfig(T, d, g, g, b, k)
-    wbytes = rac.rac_wire_size(cfg)
-    log("[bench] generating the prefill-uplink workload")
-    xb, rb, _ = wl.prefill_uplink(0)
-    x0, r0 = dev(xb), dev(rb)
-    set_bytes = 2 * T * d * 2 + 2 * T * d * 4 + wbytes
-    nsets = max(2, int(np.ceil(1.2e9 / set_bytes)))
-    sets = []
-    for i in range(nsets):
-        sets.append(dict(x=x0.clone(), ref=r0.clone(),
-                         wire=torch.empty(wbytes, dtype=torch.uint8, device="cuda"),
-                         xhat=torch.empty(T, d, dtype=torch.float32, device="cuda"),
-                         xdec=torch.empty(T, d, dtype=torch.float32, device="cuda")))
     stream = torch.cuda.current_stream()
+    if args.profile:
+        print(json.dumps(profile_run(torch, rac, wl, stream, args.profile, args.iters)), flush=True)
+        return
 
-    def encode(i):
-        s = sets[i % nsets]
-        rac.rac_encode(cfg, s["x"], s["ref"], None, s["wire"], s["xhat"], stream=stream)
+    cfg, x0, r0, xd_bits, ref_bits = downlink_workload(torch, rac, wl, stream)
+    T, d = cfg.tokens, cfg.hidden
+    C = Codec(torch, rac, cfg, x0, r0, 3, stream)
 
-    def decode(i):
-        s = sets[i % nsets]
-        rac.rac_decode(cfg, s["wire"], s["ref"], None, s["xdec"], stream=stream)
+    # one step: encode batch i into set i % 3, decode the batch of step i - 1.
+    # With three sets no launch reads what the launch before it touched: the
+    # decode of set i - 1 follows the encode of set i, and the next encode
+    # (set i + 1) follows the decode of set i - 1.
+    def step(i):
+        C.enc(i)
+        C.dec(i - 1)
 
-    log(f"[bench] warmup {args.warmup} steps, then {args.warm_ms:g} ms ({nsets} rotating buffer sets)")
-    for i in range(args.warmup):
-        encode(i)
-        decode(i)
+    log(f"[bench] warmup {args.warmup} steps, then {args.warm_ms:g} ms")
+    C.enc(-1)  # the first step decodes the other set
+    for i in range(max(args.warmup, 2)):
+        step(i)
     torch.cuda.synchronize()
     t_warm, i = time.perf_counter(), 0
     while (time.perf_counter() - t_warm) * 1e3 < args.warm_ms:
-        for _ in range(10):
-            encode(i)
-            decode(i)
+        for _ in range(4):
+            step(i)
             i += 1
         torch.cuda.synchronize()
-    # The timed steps: encode + decode per step, back to back on one stream.
+    # The timed steps, back to back on one stream; HIP events on that stream
+    # bracket every encode, which gives the dominant kernel's launch time.
     log(f"[bench] timing {args.steps} steps")
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+    ea = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    eb = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    ev[0].record(stream)
+    e0.record(stream)
     for i in range(args.steps):
-        encode(i)
-        decode(i)
-    ev[1].record(stream)
+        ea[i].record(stream)
+        C.enc(i)
+        eb[i].record(stream)
+        C.dec(i - 1)
+    e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / args.steps
-    gpu_ms_per_step = ev[0].elapsed_time(ev[1]) / args.steps
-    # Per-launch durations of each kernel on the same stream, as in the timed
-    # steps (back to back, rotating buffers): the encodes of the timed steps
-    # again, then their decodes, each run bracketed by HIP events.
-    ev[2].record(stream)
-    for i in range(args.steps):
-        encode(i)
-    ev[3].record(stream)
-    for i in range(args.steps):
-        decode(i)
-    ev[4].record(stream)
-    torch.cuda.synchronize()
-    enc_ms = ev[2].elapsed_time(ev[3]) / args.steps
-    dec_ms = ev[3].elapsed_time(ev[4]) / args.steps
+    gpu_ms_per_step = e0.elapsed_time(e1) / args.steps
+    enc_us = float(np.mean([a.elapsed_time(b) for a, b in zip(ea, eb)])) * 1e3
     act_bytes = T * d * 2
     value = act_bytes / (ms_per_step * 1e-3) / 1e9
+    # sender and receiver agree on the last batch decoded in the timed steps
+    s = C.sets[(args.steps - 2) % 3]
+    assert torch.equal(s["xhat"], s["xdec"]), "sender and receiver reconstructions differ"
 
-    # parity spot check of the timed configuration (first rows) vs the sender
-    s0 = sets[0]
-    assert torch.equal(s0["xhat"], s0["xdec"]), "sender and receiver reconstructions differ"
-
-    enc_alg = algorithmic_bytes(T, d, wbytes)
-    dec_alg = algorithmic_bytes(T, d, wbytes, encode=False)
-    enc_avg_s = enc_ms * 1e-3
-    dec_avg_s = dec_ms * 1e-3
-    achieved = enc_alg / enc_avg_s / 1e9
-    # HBM bytes per launch from the committed rocprofv3 counter runs, valid
-    # only for the kernel source they were taken on
+    enc_alg = C.alg()
+    achieved = enc_alg / (enc_us * 1e-6) / 1e9
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
         t = json.load(open(TRAFFIC_FILE))
@@ -187,52 +284,121 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": "prefill uplink, Llama-3-8B-shaped: x,ref bf16 4096 tokens x 4096 hidden, "
-                               "group 128, 4-bit, top-8 outliers/token; step = rac_encode (fused sender "
-                               "reconstruction, fp32) + rac_decode",
-                   "tokens": T, "hidden": d, "group": g, "bits": b, "outlier_k": k,
-                   "wire_bytes": wbytes, "rotating_buffer_sets": nsets},
-        "roofline": {"kernel": "rac_encode_rows_kernel<4,4,4,4,2,false>", "bound": "hbm",
+        "config": {"workload": "prefill downlink reuse, Qwen2-7B-shaped: x,ref bf16 8 x 8192 = 65536 tokens x "
+                               "3584 hidden, group 128, 4-bit, top-4 outliers/token, ref = bf16 sender "
+                               "reconstruction of a synthetic uplink; step = rac_encode of one batch (fused fp32 "
+                               "sender reconstruction) + rac_decode of the previous step's batch",
+                   "tokens": T, "hidden": d, "group": 128, "bits": 4, "outlier_k": 4,
+                   "wire_bytes": C.wbytes, "buffer_sets": 3},
+        "roofline": {"kernel": HEADLINE_KERNEL, "bound": "hbm",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "algorithmic_bytes_per_launch": enc_alg,
-                     "avg_launch_us": round(enc_avg_s * 1e6, 3)},
+                     "avg_launch_us": round(enc_us, 3)},
     }
-    extras = {
-        "encode_recon_GBps_activation": round(act_bytes / enc_avg_s / 1e9, 1),
-        "encode_us": round(enc_avg_s * 1e6, 2),
-        "decode_us": round(dec_avg_s * 1e6, 2),
-        "decode_GBps_activation": round(act_bytes / dec_avg_s / 1e9, 1),
-        "decode_hbm_frac": round(dec_alg / dec_avg_s / 1e9 / HBM_PEAK_GBPS, 4),
-        "gpu_ms_per_step": round(gpu_ms_per_step, 5),
-    }
+    log(f"[bench] step {ms_per_step * 1e3:.1f} us, encode {enc_us:.1f} us ({achieved / HBM_PEAK_GBPS:.4f})")
+    extras = {"gpu_ms_per_step": round(gpu_ms_per_step, 5), "decode_kernel": "rac_decode_kernel<4, 1, false>"}
     if not args.no_extras:
-        extras["decode_step"] = decode_step_latency(torch, rac, wl, dev, stream)
-        # graph-replayed encode + decode pair, µs, across the bit widths and
-        # with one scale per token row (quantization group = hidden)
-        extras["decode_step_graph_pair_us"] = {
-            f"b{bits}_gq{gq}": decode_step_latency(torch, rac, wl, dev, stream, bits, gq, detail=False)
-            for bits, gq in ((2, 128), (8, 128), (4, 4096))}
-        extras["outlier_modes_4096x4096_g128_b4"] = outlier_mode_rates(
-            torch, rac, sets, nsets, stream, args.steps)
-        extras["gathered_reference"] = gather_rates(torch, rac, cfg, rb, sets, nsets, stream, args.steps)
-        extras["span_selection"] = span_selection_cost(rac, T)
-        extras["pooled_fit"] = pooled_rates(torch, rac, cfg, sets, nsets, stream, args.steps)
-    if args.all_configs:
-        del sets
-        torch.cuda.empty_cache()
-        extras["all_configs"] = all_config_rates(torch, rac, wl, dev, stream)
+        # (after the timed steps, so that without extras the last launches of
+        # the encode kernel in a kernel trace are those of the timed steps)
+        e_us, d_us = C.back_to_back(args.steps)
+        extras.update({"encode_us_back_to_back": round(e_us, 2),
+                       "encode_hbm_frac_back_to_back": frac(enc_alg, e_us),
+                       "decode_us_back_to_back": round(d_us, 2),
+                       "decode_hbm_frac_back_to_back": frac(C.alg(False), d_us)})
+    C.free()
+    del C, x0, r0
+    torch.cuda.empty_cache()
+    if not args.no_extras:
+        extras.update(all_extras(torch, rac, wl, stream))
     out["extras"] = extras
-
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(xb, rb, cfg)
+        out["cpu_baseline"] = cpu_baseline(xd_bits, ref_bits, cfg)
     print(json.dumps(out), flush=True)
 
 
-def outlier_mode_rates(torch, rac, sets, nsets, stream, steps):
+def prefill_uplink(torch, rac, wl, stream):
+    """The 4096 x 4096 uplink on rotating buffer sets (> 1.2 GB in total)."""
+    T, d = 4096, 4096
+    cfg = rac.RacConfig(T, d, 128, 128, 4, 8)
+    xb, rb, _ = wl.prefill_uplink(0)
+    set_bytes = 2 * T * d * 2 + 2 * T * d * 4 + rac.rac_wire_size(cfg)
+    nsets = max(2, int(np.ceil(1.2e9 / set_bytes)))
+    return Codec(torch, rac, cfg, to_dev(torch, xb), to_dev(torch, rb), nsets, stream), rb
+
+
+def all_extras(torch, rac, wl, stream):
+    ex = {}
+    log("[bench] prefill uplink 4096 x 4096")
+    U, rb = prefill_uplink(torch, rac, wl, stream)
+    U.warm()
+    e, dcd = U.back_to_back(50)
+    ex["prefill_uplink_4096x4096_g128_b4_k8"] = {
+        "encode_us": round(e, 2), "encode_hbm_frac": frac(U.alg(), e),
+        "decode_us": round(dcd, 2), "decode_hbm_frac": frac(U.alg(False), dcd),
+        "wire_over_bf16": round(U.wbytes / (4096 * 4096 * 2), 4),
+        "encode_kernel": "rac_encode_rows_kernel<4, 4, 4, 4, 2, false>"}
+    log(f"[bench] uplink: {ex['prefill_uplink_4096x4096_g128_b4_k8']}")
+    ex["outlier_modes_4096x4096_g128_b4"] = outlier_mode_rates(torch, rac, U, 50)
+    ex["gathered_reference"] = gather_rates(torch, rac, U, 50)
+    ex["pooled_fit"] = pooled_rates(torch, rac, U, 50)
+    ex["span_selection"] = span_selection_cost(rac, 4096)
+    U.free()
+    del U
+    ex["long_context_32768x4096_k16"] = long_context_rates(torch, rac, wl, stream)
+    ex["tiny_64x512_g64_b4"] = tiny_rates(torch, rac, wl, stream)
+    ex["decode_step"] = decode_step_latency(torch, rac, wl, stream)
+    # graph-replayed encode + decode pair, µs, across the bit widths and with
+    # one scale per token row (quantization group = hidden)
+    ex["decode_step_graph_pair_us"] = {
+        f"b{bits}_gq{gq}": decode_step_latency(torch, rac, wl, stream, bits, gq, detail=False)
+        for bits, gq in ((2, 128), (8, 128), (4, 4096))}
+    return ex
+
+
+def long_context_rates(torch, rac, wl, stream, iters=20):
+    """32768 x 4096 at groups 64 and 128 and 2/3/4/8 bits, k = 16, each on
+    its own data: encode, decode (back to back over two sets, each far above
+    the last-level cache) and the encode + decode round trip on one stream."""
+    out = {}
+    T, d = 32768, 4096
+    for g in (64, 128):
+        log(f"[bench] generating the long-context workload, group {g}")
+        xb, rb, _ = wl.long_context(0, group=g)
+        x, r = to_dev(torch, xb), to_dev(torch, rb)
+        for bits in (2, 3, 4, 8):
+            cfg = rac.RacConfig(T, d, g, g, bits, 16)
+            C = Codec(torch, rac, cfg, x, r, 2, stream)
+            C.warm()
+            e, dcd = C.back_to_back(iters)
+            rt = C.round_trip(iters)
+            res = {"encode_us": round(e, 2), "encode_hbm_frac": frac(C.alg(), e),
+                   "decode_us": round(dcd, 2), "decode_hbm_frac": frac(C.alg(False), dcd),
+                   "round_trip_us": round(rt, 2), "activation_GBps_round_trip": round(T * d * 2 / rt / 1e3, 1),
+                   "wire_over_bf16": round(C.wbytes / (T * d * 2), 4)}
+            out[f"g{g}_b{bits}"] = res
+            log(f"[bench] long context g{g} b{bits}: {res}")
+            C.free()
+            del C
+        del x, r
+        torch.cuda.empty_cache()
+    return out
+
+
+def tiny_rates(torch, rac, wl, stream, iters=200):
+    """64 x 512, group 64, 4-bit: launch-bound, µs per call only (64 sets)."""
+    xb, rb, _ = wl.tiny(0)
+    C = Codec(torch, rac, rac.RacConfig(64, 512, 64, 64, 4, 0), to_dev(torch, xb), to_dev(torch, rb), 64, stream)
+    C.warm()
+    e, dcd = C.back_to_back(iters)
+    C.free()
+    return {"encode_us": round(e, 2), "decode_us": round(dcd, 2)}
+
+
+def outlier_mode_rates(torch, rac, U, steps):
     """Average launch time (HIP events around `steps` back-to-back launches
     over the rotating buffer sets) of rac_encode and of rac_decode on the
-    benchmark inputs with other outlier settings: k_g = 1, 2, 4 outliers per
+    uplink inputs with other outlier settings: k_g = 1, 2, 4 outliers per
     quantization group (u8 offsets), and none.  Each entry gives µs, the
     fraction of 8 TB/s by algorithmic bytes, and the wire size relative to
     the bf16 tensor."""
@@ -241,6 +407,7 @@ def outlier_mode_rates(torch, rac, sets, nsets, stream, steps):
                 "per_group_kg2": (2, rac.RAC_FLAG_GROUP_OUTLIERS),
                 "per_group_kg4": (4, rac.RAC_FLAG_GROUP_OUTLIERS)}
     T, d = 4096, 4096
+    sets, nsets, stream = U.sets, U.n, U.stream
     for name, (k, flags) in variants.items():
         cfg = rac.RacConfig(T, d, 128, 128, 4, k, flags)
         wb = rac.rac_wire_size(cfg)
@@ -271,119 +438,21 @@ def outlier_mode_rates(torch, rac, sets, nsets, stream, steps):
         e_us = ev[0].elapsed_time(ev[1]) / steps * 1e3
         d_us = ev[1].elapsed_time(ev[2]) / steps * 1e3
         res[name] = {"encode_us": round(e_us, 2),
-                     "encode_hbm_frac": round(algorithmic_bytes(T, d, wb) / e_us / 1e3 / HBM_PEAK_GBPS, 4),
+                     "encode_hbm_frac": frac(algorithmic_bytes(T, d, wb), e_us),
                      "decode_us": round(d_us, 2),
-                     "decode_hbm_frac": round(algorithmic_bytes(T, d, wb, encode=False) / d_us / 1e3
-                                              / HBM_PEAK_GBPS, 4),
+                     "decode_hbm_frac": frac(algorithmic_bytes(T, d, wb, encode=False), d_us),
                      "wire_over_bf16": round(wb / (T * d * 2), 4)}
         del wires
     return res
 
 
-def time_pair(torch, rac, cfg, sets, stream, iters=20):
-    """Average µs of rac_encode (fused fp32 reconstruction), of rac_decode,
-    and of encode + decode on one stream, each over `iters` back-to-back
-    launches rotating over `sets` (inputs and outputs per set), after at
-    least 60 ms of untimed launches."""
-    n = len(sets)
-
-    def enc(i):
-        s = sets[i % n]
-        rac.rac_encode(cfg, s["x"], s["ref"], None, s["wire"], s["xhat"], stream=stream)
-
-    def dec(i):
-        s = sets[i % n]
-        rac.rac_decode(cfg, s["wire"], s["ref"], None, s["xdec"], stream=stream)
-
-    # untimed launches for at least 60 ms first: the data of each workload is
-    # generated on the host while the GPU idles, and its clock drops meanwhile
-    t0, i = time.perf_counter(), 0
-    while (time.perf_counter() - t0) < 0.06 or i < 2 * n:
-        enc(i)
-        dec(i)
-        i += 1
-        if i % 4 == 0:
-            torch.cuda.synchronize()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
-    torch.cuda.synchronize()
-    ev[0].record(stream)
-    for i in range(iters):
-        enc(i)
-    ev[1].record(stream)
-    for i in range(iters):
-        dec(i)
-    ev[2].record(stream)
-    for i in range(iters):
-        enc(i)
-        dec(i)
-    ev[3].record(stream)
-    torch.cuda.synchronize()
-    assert torch.equal(sets[0]["xhat"], sets[0]["xdec"])
-    return [ev[j].elapsed_time(ev[j + 1]) / iters * 1e3 for j in range(3)]
-
-
-def all_config_rates(torch, rac, wl, dev, stream):
-    """Every other workload at its full size, on its own synthetic data: µs
-    per call of encode, decode and the encode + decode round trip on one
-    stream, with the fraction of 8 TB/s by algorithmic bytes (the tiny case
-    is launch-bound and reports µs only).  Two buffer sets rotate (each set of
-    the large shapes is far above the 256 MB last-level cache; the tiny case
-    uses 64)."""
-    out = {}
-
-    def run(name, cfg, xb, rb, nsets, report_frac=True):
-        T, d = cfg.tokens, cfg.hidden
-        wb = rac.rac_wire_size(cfg)
-        x, r = dev(xb), dev(rb)
-        sets = [dict(x=x if i == 0 else x.clone(), ref=r if i == 0 else r.clone(),
-                     wire=torch.empty(wb, dtype=torch.uint8, device="cuda"),
-                     xhat=torch.empty(T, d, dtype=torch.float32, device="cuda"),
-                     xdec=torch.empty(T, d, dtype=torch.float32, device="cuda")) for i in range(nsets)]
-        e, dcd, rt = time_pair(torch, rac, cfg, sets, stream)
-        res = {"encode_us": round(e, 2), "decode_us": round(dcd, 2), "round_trip_us": round(rt, 2),
-               "wire_over_bf16": round(wb / (T * d * 2), 4)}
-        if report_frac:
-            res["encode_hbm_frac"] = round(algorithmic_bytes(T, d, wb) / e / 1e3 / HBM_PEAK_GBPS, 4)
-            res["decode_hbm_frac"] = round(algorithmic_bytes(T, d, wb, encode=False) / dcd / 1e3 / HBM_PEAK_GBPS, 4)
-            res["activation_GBps_round_trip"] = round(T * d * 2 / rt / 1e3, 1)
-        out[name] = res
-        log(f"[bench] {name}: {res}")
-        del sets
-        torch.cuda.empty_cache()
-
-    xb, rb, _ = wl.tiny(0)
-    run("tiny_64x512_g64_b4", rac.RacConfig(64, 512, 64, 64, 4, 0), xb, rb, 64, report_frac=False)
-    # prefill downlink: the reference is the sender reconstruction (bf16) of a
-    # synthetic uplink, made here by the GPU encode (bit-identical to the
-    # oracle's, which the GPU tests check on sampled rows)
-    T, d = 65536, 3584
-    cfg = rac.RacConfig(T, d, 128, 128, 4, 4)
-    log("[bench] generating the prefill-downlink workload")
-    xu, ru, _ = wl.prefill_downlink_uplink(0)
-    xh = torch.empty(T, d, dtype=torch.float32, device="cuda")
-    w = torch.empty(rac.rac_wire_size(cfg), dtype=torch.uint8, device="cuda")
-    rac.rac_encode(cfg, dev(xu), dev(ru), None, w, xh, stream=stream)
-    torch.cuda.synchronize()
-    ref = wl.f32_to_bf16_bits(xh.cpu().numpy())
-    del xh, w, xu, ru
-    torch.cuda.empty_cache()
-    xd = wl.prefill_downlink(ref, 0)
-    run("prefill_downlink_65536x3584_g128_b4_k4", cfg, xd, ref, 2)
-    del xd, ref
-    for g in (64, 128):
-        log(f"[bench] generating the long-context workload, group {g}")
-        xb, rb, _ = wl.long_context(0, group=g)
-        for bits in (2, 3, 4, 8):
-            run(f"long_context_32768x4096_g{g}_b{bits}_k16", rac.RacConfig(32768, 4096, g, g, bits, 16), xb, rb, 2)
-    return out
-
-
-def pooled_rates(torch, rac, cfg, sets, nsets, stream, steps):
-    """rac_encode_pooled on the benchmark inputs, with segments standing for
+def pooled_rates(torch, rac, U, steps):
+    """rac_encode_pooled on the uplink inputs, with segments standing for
     retrieved spans (random lengths of 1 to 600 rows): average time of the
     whole call (its three launches) over `steps` back-to-back calls, and the
-    fraction of 8 TB/s by the per-token encode's algorithmic bytes (the
-    pooled call also reads x and ref a second time for the moments)."""
+    fraction of 8 TB/s by the per-token encode's algorithmic bytes and by the
+    pooled call's own (the moments pass reads x and ref a second time)."""
+    cfg, sets, nsets, stream = U.cfg, U.sets, U.n, U.stream
     T, d = cfg.tokens, cfg.hidden
     rng = np.random.default_rng(12)
     cuts = np.unique(np.concatenate([[0, T], np.cumsum(rng.integers(1, 600, 40))]))
@@ -406,8 +475,10 @@ def pooled_rates(torch, rac, cfg, sets, nsets, stream, steps):
     torch.cuda.synchronize()
     us = ev[0].elapsed_time(ev[1]) / steps * 1e3
     del wires
+    own = algorithmic_bytes(T, d, wb) + T * d * 4
     return {"segments": int(seg.numel()) - 1, "encode_us": round(us, 2),
-            "hbm_frac_by_encode_bytes": round(algorithmic_bytes(T, d, wb) / us / 1e3 / HBM_PEAK_GBPS, 4)}
+            "hbm_frac_by_encode_bytes": frac(algorithmic_bytes(T, d, wb), us),
+            "hbm_frac_by_own_bytes": frac(own, us)}
 
 
 def span_selection_cost(rac, T, window=16, n_hist=7):
@@ -446,12 +517,12 @@ def span_selection_cost(rac, T, window=16, n_hist=7):
             "covered_fraction": round(cov / T, 4)}
 
 
-def gather_rates(torch, rac, cfg, rb, sets, nsets, stream, steps):
-    """rac_encode_gather / rac_decode_gather on the benchmark configuration:
+def gather_rates(torch, rac, U, steps):
+    """rac_encode_gather / rac_decode_gather on the uplink configuration:
     each row's reference sits at a random row of an 8192-row bf16 store of
     earlier rows (one store per buffer set), a fifth of the rows name no row
-    (zero reference).  Average launch time over `steps` back-to-back launches,
-    next to the same calls with the reference materialized."""
+    (zero reference).  Average launch time over `steps` back-to-back launches."""
+    cfg, sets, nsets, stream = U.cfg, U.sets, U.n, U.stream
     T, d = cfg.tokens, cfg.hidden
     rng = np.random.default_rng(11)
     pos = rng.permutation(2 * T)[:T].astype(np.int32)
@@ -494,17 +565,19 @@ def gather_rates(torch, rac, cfg, rb, sets, nsets, stream, steps):
             "decode_us": round(ev[1].elapsed_time(ev[2]) / steps * 1e3, 2)}
 
 
-def decode_step_latency(torch, rac, wl, dev, stream, bits=4, gq=128, detail=True):
+def decode_step_latency(torch, rac, wl, stream, bits=4, gq=128, detail=True):
     """µs per call of rac_encode and rac_decode for decode-phase batches
     (1 token per sequence, 4096 hidden, alignment group 128, quantization
     group gq, no outliers): wall time per call with back-to-back launches,
-    kernel time from HIP events (with detail), and the time per encode +
-    decode pair when 20 pairs are captured in one HIP graph and replayed."""
+    per-call HIP-event time (with detail; events add their own dispatch
+    overhead, the rocprofv3 kernel trace under profiles/ gives kernel-only
+    time per batch), and the time per encode + decode pair when 20 pairs are
+    captured in one HIP graph and replayed."""
     res = {}
     for B in (1, 16, 64, 256):
         cfg = rac.RacConfig(B, 4096, 128, gq, bits, 0)
         xb, rb = wl.decode_step(B)
-        x, ref = dev(xb), dev(rb)
+        x, ref = to_dev(torch, xb), to_dev(torch, rb)
         wire = torch.empty(rac.rac_wire_size(cfg), dtype=torch.uint8, device="cuda")
         xh = torch.empty(B, 4096, dtype=torch.float32, device="cuda")
         xd = torch.empty_like(xh)
@@ -558,28 +631,78 @@ def decode_step_latency(torch, rac, wl, dev, stream, bits=4, gq=128, detail=True
     return res
 
 
-def cpu_baseline(xb, rb, cfg):
-    """The CPU oracle, single-threaded, on the same step (all rows: encode
-    with sender reconstruction, then decode), repeated until at least 10 s of
-    CPU time have been spent (at most 30 s)."""
+def profile_run(torch, rac, wl, stream, workload, iters):
+    """One workload alone, for rocprofv3: warm, then `iters` back-to-back
+    encodes and `iters` back-to-back decodes over rotating buffer sets, per
+    configuration of the workload.  Returns the event timings."""
+    out = {"profile": workload, "iters": iters}
+    if workload == "downlink":
+        cfg, x, r, _, _ = downlink_workload(torch, rac, wl, stream)
+        C = Codec(torch, rac, cfg, x, r, 3, stream)
+        C.warm()
+        e, dcd = C.back_to_back(iters)
+        out["downlink_65536x3584_g128_b4_k4"] = {"encode_us": round(e, 2), "encode_hbm_frac": frac(C.alg(), e),
+                                                 "decode_us": round(dcd, 2),
+                                                 "decode_hbm_frac": frac(C.alg(False), dcd),
+                                                 "encode_alg_bytes": C.alg(), "decode_alg_bytes": C.alg(False)}
+    elif workload == "uplink":
+        U, _ = prefill_uplink(torch, rac, wl, stream)
+        U.warm()
+        e, dcd = U.back_to_back(iters)
+        out["uplink_4096x4096_g128_b4_k8"] = {"encode_us": round(e, 2), "encode_hbm_frac": frac(U.alg(), e),
+                                              "decode_us": round(dcd, 2), "decode_hbm_frac": frac(U.alg(False), dcd),
+                                              "encode_alg_bytes": U.alg(), "decode_alg_bytes": U.alg(False)}
+    elif workload == "long_context":
+        out.update(long_context_rates(torch, rac, wl, stream, iters))
+    elif workload == "tiny":
+        out.update(tiny_rates(torch, rac, wl, stream, iters))
+    else:
+        for bits, gq in ((2, 128), (4, 128), (8, 128), (4, 4096)):
+            out[f"b{bits}_gq{gq}"] = decode_step_latency(torch, rac, wl, stream, bits, gq, detail=True)
+    log(f"[bench] profile {workload} done")
+    return out
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(xb, rb, cfg, rows=1024, min_s=10.0, max_s=30.0):
+    """The CPU oracle on a sample of the headline workload: its first `rows`
+    token rows (encode with sender reconstruction, then decode), repeated
+    until at least `min_s` seconds have passed, on one thread pinned to one
+    core (the calling thread's affinity is restored afterwards)."""
     import oracle
-    c = dict(tokens=cfg.tokens, hidden=cfg.hidden, group_align=cfg.group_align,
+    c = dict(tokens=rows, hidden=cfg.hidden, group_align=cfg.group_align,
              group_quant=cfg.group_quant, bits=cfg.bits, outlier_k=cfg.outlier_k, flags=cfg.flags)
-    log("[bench] CPU oracle baseline (full steps, single thread)")
-    reps, dt = 0, 0.0
-    while dt < 10.0 and reps < 30:
-        t0 = time.perf_counter()
-        rc, wire, _ = oracle.encode(xb, rb, **c)
-        rc2, _ = oracle.decode(wire, rb, **c)
-        dt += time.perf_counter() - t0
-        reps += 1
-        assert rc == 0 and rc2 == 0
-        log(f"[bench] oracle step {reps}: {dt:.1f} s so far")
-    return {"value": round(reps * cfg.tokens * cfg.hidden * 2 / dt / 1e9, 5), "unit": "GB/s", "cores": 1,
+    xs, rs = np.ascontiguousarray(xb[:rows]), np.ascontiguousarray(rb[:rows])
+    allowed = os.sched_getaffinity(0)
+    core = max(allowed)
+    os.sched_setaffinity(0, {core})
+    log(f"[bench] CPU oracle baseline on core {core} ({rows} rows per pass)")
+    try:
+        reps, dt = 0, 0.0
+        while dt < min_s and dt < max_s:
+            t0 = time.perf_counter()
+            rc, wire, _ = oracle.encode(xs, rs, **c)
+            rc2, _ = oracle.decode(wire, rs, **c)
+            dt += time.perf_counter() - t0
+            reps += 1
+            assert rc == 0 and rc2 == 0
+    finally:
+        os.sched_setaffinity(0, allowed)
+    return {"value": round(reps * rows * cfg.hidden * 2 / dt / 1e9, 5), "unit": "GB/s", "cores": 1,
             "kind": "oracle",
-            "sample": f"{reps} full steps of the benchmark workload ({cfg.tokens}x{cfg.hidden} encode with "
-                      f"sender reconstruction + decode), {dt:.1f} s, single thread on a host with "
-                      f"{os.cpu_count()} visible cores"}
+            "sample": f"{reps} passes over the first {rows} token rows of the headline workload "
+                      f"({rows}x{cfg.hidden}: encode with sender reconstruction + decode), {dt:.1f} s, "
+                      f"one thread pinned to core {core} of {len(allowed)} allowed ({os.cpu_count()} visible)",
+            "cpu_model": cpu_model()}
 
 
 if __name__ == "__main__":

@@ -15,6 +15,7 @@ There is no fallback: if librac.so is missing the calls raise.
 from __future__ import annotations
 
 import ctypes
+import functools
 import os
 from dataclasses import dataclass
 
@@ -69,8 +70,15 @@ class RacConfig:
     flags: int = 0
 
     def _c(self) -> _Config:
-        return _Config(self.tokens, self.hidden, self.group_align, self.group_quant, self.bits,
-                       self.outlier_k, self.flags)
+        return _cfg_struct(self)
+
+
+@functools.lru_cache(maxsize=512)
+def _cfg_struct(cfg: "RacConfig") -> _Config:
+    # (the library reads the struct during the call only, so one instance per
+    # configuration can be passed to every call)
+    return _Config(cfg.tokens, cfg.hidden, cfg.group_align, cfg.group_quant, cfg.bits,
+                   cfg.outlier_k, cfg.flags)
 
 
 _lib = None
@@ -127,6 +135,33 @@ def _ptr(t):
     return t.data_ptr()
 
 
+def _dev(t, what: str, elem_bytes, count: int):
+    """Address of a device tensor argument after checking, before anything is
+    enqueued, that the kernels can read or write `count` elements of
+    `elem_bytes` bytes there: a GPU tensor,
+    contiguous, of that element size, holding at least `count` elements.
+    None and raw integer addresses pass through unchecked (the C ABI checks
+    what it can)."""
+    if t is None or isinstance(t, int):
+        return t
+    if not (getattr(t, "is_cuda", False) and t.is_contiguous()):
+        raise ValueError(f"{what}: expected a contiguous GPU tensor")
+    es = t.element_size()
+    if es != elem_bytes:
+        raise ValueError(f"{what}: expected {elem_bytes}-byte elements, got {es}")
+    if t.numel() < count:
+        raise ValueError(f"{what}: holds {t.numel()} elements, needs {count}")
+    return t.data_ptr()
+
+
+def _xhat_bytes(cfg) -> int:
+    return 2 if cfg.flags & RAC_FLAG_XHAT_BF16 else 4
+
+
+def _nsteps(cfg) -> int:
+    return cfg.hidden // cfg.group_quant if cfg.flags & RAC_FLAG_FIXED_STEP else 0
+
+
 def _nbytes(t) -> int:
     return t.numel() * t.element_size()
 
@@ -156,7 +191,12 @@ def rac_wire_layout(cfg: RacConfig) -> dict:
 
 
 def rac_wire_size(cfg: RacConfig) -> int:
-    return int(library().rac_wire_size(ctypes.byref(cfg._c())))
+    return _wire_size(cfg, library())
+
+
+@functools.lru_cache(maxsize=512)
+def _wire_size(cfg: RacConfig, lib) -> int:
+    return int(lib.rac_wire_size(ctypes.byref(cfg._c())))
 
 
 def rac_parse_header(header: bytes):
@@ -174,21 +214,27 @@ def rac_encode(cfg: RacConfig, x, ref, fixed_steps, wire, xhat=None, stream=None
                wire_cap: int | None = None) -> None:
     """Encode x against ref into wire (+ fused sender reconstruction)."""
     cap = wire_cap if wire_cap is not None else (_nbytes(wire) if not isinstance(wire, int) else 0)
-    _check(library().rac_encode(ctypes.byref(cfg._c()), _ptr(x), _ptr(ref), _ptr(fixed_steps),
-                                _ptr(wire), cap, _ptr(xhat), _stream(stream)), "rac_encode")
+    n = cfg.tokens * cfg.hidden
+    _check(library().rac_encode(ctypes.byref(cfg._c()), _dev(x, "x", 2, n), _dev(ref, "ref", 2, n),
+                                _dev(fixed_steps, "fixed_steps", 4, _nsteps(cfg)), _dev(wire, "wire", 1, 0),
+                                cap, _dev(xhat, "xhat", _xhat_bytes(cfg), n), _stream(stream)), "rac_encode")
 
 
 def rac_reconstruct(cfg: RacConfig, wire, ref, fixed_steps, xhat, stream=None) -> None:
     """Sender-side reconstruction from the sender's own wire."""
-    _check(library().rac_reconstruct(ctypes.byref(cfg._c()), _ptr(wire), _ptr(ref),
-                                     _ptr(fixed_steps), _ptr(xhat), _stream(stream)),
+    n = cfg.tokens * cfg.hidden
+    _check(library().rac_reconstruct(ctypes.byref(cfg._c()), _dev(wire, "wire", 1, rac_wire_size(cfg)),
+                                     _dev(ref, "ref", 2, n), _dev(fixed_steps, "fixed_steps", 4, _nsteps(cfg)),
+                                     _dev(xhat, "xhat", _xhat_bytes(cfg), n), _stream(stream)),
            "rac_reconstruct")
 
 
 def rac_decode(cfg: RacConfig, wire, ref, fixed_steps, xhat, stream=None) -> None:
     """Receiver-side reconstruction from a wire and the receiver's reference."""
-    _check(library().rac_decode(ctypes.byref(cfg._c()), _ptr(wire), _ptr(ref),
-                                _ptr(fixed_steps), _ptr(xhat), _stream(stream)), "rac_decode")
+    n = cfg.tokens * cfg.hidden
+    _check(library().rac_decode(ctypes.byref(cfg._c()), _dev(wire, "wire", 1, rac_wire_size(cfg)),
+                                _dev(ref, "ref", 2, n), _dev(fixed_steps, "fixed_steps", 4, _nsteps(cfg)),
+                                _dev(xhat, "xhat", _xhat_bytes(cfg), n), _stream(stream)), "rac_decode")
 
 
 def _rows(store, store_rows):
@@ -202,16 +248,24 @@ def rac_encode_gather(cfg: RacConfig, x, store, ref_rows, fixed_steps, wire, xha
     """Encode x against the store rows that ref_rows names (int32 [T]; an index
     outside the store means a zero reference row)."""
     cap = wire_cap if wire_cap is not None else (_nbytes(wire) if not isinstance(wire, int) else 0)
-    _check(library().rac_encode_gather(ctypes.byref(cfg._c()), _ptr(x), _ptr(store), _rows(store, store_rows),
-                                       _ptr(ref_rows), _ptr(fixed_steps), _ptr(wire), cap, _ptr(xhat),
-                                       _stream(stream)), "rac_encode_gather")
+    n, sr = cfg.tokens * cfg.hidden, _rows(store, store_rows)
+    _check(library().rac_encode_gather(ctypes.byref(cfg._c()), _dev(x, "x", 2, n),
+                                       _dev(store, "store", 2, sr * cfg.hidden), sr,
+                                       _dev(ref_rows, "ref_rows", 4, cfg.tokens),
+                                       _dev(fixed_steps, "fixed_steps", 4, _nsteps(cfg)), _dev(wire, "wire", 1, 0),
+                                       cap, _dev(xhat, "xhat", _xhat_bytes(cfg), n), _stream(stream)),
+           "rac_encode_gather")
 
 
 def rac_decode_gather(cfg: RacConfig, wire, store, ref_rows, fixed_steps, xhat, stream=None,
                       store_rows: int | None = None) -> None:
     """Receiver-side reconstruction with the reference gathered from a store."""
-    _check(library().rac_decode_gather(ctypes.byref(cfg._c()), _ptr(wire), _ptr(store), _rows(store, store_rows),
-                                       _ptr(ref_rows), _ptr(fixed_steps), _ptr(xhat), _stream(stream)),
+    n, sr = cfg.tokens * cfg.hidden, _rows(store, store_rows)
+    _check(library().rac_decode_gather(ctypes.byref(cfg._c()), _dev(wire, "wire", 1, rac_wire_size(cfg)),
+                                       _dev(store, "store", 2, sr * cfg.hidden), sr,
+                                       _dev(ref_rows, "ref_rows", 4, cfg.tokens),
+                                       _dev(fixed_steps, "fixed_steps", 4, _nsteps(cfg)),
+                                       _dev(xhat, "xhat", _xhat_bytes(cfg), n), _stream(stream)),
            "rac_decode_gather")
 
 
@@ -257,6 +311,9 @@ def rac_encode_pooled(cfg: RacConfig, x, ref, seg_start, fixed_steps, wire, xhat
     int32 [segments + 1] row starts)."""
     cap = wire_cap if wire_cap is not None else (_nbytes(wire) if not isinstance(wire, int) else 0)
     nseg = int(segments) if segments is not None else int(seg_start.numel()) - 1
-    _check(library().rac_encode_pooled(ctypes.byref(cfg._c()), _ptr(x), _ptr(ref), nseg, _ptr(seg_start),
-                                       _ptr(fixed_steps), _ptr(wire), cap, _ptr(xhat), _stream(stream)),
+    n = cfg.tokens * cfg.hidden
+    _check(library().rac_encode_pooled(ctypes.byref(cfg._c()), _dev(x, "x", 2, n), _dev(ref, "ref", 2, n), nseg,
+                                       _dev(seg_start, "seg_start", 4, nseg + 1),
+                                       _dev(fixed_steps, "fixed_steps", 4, _nsteps(cfg)), _dev(wire, "wire", 1, 0),
+                                       cap, _dev(xhat, "xhat", _xhat_bytes(cfg), n), _stream(stream)),
            "rac_encode_pooled")

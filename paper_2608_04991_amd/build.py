@@ -35,13 +35,20 @@ def build(verbose: bool = True) -> str:
     os.makedirs(os.path.dirname(LIB), exist_ok=True)
     tmp = LIB + ".tmp"
     cmd = [HIPCC, *FLAGS, "-I", INC, "-o", tmp, SRC, HOST_SRC]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
     asm = LIB + ".s"
     dev = [HIPCC, *[f for f in FLAGS if f not in ("-fPIC", "-shared")], "--cuda-device-only", "-S",
            "-I", INC, "-o", asm, SRC]
-    subprocess.run(dev, check=True)
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    # the library and the device assembly that is scanned are independent
+    # compiles: run them side by side
+    procs = [subprocess.Popen(cmd), subprocess.Popen(dev)]
+    codes = [p.wait() for p in procs]
+    if any(codes):
+        for f in (tmp, asm):
+            if os.path.exists(f):
+                os.remove(f)
+        raise subprocess.CalledProcessError(next(c for c in codes if c), cmd if codes[0] else dev)
     bad = isa_check.scan(open(asm).read())
     os.remove(asm)
     if bad:

@@ -28,6 +28,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "rac.h"
 
 namespace {
@@ -2212,6 +2214,53 @@ KernelFn pick_decode(const Args& A, int bits) {
     }
 }
 
+// Launch facts of one kernel on one device: compute units and resident
+// workgroups per compute unit at a block size and dynamic LDS size.  They do
+// not change while the process runs, so each is queried once and kept in a
+// fixed table (no host or device allocation); a full table only means that
+// later combinations are queried on every launch.
+struct Occupancy {
+    const void* fn;
+    int dev, threads;
+    size_t lds;
+    int cus, per_cu;
+};
+constexpr int kOccSlots = 256;
+Occupancy g_occ[kOccSlots];
+int g_occ_used = 0;
+std::mutex g_occ_mu;
+
+rac_status resident(const void* fn, int threads, size_t lds, int* cus, int* per_cu) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return RAC_ERR_HIP;
+    {
+        std::lock_guard<std::mutex> lock(g_occ_mu);
+        for (int i = 0; i < g_occ_used; ++i) {
+            const Occupancy& o = g_occ[i];
+            if (o.fn == fn && o.dev == dev && o.threads == threads && o.lds == lds) {
+                *cus = o.cus;
+                *per_cu = o.per_cu;
+                return RAC_OK;
+            }
+        }
+    }
+    int c = 0, p = 0;
+    if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        (fn && hipOccupancyMaxActiveBlocksPerMultiprocessor(&p, fn, threads, lds) != hipSuccess))
+        return RAC_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_occ_mu);
+    if (g_occ_used < kOccSlots) g_occ[g_occ_used++] = Occupancy{fn, dev, threads, lds, c, p};
+    *cus = c;
+    *per_cu = p;
+    return RAC_OK;
+}
+
+// Compute units of the current device (cached like the occupancy).
+rac_status device_cus(int* cus) {
+    int unused = 0;
+    return resident(nullptr, 0, 0, cus, &unused);
+}
+
 // One workgroup per token row.  Large row counts use a grid of as many
 // workgroups as the device keeps resident (at most max_per_cu per compute
 // unit), each taking rows in strides (and prefetching its next row); small
@@ -2225,12 +2274,8 @@ rac_status launch(KernelFn fn, Args A, hipStream_t stream, int threads = 0, int 
     const size_t lds = staged ? (size_t)A.nch * kSlice * sizeof(float4) : 0;
     int64_t blocks = rows <= 0 ? 1 : rows;
     if (rows > 256) {
-        int dev = 0, cus = 0, per_cu = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(fn), threads, lds) !=
-                hipSuccess)
-            return RAC_ERR_HIP;
+        int cus = 0, per_cu = 0;
+        if (resident(reinterpret_cast<const void*>(fn), threads, lds, &cus, &per_cu) != RAC_OK) return RAC_ERR_HIP;
         if (max_per_cu > 0 && per_cu > max_per_cu) per_cu = max_per_cu;
         int64_t resident = (int64_t)cus * (per_cu > 0 ? per_cu : 1);
         // a gathered reference: at most kMaxGatherRows rows per workgroup,
@@ -2407,6 +2452,13 @@ rac_status rac_encode_pooled(const rac_config* cfg, const void* x, const void* r
         return RAC_ERR_ALIGN;
     const Sizes S = sizes_of(cfg);
     if (wire_cap < S.L.total) return RAC_ERR_CAPACITY;
+    // every check and device query before the first launch: a rejected call
+    // leaves the wire untouched
+    const uint64_t nga = (uint64_t)(cfg->hidden / cfg->group_align);
+    const uint64_t pblocks = (uint64_t)segments * nga;
+    if (pblocks > 0x7FFFFFFFull) return RAC_ERR_UNSUPPORTED;
+    int cus = 0;
+    if (device_cus(&cus) != RAC_OK) return RAC_ERR_HIP;
     Args A = make_args(cfg, S);
     A.x = static_cast<const uint16_t*>(x);
     A.ref = static_cast<const uint16_t*>(ref);
@@ -2423,17 +2475,10 @@ rac_status rac_encode_pooled(const rac_config* cfg, const void* x, const void* r
     const void* mfn = A.lane_lv_a == 3 ? reinterpret_cast<const void*>(rac_moments_kernel<3>)
                     : A.lane_lv_a == 4 ? reinterpret_cast<const void*>(rac_moments_kernel<4>)
                                        : reinterpret_cast<const void*>(rac_moments_kernel<-1>);
-    int dev = 0, cus = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-        return RAC_ERR_HIP;
     const int64_t mblocks = cfg->tokens < (int64_t)cus * 4 ? cfg->tokens : (int64_t)cus * 4;
     if (hipLaunchKernel(mfn, dim3((unsigned)mblocks), dim3((unsigned)threads), margs, 0, stream) != hipSuccess)
         return RAC_ERR_HIP;
     // 2. merge per (segment, group) into every row's coefficient slot
-    const uint64_t nga = (uint64_t)(cfg->hidden / cfg->group_align);
-    const uint64_t pblocks = (uint64_t)segments * nga;
-    if (pblocks > 0x7FFFFFFFull) return RAC_ERR_UNSUPPORTED;
     void* pargs[] = {&A, &mom};
     if (hipLaunchKernel(reinterpret_cast<const void*>(rac_pool_kernel), dim3((unsigned)pblocks),
                         dim3(kWave * kPoolWaves), pargs, 0, stream) != hipSuccess)

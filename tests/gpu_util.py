@@ -77,7 +77,8 @@ def row_sections(wire: np.ndarray, rows) -> dict:
     return out
 
 
-def assert_parity(c, g_wire, g_xhat, o_wire, o_xhat, g_rows=None, o_rows=None, strict=True):
+def assert_parity(c, g_wire, g_xhat, o_wire, o_xhat, g_rows=None, o_rows=None, strict=True,
+                  g_xhat_sampled=False):
     """Compare GPU and oracle outputs.
 
     The bar (per element): header, coefficients, scales, outlier channels and
@@ -85,7 +86,8 @@ def assert_parity(c, g_wire, g_xhat, o_wire, o_xhat, g_rows=None, o_rows=None, s
     elements (rounding ties); reconstruction within 1e-5 relative / 1e-6
     absolute where codes agree and off by exactly one step where they do not.
     With strict=True the wire and reconstruction must also be bit-identical,
-    which is what the fixed evaluation order guarantees.
+    which is what the fixed evaluation order guarantees.  g_xhat_sampled: the
+    GPU reconstruction holds only the rows g_rows, in that order.
     """
     T, d, b, gq = c["tokens"], c["hidden"], c["bits"], c["group_quant"]
     if g_rows is None:
@@ -95,7 +97,8 @@ def assert_parity(c, g_wire, g_xhat, o_wire, o_xhat, g_rows=None, o_rows=None, s
         gx, ox = g_xhat, o_xhat
     else:
         gs, os_ = row_sections(g_wire, g_rows), row_sections(o_wire, o_rows)
-        gx, ox = g_xhat[g_rows], o_xhat[o_rows]
+        gx = g_xhat if g_xhat_sampled else g_xhat[g_rows]
+        ox = o_xhat[o_rows]
     n = gs["codes"].shape[0]
     assert np.array_equal(gs["coef"], os_["coef"]), \
         f"coef differ at {np.argwhere(gs['coef'] != os_['coef'])[:5].tolist()}"
@@ -126,3 +129,38 @@ def assert_parity(c, g_wire, g_xhat, o_wire, o_xhat, g_rows=None, o_rows=None, s
             assert np.array_equal(gx.view(np.uint8), ox.view(np.uint8)), \
                 f"xhat not bitwise at {np.argwhere(gx.view(np.uint32 if gx.dtype == np.float32 else np.uint16) != ox.view(np.uint32 if ox.dtype == np.float32 else np.uint16))[:5].tolist()}"
     return n
+
+
+def gpu_run_rows(c, xb, rb, rows, steps=None):
+    """Full-size encode (fused reconstruction), decode and reconstruct on the
+    GPU; asserts on the device that the three reconstructions are bitwise
+    equal, then returns the whole wire and only the given rows of the
+    sender's reconstruction (numpy), so shapes of several GB stay on the
+    device."""
+    import torch
+    check_shapes(c, xb, rb, steps)
+    cfg = rac.RacConfig(**c)
+    T, d = c["tokens"], c["hidden"]
+    x = to_dev(xb)
+    ref = to_dev(rb) if rb is not None else None
+    st = torch.from_numpy(np.asarray(steps, np.float32)).cuda() if steps is not None else None
+    wire = torch.full((rac.rac_wire_size(cfg),), 0xAB, dtype=torch.uint8, device="cuda")
+    bf16 = bool(c["flags"] & rac.RAC_FLAG_XHAT_BF16)
+    dt = torch.int16 if bf16 else torch.float32
+    xh = torch.full((T, d), -1, dtype=dt, device="cuda")
+    rac.rac_encode(cfg, x, ref, st, wire, xh)
+    del x
+    xo = torch.full((T, d), -1, dtype=dt, device="cuda")
+    rac.rac_decode(cfg, wire, ref, st, xo)
+    torch.cuda.synchronize()
+    assert torch.equal(xh, xo), "receiver decode differs from the sender reconstruction"
+    xo.fill_(-1)
+    rac.rac_reconstruct(cfg, wire, ref, st, xo)
+    torch.cuda.synchronize()
+    assert torch.equal(xh, xo), "rac_reconstruct differs from the sender reconstruction"
+    del xo
+    sel = xh.index_select(0, torch.from_numpy(np.asarray(rows, np.int64)).cuda()).cpu().numpy()
+    out = wire.cpu().numpy()
+    del xh, wire, ref
+    torch.cuda.empty_cache()
+    return out, (sel.view(np.uint16) if bf16 else sel)

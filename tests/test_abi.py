@@ -232,3 +232,64 @@ def test_pooled_argument_errors_are_synchronous(lib):
     assert enc(rac.RacConfig(64, 2048, 1024, 64, 4)) == 6        # groups wider than a chunk
     assert enc(rac.RacConfig(64, 512, 32, 64, 2)) == 6           # moments do not fit the code section
     assert enc(rac.RacConfig(0, 512, 64, 64, 4), segs=1) == 1    # no rows to pool
+
+
+def test_rejected_pooled_call_leaves_the_wire_untouched(lib):
+    """Every argument check of rac_encode_pooled, the UNSUPPORTED one for
+    segments * (d / g_a) >= 2^31 included, comes before its first launch: a
+    rejected call writes nothing.  The wire here is host memory the call
+    would fault on if it launched anything."""
+    T = 1 << 25
+    cfg = rac.RacConfig(T, 4096, 32, 128, 4)          # 128 groups per row, T segments
+    buf = np.full(4096, 0x5A, dtype=np.uint8)
+    base = (buf.ctypes.data + 255) & ~255
+    st = rac.library().rac_encode_pooled(ctypes.byref(cfg._c()), FAKE, FAKE, T, FAKE, None, base,
+                                         1 << 62, FAKE, 0)
+    assert st == 6
+    assert (buf == 0x5A).all()
+
+
+class _FakeTensor:
+    """Stands in for a torch tensor in the binding's argument checks."""
+
+    def __init__(self, numel, esize, cuda=True, contiguous=True):
+        self._n, self._e, self.is_cuda, self._c = numel, esize, cuda, contiguous
+
+    def numel(self):
+        return self._n
+
+    def element_size(self):
+        return self._e
+
+    def is_contiguous(self):
+        return self._c
+
+    def data_ptr(self):
+        return FAKE
+
+
+def test_binding_checks_tensor_arguments_before_the_call(lib, monkeypatch):
+    """Host-side checks of the binding: a CPU tensor, a non-contiguous one, a
+    wrong element size or too few elements raise ValueError before the
+    library is called."""
+    called = []
+    monkeypatch.setattr(rac, "library", lambda: type("L", (), {
+        "rac_encode": lambda *a: called.append(a) or 0,
+        "rac_decode": lambda *a: called.append(a) or 0,
+        "rac_wire_size": lib.rac_wire_size})())
+    cfg = rac.RacConfig(4, 512, 64, 64, 4)
+    n = 4 * 512
+    ok = dict(x=_FakeTensor(n, 2), ref=_FakeTensor(n, 2), wire=_FakeTensor(1 << 20, 1),
+              xhat=_FakeTensor(n, 4))
+    rac.rac_encode(cfg, ok["x"], ok["ref"], None, ok["wire"], ok["xhat"], stream=0)
+    assert len(called) == 1
+    bad = [dict(x=_FakeTensor(n, 2, cuda=False)), dict(x=_FakeTensor(n, 2, contiguous=False)),
+           dict(x=_FakeTensor(n, 4)), dict(ref=_FakeTensor(n - 1, 2)), dict(xhat=_FakeTensor(n, 2)),
+           dict(xhat=_FakeTensor(n - 8, 4))]
+    for b in bad:
+        a = dict(ok, **b)
+        with pytest.raises(ValueError):
+            rac.rac_encode(cfg, a["x"], a["ref"], None, a["wire"], a["xhat"], stream=0)
+    with pytest.raises(ValueError):
+        rac.rac_decode(cfg, _FakeTensor(100, 1), ok["ref"], None, ok["xhat"], stream=0)
+    assert len(called) == 1

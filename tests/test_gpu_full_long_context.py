@@ -1,0 +1,65 @@
+"""Full-size parity of the long-context workload (32768 tokens x 4096 hidden,
+Student-t residual noise, half the rows without a reference, 16 outliers per
+token) at every group size and bit width the benchmark times.
+
+At this row count every kernel runs as a persistent grid whose workgroups
+stride over rows, prefetch the next row and alternate row buffers; small
+cases launch one workgroup per row and never reach that loop.  The GPU codes
+all 32768 rows; the oracle recomputes sampled rows one by one (rows are
+independent), and the wire sections and the sender reconstruction of those
+rows must be bit-identical.  Decode and reconstruct are checked bitwise
+against the sender reconstruction on every row, on the device.
+"""
+from __future__ import annotations
+
+import functools
+
+import numpy as np
+import pytest
+
+import paper_2608_04991_amd as rac
+from paper_2608_04991_amd import workloads as wl
+from tests import wirefmt
+from tests.gpu_util import assert_parity, cfgd, gpu_run_rows, oracle_run, say
+
+pytestmark = pytest.mark.gpu
+
+T, D, K = 32768, 4096, 16
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    rac.library()
+
+
+@functools.lru_cache(maxsize=1)
+def _data(group):
+    say(f"[gpu] long context 32768x4096, group {group}: generating")
+    xb, rb, _ = wl.long_context(0, group=group)
+    return xb, rb
+
+
+def _rows(seed):
+    rng = np.random.default_rng(seed)
+    # the first and last rows of the grid's first and last rounds, and random ones
+    fixed = [0, 1, 2, 1791, 1792, 2047, 2048, T - 513, T - 512, T - 2, T - 1]
+    return np.unique(np.concatenate([fixed, rng.choice(T, 36, replace=False)]))
+
+
+# (group, bits): every combination the benchmark reports; group 128 at 4 bits
+# is covered by test_gpu_parity.py
+@pytest.mark.parametrize("group,bits", [(64, 2), (64, 3), (64, 4), (64, 8), (128, 2), (128, 3), (128, 8)])
+def test_long_context_full_sampled(group, bits):
+    c = cfgd(T, D, group, group, bits, K)
+    xb, rb = _data(group)
+    rows = _rows(100 * group + bits)
+    say(f"[gpu] long context g{group} b{bits}: full-size encode/decode, {rows.size} sampled rows")
+    gw, gx = gpu_run_rows(c, xb, rb, rows)
+    ow, ox = oracle_run(dict(c, tokens=rows.size), xb[rows], rb[rows])
+    n = assert_parity(c, gw, gx, ow, ox, g_rows=rows, o_rows=slice(None), g_xhat_sampled=True)
+    assert n == rows.size
+    h = wirefmt.header(gw)
+    assert h["tokens"] == T and wirefmt.padding_is_zero(gw)
