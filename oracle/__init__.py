@@ -45,7 +45,8 @@ class _Cfg(ctypes.Structure):
 class _Layout(ctypes.Structure):
     _fields_ = [("off_coef", ctypes.c_uint64), ("off_scale", ctypes.c_uint64),
                 ("off_codes", ctypes.c_uint64), ("off_outl", ctypes.c_uint64),
-                ("total", ctypes.c_uint64), ("off_ooff", ctypes.c_uint64)]
+                ("total", ctypes.c_uint64), ("off_ooff", ctypes.c_uint64),
+                ("off_sat", ctypes.c_uint64)]
 
 
 class Moments(ctypes.Structure):

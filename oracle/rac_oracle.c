@@ -41,9 +41,17 @@
 #include <string.h>
 
 #define ORC_MAGIC 0x31434152u /* bytes 'R','A','C','1' */
-#define ORC_VERSION 1u
+#define ORC_VERSION 2u
 #define ORC_HDR 256u
 #define ORC_F16_MAX_BITS 0x7BFFu
+/* Saturation report: one byte per 512-channel block of every row. */
+#define ORC_SAT_BLOCK 512
+#define ORC_SAT_COEF 1u   /* an alpha* or beta* of a group starting in the block overflowed fp16 */
+#define ORC_SAT_SCALE 2u  /* no fp16 scale covers a group starting in the block: codes clip */
+#define ORC_SAT_OUTLIER 4u /* an outlier value of a channel in the block overflowed fp16 */
+/* The smallest magnitude that round-to-nearest-even fp16 rounds to infinity:
+ * the midpoint between 65504 and the next step up, 65536. */
+#define ORC_F16_OVERFLOW 65520.0f
 
 /* ------------------------------------------------------------------------ */
 /* Number formats.  Written from the IEEE-754 definitions: an fp16 pattern
@@ -254,6 +262,8 @@ static int orc_valid(const orc_config* c) {
 
 static uint64_t up256(uint64_t v) { return (v + 255u) & ~(uint64_t)255u; }
 
+static int32_t orc_sat_blocks(int32_t d) { return (d + ORC_SAT_BLOCK - 1) / ORC_SAT_BLOCK; }
+
 int orc_layout_of(const orc_config* cfg, orc_layout* out) {
     if (!orc_valid(cfg) || !out) return ORC_ERR_INVALID;
     const uint64_t T = (uint64_t)cfg->tokens, d = (uint64_t)cfg->hidden;
@@ -265,15 +275,19 @@ int orc_layout_of(const orc_config* cfg, orc_layout* out) {
     out->off_scale = up256(out->off_coef + coef);
     out->off_codes = up256(out->off_scale + scale);
     out->off_outl = up256(out->off_codes + codes);
+    uint64_t end;
     if (cfg->flags & ORC_FLAG_GROUP_OUTLIERS) {
         /* fp16 values [T][d/g_q][k_g], then u8 offsets [T][d/g_q][k_g] */
         const uint64_t n = T * (d / (uint64_t)cfg->group_quant) * (uint64_t)cfg->outlier_k;
         out->off_ooff = up256(out->off_outl + 2u * n);
-        out->total = up256(out->off_ooff + n);
+        end = out->off_ooff + n;
     } else {
         out->off_ooff = 0;
-        out->total = up256(out->off_outl + T * (uint64_t)cfg->outlier_k * 4u);
+        end = out->off_outl + T * (uint64_t)cfg->outlier_k * 4u;
     }
+    /* saturation report: u8 [T][ceil(d/512)] */
+    out->off_sat = up256(end);
+    out->total = up256(out->off_sat + T * (uint64_t)orc_sat_blocks(cfg->hidden));
     return ORC_OK;
 }
 
@@ -329,6 +343,7 @@ static void orc_write_header(const orc_config* cfg, const orc_layout* L, int zer
     put64(w + 56, L->off_outl);
     put64(w + 64, L->total);
     put64(w + 72, L->off_ooff);
+    put64(w + 80, L->off_sat);
 }
 
 /* q-bit two's complement code of channel c goes to bits [c*q, c*q+q) of the
@@ -397,6 +412,7 @@ static int orc_encode_impl(const orc_config* cfg, const uint16_t* x, const uint1
     uint16_t* oval = (uint16_t*)calloc((size_t)d, sizeof(uint16_t));
     uint8_t* is_out = (uint8_t*)calloc((size_t)d, 1);
     uint16_t sel[64];
+    const int32_t nsat = orc_sat_blocks(d);
 
     for (int64_t t = 0; t < T; ++t) {
         /* step 1: widen the row (exact) */
@@ -408,6 +424,7 @@ static int orc_encode_impl(const orc_config* cfg, const uint16_t* x, const uint1
          * fp16, then the aligned reference and residual (Eq. aligned-residual)
          * formed with the serialized coefficients */
         uint8_t* coef = wire + L.off_coef + (uint64_t)t * (uint64_t)(d / ga) * 4u;
+        uint8_t* sat = wire + L.off_sat + (uint64_t)t * (uint64_t)nsat;
         for (int32_t j = 0; j < d / ga; ++j) {
             float as, bs;
             if (pooled) {
@@ -417,6 +434,9 @@ static int orc_encode_impl(const orc_config* cfg, const uint16_t* x, const uint1
                 orc_fit_group(r + j * ga, xv + j * ga, ga, &as, &bs);
             }
             const uint16_t ah = orc_f16_rne_sat(as), bh = orc_f16_rne_sat(bs);
+            /* Round_wire overflowed: the field holds +-65504 instead of +-inf */
+            if (fabsf(as) >= ORC_F16_OVERFLOW || fabsf(bs) >= ORC_F16_OVERFLOW)
+                sat[(j * ga) / ORC_SAT_BLOCK] |= (uint8_t)ORC_SAT_COEF;
             put16(coef + 4 * j, ah);
             put16(coef + 4 * j + 2, bh);
             const float a = orc_f16_to_f32(ah), b0 = orc_f16_to_f32(bh);
@@ -439,6 +459,7 @@ static int orc_encode_impl(const orc_config* cfg, const uint16_t* x, const uint1
                 for (int32_t i = 0; i < k; ++i) {
                     const int32_t c = g * gq + sel[i];
                     oval[c] = orc_f16_rne_sat(e[c]);
+                    if (fabsf(e[c]) >= ORC_F16_OVERFLOW) sat[c / ORC_SAT_BLOCK] |= (uint8_t)ORC_SAT_OUTLIER;
                     is_out[c] = 1;
                     ed[c] = 0.0f;
                     put16(vrow + 2 * ((uint64_t)g * k + i), oval[c]);
@@ -451,6 +472,7 @@ static int orc_encode_impl(const orc_config* cfg, const uint16_t* x, const uint1
             for (int32_t i = 0; i < k; ++i) {
                 const int32_t c = sel[i];
                 oval[c] = orc_f16_rne_sat(e[c]); /* O-hat = Round_FP16(O) */
+                if (fabsf(e[c]) >= ORC_F16_OVERFLOW) sat[c / ORC_SAT_BLOCK] |= (uint8_t)ORC_SAT_OUTLIER;
                 is_out[c] = 1;
                 ed[c] = 0.0f;
                 put32(ol + 4 * i, (uint32_t)c | ((uint32_t)oval[c] << 16));
@@ -469,6 +491,9 @@ static int orc_encode_impl(const orc_config* cfg, const uint16_t* x, const uint1
                 for (int32_t c = g * gq; c < (g + 1) * gq; ++c)
                     if (fabsf(ed[c]) > m) m = fabsf(ed[c]);
                 sh = (m == 0.0f) ? 0u : orc_scale_roundup(m, qmax); /* 0 = zero group */
+                /* no fp16 step covers the maximum (65504 * Qmax is exact) */
+                if (m > orc_f16_to_f32(ORC_F16_MAX_BITS) * (float)qmax)
+                    sat[(g * gq) / ORC_SAT_BLOCK] |= (uint8_t)ORC_SAT_SCALE;
                 put16(srow + 2 * g, sh);
             }
             const float s = orc_f16_to_f32(sh);
@@ -634,7 +659,7 @@ int orc_decode(const orc_config* cfg, const uint8_t* wire, const uint16_t* ref,
         get16(wire + 28) != (uint16_t)cfg->outlier_k || get64(wire + 32) != L.off_coef ||
         get64(wire + 40) != L.off_scale || get64(wire + 48) != L.off_codes ||
         get64(wire + 56) != L.off_outl || get64(wire + 64) != L.total ||
-        get64(wire + 72) != L.off_ooff)
+        get64(wire + 72) != L.off_ooff || get64(wire + 80) != L.off_sat)
         return ORC_ERR_FORMAT;
 
     const int64_t T = cfg->tokens;

@@ -53,9 +53,15 @@ typedef struct {
 
 /* Byte offsets of the wire sections (all 256-byte aligned).  off_ooff is the
  * in-group offset array of the per-group outlier mode (0 otherwise); off_outl
- * then holds the fp16 values. */
+ * then holds the fp16 values.  off_sat is the saturation report, u8
+ * [T][ceil(d/512)]: per row and 512-channel block, bit 1 = an alpha* or beta*
+ * of a group whose first channel is in the block overflowed fp16 (|v| >=
+ * 65520, stored as +-65504), bit 2 = the scale of a quantization group whose
+ * first channel is in the block saturated (max|E^d| > 65504 * Qmax, its codes
+ * clip; dynamic scales only), bit 4 = an outlier value of a channel in the
+ * block overflowed fp16. */
 typedef struct {
-    uint64_t off_coef, off_scale, off_codes, off_outl, total, off_ooff;
+    uint64_t off_coef, off_scale, off_codes, off_outl, total, off_ooff, off_sat;
 } orc_layout;
 
 int orc_layout_of(const orc_config* cfg, orc_layout* out);

@@ -24,7 +24,7 @@ __all__ = [
     "STATUS",
     "library", "library_path", "rac_wire_layout", "rac_wire_size", "rac_parse_header",
     "rac_encode", "rac_reconstruct", "rac_decode", "rac_encode_gather", "rac_decode_gather",
-    "rac_status_string", "SpanIndex", "rac_encode_pooled",
+    "rac_status_string", "SpanIndex", "rac_encode_pooled", "rac_saturation_summary",
 ]
 
 RAC_FLAG_FIXED_STEP = 1
@@ -56,7 +56,8 @@ class _Config(ctypes.Structure):
 class _Layout(ctypes.Structure):
     _fields_ = [("off_coef", ctypes.c_uint64), ("off_scale", ctypes.c_uint64),
                 ("off_codes", ctypes.c_uint64), ("off_outl", ctypes.c_uint64),
-                ("total", ctypes.c_uint64), ("off_ooff", ctypes.c_uint64)]
+                ("total", ctypes.c_uint64), ("off_ooff", ctypes.c_uint64),
+                ("off_sat", ctypes.c_uint64)]
 
 
 @dataclass(frozen=True)
@@ -120,6 +121,9 @@ def library():
         L.rac_span_index_add.restype = ctypes.c_int
         L.rac_span_select.argtypes = [vp, vp, ctypes.c_int64, vp, ctypes.POINTER(ctypes.c_int64)]
         L.rac_span_select.restype = ctypes.c_int
+        L.rac_saturation_summary.argtypes = [cp, vp, ctypes.c_size_t, ctypes.POINTER(ctypes.c_int64),
+                                             ctypes.POINTER(ctypes.c_uint32)]
+        L.rac_saturation_summary.restype = ctypes.c_int
         L.rac_status_string.argtypes = [ctypes.c_int]
         L.rac_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -208,6 +212,19 @@ def rac_parse_header(header: bytes):
            "rac_parse_header")
     return RacConfig(c.tokens, c.hidden, c.group_align, c.group_quant, c.bits, c.outlier_k,
                      c.flags), bool(zr.value)
+
+
+def rac_saturation_summary(cfg: RacConfig, sat) -> tuple[int, int]:
+    """(rows with any saturation bit, OR of all bits) of a saturation report
+    in host memory (bytes-like or a numpy uint8 array of tokens *
+    ceil(hidden / 512) bytes, e.g. wire[layout['off_sat']:])."""
+    import numpy as np
+    a = np.ascontiguousarray(np.frombuffer(bytes(sat), dtype=np.uint8) if isinstance(sat, (bytes, bytearray))
+                             else np.asarray(sat, dtype=np.uint8))
+    rows, bits = ctypes.c_int64(0), ctypes.c_uint32(0)
+    _check(library().rac_saturation_summary(ctypes.byref(cfg._c()), a.ctypes.data, a.size, ctypes.byref(rows),
+                                            ctypes.byref(bits)), "rac_saturation_summary")
+    return int(rows.value), int(bits.value)
 
 
 def rac_encode(cfg: RacConfig, x, ref, fixed_steps, wire, xhat=None, stream=None,

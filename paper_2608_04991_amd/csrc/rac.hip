@@ -58,6 +58,7 @@ struct alignas(8) Args {
     uint32_t* outl;     // per-token outliers, or the fp16 values of per-group ones
     uint16_t* gval;     // per-group outliers: fp16 values [T][d/g_q][k_g] (= outl)
     uint8_t* goff;      //                     u8 in-group offsets [T][d/g_q][k_g]
+    uint8_t* sat;       // saturation report [T][nch]: one byte per row and 512-channel chunk
     void* xhat;
     uint32_t tokens;    // < 2^31, so row + gridDim.x never wraps
     int32_t d;
@@ -79,8 +80,8 @@ struct alignas(8) Args {
     // header and padding (written once, by the first wavefront)
     int32_t write_header;
     uint8_t* wire;
-    uint64_t off_scale, off_codes, off_outl, off_ooff, total;
-    uint64_t end_coef, end_scale, end_codes, end_outl, end_ooff;  // first byte after each section
+    uint64_t off_scale, off_codes, off_outl, off_ooff, off_sat, total;
+    uint64_t end_coef, end_scale, end_codes, end_outl, end_ooff, end_sat;  // first byte after each section
     uint32_t hdr[24];   // first 96 bytes of the header; the rest is zero
 };
 
@@ -207,6 +208,23 @@ __device__ __forceinline__ uint32_t fit_coef(float crr, float crx, float mr, flo
     const float bs = flat ? mx : mx - as * mr;
     return f16_rne_sat(as) | (f16_rne_sat(bs) << 16);
 }
+
+// The same, also reporting whether alpha* or beta* overflowed fp16: |v| >=
+// 65520 (the midpoint between 65504 and the next step, 65536, from which
+// round-to-nearest-even goes to infinity); the field then holds +-65504.
+constexpr float kF16Overflow = 65520.0f;
+__device__ __forceinline__ uint32_t fit_coef(float crr, float crx, float mr, float mx, bool& sat) {
+    const bool flat = crr == 0.0f;
+    const float as = flat ? 0.0f : crx / crr;
+    const float bs = flat ? mx : mx - as * mr;
+    sat = (__builtin_fabsf(as) >= kF16Overflow) | (__builtin_fabsf(bs) >= kF16Overflow);
+    return f16_rne_sat(as) | (f16_rne_sat(bs) << 16);
+}
+
+// Saturation report bits (one byte per row and 512-channel chunk).
+constexpr uint32_t kSatCoef = 1u;     // a coefficient of a group starting in the chunk overflowed fp16
+constexpr uint32_t kSatScale = 2u;    // a scale of a group starting in the chunk saturated (codes clip)
+constexpr uint32_t kSatOutlier = 4u;  // an outlier value of a channel in the chunk overflowed fp16
 
 // ---------------------------------------------------------------------------
 // Cross-lane partner of the adjacent aligned block at butterfly level `lv`
@@ -354,7 +372,8 @@ __device__ __forceinline__ void write_header(const Args& A, uint32_t lane) {
     zero_bytes(A.wire, A.end_scale, A.off_codes, lane);
     zero_bytes(A.wire, A.end_codes, A.off_outl, lane);
     zero_bytes(A.wire, A.end_outl, A.off_ooff, lane);
-    zero_bytes(A.wire, A.end_ooff, A.total, lane);
+    zero_bytes(A.wire, A.end_ooff, A.off_sat, lane);
+    zero_bytes(A.wire, A.end_sat, A.total, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -1135,9 +1154,14 @@ void rac_encode_kernel(Args A) {
             crr = tree_n(&S.part[2][g0], cpg_a);
             crx = tree_n(&S.part[3][g0], cpg_a);
         }
+        bool csat = false;
         const uint32_t cf = A.cf_given ? bload32(rsrc(A.coef, (uint64_t)row * nga, nga * 4u), (uint32_t)grp_a * 4u)
-                                       : fit_coef(crr, crx, mr, mx);
+                                       : fit_coef(crr, crx, mr, mx, csat);
         bstore32(rsrc(A.coef, (uint64_t)row * nga, nga * 4u), (first_a && !A.cf_given) ? (uint32_t)grp_a * 4u : kOut, cf);
+        // saturation report of this row and chunk; given pairs come with
+        // their coefficient bit already in the report (set by the pooling)
+        const Rsrc rsat = rsrc(A.sat, (uint64_t)row * (uint32_t)A.nch, (uint32_t)A.nch);
+        uint32_t satb = A.cf_given ? (bload8(rsat, (uint32_t)w) & kSatCoef) : (ballot(first_a && csat) ? kSatCoef : 0u);
 
         // a3: aligned reference R~ = fma(alpha, r, beta) and residual E = x - R~
         const float a = f16_value(cf & 0xFFFFu), b0 = f16_value(cf >> 16);
@@ -1161,6 +1185,12 @@ void rac_encode_kernel(Args A) {
         float ed[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) ed[j] = e[j];
+        if constexpr (OM != 0) {
+            bool osat = false;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) osat |= ((selm >> j) & 1u) && __builtin_fabsf(e[j]) >= kF16Overflow;
+            satb |= ballot(osat) ? kSatOutlier : 0u;
+        }
         if (selm) {
 #pragma unroll
             for (int j = 0; j < 8; ++j)
@@ -1190,6 +1220,7 @@ void rac_encode_kernel(Args A) {
             }
             sh = m == 0.0f ? 0u : scale_roundup(m, q, inv_q);
             bstore16(rsrc(A.scale, (uint64_t)row * ngq, ngq * 2u), first_q ? (uint32_t)grp_q * 2u : kOut, sh);
+            satb |= ballot(first_q && m > 65504.0f * q) ? kSatScale : 0u;
         }
         const float s = f16_value(sh);
         const float inv = sh ? __builtin_amdgcn_rcpf(s) : 0.0f;
@@ -1227,6 +1258,7 @@ void rac_encode_kernel(Args A) {
         }
         const uint32_t crb = (uint32_t)A.code_row_bytes;
         store_codes<BITS>(rsrc(A.codes, (uint64_t)row * crb, crb), w, lane, dword3, pk);
+        bstore8(rsat, lane == 0u ? (uint32_t)w : kOut, satb);
         store_xhat_t(xhat_row(A, row), A.xhat_bf16 != 0, (uint32_t)(w * kChunk), lane, XT + w * kSlice, H);
     }
 }
@@ -1426,6 +1458,10 @@ void rac_encode_rows_kernel(Args A) {
         // a2-a3 per chunk: fit of the lane's group, E; lane maxima of |E|
         // (per chunk, and over the wavefront's chunks)
         const Rsrc rcoef = rsrc(A.coef, (uint64_t)row * nga, nga * 4u);
+        const Rsrc rsat = rsrc(A.sat, (uint64_t)row * (uint32_t)A.nch, (uint32_t)A.nch);
+        // saturation report bits of each chunk (given pairs come with their
+        // coefficient bit already in the report, set by the pooling)
+        uint32_t satc[CPW];
         float lmc[CPW];
 #pragma unroll
         for (int i = 0; i < CPW; ++i) lmc[i] = 0.0f;
@@ -1447,9 +1483,12 @@ void rac_encode_rows_kernel(Args A) {
             const float crr = lsum<GA>(tree8(uu), lv_a), crx = lsum<GA>(tree8(uv), lv_a);
             if constexpr (GIVEN) {
                 cf[i] = bload32(rcoef, (c0 >> A.lg_a) * 4u);
+                satc[i] = bload8(rsat, (uint32_t)(chunk_at(i) / kChunk)) & kSatCoef;
             } else {
-                cf[i] = fit_coef(crr, crx, mr, mx);
+                bool cs;
+                cf[i] = fit_coef(crr, crx, mr, mx, cs);
                 bstore32(rcoef, first_a ? (c0 >> A.lg_a) * 4u : kOut, cf[i]);
+                satc[i] = ballot(first_a && cs) ? kSatCoef : 0u;
             }
             const float a = f16_value(cf[i] & 0xFFFFu), b0 = f16_value(cf[i] >> 16);
             float e[8];
@@ -1609,6 +1648,7 @@ void rac_encode_rows_kernel(Args A) {
         // keys >= kst.
         const bool chosen = have && key >= kst;
         const uint32_t och = chosen ? key_channel(key) : 0xFFFFFFFFu;
+        const bool osat = chosen && __builtin_fabsf(__uint_as_float(S.cval[lane])) >= kF16Overflow;
         uint32_t oval = 0u;
         float ohat = 0.0f;
         if (chosen) {
@@ -1658,6 +1698,9 @@ void rac_encode_rows_kernel(Args A) {
             m = lmax<GQ>(m, lv_q);
             const uint32_t sh = m == 0.0f ? 0u : scale_roundup(m, q, inv_q);
             bstore16(rsc, first_q ? (c0 >> A.lg_q) * 2u : kOut, sh);
+            const uint32_t satb = satc[i] | (ballot(first_q && m > 65504.0f * q) ? kSatScale : 0u) |
+                                  (ballot(osat && och - chunk0 < (uint32_t)kChunk) ? kSatOutlier : 0u);
+            bstore8(rsat, lane == 0u ? chunk0 / (uint32_t)kChunk : kOut, satb);
             const float s = f16_value(sh);
             const float inv = sh ? __builtin_amdgcn_rcpf(s) : 0.0f;
             // |E^d| <= s q, so E^d * (1/s) stays below q + 1/2 unless the
@@ -1861,6 +1904,8 @@ __device__ __forceinline__ Mom mom_merge(const Mom& a, const Mom& b) {
 // them: one workgroup per row (strided), one wavefront per 512-channel chunk,
 // groups inside a chunk.  Written as float4 (m_r, m_x, C_rr, C_rx) to `mom`
 // [T][d/g_a] (the wire's code section, which the encode overwrites later).
+// The row's saturation report is cleared here: the pooling sets the
+// coefficient bits, the encode adds the others.
 template <int GA>
 __global__ __launch_bounds__(kWave * kMaxWaves) void rac_moments_kernel(Args A, float4* mom) {
     const uint32_t lane = threadIdx.x & (kWave - 1);
@@ -1889,6 +1934,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_moments_kernel(Args A, 
         const float crr = lsum<GA>(tree8(uu), lv_a);
         const float crx = lsum<GA>(tree8(uv), lv_a);
         if (first_a && c0 < d) mom[(uint64_t)row * nga + grp_a] = make_float4(mr, mx, crr, crx);
+        bstore8(rsrc(A.sat, (uint64_t)row * (uint32_t)A.nch, (uint32_t)A.nch), lane == 0u ? (uint32_t)w : kOut, 0u);
     }
 }
 
@@ -1903,8 +1949,10 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_moments_kernel(Args A, 
 // One thread takes the pass results in row order onto a stack of
 // power-of-two sizes, merging whenever the top two are equal, and merges the
 // stack from the top down at the end.  The fp16 pair goes to the coefficient
-// slot of every row of the segment.  Segment bounds are clamped to [0, T], so
-// no access leaves the buffers whatever the starts hold.
+// slot of every row of the segment, and a pair that overflowed fp16 sets the
+// coefficient bit of the group's chunk in every row's saturation report.
+// Segment bounds are clamped to [0, T], so no access leaves the buffers
+// whatever the starts hold.
 constexpr int kPoolWaves = 16;
 
 __global__ __launch_bounds__(kWave * kPoolWaves) void rac_pool_kernel(Args A, const float4* mom) {
@@ -1912,7 +1960,7 @@ __global__ __launch_bounds__(kWave * kPoolWaves) void rac_pool_kernel(Args A, co
     __shared__ uint32_t bsz[kPoolWaves];
     __shared__ Mom stk[40];
     __shared__ uint32_t ssz[40];
-    __shared__ uint32_t cf_shared;
+    __shared__ uint32_t cf_shared, sat_shared;
     const uint32_t lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
     const uint32_t nga = (uint32_t)A.d >> A.lg_a;
     const uint32_t s = blockIdx.x / nga, j = blockIdx.x % nga;
@@ -1977,17 +2025,22 @@ __global__ __launch_bounds__(kWave * kPoolWaves) void rac_pool_kernel(Args A, co
     }
     if (threadIdx.x == 0u) {
         uint32_t cf = 0u;
+        bool sat = false;
         if (top > 0) {
             Mom r = stk[top - 1];
             for (int i = top - 2; i >= 0; --i) r = mom_merge(stk[i], r);
-            cf = fit_coef(r.crr, r.crx, r.mr, r.mx);
+            cf = fit_coef(r.crr, r.crx, r.mr, r.mx, sat);
         }
         cf_shared = cf;
+        sat_shared = sat ? 1u : 0u;
     }
     __syncthreads();
     const uint32_t cf = cf_shared;
-    for (int64_t t = lo + threadIdx.x; t < hi; t += (int64_t)kWave * kPoolWaves)
+    const uint32_t sat_off = sat_shared ? (j << A.lg_a) / (uint32_t)kChunk : kOut;
+    for (int64_t t = lo + threadIdx.x; t < hi; t += (int64_t)kWave * kPoolWaves) {
         bstore32(rsrc(A.coef, (uint64_t)t * nga, nga * 4u), j * 4u, cf);
+        bstore8(rsrc(A.sat, (uint64_t)t * (uint32_t)A.nch, (uint32_t)A.nch), sat_off, kSatCoef);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -2022,8 +2075,10 @@ bool grouped(const rac_config* c) { return (c->flags & RAC_FLAG_GROUP_OUTLIERS) 
 
 struct Sizes {
     rac_layout L;
-    uint64_t coef, scale, codes, outl, ooff;
+    uint64_t coef, scale, codes, outl, ooff, sat;
 };
+
+uint64_t sat_chunks(int64_t d) { return (uint64_t)((d + kChunk - 1) / kChunk); }
 
 Sizes sizes_of(const rac_config* c) {
     Sizes s;
@@ -2039,7 +2094,9 @@ Sizes sizes_of(const rac_config* c) {
     s.L.off_codes = up256(s.L.off_scale + s.scale);
     s.L.off_outl = up256(s.L.off_codes + s.codes);
     s.L.off_ooff = grouped(c) ? up256(s.L.off_outl + s.outl) : 0u;
-    s.L.total = grouped(c) ? up256(s.L.off_ooff + s.ooff) : up256(s.L.off_outl + s.outl);
+    s.sat = T * sat_chunks(c->hidden);
+    s.L.off_sat = grouped(c) ? up256(s.L.off_ooff + s.ooff) : up256(s.L.off_outl + s.outl);
+    s.L.total = up256(s.L.off_sat + s.sat);
     return s;
 }
 
@@ -2051,8 +2108,10 @@ Args make_args(const rac_config* c, const Sizes& S) {
     A.off_codes = S.L.off_codes;
     A.off_outl = S.L.off_outl;
     A.total = S.L.total;
-    // without per-group outliers the offset array is empty, at the end
-    A.off_ooff = grouped(c) ? S.L.off_ooff : S.L.total;
+    A.off_sat = S.L.off_sat;
+    A.end_sat = S.L.off_sat + S.sat;
+    // without per-group outliers the offset array is empty, at the saturation report
+    A.off_ooff = grouped(c) ? S.L.off_ooff : S.L.off_sat;
     A.end_ooff = A.off_ooff + S.ooff;
     A.end_coef = S.L.off_coef + S.coef;
     A.end_scale = S.L.off_scale + S.scale;
@@ -2082,7 +2141,8 @@ void set_sections(Args& A, const Sizes& S) {
     A.codes = A.wire + S.L.off_codes;
     A.outl = reinterpret_cast<uint32_t*>(A.wire + S.L.off_outl);
     A.gval = reinterpret_cast<uint16_t*>(A.wire + S.L.off_outl);
-    A.goff = A.wire + (A.gout ? S.L.off_ooff : S.L.total);
+    A.goff = A.wire + (A.gout ? S.L.off_ooff : S.L.off_sat);
+    A.sat = A.wire + S.L.off_sat;
 }
 
 void fill_header(Args& A, const rac_config* c, bool zero_ref, bool pooled = false) {
@@ -2097,7 +2157,7 @@ void fill_header(Args& A, const rac_config* c, bool zero_ref, bool pooled = fals
     if (grouped(c)) flags |= 8u;
     if (pooled) flags |= 16u;
     put32(0, 0x31434152u);
-    put16(4, 1u);
+    put16(4, 2u);
     put16(6, flags);
     put32(8, (uint32_t)c->tokens);
     put32(12, (uint32_t)c->hidden);
@@ -2114,6 +2174,7 @@ void fill_header(Args& A, const rac_config* c, bool zero_ref, bool pooled = fals
     put64(56, A.off_outl);
     put64(64, A.total);
     put64(72, grouped(c) ? A.off_ooff : 0u);
+    put64(80, A.off_sat);
     for (int i = 0; i < 24; ++i)
         A.hdr[i] = (uint32_t)h[4 * i] | ((uint32_t)h[4 * i + 1] << 8) | ((uint32_t)h[4 * i + 2] << 16) |
                    ((uint32_t)h[4 * i + 3] << 24);
@@ -2342,6 +2403,25 @@ rac_status rac_wire_layout(const rac_config* cfg, rac_layout* out) {
     return RAC_OK;
 }
 
+rac_status rac_saturation_summary(const rac_config* cfg, const void* sat_host, size_t len, int64_t* rows,
+                                  uint32_t* bits) {
+    if (!config_valid(cfg) || (cfg->tokens > 0 && !sat_host)) return RAC_ERR_INVALID;
+    const uint64_t nb = sat_chunks(cfg->hidden), T = (uint64_t)cfg->tokens;
+    if (len < T * nb) return RAC_ERR_INVALID;
+    const uint8_t* p = static_cast<const uint8_t*>(sat_host);
+    int64_t n = 0;
+    uint32_t all = 0;
+    for (uint64_t t = 0; t < T; ++t) {
+        uint32_t r = 0;
+        for (uint64_t b = 0; b < nb; ++b) r |= p[t * nb + b];
+        n += r ? 1 : 0;
+        all |= r;
+    }
+    if (rows) *rows = n;
+    if (bits) *bits = all;
+    return RAC_OK;
+}
+
 size_t rac_wire_size(const rac_config* cfg) {
     if (!config_valid(cfg)) return 0;
     return (size_t)sizes_of(cfg).L.total;
@@ -2354,7 +2434,7 @@ rac_status rac_parse_header(const void* header_host, size_t len, rac_config* out
     auto g16 = [&](int o) { return (uint32_t)h[o] | ((uint32_t)h[o + 1] << 8); };
     auto g32 = [&](int o) { uint32_t v = 0; for (int i = 3; i >= 0; --i) v = (v << 8) | h[o + i]; return v; };
     auto g64 = [&](int o) { uint64_t v = 0; for (int i = 7; i >= 0; --i) v = (v << 8) | h[o + i]; return v; };
-    if (g32(0) != 0x31434152u || g16(4) != 1u) return RAC_ERR_FORMAT;
+    if (g32(0) != 0x31434152u || g16(4) != 2u) return RAC_ERR_FORMAT;
     const uint32_t flags = g16(6);
     if (flags & ~31u) return RAC_ERR_FORMAT;
     if ((flags & 1u) && (flags & 8u)) return RAC_ERR_FORMAT;
@@ -2373,11 +2453,12 @@ rac_status rac_parse_header(const void* header_host, size_t len, rac_config* out
     if (h[25] != 1 || h[26] != ((flags & 2u) ? 0 : 1) || h[27] != ofmt) return RAC_ERR_FORMAT;
     const Sizes S = sizes_of(&c);
     if (g64(32) != S.L.off_coef || g64(40) != S.L.off_scale || g64(48) != S.L.off_codes ||
-        g64(56) != S.L.off_outl || g64(64) != S.L.total || g64(72) != S.L.off_ooff)
+        g64(56) != S.L.off_outl || g64(64) != S.L.total || g64(72) != S.L.off_ooff ||
+        g64(80) != S.L.off_sat)
         return RAC_ERR_FORMAT;
     for (int i = 30; i < 32; ++i)
         if (h[i]) return RAC_ERR_FORMAT;
-    for (int i = 80; i < 256; ++i)
+    for (int i = 88; i < 256; ++i)
         if (h[i]) return RAC_ERR_FORMAT;
     *out = c;
     if (zero_ref) *zero_ref = (flags & 4u) ? 1 : 0;

@@ -37,7 +37,8 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == {"rac_wire_layout", "rac_wire_size", "rac_parse_header", "rac_encode",
                           "rac_reconstruct", "rac_decode", "rac_encode_gather", "rac_decode_gather",
                           "rac_status_string", "rac_span_index_create", "rac_span_index_destroy",
-                          "rac_span_index_add", "rac_span_select", "rac_encode_pooled"}
+                          "rac_span_index_add", "rac_span_select", "rac_encode_pooled",
+                          "rac_saturation_summary"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -75,7 +76,7 @@ def test_layout_matches_documented_format(lib, c):
 def test_payload_ratio_of_the_prefill_uplink_shape(lib):
     cfg = rac.RacConfig(4096, 4096, 128, 128, 4, 8)
     ratio = rac.rac_wire_size(cfg) / (4096 * 4096 * 2)
-    assert abs(ratio - 0.2774) < 5e-4   # 4-bit codes + fp16 scale/coef + 8 outliers per row
+    assert abs(ratio - 0.2783) < 5e-4   # 4-bit codes + fp16 scale/coef + 8 outliers + 8 flag bytes per row
 
 
 @pytest.mark.parametrize("bad", [dict(bits=5), dict(group_align=96), dict(group_quant=4),
@@ -123,7 +124,8 @@ def test_group_outlier_payload_of_the_prefill_uplink_shape(lib):
     cfg = rac.RacConfig(4096, 4096, 128, 128, 4, 1, rac.RAC_FLAG_GROUP_OUTLIERS)
     ratio = rac.rac_wire_size(cfg) / (4096 * 4096 * 2)
     # 4-bit codes + fp16 scale/coef + one (u8 offset, fp16 value) per group of 128
-    assert abs(ratio - (0.25 + 6 / 256 + 3 / 256)) < 1e-5
+    # + one saturation byte per 512 channels
+    assert abs(ratio - (0.25 + 6 / 256 + 3 / 256 + 1 / 1024)) < 1e-5
 
 
 def test_parse_header_rejects_corruption_of_group_outlier_headers(lib):
@@ -135,8 +137,9 @@ def test_parse_header_rejects_corruption_of_group_outlier_headers(lib):
     cfg, _ = rac.rac_parse_header(good)
     assert cfg == rac.RacConfig(**c)
     # flags 9 (both outlier kinds), format 1 with flag 8, a moved offset array,
-    # k_g above a quarter of the group, a byte past the fields
-    for off, val in [(6, 9), (27, 1), (73, 0), (28, 17), (80, 1)]:
+    # k_g above a quarter of the group, a moved saturation report, a byte past
+    # the fields
+    for off, val in [(6, 9), (27, 1), (73, 0), (28, 17), (80, 1), (90, 1)]:
         bad = bytearray(good)
         bad[off] = val
         with pytest.raises(rac.RacError) as e:
@@ -150,7 +153,7 @@ def test_parse_header_rejects_corruption(lib):
     rc, wire, _ = oracle.encode(xb, None, want_xhat=False, **c)
     good = wire[:256].tobytes()
     rac.rac_parse_header(good)
-    for off, val in [(0, 0x00), (4, 2), (24, 5), (28, 0), (40, 0x11), (100, 1), (6, 0x08), (25, 2)]:
+    for off, val in [(0, 0x00), (4, 1), (24, 5), (28, 0), (40, 0x11), (80, 0x13), (100, 1), (6, 0x08), (25, 2)]:
         bad = bytearray(good)
         bad[off] = val
         with pytest.raises(rac.RacError) as e:

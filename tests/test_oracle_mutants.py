@@ -17,6 +17,7 @@ import oracle
 from tests import test_oracle_group_outliers as gpins
 from tests import test_oracle_pooled as ppins
 from tests import test_oracle_pins as pins
+from tests import test_oracle_saturation as spins
 
 # (name, text in rac_oracle.c, replacement)
 MUTANTS = [
@@ -54,6 +55,13 @@ MUTANTS = [
     ("pool_repeats_the_first_row", "seg[i] = mom[(lo + i) * G + j];", "seg[i] = mom[lo * G + j];"),
     ("group_values_in_reverse", "put16(vrow + 2 * ((uint64_t)g * k + i), oval[c]);",
      "put16(vrow + 2 * ((uint64_t)g * k + (k - 1 - i)), oval[c]);"),
+    ("sat_threshold_at_the_largest_fp16", "#define ORC_F16_OVERFLOW 65520.0f", "#define ORC_F16_OVERFLOW 65504.0f"),
+    ("sat_coef_block_by_group_index", "sat[(j * ga) / ORC_SAT_BLOCK] |= (uint8_t)ORC_SAT_COEF;",
+     "sat[j / ORC_SAT_BLOCK] |= (uint8_t)ORC_SAT_COEF;"),
+    ("sat_scale_ignores_qmax", "if (m > orc_f16_to_f32(ORC_F16_MAX_BITS) * (float)qmax)",
+     "if (m > orc_f16_to_f32(ORC_F16_MAX_BITS))"),
+    ("sat_outlier_block_of_the_rank", "if (fabsf(e[c]) >= ORC_F16_OVERFLOW) sat[c / ORC_SAT_BLOCK] |= (uint8_t)ORC_SAT_OUTLIER;\n                is_out",
+     "if (fabsf(e[c]) >= ORC_F16_OVERFLOW) sat[i / ORC_SAT_BLOCK] |= (uint8_t)ORC_SAT_OUTLIER;\n                is_out"),
 ]
 
 PINS = [
@@ -75,6 +83,12 @@ PINS = [
     lambda: ppins.test_pooled_fit_matches_exact_rational_least_squares(0),
     ppins.test_pooled_moments_match_float64,
     ppins.test_constant_reference_over_a_segment_gives_alpha_zero_and_the_pooled_mean,
+    spins.test_ordinary_rows_report_nothing,
+    spins.test_scale_saturation_depends_on_qmax_and_marks_the_group_block,
+    spins.test_beta_overflow_threshold_is_the_fp16_rounding_overflow,
+    spins.test_alpha_overflow_marks_the_alignment_group_block,
+    spins.test_outlier_value_overflow_marks_the_channel_block,
+    spins.test_pooled_fit_reports_every_row_of_a_saturated_segment,
 ]
 
 

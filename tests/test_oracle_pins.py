@@ -367,12 +367,15 @@ def test_wire_layout_closed_form_and_zero_padding():
     for c in [cfgd(4096, 4096, 128, 128, 4, 8), cfgd(3, 520, 8, 8, 3, 64),
               cfgd(0, 64, 64, 64, 2), cfgd(5, 256, 32, 16, 8, 0, oracle.FLAG_FIXED_STEP)]:
         assert oracle.layout(**c) == wirefmt.expected_layout(**c)
-    assert oracle.layout(**cfgd(4096, 4096, 128, 128, 4, 8))["total"] == 9306368  # 27.7% of bf16
+    # 27.8% of bf16: 4-bit codes, fp16 scale and (alpha, beta) per group of 128, eight 4-byte
+    # outliers and eight saturation bytes per row, a 256-byte header
+    assert oracle.layout(**cfgd(4096, 4096, 128, 128, 4, 8))["total"] == \
+        256 + 4096 * (2048 + 32 * 2 + 32 * 4 + 8 * 4 + 8)
     T, d = 5, 520
     xb, rb, _ = wl.affine_pair(wl.AffineRecipe(T, d, 8), 0)
     rc, wire, _ = oracle.encode(xb, rb, **cfgd(T, d, 8, 8, 3, 7))
     h = wirefmt.header(wire)
-    assert h["magic"] == wirefmt.MAGIC and h["version"] == 1 and h["flags"] == 1
+    assert h["magic"] == wirefmt.MAGIC and h["version"] == 2 and h["flags"] == 1
     assert wirefmt.padding_is_zero(wire)
 
 
