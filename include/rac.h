@@ -249,6 +249,72 @@ rac_status rac_encode_pooled(const rac_config* cfg, const void* x, const void* r
                              const int32_t* seg_start, const float* fixed_steps, void* wire, size_t wire_cap,
                              void* xhat, rac_stream_t stream);
 
+/* ---- Offline calibration -----------------------------------------------
+ * The encoding subsection's opening paragraph, the last sentence of "Grouped
+ * Residual Quantization" and "Outlier Metadata and Calibration": offline, the
+ * sender's reconstruction path is run over candidate configurations (the
+ * groupings g_a and g_q, the bit width q and, with outliers, the count k_g)
+ * on a calibration sample, and a configuration meeting a quality target is
+ * kept while the packed bytes (values, scales, coefficients, outliers) are
+ * counted.  This library's reading: quality is the normalized squared error
+ * NMSE = sum (x - H-hat)^2 / sum x^2 of the sender reconstruction; cost is
+ * the configuration's whole wire (rac_wire_size); the choice is the fewest
+ * bytes among candidates with NMSE <= target (ties: smaller squared error,
+ * then the earlier candidate), or, when none meets the target, the smallest
+ * squared error (ties: fewer bytes, then the earlier candidate). */
+
+/* Host-only, pure.  Workspace bytes of rac_recon_error for `tokens` rows
+ * (24 bytes per group of 8 rows), or 0 for a negative count. */
+size_t rac_recon_error_workspace(int64_t tokens);
+
+/* Reconstruction error of a coded sample: stats (a DEVICE double[3])
+ * receives sum (x - H-hat)^2, sum x^2 and max |x - H-hat| in binary64 (each
+ * difference and square one rounded binary64 operation, the sums in a fixed
+ * order that does not depend on the device).
+ *   x         : bf16 [tokens][hidden], 16-byte aligned
+ *   xhat      : fp32 [tokens][hidden] (bf16 with RAC_FLAG_XHAT_BF16), 16-byte aligned
+ *   flags     : 0 or RAC_FLAG_XHAT_BF16
+ *   workspace : device scratch of rac_recon_error_workspace(tokens) bytes,
+ *               8-byte aligned, owned by the caller (its contents on return
+ *               are unspecified)
+ * hidden must be a positive multiple of 8.  RAC_ERR_INVALID / RAC_ERR_ALIGN /
+ * RAC_ERR_CAPACITY (workspace too small) are returned before any launch.  Two
+ * kernel launches on `stream`. */
+rac_status rac_recon_error(int64_t tokens, int32_t hidden, uint32_t flags, const void* x, const void* xhat,
+                           double* stats, void* workspace, size_t workspace_bytes, rac_stream_t stream);
+
+/* One candidate of rac_calibrate: the configuration in, the measurements out. */
+typedef struct {
+    rac_config cfg;      /* in: tokens and hidden of the sample; no RAC_FLAG_FIXED_STEP */
+    uint64_t wire_bytes; /* out: rac_wire_size(&cfg), the packed cost */
+    double sq_err;       /* out: sum (x - H-hat)^2 over the sample */
+    double sq_x;         /* out: sum x^2 */
+    double max_abs;      /* out: max |x - H-hat| */
+    double nmse;         /* out: sq_err / sq_x (0 when sq_x is 0) */
+    int32_t feasible;    /* out: nmse <= target */
+    int32_t reserved;
+} rac_candidate;
+
+/* Host-only, pure.  Workspace bytes rac_calibrate needs for these candidates
+ * (a reconstruction of the sample, the largest wire, the error partials and
+ * per-candidate sums), or 0 if a candidate is invalid, uses a step table,
+ * exceeds the kernels' 8192 channels or differs from the first in tokens or
+ * hidden. */
+size_t rac_calibrate_workspace(const rac_candidate* candidates, int32_t n);
+
+/* Offline calibration over n candidates (HOST array, filled in place) on the
+ * sample x against ref (DEVICE bf16 [tokens][hidden]; ref NULL = zero
+ * reference): for each candidate, rac_encode with the fused reconstruction,
+ * then rac_recon_error of that reconstruction; then the choice above,
+ * written to *chosen (a host int).  workspace: DEVICE memory of
+ * rac_calibrate_workspace() bytes, 256-byte aligned.  Unlike every other
+ * entry point, this offline routine reads its results back: it copies them
+ * to the host and synchronizes `stream` before returning.  Argument errors
+ * come before any launch; RAC_ERR_HIP if a launch, copy or the
+ * synchronization fails. */
+rac_status rac_calibrate(const void* x, const void* ref, rac_candidate* candidates, int32_t n, double target_nmse,
+                         void* workspace, size_t workspace_bytes, int32_t* chosen, rac_stream_t stream);
+
 /* ---- Reference selection for the prefill uplink (host only) ------------
  * Subsection "Repeated-Span Retrieval for Prefill Uplinks",
  * Eq. prefill-reference-selection.  A span index holds the token streams of

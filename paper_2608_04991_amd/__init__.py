@@ -25,6 +25,7 @@ __all__ = [
     "library", "library_path", "rac_wire_layout", "rac_wire_size", "rac_parse_header",
     "rac_encode", "rac_reconstruct", "rac_decode", "rac_encode_gather", "rac_decode_gather",
     "rac_status_string", "SpanIndex", "rac_encode_pooled", "rac_saturation_summary",
+    "rac_recon_error_workspace", "rac_recon_error", "rac_calibrate_workspace", "rac_calibrate",
 ]
 
 RAC_FLAG_FIXED_STEP = 1
@@ -58,6 +59,12 @@ class _Layout(ctypes.Structure):
                 ("off_codes", ctypes.c_uint64), ("off_outl", ctypes.c_uint64),
                 ("total", ctypes.c_uint64), ("off_ooff", ctypes.c_uint64),
                 ("off_sat", ctypes.c_uint64)]
+
+
+class _Candidate(ctypes.Structure):
+    _fields_ = [("cfg", _Config), ("wire_bytes", ctypes.c_uint64), ("sq_err", ctypes.c_double),
+                ("sq_x", ctypes.c_double), ("max_abs", ctypes.c_double), ("nmse", ctypes.c_double),
+                ("feasible", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 @dataclass(frozen=True)
@@ -124,6 +131,17 @@ def library():
         L.rac_saturation_summary.argtypes = [cp, vp, ctypes.c_size_t, ctypes.POINTER(ctypes.c_int64),
                                              ctypes.POINTER(ctypes.c_uint32)]
         L.rac_saturation_summary.restype = ctypes.c_int
+        L.rac_recon_error_workspace.argtypes = [ctypes.c_int64]
+        L.rac_recon_error_workspace.restype = ctypes.c_size_t
+        L.rac_recon_error.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, vp, vp, vp, vp,
+                                      ctypes.c_size_t, vp]
+        L.rac_recon_error.restype = ctypes.c_int
+        candp = ctypes.POINTER(_Candidate)
+        L.rac_calibrate_workspace.argtypes = [candp, ctypes.c_int32]
+        L.rac_calibrate_workspace.restype = ctypes.c_size_t
+        L.rac_calibrate.argtypes = [vp, vp, candp, ctypes.c_int32, ctypes.c_double, vp, ctypes.c_size_t,
+                                    ctypes.POINTER(ctypes.c_int32), vp]
+        L.rac_calibrate.restype = ctypes.c_int
         L.rac_status_string.argtypes = [ctypes.c_int]
         L.rac_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -334,3 +352,55 @@ def rac_encode_pooled(cfg: RacConfig, x, ref, seg_start, fixed_steps, wire, xhat
                                        _dev(fixed_steps, "fixed_steps", 4, _nsteps(cfg)), _dev(wire, "wire", 1, 0),
                                        cap, _dev(xhat, "xhat", _xhat_bytes(cfg), n), _stream(stream)),
            "rac_encode_pooled")
+
+
+def rac_recon_error_workspace(tokens: int) -> int:
+    return int(library().rac_recon_error_workspace(int(tokens)))
+
+
+def rac_recon_error(tokens: int, hidden: int, x, xhat, stats, workspace, flags: int = 0, stream=None,
+                    workspace_bytes: int | None = None) -> None:
+    """Reconstruction error of xhat against x into stats (device float64[3]:
+    sum of squared errors, sum of x^2, max |x - xhat|)."""
+    n = int(tokens) * int(hidden)
+    cap = workspace_bytes if workspace_bytes is not None else (
+        _nbytes(workspace) if workspace is not None and not isinstance(workspace, int) else 0)
+    _check(library().rac_recon_error(int(tokens), int(hidden), int(flags), _dev(x, "x", 2, n),
+                                     _dev(xhat, "xhat", 2 if flags & RAC_FLAG_XHAT_BF16 else 4, n),
+                                     _dev(stats, "stats", 8, 3), _dev(workspace, "workspace", 1, 0), cap,
+                                     _stream(stream)), "rac_recon_error")
+
+
+def _candidates(configs):
+    arr = (_Candidate * len(configs))()
+    for i, c in enumerate(configs):
+        arr[i].cfg = _Config(c.tokens, c.hidden, c.group_align, c.group_quant, c.bits, c.outlier_k, c.flags)
+    return arr
+
+
+def rac_calibrate_workspace(configs) -> int:
+    arr = _candidates(configs)
+    return int(library().rac_calibrate_workspace(arr, len(configs)))
+
+
+def rac_calibrate(x, ref, configs, target_nmse: float, workspace=None, stream=None):
+    """Offline calibration over candidate configurations (RacConfig with the
+    sample's tokens and hidden) on the device sample x against ref.  Returns
+    (chosen index, per-candidate dicts of wire_bytes, sq_err, sq_x, max_abs,
+    nmse, feasible).  Allocates the workspace with torch when none is given."""
+    arr = _candidates(configs)
+    need = int(library().rac_calibrate_workspace(arr, len(configs)))
+    if need == 0:
+        raise RacError(1, "rac_calibrate_workspace")
+    if workspace is None:
+        import torch
+        workspace = torch.empty(need, dtype=torch.uint8, device="cuda")
+    cap = _nbytes(workspace) if not isinstance(workspace, int) else need
+    n = configs[0].tokens * configs[0].hidden
+    chosen = ctypes.c_int32(-1)
+    _check(library().rac_calibrate(_dev(x, "x", 2, n), _dev(ref, "ref", 2, n), arr, len(configs),
+                                   float(target_nmse), _dev(workspace, "workspace", 1, need), cap,
+                                   ctypes.byref(chosen), _stream(stream)), "rac_calibrate")
+    res = [dict(cfg=configs[i], wire_bytes=int(a.wire_bytes), sq_err=a.sq_err, sq_x=a.sq_x, max_abs=a.max_abs,
+                nmse=a.nmse, feasible=bool(a.feasible)) for i, a in enumerate(arr)]
+    return int(chosen.value), res

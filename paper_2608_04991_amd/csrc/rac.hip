@@ -2044,6 +2044,92 @@ __global__ __launch_bounds__(kWave * kPoolWaves) void rac_pool_kernel(Args A, co
 }
 
 // ---------------------------------------------------------------------------
+// Reconstruction error of a coded sample (the offline calibration's quality
+// measure): sum (x - H-hat)^2, sum x^2 and max |x - H-hat| in binary64.
+// Every difference is one binary64 subtraction of the exact widened values,
+// every square one rounded multiply.  The sums have a fixed order whatever
+// the device: block b takes rows [8b, 8b + 8), thread t its 8-element pieces
+// t, t + 256, ... in sequence, then a pairwise tree over the 256 threads
+// gives the block's partial; a single block reduces the partials the same
+// way (thread t: partials t, t + 256, ..., then the tree).
+
+constexpr int kErrRows = 8;         // token rows per partial
+constexpr int kErrThreads = 256;
+
+struct ErrSums {
+    double se, sx, mx;
+};
+
+__device__ __forceinline__ ErrSums err_tree(ErrSums v, double (*sh)[kErrThreads]) {
+    const uint32_t t = threadIdx.x;
+    sh[0][t] = v.se;
+    sh[1][t] = v.sx;
+    sh[2][t] = v.mx;
+    __syncthreads();
+    for (uint32_t s = kErrThreads / 2; s > 0; s >>= 1) {
+        if (t < s) {
+            sh[0][t] = sh[0][t] + sh[0][t + s];
+            sh[1][t] = sh[1][t] + sh[1][t + s];
+            sh[2][t] = __builtin_fmax(sh[2][t], sh[2][t + s]);
+        }
+        __syncthreads();
+    }
+    return ErrSums{sh[0][0], sh[1][0], sh[2][0]};
+}
+
+__global__ __launch_bounds__(kErrThreads) void rac_error_kernel(const uint16_t* x, const void* xhat, int32_t bf16,
+                                                                uint32_t tokens, int32_t d, double* part) {
+    __shared__ double sh[3][kErrThreads];
+    const uint64_t row0 = (uint64_t)blockIdx.x * kErrRows;
+    const uint64_t rows = tokens - row0 < (uint64_t)kErrRows ? tokens - row0 : (uint64_t)kErrRows;
+    const uint64_t base = row0 * (uint64_t)d, n = rows * (uint64_t)d;  // n is a multiple of 8
+    ErrSums v{0.0, 0.0, 0.0};
+    for (uint64_t e = (uint64_t)threadIdx.x * 8u; e < n; e += (uint64_t)kErrThreads * 8u) {
+        float xf[8], hf[8];
+        widen8(*reinterpret_cast<const uint4*>(x + base + e), xf);
+        if (bf16) {
+            widen8(*reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(xhat) + base + e), hf);
+        } else {
+            const float4* hp = reinterpret_cast<const float4*>(static_cast<const float*>(xhat) + base + e);
+            const float4 a = hp[0], b = hp[1];
+            hf[0] = a.x; hf[1] = a.y; hf[2] = a.z; hf[3] = a.w;
+            hf[4] = b.x; hf[5] = b.y; hf[6] = b.z; hf[7] = b.w;
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const double xv = (double)xf[j];
+            const double dd = xv - (double)hf[j];
+            v.se = v.se + dd * dd;
+            v.sx = v.sx + xv * xv;
+            v.mx = __builtin_fmax(v.mx, __builtin_fabs(dd));
+        }
+    }
+    const ErrSums r = err_tree(v, sh);
+    if (threadIdx.x == 0) {
+        part[3u * blockIdx.x + 0u] = r.se;
+        part[3u * blockIdx.x + 1u] = r.sx;
+        part[3u * blockIdx.x + 2u] = r.mx;
+    }
+}
+
+__global__ __launch_bounds__(kErrThreads) void rac_error_final_kernel(const double* part, uint32_t nparts,
+                                                                      double* out) {
+    __shared__ double sh[3][kErrThreads];
+    ErrSums v{0.0, 0.0, 0.0};
+    for (uint32_t p = threadIdx.x; p < nparts; p += kErrThreads) {
+        v.se = v.se + part[3u * p + 0u];
+        v.sx = v.sx + part[3u * p + 1u];
+        v.mx = __builtin_fmax(v.mx, part[3u * p + 2u]);
+    }
+    const ErrSums r = err_tree(v, sh);
+    if (threadIdx.x == 0) {
+        out[0] = r.se;
+        out[1] = r.sx;
+        out[2] = r.mx;
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Host side
 
 bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
@@ -2580,6 +2666,159 @@ rac_status rac_reconstruct(const rac_config* cfg, const void* wire, const void* 
 rac_status rac_decode(const rac_config* cfg, const void* wire, const void* ref, const float* fixed_steps,
                       void* xhat, rac_stream_t stream) {
     return run_decode(cfg, wire, ref, fixed_steps, xhat, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+uint64_t err_parts(int64_t tokens) { return (uint64_t)((tokens + kErrRows - 1) / kErrRows); }
+
+bool error_args_ok(int64_t tokens, int32_t hidden, uint32_t flags) {
+    return tokens >= 0 && tokens <= 0x7FFFFFFFll && hidden >= 8 && hidden % 8 == 0 &&
+           (flags & ~uint32_t(RAC_FLAG_XHAT_BF16)) == 0 && (uint64_t)tokens * (uint64_t)hidden < (1ull << 40);
+}
+
+// The two launches of the error reduction, with `part` holding err_parts(T)
+// partials (3 doubles each).
+rac_status run_error(int64_t tokens, int32_t hidden, uint32_t flags, const void* x, const void* xhat,
+                     double* stats, double* part, hipStream_t stream) {
+    const uint32_t T = (uint32_t)tokens, P = (uint32_t)err_parts(tokens);
+    int32_t bf16 = (flags & RAC_FLAG_XHAT_BF16) ? 1 : 0;
+    const uint16_t* xp = static_cast<const uint16_t*>(x);
+    if (P > 0) {
+        uint32_t rows = T;
+        void* a[] = {(void*)&xp, (void*)&xhat, (void*)&bf16, (void*)&rows, (void*)&hidden, (void*)&part};
+        if (hipLaunchKernel(reinterpret_cast<const void*>(rac_error_kernel), dim3(P), dim3(kErrThreads), a, 0,
+                            stream) != hipSuccess)
+            return RAC_ERR_HIP;
+    }
+    uint32_t np = P;
+    void* b[] = {(void*)&part, (void*)&np, (void*)&stats};
+    if (hipLaunchKernel(reinterpret_cast<const void*>(rac_error_final_kernel), dim3(1), dim3(kErrThreads), b, 0,
+                        stream) != hipSuccess)
+        return RAC_ERR_HIP;
+    return RAC_OK;
+}
+
+rac_status check_error_call(int64_t tokens, int32_t hidden, uint32_t flags, const void* x, const void* xhat,
+                            const double* stats) {
+    if (!error_args_ok(tokens, hidden, flags) || !stats || (tokens > 0 && (!x || !xhat))) return RAC_ERR_INVALID;
+    if (!aligned(x, 16) || !aligned(xhat, 16) || !aligned(stats, 8)) return RAC_ERR_ALIGN;
+    return RAC_OK;
+}
+
+uint64_t calib_xhat_bytes(const rac_config& c) {
+    return (uint64_t)c.tokens * (uint64_t)c.hidden * ((c.flags & RAC_FLAG_XHAT_BF16) ? 2u : 4u);
+}
+
+// Workspace of rac_calibrate: x-hat, wire, error partials, per-candidate
+// sums, each piece 256-byte aligned.  0 when the candidates are invalid.
+struct CalibSpace {
+    uint64_t xhat, wire, part, stats, total;
+};
+
+bool calib_space(const rac_candidate* c, int32_t n, CalibSpace* out) {
+    if (!c || n < 1) return false;
+    uint64_t xh = 0, wmax = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        const rac_config& k = c[i].cfg;
+        if (!config_valid(&k) || k.tokens != c[0].cfg.tokens || k.hidden != c[0].cfg.hidden ||
+            (k.flags & RAC_FLAG_FIXED_STEP) || k.hidden > kMaxWaves * kChunk)
+            return false;
+        const uint64_t w = sizes_of(&k).L.total;
+        wmax = w > wmax ? w : wmax;
+        const uint64_t b = calib_xhat_bytes(k);
+        xh = b > xh ? b : xh;
+    }
+    out->xhat = 0;
+    out->wire = up256(xh);
+    out->part = out->wire + up256(wmax);
+    out->stats = out->part + up256(err_parts(c[0].cfg.tokens) * 24u);
+    out->total = out->stats + up256((uint64_t)n * 24u);
+    return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t rac_recon_error_workspace(int64_t tokens) {
+    if (tokens < 0 || tokens > 0x7FFFFFFFll) return 0;
+    return (size_t)(err_parts(tokens) * 24u);
+}
+
+rac_status rac_recon_error(int64_t tokens, int32_t hidden, uint32_t flags, const void* x, const void* xhat,
+                           double* stats, void* workspace, size_t workspace_bytes, rac_stream_t stream) {
+    rac_status st = check_error_call(tokens, hidden, flags, x, xhat, stats);
+    if (st != RAC_OK) return st;
+    if (workspace_bytes < err_parts(tokens) * 24u || (tokens > 0 && !workspace)) return RAC_ERR_CAPACITY;
+    if (!aligned(workspace, 8)) return RAC_ERR_ALIGN;
+    return run_error(tokens, hidden, flags, x, xhat, stats, static_cast<double*>(workspace), stream);
+}
+
+size_t rac_calibrate_workspace(const rac_candidate* candidates, int32_t n) {
+    CalibSpace sp;
+    return calib_space(candidates, n, &sp) ? (size_t)sp.total : 0;
+}
+
+rac_status rac_calibrate(const void* x, const void* ref, rac_candidate* candidates, int32_t n, double target_nmse,
+                         void* workspace, size_t workspace_bytes, int32_t* chosen, rac_stream_t stream) {
+    CalibSpace sp;
+    if (!calib_space(candidates, n, &sp) || !chosen || !x || !(target_nmse >= 0.0)) return RAC_ERR_INVALID;
+    if (!workspace || workspace_bytes < sp.total) return RAC_ERR_CAPACITY;
+    if (!aligned(workspace, 256) || !aligned(x, 16) || (ref && !aligned(ref, 16))) return RAC_ERR_ALIGN;
+    uint8_t* ws = static_cast<uint8_t*>(workspace);
+    void* xh = ws + sp.xhat;
+    void* wire = ws + sp.wire;
+    double* part = reinterpret_cast<double*>(ws + sp.part);
+    double* sums = reinterpret_cast<double*>(ws + sp.stats);
+    const uint64_t cap = sp.part - sp.wire;
+    for (int32_t i = 0; i < n; ++i) {
+        const rac_config& c = candidates[i].cfg;
+        rac_status st = run_encode(&c, x, ref, nullptr, wire, cap, xh, stream, false, 0, nullptr);
+        if (st != RAC_OK) return st;
+        st = run_error(c.tokens, c.hidden, c.flags & RAC_FLAG_XHAT_BF16, x, xh, sums + 3 * i, part, stream);
+        if (st != RAC_OK) return st;
+    }
+    // (an offline routine: the results are read back and the stream is
+    // synchronized, in chunks of a small host buffer)
+    double host[3 * 64];
+    for (int32_t i0 = 0; i0 < n; i0 += 64) {
+        const int32_t m = n - i0 < 64 ? n - i0 : 64;
+        if (hipMemcpyAsync(host, sums + 3 * i0, sizeof(double) * 3u * (size_t)m, hipMemcpyDeviceToHost, stream) !=
+                hipSuccess ||
+            hipStreamSynchronize(stream) != hipSuccess)
+            return RAC_ERR_HIP;
+        for (int32_t j = 0; j < m; ++j) {
+            rac_candidate& k = candidates[i0 + j];
+            k.sq_err = host[3 * j];
+            k.sq_x = host[3 * j + 1];
+            k.max_abs = host[3 * j + 2];
+            k.nmse = k.sq_x > 0.0 ? k.sq_err / k.sq_x : 0.0;
+            k.wire_bytes = sizes_of(&k.cfg).L.total;
+            k.feasible = k.nmse <= target_nmse ? 1 : 0;
+        }
+    }
+    // fewest wire bytes among the feasible (ties: smaller error, earlier);
+    // with none feasible, the smallest error (ties: fewer bytes, earlier)
+    int32_t best = -1;
+    bool any = false;
+    for (int32_t i = 0; i < n; ++i) any = any || candidates[i].feasible;
+    for (int32_t i = 0; i < n; ++i) {
+        const rac_candidate& k = candidates[i];
+        if (any && !k.feasible) continue;
+        if (best < 0) {
+            best = i;
+            continue;
+        }
+        const rac_candidate& b = candidates[best];
+        const bool better = any ? (k.wire_bytes < b.wire_bytes || (k.wire_bytes == b.wire_bytes && k.sq_err < b.sq_err))
+                                : (k.sq_err < b.sq_err || (k.sq_err == b.sq_err && k.wire_bytes < b.wire_bytes));
+        if (better) best = i;
+    }
+    *chosen = best;
+    return RAC_OK;
 }
 
 const char* rac_status_string(rac_status s) {

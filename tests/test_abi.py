@@ -38,7 +38,8 @@ def test_exports_every_declared_symbol(lib):
                           "rac_reconstruct", "rac_decode", "rac_encode_gather", "rac_decode_gather",
                           "rac_status_string", "rac_span_index_create", "rac_span_index_destroy",
                           "rac_span_index_add", "rac_span_select", "rac_encode_pooled",
-                          "rac_saturation_summary"}
+                          "rac_saturation_summary", "rac_recon_error_workspace", "rac_recon_error",
+                          "rac_calibrate_workspace", "rac_calibrate"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -296,3 +297,27 @@ def test_binding_checks_tensor_arguments_before_the_call(lib, monkeypatch):
     with pytest.raises(ValueError):
         rac.rac_decode(cfg, _FakeTensor(100, 1), ok["ref"], None, ok["xhat"], stream=0)
     assert len(called) == 1
+
+
+def test_calibration_argument_errors_are_synchronous(lib):
+    L = rac.library()
+    # error reduction: hidden not a multiple of 8, bad flags, misalignment, small workspace
+    err = lambda T=16, d=512, flags=0, x=FAKE, xh=FAKE, st=FAKE, ws=FAKE, cap=1 << 20: L.rac_recon_error(
+        T, d, flags, x, xh, st, ws, cap, 0)
+    assert err(d=516) == 1 and err(flags=rac.RAC_FLAG_FIXED_STEP) == 1 and err(st=None) == 1
+    assert err(x=FAKE + 2) == 2 and err(xh=FAKE + 8) == 2 and err(st=FAKE + 4) == 2
+    assert err(cap=rac.rac_recon_error_workspace(16) - 1) == 3
+    assert rac.rac_recon_error_workspace(16) == 48 and rac.rac_recon_error_workspace(17) == 72
+    # calibration: candidates must share the sample's shape and use no step table
+    good = [rac.RacConfig(64, 512, 64, 64, 4), rac.RacConfig(64, 512, 128, 128, 2, 1, rac.RAC_FLAG_GROUP_OUTLIERS)]
+    assert rac.rac_calibrate_workspace(good) > 64 * 512 * 4
+    assert rac.rac_calibrate_workspace(good + [rac.RacConfig(32, 512, 64, 64, 4)]) == 0
+    assert rac.rac_calibrate_workspace(good + [rac.RacConfig(64, 512, 64, 64, 4, 0, rac.RAC_FLAG_FIXED_STEP)]) == 0
+    arr = rac._candidates(good)
+    ch = ctypes.c_int32(-7)
+    need = rac.rac_calibrate_workspace(good)
+    cal = lambda x=FAKE, tgt=0.01, ws=FAKE, cap=need, chosen=ctypes.byref(ch): L.rac_calibrate(
+        x, FAKE, arr, 2, tgt, ws, cap, chosen, 0)
+    assert cal(tgt=-1.0) == 1 and cal(tgt=float("nan")) == 1 and cal(x=None) == 1 and cal(chosen=None) == 1
+    assert cal(cap=need - 1) == 3 and cal(ws=FAKE + 16) == 2 and cal(x=FAKE + 2) == 2
+    assert ch.value == -7
