@@ -283,6 +283,21 @@ size_t rac_recon_error_workspace(int64_t tokens);
 rac_status rac_recon_error(int64_t tokens, int32_t hidden, uint32_t flags, const void* x, const void* xhat,
                            double* stats, void* workspace, size_t workspace_bytes, rac_stream_t stream);
 
+/* rac_recon_error for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same two kernel launches and the same result, bit for bit,
+ * but the partials live in a fixed array inside the library (384 KiB per
+ * device, held until the process ends) instead of a workspace.  This call
+ * allocates nothing: on its first call on a device it looks up that array's
+ * address (with the device current) and keeps it.  tokens is limited to
+ * 131072 (RAC_ERR_CAPACITY beyond, before any launch).  Every call on one
+ * device shares the array: calls that overlap on one device (different
+ * streams, or different host threads) race and give unspecified results;
+ * calls ordered on one stream are fine, and nothing left by an earlier call
+ * is read.  Other arguments and errors as rac_recon_error. */
+rac_status rac_recon_error_noalloc(int64_t tokens, int32_t hidden, uint32_t flags, const void* x, const void* xhat,
+                                   double* stats, rac_stream_t stream);
+
 /* One candidate of rac_calibrate: the configuration in, the measurements out. */
 typedef struct {
     rac_config cfg;      /* in: tokens and hidden of the sample; no RAC_FLAG_FIXED_STEP */

@@ -2129,6 +2129,18 @@ __global__ __launch_bounds__(kErrThreads) void rac_error_final_kernel(const doub
     }
 }
 
+}  // namespace
+
+// The allocation-free variant of the error reduction keeps its partials in
+// this array instead of a caller workspace: one copy per device, held until
+// the process ends.  Host code never uses the name itself (on the host it is
+// only a stand-in for the device symbol); it uses the device address that
+// hipGetSymbolAddress gives for the current device.
+constexpr uint32_t kScratchParts = 16384;  // partials of 8 rows: up to 131072 token rows
+static __device__ __align__(256) double scratch[3 * kScratchParts];
+
+namespace {
+
 // ---------------------------------------------------------------------------
 // Host side
 
@@ -2755,6 +2767,46 @@ rac_status rac_recon_error(int64_t tokens, int32_t hidden, uint32_t flags, const
     if (workspace_bytes < err_parts(tokens) * 24u || (tokens > 0 && !workspace)) return RAC_ERR_CAPACITY;
     if (!aligned(workspace, 8)) return RAC_ERR_ALIGN;
     return run_error(tokens, hidden, flags, x, xhat, stats, static_cast<double*>(workspace), stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+double* g_scratch_dev[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept.
+rac_status scratch_address(double** out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return RAC_ERR_HIP;
+    if (dev < 0 || dev >= kMaxDevices) return RAC_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return RAC_ERR_HIP;
+        g_scratch_dev[dev] = static_cast<double*>(p);
+    }
+    *out = g_scratch_dev[dev];
+    return RAC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+rac_status rac_recon_error_noalloc(int64_t tokens, int32_t hidden, uint32_t flags, const void* x, const void* xhat,
+                                   double* stats, rac_stream_t stream) {
+    rac_status st = check_error_call(tokens, hidden, flags, x, xhat, stats);
+    if (st != RAC_OK) return st;
+    if (err_parts(tokens) > kScratchParts) return RAC_ERR_CAPACITY;
+    double* part = nullptr;
+    if ((st = scratch_address(&part)) != RAC_OK) return st;
+    // (every partial the final launch reads is written by the first, so
+    // nothing left by an earlier call is read)
+    return run_error(tokens, hidden, flags, x, xhat, stats, part, stream);
 }
 
 size_t rac_calibrate_workspace(const rac_candidate* candidates, int32_t n) {

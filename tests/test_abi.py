@@ -39,7 +39,7 @@ def test_exports_every_declared_symbol(lib):
                           "rac_status_string", "rac_span_index_create", "rac_span_index_destroy",
                           "rac_span_index_add", "rac_span_select", "rac_encode_pooled",
                           "rac_saturation_summary", "rac_recon_error_workspace", "rac_recon_error",
-                          "rac_calibrate_workspace", "rac_calibrate"}
+                          "rac_calibrate_workspace", "rac_calibrate", "rac_recon_error_noalloc"}
     for n in names:
         assert hasattr(lib, n), n
 
