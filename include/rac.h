@@ -43,14 +43,15 @@
  *     enqueued.  RAC_ERR_HIP reports a failed kernel launch.  Kernels never
  *     trap; inputs must be finite (results for NaN/Inf inputs are unspecified
  *     but every memory access stays in bounds).
- *   - Saturation: coefficients, scales and outlier values are fp16.  A value
- *     whose fp16 rounding overflows (|v| >= 65520) is stored as +-65504, and
- *     a quantization group whose largest |E^d| exceeds 65504 * Qmax gets the
- *     scale 65504 with clipped codes (the no-clipping guarantee of
- *     Eq. residual-quantization fails there).  Each is reported, per token
- *     row and 512-channel block, in the wire's saturation section, which the
- *     encode writes asynchronously like the rest of the wire
- *     (rac_saturation_summary reads a host copy of it).
+ *   - Saturation is reported in the wire itself.  Coefficients, scales and
+ *     outlier values are fp16 fields holding the IEEE result of their
+ *     rounding: a value whose round-to-nearest-even overflows (|v| >= 65520)
+ *     is stored as +-infinity, and the scale of a quantization group whose
+ *     largest |E^d| exceeds 65504 * Qmax (no finite fp16 step covers it, so
+ *     the no-clipping guarantee of Eq. residual-quantization fails and the
+ *     codes clip) is +infinity.  Both ends compute with +-65504 wherever a
+ *     field holds +-infinity, so the reconstruction stays finite.
+ *     rac_saturation_summary reads a host copy of a wire for these marks.
  *
  * Wire format (little-endian, self-describing, all padding zero):
  *   header (256 B): u32 magic 'RAC1', u16 version 2, u16 flags (1 per-token
@@ -60,10 +61,9 @@
  *     u8 scale fmt (1 = fp16, 0 = absent), u8 outlier fmt (1 = u16 channel in
  *     the low half and fp16 value in the high half of a u32, 2 = per-group
  *     fp16 values and u8 offsets, 0 = absent), u16 k, u16 0, then u64 offsets
- *     of the coef, scale, code and outlier sections, the total size, the
- *     offset of the per-group offset array (0 without per-group outliers) and
- *     the offset of the saturation report; sections start at 256-byte
- *     boundaries.
+ *     of the coef, scale, code and outlier sections, the total size and the
+ *     offset of the per-group offset array (0 without per-group outliers);
+ *     sections start at 256-byte boundaries.
  *   coef   : fp16 [tokens][hidden/g_a][2]   (alpha, beta)
  *   scale  : fp16 [tokens][hidden/g_q]      (absent with RAC_FLAG_FIXED_STEP)
  *   codes  : u8   [tokens][hidden*bits/8]   channel c of a row occupies bits
@@ -75,14 +75,8 @@
  *   oval   : fp16 [tokens][hidden/g_q][k_g] at the outlier offset
  *   ooff   : u8   [tokens][hidden/g_q][k_g] in-group offsets, ascending within
  *            each group, aligned with oval
- *   sat    : u8   [tokens][ceil(hidden/512)]    saturation report, the last
- *            section: one byte per token row and 512-channel block, bit 1 =
- *            an alpha* or beta* of an alignment group whose first channel is
- *            in the block overflowed fp16, bit 2 = a quantization group whose
- *            first channel is in the block has max|E^d| > 65504 * Qmax (scale
- *            65504, codes clipped; never set with RAC_FLAG_FIXED_STEP, whose
- *            codes clip by design), bit 4 = an outlier value of a channel in
- *            the block overflowed fp16; 0 everywhere for ordinary activations
+ *   every fp16 field may hold +-infinity, which stands for +-65504 and
+ *   marks a saturation (see above)
  */
 #ifndef RAC_H
 #define RAC_H
@@ -136,7 +130,6 @@ typedef struct {
 typedef struct {
     uint64_t off_coef, off_scale, off_codes, off_outl, total; /* bytes */
     uint64_t off_ooff; /* per-group outlier offsets (0 without that mode) */
-    uint64_t off_sat;  /* saturation report, tokens * ceil(hidden / 512) bytes */
 } rac_layout;
 
 /* Host-only, pure.  Section offsets and total wire size for `cfg`.
@@ -155,13 +148,13 @@ size_t rac_wire_size(const rac_config* cfg);
 rac_status rac_parse_header(const void* header_host, size_t len, rac_config* out,
                             int* zero_ref);
 
-/* Host-only, pure.  Summary of a saturation report the caller has copied to
- * HOST memory (the tokens * ceil(hidden / 512) bytes at layout.off_sat of a
- * wire produced for `cfg`; len must be at least that): `rows` (may be NULL)
- * receives the number of token rows with any bit set and `bits` (may be
- * NULL) the OR of all bytes.  RAC_ERR_INVALID for a bad configuration or a
- * short buffer. */
-rac_status rac_saturation_summary(const rac_config* cfg, const void* sat_host, size_t len, int64_t* rows,
+/* Host-only, pure.  Saturation marks of a wire produced for `cfg` that the
+ * caller has copied to HOST memory (len >= rac_wire_size(cfg)): `rows` (may
+ * be NULL) receives the number of token rows with any fp16 field holding
+ * +-infinity, `bits` (may be NULL) the OR over the wire of 1 (an alpha or
+ * beta), 2 (a scale; codes clipped) and 4 (an outlier value).  RAC_ERR_INVALID
+ * for a bad configuration or a short buffer. */
+rac_status rac_saturation_summary(const rac_config* cfg, const void* wire_host, size_t len, int64_t* rows,
                                   uint32_t* bits);
 
 /* Sender side: encode x against ref into `wire`, and optionally write the

@@ -45,8 +45,7 @@ class _Cfg(ctypes.Structure):
 class _Layout(ctypes.Structure):
     _fields_ = [("off_coef", ctypes.c_uint64), ("off_scale", ctypes.c_uint64),
                 ("off_codes", ctypes.c_uint64), ("off_outl", ctypes.c_uint64),
-                ("total", ctypes.c_uint64), ("off_ooff", ctypes.c_uint64),
-                ("off_sat", ctypes.c_uint64)]
+                ("total", ctypes.c_uint64), ("off_ooff", ctypes.c_uint64)]
 
 
 class Moments(ctypes.Structure):
@@ -71,6 +70,10 @@ def _load(path: str):
     L.orc_f16_to_f32.restype = ctypes.c_float
     L.orc_f16_rne_sat.argtypes = [ctypes.c_float]
     L.orc_f16_rne_sat.restype = ctypes.c_uint16
+    L.orc_f16_rne.argtypes = [ctypes.c_float]
+    L.orc_f16_rne.restype = ctypes.c_uint16
+    L.orc_f16_wire.argtypes = [ctypes.c_uint16]
+    L.orc_f16_wire.restype = ctypes.c_float
     L.orc_scale_roundup.argtypes = [ctypes.c_float, ctypes.c_int32]
     L.orc_scale_roundup.restype = ctypes.c_uint16
     L.orc_step_roundup.argtypes = [ctypes.c_float]
@@ -179,6 +182,14 @@ def f16_to_f32(h: int) -> float:
 
 def f16_rne_sat(v: float) -> int:
     return int(lib().orc_f16_rne_sat(float(v)))
+
+
+def f16_rne(v: float) -> int:
+    return int(lib().orc_f16_rne(float(v)))
+
+
+def f16_wire(h: int) -> float:
+    return float(lib().orc_f16_wire(int(h)))
 
 
 def scale_roundup(m: float, qmax: int) -> int:

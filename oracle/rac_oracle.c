@@ -44,13 +44,10 @@
 #define ORC_VERSION 2u
 #define ORC_HDR 256u
 #define ORC_F16_MAX_BITS 0x7BFFu
-/* Saturation report: one byte per 512-channel block of every row. */
-#define ORC_SAT_BLOCK 512
-#define ORC_SAT_COEF 1u   /* an alpha* or beta* of a group starting in the block overflowed fp16 */
-#define ORC_SAT_SCALE 2u  /* no fp16 scale covers a group starting in the block: codes clip */
-#define ORC_SAT_OUTLIER 4u /* an outlier value of a channel in the block overflowed fp16 */
+#define ORC_F16_INF_BITS 0x7C00u
 /* The smallest magnitude that round-to-nearest-even fp16 rounds to infinity:
- * the midpoint between 65504 and the next step up, 65536. */
+ * the midpoint between 65504 and the next step up, 65536 (a tie, which goes
+ * to the even significand, i.e. past the range). */
 #define ORC_F16_OVERFLOW 65520.0f
 
 /* ------------------------------------------------------------------------ */
@@ -109,6 +106,21 @@ uint16_t orc_f16_rne_sat(float f) {
     return (uint16_t)(sign | p);
 }
 
+/* IEEE round-to-nearest-even fp32 -> fp16 with overflow to +-infinity: the
+ * rounding the wire's fp16 fields hold, so a saturation is visible there. */
+uint16_t orc_f16_rne(float f) {
+    if (fabsf(f) >= ORC_F16_OVERFLOW) return (uint16_t)((signbit(f) ? 0x8000u : 0u) | ORC_F16_INF_BITS);
+    return orc_f16_rne_sat(f);
+}
+
+/* The value a wire fp16 field stands for in the arithmetic of both ends:
+ * +-infinity (an overflowed rounding) counts as +-65504. */
+float orc_f16_wire(uint16_t h) {
+    const float v = orc_f16_to_f32(h);
+    const float m = orc_f16_to_f32(ORC_F16_MAX_BITS);
+    return v > m ? m : (v < -m ? -m : v);
+}
+
 uint16_t orc_f32_to_bf16(float f) {
     uint32_t u;
     memcpy(&u, &f, sizeof u);
@@ -134,7 +146,8 @@ uint16_t orc_scale_roundup(float m, int32_t qmax) {
     /* value(h)*qmax is exact in binary32 (11-bit by 7-bit significands), so
      * the predicate is an exact comparison and is monotone in h */
     const float q = (float)qmax;
-    if (orc_f16_to_f32(ORC_F16_MAX_BITS) * q < m) return ORC_F16_MAX_BITS;
+    /* no finite fp16 covers m: the upward rounding goes past the range */
+    if (orc_f16_to_f32(ORC_F16_MAX_BITS) * q < m) return ORC_F16_INF_BITS;
     uint32_t lo = 1, hi = ORC_F16_MAX_BITS;
     while (lo < hi) {
         uint32_t mid = (lo + hi) / 2;
@@ -262,7 +275,6 @@ static int orc_valid(const orc_config* c) {
 
 static uint64_t up256(uint64_t v) { return (v + 255u) & ~(uint64_t)255u; }
 
-static int32_t orc_sat_blocks(int32_t d) { return (d + ORC_SAT_BLOCK - 1) / ORC_SAT_BLOCK; }
 
 int orc_layout_of(const orc_config* cfg, orc_layout* out) {
     if (!orc_valid(cfg) || !out) return ORC_ERR_INVALID;
@@ -275,19 +287,15 @@ int orc_layout_of(const orc_config* cfg, orc_layout* out) {
     out->off_scale = up256(out->off_coef + coef);
     out->off_codes = up256(out->off_scale + scale);
     out->off_outl = up256(out->off_codes + codes);
-    uint64_t end;
     if (cfg->flags & ORC_FLAG_GROUP_OUTLIERS) {
         /* fp16 values [T][d/g_q][k_g], then u8 offsets [T][d/g_q][k_g] */
         const uint64_t n = T * (d / (uint64_t)cfg->group_quant) * (uint64_t)cfg->outlier_k;
         out->off_ooff = up256(out->off_outl + 2u * n);
-        end = out->off_ooff + n;
+        out->total = up256(out->off_ooff + n);
     } else {
         out->off_ooff = 0;
-        end = out->off_outl + T * (uint64_t)cfg->outlier_k * 4u;
+        out->total = up256(out->off_outl + T * (uint64_t)cfg->outlier_k * 4u);
     }
-    /* saturation report: u8 [T][ceil(d/512)] */
-    out->off_sat = up256(end);
-    out->total = up256(out->off_sat + T * (uint64_t)orc_sat_blocks(cfg->hidden));
     return ORC_OK;
 }
 
@@ -343,7 +351,6 @@ static void orc_write_header(const orc_config* cfg, const orc_layout* L, int zer
     put64(w + 56, L->off_outl);
     put64(w + 64, L->total);
     put64(w + 72, L->off_ooff);
-    put64(w + 80, L->off_sat);
 }
 
 /* q-bit two's complement code of channel c goes to bits [c*q, c*q+q) of the
@@ -412,7 +419,6 @@ static int orc_encode_impl(const orc_config* cfg, const uint16_t* x, const uint1
     uint16_t* oval = (uint16_t*)calloc((size_t)d, sizeof(uint16_t));
     uint8_t* is_out = (uint8_t*)calloc((size_t)d, 1);
     uint16_t sel[64];
-    const int32_t nsat = orc_sat_blocks(d);
 
     for (int64_t t = 0; t < T; ++t) {
         /* step 1: widen the row (exact) */
@@ -424,7 +430,6 @@ static int orc_encode_impl(const orc_config* cfg, const uint16_t* x, const uint1
          * fp16, then the aligned reference and residual (Eq. aligned-residual)
          * formed with the serialized coefficients */
         uint8_t* coef = wire + L.off_coef + (uint64_t)t * (uint64_t)(d / ga) * 4u;
-        uint8_t* sat = wire + L.off_sat + (uint64_t)t * (uint64_t)nsat;
         for (int32_t j = 0; j < d / ga; ++j) {
             float as, bs;
             if (pooled) {
@@ -433,13 +438,11 @@ static int orc_encode_impl(const orc_config* cfg, const uint16_t* x, const uint1
             } else {
                 orc_fit_group(r + j * ga, xv + j * ga, ga, &as, &bs);
             }
-            const uint16_t ah = orc_f16_rne_sat(as), bh = orc_f16_rne_sat(bs);
-            /* Round_wire overflowed: the field holds +-65504 instead of +-inf */
-            if (fabsf(as) >= ORC_F16_OVERFLOW || fabsf(bs) >= ORC_F16_OVERFLOW)
-                sat[(j * ga) / ORC_SAT_BLOCK] |= (uint8_t)ORC_SAT_COEF;
+            /* Round_wire: fp16 (+-infinity past the range, read as +-65504) */
+            const uint16_t ah = orc_f16_rne(as), bh = orc_f16_rne(bs);
             put16(coef + 4 * j, ah);
             put16(coef + 4 * j + 2, bh);
-            const float a = orc_f16_to_f32(ah), b0 = orc_f16_to_f32(bh);
+            const float a = orc_f16_wire(ah), b0 = orc_f16_wire(bh);
             for (int32_t c = j * ga; c < (j + 1) * ga; ++c) {
                 rt[c] = fmaf(a, r[c], b0);
                 e[c] = xv[c] - rt[c];
@@ -458,8 +461,7 @@ static int orc_encode_impl(const orc_config* cfg, const uint16_t* x, const uint1
                 orc_topk_row(e + g * gq, gq, k, sel); /* ascending in-group offsets */
                 for (int32_t i = 0; i < k; ++i) {
                     const int32_t c = g * gq + sel[i];
-                    oval[c] = orc_f16_rne_sat(e[c]);
-                    if (fabsf(e[c]) >= ORC_F16_OVERFLOW) sat[c / ORC_SAT_BLOCK] |= (uint8_t)ORC_SAT_OUTLIER;
+                    oval[c] = orc_f16_rne(e[c]);
                     is_out[c] = 1;
                     ed[c] = 0.0f;
                     put16(vrow + 2 * ((uint64_t)g * k + i), oval[c]);
@@ -471,8 +473,7 @@ static int orc_encode_impl(const orc_config* cfg, const uint16_t* x, const uint1
             uint8_t* ol = wire + L.off_outl + (uint64_t)t * (uint64_t)k * 4u;
             for (int32_t i = 0; i < k; ++i) {
                 const int32_t c = sel[i];
-                oval[c] = orc_f16_rne_sat(e[c]); /* O-hat = Round_FP16(O) */
-                if (fabsf(e[c]) >= ORC_F16_OVERFLOW) sat[c / ORC_SAT_BLOCK] |= (uint8_t)ORC_SAT_OUTLIER;
+                oval[c] = orc_f16_rne(e[c]); /* O-hat = Round_FP16(O) */
                 is_out[c] = 1;
                 ed[c] = 0.0f;
                 put32(ol + 4 * i, (uint32_t)c | ((uint32_t)oval[c] << 16));
@@ -491,12 +492,9 @@ static int orc_encode_impl(const orc_config* cfg, const uint16_t* x, const uint1
                 for (int32_t c = g * gq; c < (g + 1) * gq; ++c)
                     if (fabsf(ed[c]) > m) m = fabsf(ed[c]);
                 sh = (m == 0.0f) ? 0u : orc_scale_roundup(m, qmax); /* 0 = zero group */
-                /* no fp16 step covers the maximum (65504 * Qmax is exact) */
-                if (m > orc_f16_to_f32(ORC_F16_MAX_BITS) * (float)qmax)
-                    sat[(g * gq) / ORC_SAT_BLOCK] |= (uint8_t)ORC_SAT_SCALE;
                 put16(srow + 2 * g, sh);
             }
-            const float s = orc_f16_to_f32(sh);
+            const float s = orc_f16_wire(sh);
             for (int32_t c = g * gq; c < (g + 1) * gq; ++c) {
                 int32_t q = 0;
                 if (sh != 0u) { /* a zero group skips the division */
@@ -508,7 +506,7 @@ static int orc_encode_impl(const orc_config* cfg, const uint16_t* x, const uint1
                 }
                 orc_put_code(crow, c, bits, q);
                 if (xhat) {
-                    const float eh = is_out[c] ? orc_f16_to_f32(oval[c]) : (float)q * s;
+                    const float eh = is_out[c] ? orc_f16_wire(oval[c]) : (float)q * s;
                     orc_store_xhat(cfg, xhat, t * d + c, rt[c] + eh);
                 }
             }
@@ -659,7 +657,7 @@ int orc_decode(const orc_config* cfg, const uint8_t* wire, const uint16_t* ref,
         get16(wire + 28) != (uint16_t)cfg->outlier_k || get64(wire + 32) != L.off_coef ||
         get64(wire + 40) != L.off_scale || get64(wire + 48) != L.off_codes ||
         get64(wire + 56) != L.off_outl || get64(wire + 64) != L.total ||
-        get64(wire + 72) != L.off_ooff || get64(wire + 80) != L.off_sat)
+        get64(wire + 72) != L.off_ooff)
         return ORC_ERR_FORMAT;
 
     const int64_t T = cfg->tokens;
@@ -675,7 +673,7 @@ int orc_decode(const orc_config* cfg, const uint8_t* wire, const uint16_t* ref,
         /* dequantized dense residual DQ(q; s) */
         for (int32_t g = 0; g < d / gq; ++g) {
             const uint16_t sh = fixed ? orc_step_roundup(steps[g]) : get16(srow + 2 * g);
-            const float s = orc_f16_to_f32(sh);
+            const float s = orc_f16_wire(sh);
             for (int32_t c = g * gq; c < (g + 1) * gq; ++c)
                 eh[c] = (float)orc_get_code(crow, c, bits) * s;
         }
@@ -691,7 +689,7 @@ int orc_decode(const orc_config* cfg, const uint8_t* wire, const uint16_t* ref,
                         free(eh);
                         return ORC_ERR_FORMAT;
                     }
-                    eh[g * gq + (int32_t)o] = orc_f16_to_f32(get16(vrow + 2 * ((uint64_t)g * k + i)));
+                    eh[g * gq + (int32_t)o] = orc_f16_wire(get16(vrow + 2 * ((uint64_t)g * k + i)));
                 }
             }
         } else if (k > 0) {
@@ -703,13 +701,13 @@ int orc_decode(const orc_config* cfg, const uint8_t* wire, const uint16_t* ref,
                     free(eh);
                     return ORC_ERR_FORMAT;
                 }
-                eh[c] = orc_f16_to_f32((uint16_t)(w >> 16));
+                eh[c] = orc_f16_wire((uint16_t)(w >> 16));
             }
         }
         /* H-hat = R-tilde + E-hat with R-tilde from the serialized alignment */
         for (int32_t j = 0; j < d / ga; ++j) {
-            const float a = orc_f16_to_f32(get16(coef + 4 * j));
-            const float b0 = orc_f16_to_f32(get16(coef + 4 * j + 2));
+            const float a = orc_f16_wire(get16(coef + 4 * j));
+            const float b0 = orc_f16_wire(get16(coef + 4 * j + 2));
             for (int32_t c = j * ga; c < (j + 1) * ga; ++c) {
                 const float r = ref ? orc_bf16_to_f32(ref[t * d + c]) : 0.0f;
                 const float rt = fmaf(a, r, b0);

@@ -53,15 +53,12 @@ typedef struct {
 
 /* Byte offsets of the wire sections (all 256-byte aligned).  off_ooff is the
  * in-group offset array of the per-group outlier mode (0 otherwise); off_outl
- * then holds the fp16 values.  off_sat is the saturation report, u8
- * [T][ceil(d/512)]: per row and 512-channel block, bit 1 = an alpha* or beta*
- * of a group whose first channel is in the block overflowed fp16 (|v| >=
- * 65520, stored as +-65504), bit 2 = the scale of a quantization group whose
- * first channel is in the block saturated (max|E^d| > 65504 * Qmax, its codes
- * clip; dynamic scales only), bit 4 = an outlier value of a channel in the
- * block overflowed fp16. */
+ * then holds the fp16 values.  The wire's fp16 fields (alpha, beta, scale,
+ * outlier values) hold the IEEE rounding of their value: +-infinity where the
+ * rounding overflows, +infinity for a scale no finite fp16 covers; both ends
+ * compute with +-65504 there (orc_f16_wire). */
 typedef struct {
-    uint64_t off_coef, off_scale, off_codes, off_outl, total, off_ooff, off_sat;
+    uint64_t off_coef, off_scale, off_codes, off_outl, total, off_ooff;
 } orc_layout;
 
 int orc_layout_of(const orc_config* cfg, orc_layout* out);
@@ -96,8 +93,14 @@ float orc_f16_to_f32(uint16_t h);
 /* Round-to-nearest-even fp32 -> fp16 pattern, magnitudes above 65504 clamp to
  * 65504 (the largest finite fp16). */
 uint16_t orc_f16_rne_sat(float f);
+/* Round-to-nearest-even fp32 -> fp16 pattern with IEEE overflow to
+ * +-infinity (|f| >= 65520): the rounding the wire's fp16 fields hold. */
+uint16_t orc_f16_rne(float f);
+/* Value of a wire fp16 field in the codec's arithmetic: +-infinity reads as
+ * +-65504. */
+float orc_f16_wire(uint16_t h);
 /* Smallest positive fp16 h with value(h)*qmax >= m (m >= 0 finite, qmax >= 1);
- * 0x7BFF (65504) when no finite fp16 satisfies it. */
+ * +infinity (0x7C00) when no finite fp16 satisfies it. */
 uint16_t orc_scale_roundup(float m, int32_t qmax);
 /* Smallest positive fp16 h with value(h) >= step; 0x7BFF when step > 65504. */
 uint16_t orc_step_roundup(float step);

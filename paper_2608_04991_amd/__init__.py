@@ -57,8 +57,7 @@ class _Config(ctypes.Structure):
 class _Layout(ctypes.Structure):
     _fields_ = [("off_coef", ctypes.c_uint64), ("off_scale", ctypes.c_uint64),
                 ("off_codes", ctypes.c_uint64), ("off_outl", ctypes.c_uint64),
-                ("total", ctypes.c_uint64), ("off_ooff", ctypes.c_uint64),
-                ("off_sat", ctypes.c_uint64)]
+                ("total", ctypes.c_uint64), ("off_ooff", ctypes.c_uint64)]
 
 
 class _Candidate(ctypes.Structure):
@@ -232,13 +231,13 @@ def rac_parse_header(header: bytes):
                      c.flags), bool(zr.value)
 
 
-def rac_saturation_summary(cfg: RacConfig, sat) -> tuple[int, int]:
-    """(rows with any saturation bit, OR of all bits) of a saturation report
-    in host memory (bytes-like or a numpy uint8 array of tokens *
-    ceil(hidden / 512) bytes, e.g. wire[layout['off_sat']:])."""
+def rac_saturation_summary(cfg: RacConfig, wire) -> tuple[int, int]:
+    """(token rows with a saturated fp16 field, OR of 1 coefficient / 2 scale
+    / 4 outlier value) of a wire in host memory (bytes-like or a numpy uint8
+    array of at least rac_wire_size(cfg) bytes)."""
     import numpy as np
-    a = np.ascontiguousarray(np.frombuffer(bytes(sat), dtype=np.uint8) if isinstance(sat, (bytes, bytearray))
-                             else np.asarray(sat, dtype=np.uint8))
+    a = np.ascontiguousarray(np.frombuffer(bytes(wire), dtype=np.uint8) if isinstance(wire, (bytes, bytearray))
+                             else np.asarray(wire, dtype=np.uint8))
     rows, bits = ctypes.c_int64(0), ctypes.c_uint32(0)
     _check(library().rac_saturation_summary(ctypes.byref(cfg._c()), a.ctypes.data, a.size, ctypes.byref(rows),
                                             ctypes.byref(bits)), "rac_saturation_summary")

@@ -58,7 +58,6 @@ struct alignas(8) Args {
     uint32_t* outl;     // per-token outliers, or the fp16 values of per-group ones
     uint16_t* gval;     // per-group outliers: fp16 values [T][d/g_q][k_g] (= outl)
     uint8_t* goff;      //                     u8 in-group offsets [T][d/g_q][k_g]
-    uint8_t* sat;       // saturation report [T][nch]: one byte per row and 512-channel chunk
     void* xhat;
     uint32_t tokens;    // < 2^31, so row + gridDim.x never wraps
     int32_t d;
@@ -80,8 +79,8 @@ struct alignas(8) Args {
     // header and padding (written once, by the first wavefront)
     int32_t write_header;
     uint8_t* wire;
-    uint64_t off_scale, off_codes, off_outl, off_ooff, off_sat, total;
-    uint64_t end_coef, end_scale, end_codes, end_outl, end_ooff, end_sat;  // first byte after each section
+    uint64_t off_scale, off_codes, off_outl, off_ooff, total;
+    uint64_t end_coef, end_scale, end_codes, end_outl, end_ooff;  // first byte after each section
     uint32_t hdr[24];   // first 96 bytes of the header; the rest is zero
 };
 
@@ -165,13 +164,29 @@ __device__ __forceinline__ float f16_value(uint32_t bits) {
     return (float)__builtin_bit_cast(_Float16, (uint16_t)bits);
 }
 
+// The fp16 fields of the wire (alpha, beta, scale, outlier values) hold the
+// IEEE result of their rounding: a magnitude whose round-to-nearest-even
+// overflows is +-infinity, and a scale with no finite fp16 covering the
+// group is +infinity.  That reports the saturation in the wire at no cost;
+// both ends compute with +-65504 in its place.
+__device__ __forceinline__ uint32_t f16_rne(float v) {
+    const _Float16 h = (_Float16)v;
+    return (uint32_t)__builtin_bit_cast(uint16_t, h);
+}
+
+// The value a wire fp16 field stands for: +-infinity reads as +-65504.
+__device__ __forceinline__ float f16_wire(uint32_t bits) {
+    return __builtin_fminf(__builtin_fmaxf(f16_value(bits), -65504.0f), 65504.0f);
+}
+
 // fp32 -> bf16 pattern, round to nearest even (finite inputs).
 __device__ __forceinline__ uint32_t bf16_rne(float v) {
     const uint32_t u = __float_as_uint(v);
     return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
 
-// Smallest positive fp16 h with value(h) * q >= m  (m > 0); 0x7BFF if none.
+// Smallest positive fp16 h with value(h) * q >= m  (m > 0); +infinity
+// (0x7C00, read as 65504, the codes then clip) if no finite fp16 is.
 // value(h) * q is exact in binary32, so the test below is an exact
 // comparison.  y = m * fl(1/q) is within 2^-23 (relative) of m/q, so its RNE
 // fp16 rounding h0 is either the answer or one step below it: if value(h0)
@@ -182,7 +197,7 @@ __device__ __forceinline__ uint32_t scale_roundup(float m, float q, float inv_q)
     uint32_t h = f16_rne_sat(m * inv_q);
     h = h < 1u ? 1u : h;
     h = f16_value(h) * q >= m ? h : h + 1u;
-    return m > 65504.0f * q ? 0x7BFFu : h;
+    return m > 65504.0f * q ? 0x7C00u : h;
 }
 
 // Smallest positive fp16 h with value(h) >= step; 0x7BFF above 65504.
@@ -201,30 +216,14 @@ __device__ __forceinline__ uint32_t step_roundup(float step) {
 
 // Closed-form least squares of one group from its centred moments:
 // alpha* = C_rx / C_rr, beta* = m_x - alpha* m_r; a zero-variance reference
-// gives (0, m_x).  Returns the fp16 pair (alpha | beta << 16).
+// gives (0, m_x).  Returns the fp16 pair (alpha | beta << 16), each the IEEE
+// rounding (+-infinity past the fp16 range).
 __device__ __forceinline__ uint32_t fit_coef(float crr, float crx, float mr, float mx) {
     const bool flat = crr == 0.0f;
     const float as = flat ? 0.0f : crx / crr;
     const float bs = flat ? mx : mx - as * mr;
-    return f16_rne_sat(as) | (f16_rne_sat(bs) << 16);
+    return f16_rne(as) | (f16_rne(bs) << 16);
 }
-
-// The same, also reporting whether alpha* or beta* overflowed fp16: |v| >=
-// 65520 (the midpoint between 65504 and the next step, 65536, from which
-// round-to-nearest-even goes to infinity); the field then holds +-65504.
-constexpr float kF16Overflow = 65520.0f;
-__device__ __forceinline__ uint32_t fit_coef(float crr, float crx, float mr, float mx, bool& sat) {
-    const bool flat = crr == 0.0f;
-    const float as = flat ? 0.0f : crx / crr;
-    const float bs = flat ? mx : mx - as * mr;
-    sat = (__builtin_fabsf(as) >= kF16Overflow) | (__builtin_fabsf(bs) >= kF16Overflow);
-    return f16_rne_sat(as) | (f16_rne_sat(bs) << 16);
-}
-
-// Saturation report bits (one byte per row and 512-channel chunk).
-constexpr uint32_t kSatCoef = 1u;     // a coefficient of a group starting in the chunk overflowed fp16
-constexpr uint32_t kSatScale = 2u;    // a scale of a group starting in the chunk saturated (codes clip)
-constexpr uint32_t kSatOutlier = 4u;  // an outlier value of a channel in the chunk overflowed fp16
 
 // ---------------------------------------------------------------------------
 // Cross-lane partner of the adjacent aligned block at butterfly level `lv`
@@ -372,8 +371,7 @@ __device__ __forceinline__ void write_header(const Args& A, uint32_t lane) {
     zero_bytes(A.wire, A.end_scale, A.off_codes, lane);
     zero_bytes(A.wire, A.end_codes, A.off_outl, lane);
     zero_bytes(A.wire, A.end_outl, A.off_ooff, lane);
-    zero_bytes(A.wire, A.end_ooff, A.off_sat, lane);
-    zero_bytes(A.wire, A.end_sat, A.total, lane);
+    zero_bytes(A.wire, A.end_ooff, A.total, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -855,7 +853,7 @@ __device__ __forceinline__ uint32_t select_group_outliers(const float* e, int lv
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         if (sel[j] != 0ull && __builtin_amdgcn_inverse_ballot_w64(sel[j]))
-            st[slot] = f16_rne_sat(e[j]) | ((o0 + (uint32_t)j) << 16);
+            st[slot] = f16_rne(e[j]) | ((o0 + (uint32_t)j) << 16);
         slot += (selm >> j) & 1u;
     }
     return selm;
@@ -964,7 +962,7 @@ __device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S,
                 slot += (j + 1u < C && kk.y >= kst && (uint32_t)kk.y > (uint32_t)key) ? 1u : 0u;
             }
             bstore32(outl, (have && key >= kst && slot < (uint32_t)k) ? slot * 4u : kOut,
-                     ch | (f16_rne_sat(__uint_as_float(S.cval[lane])) << 16));
+                     ch | (f16_rne(__uint_as_float(S.cval[lane])) << 16));
         }
     } else {
         // 3b. radix select of T with workgroup-wide counts
@@ -1018,7 +1016,7 @@ __device__ __forceinline__ uint32_t select_outliers(const Args& A, RowShared& S,
             uint32_t pos = 0;
             for (int j = 0; j < k; ++j) pos += (key_channel(S.ckey[j]) < ch) ? 1u : 0u;
             bstore32(outl, (have && pos < (uint32_t)k) ? pos * 4u : kOut,
-                     ch | (f16_rne_sat(__uint_as_float(val)) << 16));
+                     ch | (f16_rne(__uint_as_float(val)) << 16));
         }
     }
     // 4. mark this lane's outliers: |E| > T, or |E| == T and channel <= c*
@@ -1154,17 +1152,12 @@ void rac_encode_kernel(Args A) {
             crr = tree_n(&S.part[2][g0], cpg_a);
             crx = tree_n(&S.part[3][g0], cpg_a);
         }
-        bool csat = false;
         const uint32_t cf = A.cf_given ? bload32(rsrc(A.coef, (uint64_t)row * nga, nga * 4u), (uint32_t)grp_a * 4u)
-                                       : fit_coef(crr, crx, mr, mx, csat);
+                                       : fit_coef(crr, crx, mr, mx);
         bstore32(rsrc(A.coef, (uint64_t)row * nga, nga * 4u), (first_a && !A.cf_given) ? (uint32_t)grp_a * 4u : kOut, cf);
-        // saturation report of this row and chunk; given pairs come with
-        // their coefficient bit already in the report (set by the pooling)
-        const Rsrc rsat = rsrc(A.sat, (uint64_t)row * (uint32_t)A.nch, (uint32_t)A.nch);
-        uint32_t satb = A.cf_given ? (bload8(rsat, (uint32_t)w) & kSatCoef) : (ballot(first_a && csat) ? kSatCoef : 0u);
 
         // a3: aligned reference R~ = fma(alpha, r, beta) and residual E = x - R~
-        const float a = f16_value(cf & 0xFFFFu), b0 = f16_value(cf >> 16);
+        const float a = f16_wire(cf & 0xFFFFu), b0 = f16_wire(cf >> 16);
         float rt[8], e[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
@@ -1185,12 +1178,6 @@ void rac_encode_kernel(Args A) {
         float ed[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) ed[j] = e[j];
-        if constexpr (OM != 0) {
-            bool osat = false;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) osat |= ((selm >> j) & 1u) && __builtin_fabsf(e[j]) >= kF16Overflow;
-            satb |= ballot(osat) ? kSatOutlier : 0u;
-        }
         if (selm) {
 #pragma unroll
             for (int j = 0; j < 8; ++j)
@@ -1198,7 +1185,7 @@ void rac_encode_kernel(Args A) {
                     ed[j] = 0.0f;
                     // per-group mode: R~ of a chosen channel becomes its
                     // reconstruction R~ + O-hat now, so E is dead from here on
-                    if constexpr (OM == 2) rt[j] = rt[j] + f16_value(f16_rne_sat(e[j]));
+                    if constexpr (OM == 2) rt[j] = rt[j] + f16_wire(f16_rne(e[j]));
                 }
         }
 
@@ -1220,9 +1207,8 @@ void rac_encode_kernel(Args A) {
             }
             sh = m == 0.0f ? 0u : scale_roundup(m, q, inv_q);
             bstore16(rsrc(A.scale, (uint64_t)row * ngq, ngq * 2u), first_q ? (uint32_t)grp_q * 2u : kOut, sh);
-            satb |= ballot(first_q && m > 65504.0f * q) ? kSatScale : 0u;
         }
-        const float s = f16_value(sh);
+        const float s = f16_wire(sh);
         const float inv = sh ? __builtin_amdgcn_rcpf(s) : 0.0f;
 
         // a6-a8: quantize (round half to even), pack, reconstruct
@@ -1254,11 +1240,10 @@ void rac_encode_kernel(Args A) {
         if (selm) {
 #pragma unroll
             for (int j = 0; j < 8; ++j)
-                if ((selm >> j) & 1u) H[j] = OM == 2 ? rt[j] : rt[j] + f16_value(f16_rne_sat(e[j]));
+                if ((selm >> j) & 1u) H[j] = OM == 2 ? rt[j] : rt[j] + f16_wire(f16_rne(e[j]));
         }
         const uint32_t crb = (uint32_t)A.code_row_bytes;
         store_codes<BITS>(rsrc(A.codes, (uint64_t)row * crb, crb), w, lane, dword3, pk);
-        bstore8(rsat, lane == 0u ? (uint32_t)w : kOut, satb);
         store_xhat_t(xhat_row(A, row), A.xhat_bf16 != 0, (uint32_t)(w * kChunk), lane, XT + w * kSlice, H);
     }
 }
@@ -1458,10 +1443,6 @@ void rac_encode_rows_kernel(Args A) {
         // a2-a3 per chunk: fit of the lane's group, E; lane maxima of |E|
         // (per chunk, and over the wavefront's chunks)
         const Rsrc rcoef = rsrc(A.coef, (uint64_t)row * nga, nga * 4u);
-        const Rsrc rsat = rsrc(A.sat, (uint64_t)row * (uint32_t)A.nch, (uint32_t)A.nch);
-        // saturation report bits of each chunk (given pairs come with their
-        // coefficient bit already in the report, set by the pooling)
-        uint32_t satc[CPW];
         float lmc[CPW];
 #pragma unroll
         for (int i = 0; i < CPW; ++i) lmc[i] = 0.0f;
@@ -1483,14 +1464,11 @@ void rac_encode_rows_kernel(Args A) {
             const float crr = lsum<GA>(tree8(uu), lv_a), crx = lsum<GA>(tree8(uv), lv_a);
             if constexpr (GIVEN) {
                 cf[i] = bload32(rcoef, (c0 >> A.lg_a) * 4u);
-                satc[i] = bload8(rsat, (uint32_t)(chunk_at(i) / kChunk)) & kSatCoef;
             } else {
-                bool cs;
-                cf[i] = fit_coef(crr, crx, mr, mx, cs);
+                cf[i] = fit_coef(crr, crx, mr, mx);
                 bstore32(rcoef, first_a ? (c0 >> A.lg_a) * 4u : kOut, cf[i]);
-                satc[i] = ballot(first_a && cs) ? kSatCoef : 0u;
             }
-            const float a = f16_value(cf[i] & 0xFFFFu), b0 = f16_value(cf[i] >> 16);
+            const float a = f16_wire(cf[i] & 0xFFFFu), b0 = f16_wire(cf[i] >> 16);
             float e[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j) {  // E = 0 past the row
@@ -1648,14 +1626,13 @@ void rac_encode_rows_kernel(Args A) {
         // keys >= kst.
         const bool chosen = have && key >= kst;
         const uint32_t och = chosen ? key_channel(key) : 0xFFFFFFFFu;
-        const bool osat = chosen && __builtin_fabsf(__uint_as_float(S.cval[lane])) >= kF16Overflow;
         uint32_t oval = 0u;
         float ohat = 0.0f;
         if (chosen) {
-            oval = f16_rne_sat(__uint_as_float(S.cval[lane]));
+            oval = f16_rne(__uint_as_float(S.cval[lane]));
             const uint32_t rw = S.crw[lane], cfc = S.ccf[lane];
             const float r = (och & 1u) ? bf16_hi(rw) : bf16_lo(rw);
-            ohat = __builtin_fmaf(f16_value(cfc & 0xFFFFu), r, f16_value(cfc >> 16)) + f16_value(oval);
+            ohat = __builtin_fmaf(f16_wire(cfc & 0xFFFFu), r, f16_wire(cfc >> 16)) + f16_wire(oval);
         }
         if (w == 0) {
             // the row's outliers in ascending channel order (slot = number of
@@ -1698,10 +1675,7 @@ void rac_encode_rows_kernel(Args A) {
             m = lmax<GQ>(m, lv_q);
             const uint32_t sh = m == 0.0f ? 0u : scale_roundup(m, q, inv_q);
             bstore16(rsc, first_q ? (c0 >> A.lg_q) * 2u : kOut, sh);
-            const uint32_t satb = satc[i] | (ballot(first_q && m > 65504.0f * q) ? kSatScale : 0u) |
-                                  (ballot(osat && och - chunk0 < (uint32_t)kChunk) ? kSatOutlier : 0u);
-            bstore8(rsat, lane == 0u ? chunk0 / (uint32_t)kChunk : kOut, satb);
-            const float s = f16_value(sh);
+            const float s = f16_wire(sh);
             const float inv = sh ? __builtin_amdgcn_rcpf(s) : 0.0f;
             // |E^d| <= s q, so E^d * (1/s) stays below q + 1/2 unless the
             // scale saturated; that case and quotients near a tie take the
@@ -1715,7 +1689,7 @@ void rac_encode_rows_kernel(Args A) {
                 qf[j] = mg[j] - kMagic;
                 dist = __builtin_fmaxf(dist, __builtin_fabsf(t - qf[j]));
             }
-            if ((dist > kNearHalf) | (sh == 0x7BFFu)) {
+            if ((dist > kNearHalf) | (sh == 0x7C00u)) {
                 float inv2 = inv;
                 asm volatile("" : "+v"(inv2));  // recomputed here rather than kept live
 #pragma unroll
@@ -1730,7 +1704,7 @@ void rac_encode_rows_kernel(Args A) {
             {
                 float r[8];
                 widen8(rp[i], r);
-                const float a = f16_value(cf[i] & 0xFFFFu), b0 = f16_value(cf[i] >> 16);
+                const float a = f16_wire(cf[i] & 0xFFFFu), b0 = f16_wire(cf[i] >> 16);
 #pragma unroll
                 for (int j = 0; j < 8; ++j) H[j] = __builtin_fmaf(qf[j], s, __builtin_fmaf(a, r[j], b0));  // R~ + q*s (q*s exact)
             }
@@ -1817,8 +1791,8 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
             gcf = bload32(rsrc(A.coef, (uint64_t)row * nga, nga * 4u), pch ? (ech >> A.lg_a) * 4u : kOut);
         }
         nx = load(nrow, ref_index_v(A, rix, n + 1u));
-        const float a = f16_value(in.cf & 0xFFFFu), b0 = f16_value(in.cf >> 16);
-        const float s = f16_value(in.sh);
+        const float a = f16_wire(in.cf & 0xFFFFu), b0 = f16_wire(in.cf >> 16);
+        const float s = f16_wire(in.sh);
         float r[8], rt[8], H[8];
         widen8(in.rv, r);
 #pragma unroll
@@ -1839,7 +1813,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
                 const uint32_t e1 = (uint32_t)__builtin_amdgcn_ds_bpermute(addr, (int)in.ent2);
                 const uint32_t ent = src < (uint32_t)kWave ? e0 : e1;
                 const uint32_t off = (ent >> 16) & 0xFFu;
-                const float v = f16_value(ent & 0xFFFFu);
+                const float v = f16_wire(ent & 0xFFFFu);
                 const bool here = (off >> 3) == mine;
 #pragma unroll
                 for (int j = 0; j < 8; ++j) H[j] = (here & ((off & 7u) == (uint32_t)j)) ? rt[j] + v : H[j];
@@ -1849,8 +1823,8 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
         put8(st, lane, H);
         wave_lds_sync();
         if (pch) {
-            const float rt = __builtin_fmaf(f16_value(gcf & 0xFFFFu), bf16_lo(gref), f16_value(gcf >> 16));
-            reinterpret_cast<float*>(st)[slice_float(ech & (uint32_t)(kChunk - 1))] = rt + f16_value(in.ent >> 16);
+            const float rt = __builtin_fmaf(f16_wire(gcf & 0xFFFFu), bf16_lo(gref), f16_wire(gcf >> 16));
+            reinterpret_cast<float*>(st)[slice_float(ech & (uint32_t)(kChunk - 1))] = rt + f16_wire(in.ent >> 16);
         }
         wave_lds_sync();
         emit_xhat_flat(xhat_row(A, row), BF16, (uint32_t)(w * kChunk), lane, st);
@@ -1904,8 +1878,6 @@ __device__ __forceinline__ Mom mom_merge(const Mom& a, const Mom& b) {
 // them: one workgroup per row (strided), one wavefront per 512-channel chunk,
 // groups inside a chunk.  Written as float4 (m_r, m_x, C_rr, C_rx) to `mom`
 // [T][d/g_a] (the wire's code section, which the encode overwrites later).
-// The row's saturation report is cleared here: the pooling sets the
-// coefficient bits, the encode adds the others.
 template <int GA>
 __global__ __launch_bounds__(kWave * kMaxWaves) void rac_moments_kernel(Args A, float4* mom) {
     const uint32_t lane = threadIdx.x & (kWave - 1);
@@ -1934,7 +1906,6 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_moments_kernel(Args A, 
         const float crr = lsum<GA>(tree8(uu), lv_a);
         const float crx = lsum<GA>(tree8(uv), lv_a);
         if (first_a && c0 < d) mom[(uint64_t)row * nga + grp_a] = make_float4(mr, mx, crr, crx);
-        bstore8(rsrc(A.sat, (uint64_t)row * (uint32_t)A.nch, (uint32_t)A.nch), lane == 0u ? (uint32_t)w : kOut, 0u);
     }
 }
 
@@ -1949,9 +1920,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_moments_kernel(Args A, 
 // One thread takes the pass results in row order onto a stack of
 // power-of-two sizes, merging whenever the top two are equal, and merges the
 // stack from the top down at the end.  The fp16 pair goes to the coefficient
-// slot of every row of the segment, and a pair that overflowed fp16 sets the
-// coefficient bit of the group's chunk in every row's saturation report.
-// Segment bounds are clamped to [0, T], so no access leaves the buffers
+// slot of every row of the segment.  Segment bounds are clamped to [0, T], so no access leaves the buffers
 // whatever the starts hold.
 constexpr int kPoolWaves = 16;
 
@@ -1960,7 +1929,7 @@ __global__ __launch_bounds__(kWave * kPoolWaves) void rac_pool_kernel(Args A, co
     __shared__ uint32_t bsz[kPoolWaves];
     __shared__ Mom stk[40];
     __shared__ uint32_t ssz[40];
-    __shared__ uint32_t cf_shared, sat_shared;
+    __shared__ uint32_t cf_shared;
     const uint32_t lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
     const uint32_t nga = (uint32_t)A.d >> A.lg_a;
     const uint32_t s = blockIdx.x / nga, j = blockIdx.x % nga;
@@ -2025,22 +1994,17 @@ __global__ __launch_bounds__(kWave * kPoolWaves) void rac_pool_kernel(Args A, co
     }
     if (threadIdx.x == 0u) {
         uint32_t cf = 0u;
-        bool sat = false;
         if (top > 0) {
             Mom r = stk[top - 1];
             for (int i = top - 2; i >= 0; --i) r = mom_merge(stk[i], r);
-            cf = fit_coef(r.crr, r.crx, r.mr, r.mx, sat);
+            cf = fit_coef(r.crr, r.crx, r.mr, r.mx);
         }
         cf_shared = cf;
-        sat_shared = sat ? 1u : 0u;
     }
     __syncthreads();
     const uint32_t cf = cf_shared;
-    const uint32_t sat_off = sat_shared ? (j << A.lg_a) / (uint32_t)kChunk : kOut;
-    for (int64_t t = lo + threadIdx.x; t < hi; t += (int64_t)kWave * kPoolWaves) {
+    for (int64_t t = lo + threadIdx.x; t < hi; t += (int64_t)kWave * kPoolWaves)
         bstore32(rsrc(A.coef, (uint64_t)t * nga, nga * 4u), j * 4u, cf);
-        bstore8(rsrc(A.sat, (uint64_t)t * (uint32_t)A.nch, (uint32_t)A.nch), sat_off, kSatCoef);
-    }
 }
 
 // ---------------------------------------------------------------------------
@@ -2173,10 +2137,8 @@ bool grouped(const rac_config* c) { return (c->flags & RAC_FLAG_GROUP_OUTLIERS) 
 
 struct Sizes {
     rac_layout L;
-    uint64_t coef, scale, codes, outl, ooff, sat;
+    uint64_t coef, scale, codes, outl, ooff;
 };
-
-uint64_t sat_chunks(int64_t d) { return (uint64_t)((d + kChunk - 1) / kChunk); }
 
 Sizes sizes_of(const rac_config* c) {
     Sizes s;
@@ -2192,9 +2154,7 @@ Sizes sizes_of(const rac_config* c) {
     s.L.off_codes = up256(s.L.off_scale + s.scale);
     s.L.off_outl = up256(s.L.off_codes + s.codes);
     s.L.off_ooff = grouped(c) ? up256(s.L.off_outl + s.outl) : 0u;
-    s.sat = T * sat_chunks(c->hidden);
-    s.L.off_sat = grouped(c) ? up256(s.L.off_ooff + s.ooff) : up256(s.L.off_outl + s.outl);
-    s.L.total = up256(s.L.off_sat + s.sat);
+    s.L.total = grouped(c) ? up256(s.L.off_ooff + s.ooff) : up256(s.L.off_outl + s.outl);
     return s;
 }
 
@@ -2206,10 +2166,8 @@ Args make_args(const rac_config* c, const Sizes& S) {
     A.off_codes = S.L.off_codes;
     A.off_outl = S.L.off_outl;
     A.total = S.L.total;
-    A.off_sat = S.L.off_sat;
-    A.end_sat = S.L.off_sat + S.sat;
-    // without per-group outliers the offset array is empty, at the saturation report
-    A.off_ooff = grouped(c) ? S.L.off_ooff : S.L.off_sat;
+    // without per-group outliers the offset array is empty, at the end
+    A.off_ooff = grouped(c) ? S.L.off_ooff : S.L.total;
     A.end_ooff = A.off_ooff + S.ooff;
     A.end_coef = S.L.off_coef + S.coef;
     A.end_scale = S.L.off_scale + S.scale;
@@ -2239,8 +2197,7 @@ void set_sections(Args& A, const Sizes& S) {
     A.codes = A.wire + S.L.off_codes;
     A.outl = reinterpret_cast<uint32_t*>(A.wire + S.L.off_outl);
     A.gval = reinterpret_cast<uint16_t*>(A.wire + S.L.off_outl);
-    A.goff = A.wire + (A.gout ? S.L.off_ooff : S.L.off_sat);
-    A.sat = A.wire + S.L.off_sat;
+    A.goff = A.wire + (A.gout ? S.L.off_ooff : S.L.total);
 }
 
 void fill_header(Args& A, const rac_config* c, bool zero_ref, bool pooled = false) {
@@ -2272,7 +2229,6 @@ void fill_header(Args& A, const rac_config* c, bool zero_ref, bool pooled = fals
     put64(56, A.off_outl);
     put64(64, A.total);
     put64(72, grouped(c) ? A.off_ooff : 0u);
-    put64(80, A.off_sat);
     for (int i = 0; i < 24; ++i)
         A.hdr[i] = (uint32_t)h[4 * i] | ((uint32_t)h[4 * i + 1] << 8) | ((uint32_t)h[4 * i + 2] << 16) |
                    ((uint32_t)h[4 * i + 3] << 24);
@@ -2501,17 +2457,28 @@ rac_status rac_wire_layout(const rac_config* cfg, rac_layout* out) {
     return RAC_OK;
 }
 
-rac_status rac_saturation_summary(const rac_config* cfg, const void* sat_host, size_t len, int64_t* rows,
+rac_status rac_saturation_summary(const rac_config* cfg, const void* wire_host, size_t len, int64_t* rows,
                                   uint32_t* bits) {
-    if (!config_valid(cfg) || (cfg->tokens > 0 && !sat_host)) return RAC_ERR_INVALID;
-    const uint64_t nb = sat_chunks(cfg->hidden), T = (uint64_t)cfg->tokens;
-    if (len < T * nb) return RAC_ERR_INVALID;
-    const uint8_t* p = static_cast<const uint8_t*>(sat_host);
+    if (!config_valid(cfg) || !wire_host) return RAC_ERR_INVALID;
+    const Sizes S = sizes_of(cfg);
+    if (len < S.L.total) return RAC_ERR_INVALID;
+    const uint8_t* w = static_cast<const uint8_t*>(wire_host);
+    auto inf16 = [&](uint64_t off) { return ((w[off] | (w[off + 1] << 8)) & 0x7FFFu) == 0x7C00u; };
+    const uint64_t T = (uint64_t)cfg->tokens, d = (uint64_t)cfg->hidden;
+    const uint64_t nga = d / (uint64_t)cfg->group_align, ngq = d / (uint64_t)cfg->group_quant;
+    const uint64_t k = (uint64_t)cfg->outlier_k;
     int64_t n = 0;
     uint32_t all = 0;
     for (uint64_t t = 0; t < T; ++t) {
         uint32_t r = 0;
-        for (uint64_t b = 0; b < nb; ++b) r |= p[t * nb + b];
+        for (uint64_t j = 0; j < 2 * nga; ++j) r |= inf16(S.L.off_coef + (t * 2 * nga + j) * 2) ? 1u : 0u;
+        if (!(cfg->flags & RAC_FLAG_FIXED_STEP))
+            for (uint64_t j = 0; j < ngq; ++j) r |= inf16(S.L.off_scale + (t * ngq + j) * 2) ? 2u : 0u;
+        if (grouped(cfg)) {
+            for (uint64_t j = 0; j < ngq * k; ++j) r |= inf16(S.L.off_outl + (t * ngq * k + j) * 2) ? 4u : 0u;
+        } else {
+            for (uint64_t j = 0; j < k; ++j) r |= inf16(S.L.off_outl + (t * k + j) * 4 + 2) ? 4u : 0u;
+        }
         n += r ? 1 : 0;
         all |= r;
     }
@@ -2551,12 +2518,11 @@ rac_status rac_parse_header(const void* header_host, size_t len, rac_config* out
     if (h[25] != 1 || h[26] != ((flags & 2u) ? 0 : 1) || h[27] != ofmt) return RAC_ERR_FORMAT;
     const Sizes S = sizes_of(&c);
     if (g64(32) != S.L.off_coef || g64(40) != S.L.off_scale || g64(48) != S.L.off_codes ||
-        g64(56) != S.L.off_outl || g64(64) != S.L.total || g64(72) != S.L.off_ooff ||
-        g64(80) != S.L.off_sat)
+        g64(56) != S.L.off_outl || g64(64) != S.L.total || g64(72) != S.L.off_ooff)
         return RAC_ERR_FORMAT;
     for (int i = 30; i < 32; ++i)
         if (h[i]) return RAC_ERR_FORMAT;
-    for (int i = 88; i < 256; ++i)
+    for (int i = 80; i < 256; ++i)
         if (h[i]) return RAC_ERR_FORMAT;
     *out = c;
     if (zero_ref) *zero_ref = (flags & 4u) ? 1 : 0;

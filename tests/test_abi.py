@@ -77,7 +77,7 @@ def test_layout_matches_documented_format(lib, c):
 def test_payload_ratio_of_the_prefill_uplink_shape(lib):
     cfg = rac.RacConfig(4096, 4096, 128, 128, 4, 8)
     ratio = rac.rac_wire_size(cfg) / (4096 * 4096 * 2)
-    assert abs(ratio - 0.2783) < 5e-4   # 4-bit codes + fp16 scale/coef + 8 outliers + 8 flag bytes per row
+    assert abs(ratio - 0.2774) < 5e-4   # 4-bit codes + fp16 scale/coef + 8 outliers per row
 
 
 @pytest.mark.parametrize("bad", [dict(bits=5), dict(group_align=96), dict(group_quant=4),
@@ -125,8 +125,7 @@ def test_group_outlier_payload_of_the_prefill_uplink_shape(lib):
     cfg = rac.RacConfig(4096, 4096, 128, 128, 4, 1, rac.RAC_FLAG_GROUP_OUTLIERS)
     ratio = rac.rac_wire_size(cfg) / (4096 * 4096 * 2)
     # 4-bit codes + fp16 scale/coef + one (u8 offset, fp16 value) per group of 128
-    # + one saturation byte per 512 channels
-    assert abs(ratio - (0.25 + 6 / 256 + 3 / 256 + 1 / 1024)) < 1e-5
+    assert abs(ratio - (0.25 + 6 / 256 + 3 / 256)) < 1e-5
 
 
 def test_parse_header_rejects_corruption_of_group_outlier_headers(lib):
@@ -138,8 +137,7 @@ def test_parse_header_rejects_corruption_of_group_outlier_headers(lib):
     cfg, _ = rac.rac_parse_header(good)
     assert cfg == rac.RacConfig(**c)
     # flags 9 (both outlier kinds), format 1 with flag 8, a moved offset array,
-    # k_g above a quarter of the group, a moved saturation report, a byte past
-    # the fields
+    # k_g above a quarter of the group, bytes past the fields
     for off, val in [(6, 9), (27, 1), (73, 0), (28, 17), (80, 1), (90, 1)]:
         bad = bytearray(good)
         bad[off] = val
@@ -321,3 +319,30 @@ def test_calibration_argument_errors_are_synchronous(lib):
     assert cal(tgt=-1.0) == 1 and cal(tgt=float("nan")) == 1 and cal(x=None) == 1 and cal(chosen=None) == 1
     assert cal(cap=need - 1) == 3 and cal(ws=FAKE + 16) == 2 and cal(x=FAKE + 2) == 2
     assert ch.value == -7
+
+
+def test_saturation_summary_reads_the_infinity_marks_of_oracle_wires(lib):
+    """rac_saturation_summary on wires the oracle wrote, against the
+    test-side reader of the format: per-token and per-group outliers, fixed
+    steps (no scale section), and a short buffer."""
+    x = np.zeros((4, 1024), np.float32)
+    x[0, 0:128] = np.tile([2.0 ** 20, -2.0 ** 20], 64)          # row 0: scale past the range (+ outliers)
+    x[2, 600], x[2, 601] = 131072.0, -131072.0                  # row 2: outlier values past the range
+    x[3, 512:576] = 65536.0                                      # row 3: beta past the range
+    xb = wl.f32_to_bf16_bits(x)
+    for flags, k in ((0, 2), (rac.RAC_FLAG_GROUP_OUTLIERS, 1), (0, 0)):
+        c = dict(tokens=4, hidden=1024, group_align=64, group_quant=128, bits=4, outlier_k=k, flags=flags)
+        rc, wire, _ = oracle.encode(xb, None, want_xhat=False, **c)
+        assert rc == 0
+        marks = wirefmt.saturation_marks(wire)
+        rows, bits = rac.rac_saturation_summary(rac.RacConfig(**c), wire)
+        # (without outliers row 2's large values are dense and covered by a finite scale)
+        assert rows == int((marks != 0).sum()) == (3 if k else 2) and bits == int(np.bitwise_or.reduce(marks))
+        assert marks[3] == 1 and marks[1] == 0
+        with pytest.raises(rac.RacError):
+            rac.rac_saturation_summary(rac.RacConfig(**c), wire[:-1])
+    c = dict(tokens=4, hidden=1024, group_align=64, group_quant=128, bits=4, outlier_k=2,
+             flags=rac.RAC_FLAG_FIXED_STEP)
+    rc, wire, _ = oracle.encode(xb, None, np.full(8, 1.0, np.float32), want_xhat=False, **c)
+    # rows 0 and 2: outlier values past the range; row 3: beta; no scale section
+    assert rac.rac_saturation_summary(rac.RacConfig(**c), wire) == (3, 5)

@@ -156,8 +156,7 @@ def test_group_outlier_layout_header_and_padding():
         assert oracle.layout(**c) == wirefmt.expected_layout(**c)
     lay = oracle.layout(**cfgd(4096, 4096, 128, 128, 4, 1, G))
     # 4-bit codes + fp16 scale + fp16 (alpha, beta) + one 3-byte outlier per group of 128
-    # + one saturation byte per 512-channel block
-    assert lay["total"] == 256 + 4096 * (32 * 4 + 32 * 2 + 2048) + 4096 * 32 * 3 + 4096 * 8
+    assert lay["total"] == 256 + 4096 * (32 * 4 + 32 * 2 + 2048) + 4096 * 32 * 3
     T, d = 5, 520
     xb, rb, _ = wl.affine_pair(wl.AffineRecipe(T, d, 8), 0)
     rc, wire, _ = oracle.encode(xb, rb, **cfgd(T, d, 8, 8, 3, 2, G))

@@ -36,9 +36,9 @@ MUTANTS = [
      "return (a->idx > b->idx) ? -1 : (a->idx < b->idx);"),
     ("outlier_left_in_dense", "is_out[c] = 1;\n                ed[c] = 0.0f;\n", "is_out[c] = 1;\n"),
     ("aligned_ref_drops_beta", "                rt[c] = fmaf(a, r[c], b0);", "                rt[c] = a * r[c];"),
-    ("decoder_drops_outliers", "eh[c] = orc_f16_to_f32((uint16_t)(w >> 16));", "(void)c;"),
+    ("decoder_drops_outliers", "eh[c] = orc_f16_wire((uint16_t)(w >> 16));", "(void)c;"),
     ("alpha_beta_swapped", "put16(coef + 4 * j, ah);", "put16(coef + 4 * j, bh);"),
-    ("outlier_value_unrounded_recon", "? orc_f16_to_f32(oval[c]) :", "? e[c] :"),
+    ("outlier_value_unrounded_recon", "? orc_f16_wire(oval[c]) :", "? e[c] :"),
     ("f16_ties_up", "p = (lo & 1u) ? lo + 1 : lo; /* tie: even fraction */",
      "p = lo + 1; /* tie: even fraction */"),
     ("group_offset_absolute", "orow[(uint64_t)g * k + i] = (uint8_t)sel[i];",
@@ -55,13 +55,12 @@ MUTANTS = [
     ("pool_repeats_the_first_row", "seg[i] = mom[(lo + i) * G + j];", "seg[i] = mom[lo * G + j];"),
     ("group_values_in_reverse", "put16(vrow + 2 * ((uint64_t)g * k + i), oval[c]);",
      "put16(vrow + 2 * ((uint64_t)g * k + (k - 1 - i)), oval[c]);"),
-    ("sat_threshold_at_the_largest_fp16", "#define ORC_F16_OVERFLOW 65520.0f", "#define ORC_F16_OVERFLOW 65504.0f"),
-    ("sat_coef_block_by_group_index", "sat[(j * ga) / ORC_SAT_BLOCK] |= (uint8_t)ORC_SAT_COEF;",
-     "sat[j / ORC_SAT_BLOCK] |= (uint8_t)ORC_SAT_COEF;"),
-    ("sat_scale_ignores_qmax", "if (m > orc_f16_to_f32(ORC_F16_MAX_BITS) * (float)qmax)",
-     "if (m > orc_f16_to_f32(ORC_F16_MAX_BITS))"),
-    ("sat_outlier_block_of_the_rank", "if (fabsf(e[c]) >= ORC_F16_OVERFLOW) sat[c / ORC_SAT_BLOCK] |= (uint8_t)ORC_SAT_OUTLIER;\n                is_out",
-     "if (fabsf(e[c]) >= ORC_F16_OVERFLOW) sat[i / ORC_SAT_BLOCK] |= (uint8_t)ORC_SAT_OUTLIER;\n                is_out"),
+    ("wire_fields_clamped_not_infinite", "    if (fabsf(f) >= ORC_F16_OVERFLOW) return (uint16_t)((signbit(f) ? 0x8000u : 0u) | ORC_F16_INF_BITS);",
+     "    if (fabsf(f) >= ORC_F16_OVERFLOW) return (uint16_t)((signbit(f) ? 0x8000u : 0u) | ORC_F16_MAX_BITS);"),
+    ("overflow_threshold_at_the_largest_fp16", "#define ORC_F16_OVERFLOW 65520.0f", "#define ORC_F16_OVERFLOW 65504.0f"),
+    ("scale_past_range_clamped", "    if (orc_f16_to_f32(ORC_F16_MAX_BITS) * q < m) return ORC_F16_INF_BITS;",
+     "    if (orc_f16_to_f32(ORC_F16_MAX_BITS) * q < m) return ORC_F16_MAX_BITS;"),
+    ("infinity_used_unclamped", "    return v > m ? m : (v < -m ? -m : v);", "    return v;"),
 ]
 
 PINS = [
@@ -83,12 +82,13 @@ PINS = [
     lambda: ppins.test_pooled_fit_matches_exact_rational_least_squares(0),
     ppins.test_pooled_moments_match_float64,
     ppins.test_constant_reference_over_a_segment_gives_alpha_zero_and_the_pooled_mean,
-    spins.test_ordinary_rows_report_nothing,
-    spins.test_scale_saturation_depends_on_qmax_and_marks_the_group_block,
+    spins.test_ordinary_rows_have_no_marks,
+    spins.test_scale_past_the_range_is_infinity_and_the_codes_clip,
     spins.test_beta_overflow_threshold_is_the_fp16_rounding_overflow,
-    spins.test_alpha_overflow_marks_the_alignment_group_block,
-    spins.test_outlier_value_overflow_marks_the_channel_block,
-    spins.test_pooled_fit_reports_every_row_of_a_saturated_segment,
+    spins.test_alpha_overflow_is_infinity_with_its_sign,
+    spins.test_outlier_value_overflow_is_infinity_and_reconstructs_as_65504,
+    spins.test_pooled_fit_marks_every_row_of_a_saturated_segment,
+    pins.test_f16_rne_is_the_ieee_conversion_with_overflow_to_infinity,
 ]
 
 

@@ -8,7 +8,7 @@ either the oracle or the HIP library without trusting either one's code:
   8  u32 tokens        12 u32 hidden   16 u32 g_a   20 u32 g_q
   24 u8 bits  25 u8 coef fmt  26 u8 scale fmt  27 u8 outlier fmt  28 u16 k
   32 u64 off_coef  40 off_scale  48 off_codes  56 off_outl  64 total
-  72 u64 off_ooff (per-group outliers only, else 0)  80 u64 off_sat
+  72 u64 off_ooff (per-group outliers only, else 0)
   sections 256-byte aligned, zero padded; version 2.
 
 Outliers: per token (flag 1, fmt 1) one u32 per entry, channel in the low
@@ -16,11 +16,8 @@ half and the fp16 value in the high half; per quantization group (flag 8,
 fmt 2) fp16 values [T][G][k_g] at off_outl and u8 in-group offsets
 [T][G][k_g] at off_ooff.
 
-Saturation report at off_sat, the last section: u8 [T][ceil(d/512)], one byte
-per row and 512-channel block: bit 1 an alignment coefficient of a group
-starting in the block overflowed fp16, bit 2 a scale of a quantization group
-starting in the block saturated (its codes clip), bit 4 an outlier value of a
-channel in the block overflowed fp16.
+The fp16 fields (coefficients, scales, outlier values) hold IEEE fp16: +-inf
+marks a rounding past the fp16 range (read as +-65504 by both ends).
 """
 from __future__ import annotations
 
@@ -47,18 +44,12 @@ def expected_layout(tokens, hidden, group_align, group_quant, bits, outlier_k=0,
     if flags & GROUP_OUTLIERS:
         n = tokens * (hidden // group_quant) * outlier_k
         off_ooff = up256(off_outl + 2 * n)
-        end = off_ooff + n
+        total = up256(off_ooff + n)
     else:
         off_ooff = 0
-        end = off_outl + tokens * outlier_k * 4
-    off_sat = up256(end)
-    total = up256(off_sat + tokens * sat_blocks(hidden))
+        total = up256(off_outl + tokens * outlier_k * 4)
     return dict(off_coef=off_coef, off_scale=off_scale, off_codes=off_codes,
-                off_outl=off_outl, total=total, off_ooff=off_ooff, off_sat=off_sat)
-
-
-def sat_blocks(hidden: int) -> int:
-    return (hidden + 511) // 512
+                off_outl=off_outl, total=total, off_ooff=off_ooff)
 
 
 def header(wire: np.ndarray) -> dict:
@@ -70,7 +61,7 @@ def header(wire: np.ndarray) -> dict:
                 group_align=u32(16), group_quant=u32(20), bits=int(w[24]), coef_fmt=int(w[25]),
                 scale_fmt=int(w[26]), outl_fmt=int(w[27]), outlier_k=u16(28),
                 off_coef=u64(32), off_scale=u64(40), off_codes=u64(48), off_outl=u64(56),
-                total=u64(64), off_ooff=u64(72), off_sat=u64(80))
+                total=u64(64), off_ooff=u64(72))
 
 
 def sections(wire: np.ndarray) -> dict:
@@ -99,8 +90,6 @@ def sections(wire: np.ndarray) -> dict:
         n = T * k
         out["outl"] = w[h["off_outl"]:h["off_outl"] + 4 * n].view(np.uint32).reshape(T, k)
         out["gval"] = out["goff"] = None
-    nb = sat_blocks(d)
-    out["sat"] = w[h["off_sat"]:h["off_sat"] + T * nb].reshape(T, nb)
     return out
 
 
@@ -120,8 +109,7 @@ def padding_is_zero(wire: np.ndarray) -> bool:
     T, d, ga, gq, b, k = (h["tokens"], h["hidden"], h["group_align"], h["group_quant"],
                           h["bits"], h["outlier_k"])
     used = np.zeros(w.size, dtype=bool)
-    used[:88] = True
-    used[h["off_sat"]:h["off_sat"] + T * sat_blocks(d)] = True
+    used[:80] = True
     used[h["off_coef"]:h["off_coef"] + T * (d // ga) * 4] = True
     if not (h["flags"] & 2):
         used[h["off_scale"]:h["off_scale"] + T * (d // gq) * 2] = True
@@ -134,3 +122,23 @@ def padding_is_zero(wire: np.ndarray) -> bool:
         used[h["off_outl"]:h["off_outl"] + T * k * 4] = True
         used[72:80] = False   # off_ooff is 0 without per-group outliers
     return bool(np.all(w[~used] == 0)) and bool(np.all(w[30:32] == 0))
+
+
+def _inf16(a) -> np.ndarray:
+    return (np.asarray(a, dtype=np.uint16) & 0x7FFF) == 0x7C00
+
+
+def saturation_marks(wire: np.ndarray) -> np.ndarray:
+    """Per token row, the OR of 1 (an alpha or beta field holds +-inf), 2 (a
+    scale holds +inf) and 4 (an outlier value holds +-inf)."""
+    s = sections(wire)
+    T = s["header"]["tokens"]
+    m = np.zeros(T, dtype=np.int64)
+    m |= np.where(_inf16(s["coef"]).reshape(T, -1).any(axis=1), 1, 0)
+    if s["scale"] is not None:
+        m |= np.where(_inf16(s["scale"]).reshape(T, -1).any(axis=1), 2, 0)
+    if s["outl"] is not None:
+        m |= np.where(_inf16(s["outl"] >> 16).reshape(T, -1).any(axis=1), 4, 0)
+    if s["gval"] is not None:
+        m |= np.where(_inf16(s["gval"]).reshape(T, -1).any(axis=1), 4, 0)
+    return m
