@@ -323,6 +323,73 @@ size_t rac_calibrate_workspace(const rac_candidate* candidates, int32_t n);
 rac_status rac_calibrate(const void* x, const void* ref, rac_candidate* candidates, int32_t n, double target_nmse,
                          void* workspace, size_t workspace_bytes, int32_t* chosen, rac_stream_t stream);
 
+/* ---- Decode-phase reference predictor ----------------------------------
+ * Subsection "Predicted References for Decode", Eq. decode-predictor: from
+ * the second decode step on, each boundary has a one-layer causal Transformer
+ * that keeps a bounded causal state (a key-value cache) and maps the previous
+ * reconstructed state H-hat^{t-1} of a sequence to the reference R_pred^t of
+ * the current one.  The paper gives neither its sizes nor its trained
+ * weights; this library's reading (the layers below) is a pre-norm block of
+ * width `model` with `heads` heads of 64 channels and a SwiGLU of width
+ * `ffn`, attending to the latest `window` inputs of the sequence with rotary
+ * positions, between a projection from and a residual projection back to the
+ * boundary width:
+ *   h0 = x W_in^T                         x = H-hat^{t-1} (bf16 [B][hidden])
+ *   q, k, v = RMSNorm(h0; g1) W_qkv^T     rotary: channel pair (2i, 2i+1) of
+ *                                         each head turned by pos * 10000^(-2i/64)
+ *   o  = softmax(q k^T / 8) v             over positions max(0, pos-window+1)..pos
+ *   h1 = h0 + o W_o^T
+ *   h2 = h1 + (silu(n2 W_gate^T) * (n2 W_up^T)) W_down^T,   n2 = RMSNorm(h1; g2)
+ *   R  = x + RMSNorm(h2; g3) W_out^T      (bf16 [B][hidden])
+ * RMSNorm(h; g) = h / sqrt(mean(h^2) + 1e-6) * g.  Products are bf16 x bf16
+ * with fp32 accumulation; h0, h1, h2, q, k, v are fp32; the normalized
+ * activations, o, the SwiGLU output, the cached keys (after rotation) and
+ * values, and R are bf16 (round to nearest even). */
+typedef struct {
+    int32_t hidden;    /* boundary width d: multiple of 512, 512..8192           */
+    int32_t model;     /* m: multiple of 128, 128..2048, = heads * 64            */
+    int32_t heads;
+    int32_t ffn;       /* SwiGLU width: multiple of 128, 128..8192               */
+    int32_t window;    /* inputs attended (the bounded history): 1..1024         */
+    int32_t max_batch; /* sequences per step: 1..256                             */
+} rac_predictor_config;
+
+/* Byte offsets of the weight blob's sections (bf16, each 256-byte aligned, in
+ * this order): W_in [m][d], g1 [m], W_qkv [3m][m] (rows: the q, k, v outputs),
+ * W_o [m][m], g2 [m], W_gu [2 ffn][m] (row 2j: gate j, row 2j+1: up j),
+ * W_down [m][ffn], g3 [m], W_out [d][m]; every matrix is [outputs][inputs]. */
+typedef struct {
+    uint64_t w_in, g1, w_qkv, w_o, g2, w_gu, w_down, g3, w_out, total;
+} rac_predictor_offsets;
+
+/* Host-only, pure.  Weight blob layout; RAC_ERR_INVALID outside the ranges. */
+rac_status rac_predictor_layout(const rac_predictor_config* cfg, rac_predictor_offsets* out);
+
+/* Host-only, pure.  Bytes of the key-value cache: [max_batch][window][2][m]
+ * bf16 (key, then value, of every position slot), or 0 for a bad config. */
+size_t rac_predictor_cache_bytes(const rac_predictor_config* cfg);
+
+/* Host-only, pure.  Bytes of the step's device scratch, or 0. */
+size_t rac_predictor_workspace_bytes(const rac_predictor_config* cfg);
+
+/* One decode step of `batch` sequences (batch <= max_batch).
+ *   weights   : DEVICE blob (rac_predictor_layout), 256-byte aligned
+ *   cache     : DEVICE [max_batch][window][2][model] bf16, caller-owned;
+ *               sequence b's input at position p goes to slot p mod window;
+ *               only slots of positions p - window + 1 .. p - 1 are read, so
+ *               the cache needs no clearing and a restarted sequence (p = 0)
+ *               reads nothing stale
+ *   pos       : DEVICE int32 [batch], the input's 0-based position in its
+ *               sequence (negative counts as 0)
+ *   h_prev    : DEVICE bf16 [batch][hidden], the previous reconstructions
+ *   ref_out   : DEVICE bf16 [batch][hidden], the predicted references
+ *   workspace : DEVICE scratch of rac_predictor_workspace_bytes(), 256-byte aligned
+ * Argument errors are returned before any launch.  Ten kernel launches on
+ * `stream`. */
+rac_status rac_predictor_step(const rac_predictor_config* cfg, const void* weights, void* cache, const int32_t* pos,
+                              int32_t batch, const void* h_prev, void* ref_out, void* workspace,
+                              size_t workspace_bytes, rac_stream_t stream);
+
 /* ---- Reference selection for the prefill uplink (host only) ------------
  * Subsection "Repeated-Span Retrieval for Prefill Uplinks",
  * Eq. prefill-reference-selection.  A span index holds the token streams of

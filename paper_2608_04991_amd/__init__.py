@@ -26,6 +26,8 @@ __all__ = [
     "rac_encode", "rac_reconstruct", "rac_decode", "rac_encode_gather", "rac_decode_gather",
     "rac_status_string", "SpanIndex", "rac_encode_pooled", "rac_saturation_summary",
     "rac_recon_error_workspace", "rac_recon_error", "rac_calibrate_workspace", "rac_calibrate",
+    "PredictorConfig", "rac_predictor_layout", "rac_predictor_cache_bytes", "rac_predictor_workspace_bytes",
+    "predictor_pack", "rac_predictor_step",
 ]
 
 RAC_FLAG_FIXED_STEP = 1
@@ -64,6 +66,28 @@ class _Candidate(ctypes.Structure):
     _fields_ = [("cfg", _Config), ("wire_bytes", ctypes.c_uint64), ("sq_err", ctypes.c_double),
                 ("sq_x", ctypes.c_double), ("max_abs", ctypes.c_double), ("nmse", ctypes.c_double),
                 ("feasible", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class _PredConfig(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("hidden", "model", "heads", "ffn", "window", "max_batch")]
+
+
+class _PredOffsets(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_uint64) for n in ("w_in", "g1", "w_qkv", "w_o", "g2", "w_gu", "w_down", "g3",
+                                               "w_out", "total")]
+
+
+@dataclass(frozen=True)
+class PredictorConfig:
+    hidden: int
+    model: int
+    heads: int
+    ffn: int
+    window: int
+    max_batch: int
+
+    def _c(self) -> _PredConfig:
+        return _PredConfig(self.hidden, self.model, self.heads, self.ffn, self.window, self.max_batch)
 
 
 @dataclass(frozen=True)
@@ -141,6 +165,15 @@ def library():
         L.rac_calibrate.argtypes = [vp, vp, candp, ctypes.c_int32, ctypes.c_double, vp, ctypes.c_size_t,
                                     ctypes.POINTER(ctypes.c_int32), vp]
         L.rac_calibrate.restype = ctypes.c_int
+        pcp = ctypes.POINTER(_PredConfig)
+        L.rac_predictor_layout.argtypes = [pcp, ctypes.POINTER(_PredOffsets)]
+        L.rac_predictor_layout.restype = ctypes.c_int
+        L.rac_predictor_cache_bytes.argtypes = [pcp]
+        L.rac_predictor_cache_bytes.restype = ctypes.c_size_t
+        L.rac_predictor_workspace_bytes.argtypes = [pcp]
+        L.rac_predictor_workspace_bytes.restype = ctypes.c_size_t
+        L.rac_predictor_step.argtypes = [pcp, vp, vp, vp, ctypes.c_int32, vp, vp, vp, ctypes.c_size_t, vp]
+        L.rac_predictor_step.restype = ctypes.c_int
         L.rac_status_string.argtypes = [ctypes.c_int]
         L.rac_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -403,3 +436,45 @@ def rac_calibrate(x, ref, configs, target_nmse: float, workspace=None, stream=No
     res = [dict(cfg=configs[i], wire_bytes=int(a.wire_bytes), sq_err=a.sq_err, sq_x=a.sq_x, max_abs=a.max_abs,
                 nmse=a.nmse, feasible=bool(a.feasible)) for i, a in enumerate(arr)]
     return int(chosen.value), res
+
+
+def rac_predictor_layout(cfg: PredictorConfig) -> dict:
+    out = _PredOffsets()
+    _check(library().rac_predictor_layout(ctypes.byref(cfg._c()), ctypes.byref(out)), "rac_predictor_layout")
+    return {f: int(getattr(out, f)) for f, _ in _PredOffsets._fields_}
+
+
+def rac_predictor_cache_bytes(cfg: PredictorConfig) -> int:
+    return int(library().rac_predictor_cache_bytes(ctypes.byref(cfg._c())))
+
+
+def rac_predictor_workspace_bytes(cfg: PredictorConfig) -> int:
+    return int(library().rac_predictor_workspace_bytes(ctypes.byref(cfg._c())))
+
+
+def predictor_pack(cfg: PredictorConfig, weights: dict):
+    """The weight blob (numpy uint8) from named bf16 arrays (uint16 patterns
+    of the shapes rac_predictor_layout documents), placed at the library's
+    section offsets."""
+    import numpy as np
+    lay = rac_predictor_layout(cfg)
+    blob = np.zeros(lay["total"], dtype=np.uint8)
+    for name, arr in weights.items():
+        a = np.ascontiguousarray(arr, dtype=np.uint16).view(np.uint8).ravel()
+        blob[lay[name]:lay[name] + a.size] = a
+    return blob
+
+
+def rac_predictor_step(cfg: PredictorConfig, weights, cache, pos, h_prev, ref_out, workspace, batch: int | None = None,
+                       stream=None) -> None:
+    """One predictor step: h_prev (bf16 [batch][hidden]) -> ref_out, updating
+    the key-value cache; pos: device int32 [batch]."""
+    B = int(batch) if batch is not None else int(pos.numel())
+    n = B * cfg.hidden
+    _check(library().rac_predictor_step(ctypes.byref(cfg._c()), _dev(weights, "weights", 1, 0),
+                                        _dev(cache, "cache", 2, rac_predictor_cache_bytes(cfg) // 2),
+                                        _dev(pos, "pos", 4, B), B, _dev(h_prev, "h_prev", 2, n),
+                                        _dev(ref_out, "ref_out", 2, n),
+                                        _dev(workspace, "workspace", 1, rac_predictor_workspace_bytes(cfg)),
+                                        _nbytes(workspace) if not isinstance(workspace, int) else
+                                        rac_predictor_workspace_bytes(cfg), _stream(stream)), "rac_predictor_step")

@@ -22,6 +22,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SRC = os.path.join(HERE, "csrc", "rac.hip")
 HOST_SRC = os.path.join(HERE, "csrc", "spans.cpp")   # host-only C++ (reference selection)
+PRED_SRC = os.path.join(HERE, "csrc", "predictor.hip")  # decode-phase reference predictor
 INC = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "lib", "librac.so")
 
@@ -34,7 +35,7 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
 def build(verbose: bool = True) -> str:
     os.makedirs(os.path.dirname(LIB), exist_ok=True)
     tmp = LIB + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-I", INC, "-o", tmp, SRC, HOST_SRC]
+    cmd = [HIPCC, *FLAGS, "-I", INC, "-o", tmp, SRC, PRED_SRC, HOST_SRC]
     asm = LIB + ".s"
     dev = [HIPCC, *[f for f in FLAGS if f not in ("-fPIC", "-shared")], "--cuda-device-only", "-S",
            "-I", INC, "-o", asm, SRC]

@@ -1,0 +1,417 @@
+// predictor.hip - gfx950 kernels and C ABI of the decode-phase reference
+// predictor: a one-layer causal Transformer over a sequence's earlier
+// boundary states with a bounded key-value cache (the paper's subsection
+// "Predicted References for Decode", Eq. decode-predictor).  For t >= 2 it
+// turns the previous reconstructed state H-hat^{t-1} of every sequence of a
+// decode batch into the reference R_pred^t that the codec then encodes
+// against.  The contract of each entry point is documented in include/rac.h.
+//
+// One step (every launch on the caller's stream; B sequences, width d, model
+// width m, h heads of 64 channels, SwiGLU width f, window W):
+//   h0 = x W_in^T                                     (x = H-hat^{t-1}, bf16)
+//   q, k, v = RMSNorm(h0; g1) W_qkv^T, rotary positions on q and k
+//   o  = softmax(q k^T / 8) v over the last min(pos + 1, W) inputs
+//   h1 = h0 + o W_o^T
+//   h2 = h1 + (silu(n2 W_gate^T) * (n2 W_up^T)) W_down^T,  n2 = RMSNorm(h1; g2)
+//   R  = x + RMSNorm(h2; g3) W_out^T                  (bf16)
+// The products are bf16 x bf16 with fp32 accumulation on the matrix cores
+// (v_mfma_f32_16x16x32_bf16); the residual stream h0..h2 is fp32; the
+// normalized activations, o, the SwiGLU output and the cached keys and values
+// are bf16.
+//
+// Mapping onto CDNA4.  Decode batches are skinny (B <= 256 rows against
+// weight matrices of up to 4096 x 4096), so the products are weight-streaming:
+// a workgroup owns 16 output columns and a K range, its four wavefronts split
+// that range and sum their accumulators through LDS in a fixed order, and
+// long K ranges are split further across workgroups (partials summed, again
+// in a fixed order, by the row kernel that follows).  Every weight byte is
+// read once per 64 batch rows.
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "rac.h"
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kW = 64;           // wavefront
+constexpr int kGemmWaves = 4;
+constexpr int kNt = 16;          // output columns per workgroup
+constexpr int kRt = 4;           // 16-row tiles per workgroup (64 batch rows)
+constexpr int kHd = 64;          // channels per head
+constexpr float kEps = 1e-6f;    // RMSNorm
+
+__device__ __forceinline__ float bf(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+__device__ __forceinline__ uint16_t to_bf(float v) {  // round to nearest even (finite)
+    const uint32_t u = __float_as_uint(v);
+    return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+// ---------------------------------------------------------------------------
+// C[b][n] = sum_k A[b][k] W[n][k] over one K range, A bf16 [M][K] row-major,
+// W bf16 [N][K] (each output's weights contiguous).  Grid: x = N / 16 column
+// tiles, y = K splits, z = 64-row tiles of the batch.  In one MFMA
+// (16 x 16 x 32) lane l holds A[l % 16][8 (l / 16) + j] and
+// W[n0 + l % 16][8 (l / 16) + j], j < 8, each one 16-byte load, and gets
+// C[4 (l / 16) + r][n0 + l % 16], r < 4.
+enum Epi { kPartial = 0, kStore = 1, kSwiglu = 2, kResidOut = 3 };
+
+struct Gemm {
+    const uint16_t* a;   // [M][K]
+    const uint16_t* w;   // [N][K]
+    int32_t M, N, K, ksplit;   // K range per split
+    float* out;          // kPartial: [splits][M][N]; kStore: [M][N]
+    uint16_t* out16;     // kSwiglu: [M][N/2]; kResidOut: [M][N]
+    const uint16_t* resid;     // kResidOut: bf16 [M][N] added to the product
+};
+
+template <int EPI>
+__global__ __launch_bounds__(kW * kGemmWaves) void pred_gemm(Gemm g) {
+    __shared__ f32x4 red[kGemmWaves - 1][kRt][kW];
+    const int lane = threadIdx.x & (kW - 1), w = threadIdx.x / kW;
+    const int n0 = blockIdx.x * kNt, s = blockIdx.y, m0 = blockIdx.z * (kRt * 16);
+    const int kq = g.ksplit / kGemmWaves;                // this wavefront's share (multiple of 32)
+    const int kbeg = s * g.ksplit + w * kq;
+    const int col = n0 + (lane & 15), kl = 8 * (lane >> 4);
+    const uint16_t* wrow = g.w + (size_t)col * g.K + kbeg + kl;
+    f32x4 acc[kRt];
+#pragma unroll
+    for (int r = 0; r < kRt; ++r) acc[r] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    const bool rows_in[kRt] = {m0 + (lane & 15) < g.M, m0 + 16 + (lane & 15) < g.M, m0 + 32 + (lane & 15) < g.M,
+                               m0 + 48 + (lane & 15) < g.M};
+    for (int k = 0; k < kq; k += 32) {
+        const bf16x8 bw = *reinterpret_cast<const bf16x8*>(wrow + k);
+#pragma unroll
+        for (int r = 0; r < kRt; ++r) {
+            bf16x8 av = bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
+            if (rows_in[r])
+                av = *reinterpret_cast<const bf16x8*>(g.a + (size_t)(m0 + 16 * r + (lane & 15)) * g.K + kbeg + kl + k);
+            acc[r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bw, acc[r], 0, 0, 0);
+        }
+    }
+    // the four wavefronts' sums, added in the order ((w0 + w1) + w2) + w3
+    if (w > 0) {
+#pragma unroll
+        for (int r = 0; r < kRt; ++r) red[w - 1][r][lane] = acc[r];
+    }
+    __syncthreads();
+    if (w != 0) return;
+#pragma unroll
+    for (int r = 0; r < kRt; ++r)
+#pragma unroll
+        for (int v = 0; v < kGemmWaves - 1; ++v) acc[r] = acc[r] + red[v][r][lane];
+#pragma unroll
+    for (int r = 0; r < kRt; ++r) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int row = m0 + 16 * r + 4 * (lane >> 4) + i;
+            if (row >= g.M) continue;
+            const float v = acc[r][i];
+            if constexpr (EPI == kPartial) {
+                g.out[((size_t)s * g.M + row) * g.N + col] = v;
+            } else if constexpr (EPI == kStore) {
+                g.out[(size_t)row * g.N + col] = v;
+            } else if constexpr (EPI == kResidOut) {
+                g.out16[(size_t)row * g.N + col] = to_bf(bf(g.resid[(size_t)row * g.N + col]) + v);
+            } else {
+                // interleaved rows: column 2j is gate j, 2j + 1 is up j; the
+                // even lane gets its neighbour's up value
+                const float up = __shfl_xor(v, 1);
+                if ((col & 1) == 0) {
+                    const float gate = v;
+                    const float silu = gate / (1.0f + __expf(-gate));
+                    g.out16[(size_t)row * (g.N / 2) + col / 2] = to_bf(silu * up);
+                }
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Residual stream update and RMSNorm of one batch row per workgroup:
+// h = resid + sum_s part[s] (s in order), stored fp32, and
+// n = bf16(h / sqrt(mean(h^2) + eps) * gain).
+constexpr int kRowThreads = 256;
+
+struct RowArgs {
+    const float* resid;  // [M][m] or null
+    const float* part;   // [splits][M][m]
+    int32_t splits, M, m;
+    const uint16_t* gain;  // bf16 [m]
+    float* h;            // [M][m]
+    uint16_t* n;         // bf16 [M][m]
+};
+
+__global__ __launch_bounds__(kRowThreads) void pred_row(RowArgs a) {
+    __shared__ float red[kRowThreads];
+    const int b = blockIdx.x, t = threadIdx.x;
+    float ss = 0.0f;
+    for (int c = t; c < a.m; c += kRowThreads) {
+        float v = a.resid ? a.resid[(size_t)b * a.m + c] : 0.0f;
+        for (int s = 0; s < a.splits; ++s) v = v + a.part[((size_t)s * a.M + b) * a.m + c];
+        a.h[(size_t)b * a.m + c] = v;
+        ss = ss + v * v;
+    }
+    red[t] = ss;
+    __syncthreads();
+    for (int st = kRowThreads / 2; st > 0; st >>= 1) {
+        if (t < st) red[t] = red[t] + red[t + st];
+        __syncthreads();
+    }
+    const float inv = 1.0f / __builtin_sqrtf(red[0] / (float)a.m + kEps);
+    for (int c = t; c < a.m; c += kRowThreads)
+        a.n[(size_t)b * a.m + c] = to_bf(a.h[(size_t)b * a.m + c] * inv * bf(a.gain[c]));
+}
+
+// ---------------------------------------------------------------------------
+// Attention of one (sequence, head) per wavefront.  Lane d holds channel d of
+// the head: q and k get the rotary position (pairs (2i, 2i + 1) turned by
+// pos * 10000^(-2i/64), angles in binary64), k and v go to the cache slot
+// pos mod W (bf16), and the output is the softmax-weighted sum of the values
+// of positions max(0, pos - W + 1) .. pos, the current one taken from
+// registers (it is never read back from memory in the same launch).
+struct AttnArgs {
+    const float* qkv;    // [B][3m]: q | k | v
+    uint16_t* cache;     // [B][W][2][m] bf16
+    const int32_t* pos;  // [B]
+    int32_t B, m, heads, window;
+    uint16_t* o;         // [B][m] bf16
+};
+
+__global__ __launch_bounds__(kW) void pred_attn(AttnArgs a) {
+    const int b = blockIdx.x / a.heads, hh = blockIdx.x % a.heads, d = threadIdx.x;
+    const int32_t p = a.pos[b] < 0 ? 0 : a.pos[b];
+    const float* row = a.qkv + (size_t)b * 3 * a.m + hh * kHd;
+    float q = row[d], k = row[a.m + d];
+    const float v = row[2 * a.m + d];
+    {
+        const int i = d >> 1;
+        const double th = (double)p * exp2(-(double)(2 * i) / (double)kHd * 13.287712379549449);  // 10000^(-2i/64)
+        const float c = (float)cos(th), sn = (float)sin(th);
+        const float qo = __shfl_xor(q, 1), ko = __shfl_xor(k, 1);
+        // (a, b) -> (a cos - b sin, a sin + b cos): the even lane holds a
+        q = (d & 1) ? qo * sn + q * c : q * c - qo * sn;
+        k = (d & 1) ? ko * sn + k * c : k * c - ko * sn;
+    }
+    const uint16_t kb = to_bf(k), vb = to_bf(v);
+    const int slot = p % a.window;
+    uint16_t* cs = a.cache + ((size_t)b * a.window + slot) * 2 * a.m + hh * kHd;
+    cs[d] = kb;
+    cs[a.m + d] = vb;
+    // scores of the window, 64 positions per pass: lane j takes position
+    // first + j; the current position's key is bf16(k) in registers
+    const int first = p - a.window + 1 < 0 ? 0 : p - a.window + 1;
+    const int n = p - first + 1;
+    __shared__ float qs[kHd], sc[1024];
+    __shared__ uint16_t kcur[kHd];
+    qs[d] = q;
+    kcur[d] = kb;
+    __syncthreads();
+    float mx = -INFINITY;
+    for (int j0 = 0; j0 < n; j0 += kW) {
+        const int j = j0 + d;
+        float sdot = -INFINITY;
+        if (j < n) {
+            const int pp = first + j;
+            float acc = 0.0f;
+            if (pp == p) {
+                for (int c = 0; c < kHd; ++c) acc = acc + qs[c] * bf(kcur[c]);
+            } else {
+                const uint16_t* kr = a.cache + ((size_t)b * a.window + pp % a.window) * 2 * a.m + hh * kHd;
+                for (int c = 0; c < kHd; ++c) acc = acc + qs[c] * bf(kr[c]);
+            }
+            sdot = acc * 0.125f;  // 1 / sqrt(64)
+        }
+        if (j < n) sc[j] = sdot;
+        mx = __builtin_fmaxf(mx, sdot);
+    }
+    for (int o = 1; o < kW; o <<= 1) mx = __builtin_fmaxf(mx, __shfl_xor(mx, o));
+    __syncthreads();
+    float den = 0.0f;
+    for (int j = d; j < n; j += kW) {
+        const float e = __expf(sc[j] - mx);
+        sc[j] = e;
+        den = den + e;
+    }
+    for (int o = 1; o < kW; o <<= 1) den = den + __shfl_xor(den, o);
+    __syncthreads();
+    float acc = 0.0f;
+    for (int j = 0; j < n; ++j) {
+        const int pp = first + j;
+        const float vv = pp == p ? bf(vb)
+                                 : bf(a.cache[((size_t)b * a.window + pp % a.window) * 2 * a.m + a.m + hh * kHd + d]);
+        acc = acc + sc[j] * vv;
+    }
+    a.o[(size_t)b * a.m + hh * kHd + d] = to_bf(acc / den);
+}
+
+// ---------------------------------------------------------------------------
+// Host side
+
+struct PLayout {
+    uint64_t w_in, g1, w_qkv, w_o, g2, w_gu, w_down, g3, w_out, total;  // bytes
+};
+
+uint64_t up256(uint64_t v) { return (v + 255u) & ~uint64_t(255); }
+
+bool pcfg_valid(const rac_predictor_config* c) {
+    // (every K range splits into four wavefront shares of whole 32-wide steps)
+    return c && c->hidden >= 512 && c->hidden <= 8192 && c->hidden % 512 == 0 && c->model >= 128 &&
+           c->model <= 2048 && c->model % 128 == 0 && c->heads >= 1 && c->heads * kHd == c->model &&
+           c->ffn >= 128 && c->ffn <= 8192 && c->ffn % 128 == 0 && c->window >= 1 && c->window <= 1024 &&
+           c->max_batch >= 1 && c->max_batch <= 256;
+}
+
+PLayout playout(const rac_predictor_config* c) {
+    const uint64_t d = c->hidden, m = c->model, f = c->ffn;
+    PLayout L;
+    uint64_t o = 0;
+    auto take = [&](uint64_t elems) { const uint64_t at = o; o = up256(o + elems * 2u); return at; };
+    L.w_in = take(m * d);
+    L.g1 = take(m);
+    L.w_qkv = take(3 * m * m);
+    L.w_o = take(m * m);
+    L.g2 = take(m);
+    L.w_gu = take(2 * f * m);
+    L.w_down = take(m * f);
+    L.g3 = take(m);
+    L.w_out = take(d * m);
+    L.total = o;
+    return L;
+}
+
+// K splits of the input projection: K ranges of 512 (4 wavefronts x 128)
+int in_splits(const rac_predictor_config* c) { return c->hidden / 512; }
+int down_splits(const rac_predictor_config* c) { return c->ffn % 512 == 0 ? c->ffn / 512 : 1; }
+
+struct PWork {
+    uint64_t part, h0, h1, h2, n, qkv, o, gg, total;
+};
+
+PWork pwork(const rac_predictor_config* c, int B) {
+    const uint64_t m = c->model, f = c->ffn;
+    const uint64_t S = (uint64_t)(in_splits(c) > down_splits(c) ? in_splits(c) : down_splits(c));
+    PWork W;
+    uint64_t o = 0;
+    auto take = [&](uint64_t bytes) { const uint64_t at = o; o = up256(o + bytes); return at; };
+    W.part = take(S * B * m * 4);
+    W.h0 = take((uint64_t)B * m * 4);
+    W.h1 = take((uint64_t)B * m * 4);
+    W.h2 = take((uint64_t)B * m * 4);
+    W.n = take((uint64_t)B * m * 2);
+    W.qkv = take((uint64_t)B * 3 * m * 4);
+    W.o = take((uint64_t)B * m * 2);
+    W.gg = take((uint64_t)B * f * 2);
+    W.total = o;
+    return W;
+}
+
+template <int EPI>
+rac_status gemm(const uint16_t* a, const uint16_t* w, int M, int N, int K, int splits, float* out, uint16_t* out16,
+                const uint16_t* resid, hipStream_t st) {
+    Gemm g{a, w, M, N, K, K / splits, out, out16, resid};
+    void* args[] = {&g};
+    const dim3 grid((unsigned)(N / kNt), (unsigned)splits, (unsigned)((M + kRt * 16 - 1) / (kRt * 16)));
+    return hipLaunchKernel(reinterpret_cast<const void*>(pred_gemm<EPI>), grid, dim3(kW * kGemmWaves), args, 0, st) ==
+                   hipSuccess
+               ? RAC_OK
+               : RAC_ERR_HIP;
+}
+
+rac_status row(const float* resid, const float* part, int splits, int M, int m, const uint16_t* gain, float* h,
+               uint16_t* n, hipStream_t st) {
+    RowArgs r{resid, part, splits, M, m, gain, h, n};
+    void* args[] = {&r};
+    return hipLaunchKernel(reinterpret_cast<const void*>(pred_row), dim3((unsigned)M), dim3(kRowThreads), args, 0,
+                           st) == hipSuccess
+               ? RAC_OK
+               : RAC_ERR_HIP;
+}
+
+bool al(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+rac_status rac_predictor_layout(const rac_predictor_config* cfg, rac_predictor_offsets* out) {
+    if (!pcfg_valid(cfg) || !out) return RAC_ERR_INVALID;
+    const PLayout L = playout(cfg);
+    out->w_in = L.w_in;
+    out->g1 = L.g1;
+    out->w_qkv = L.w_qkv;
+    out->w_o = L.w_o;
+    out->g2 = L.g2;
+    out->w_gu = L.w_gu;
+    out->w_down = L.w_down;
+    out->g3 = L.g3;
+    out->w_out = L.w_out;
+    out->total = L.total;
+    return RAC_OK;
+}
+
+size_t rac_predictor_cache_bytes(const rac_predictor_config* cfg) {
+    if (!pcfg_valid(cfg)) return 0;
+    return (size_t)cfg->max_batch * (size_t)cfg->window * 2u * (size_t)cfg->model * 2u;
+}
+
+size_t rac_predictor_workspace_bytes(const rac_predictor_config* cfg) {
+    if (!pcfg_valid(cfg)) return 0;
+    return (size_t)pwork(cfg, cfg->max_batch).total;
+}
+
+rac_status rac_predictor_step(const rac_predictor_config* cfg, const void* weights, void* cache, const int32_t* pos,
+                              int32_t batch, const void* h_prev, void* ref_out, void* workspace,
+                              size_t workspace_bytes, rac_stream_t stream) {
+    if (!pcfg_valid(cfg) || batch < 0 || batch > cfg->max_batch) return RAC_ERR_INVALID;
+    if (batch == 0) return RAC_OK;
+    if (!weights || !cache || !pos || !h_prev || !ref_out || !workspace) return RAC_ERR_INVALID;
+    if (!al(weights, 256) || !al(cache, 16) || !al(pos, 4) || !al(h_prev, 16) || !al(ref_out, 16) ||
+        !al(workspace, 256))
+        return RAC_ERR_ALIGN;
+    const PWork W = pwork(cfg, cfg->max_batch);
+    if (workspace_bytes < W.total) return RAC_ERR_CAPACITY;
+    const PWork Wb = pwork(cfg, batch);  // (layout for this batch; fits in the max-batch one)
+    const PLayout L = playout(cfg);
+    const int B = batch, d = cfg->hidden, m = cfg->model, f = cfg->ffn;
+    const uint8_t* wb = static_cast<const uint8_t*>(weights);
+    auto wt = [&](uint64_t off) { return reinterpret_cast<const uint16_t*>(wb + off); };
+    uint8_t* ws = static_cast<uint8_t*>(workspace);
+    float* part = reinterpret_cast<float*>(ws + Wb.part);
+    float* h0 = reinterpret_cast<float*>(ws + Wb.h0);
+    float* h1 = reinterpret_cast<float*>(ws + Wb.h1);
+    float* h2 = reinterpret_cast<float*>(ws + Wb.h2);
+    uint16_t* n = reinterpret_cast<uint16_t*>(ws + Wb.n);
+    float* qkv = reinterpret_cast<float*>(ws + Wb.qkv);
+    uint16_t* o = reinterpret_cast<uint16_t*>(ws + Wb.o);
+    uint16_t* gg = reinterpret_cast<uint16_t*>(ws + Wb.gg);
+    const uint16_t* x = static_cast<const uint16_t*>(h_prev);
+    hipStream_t st = stream;
+    rac_status s;
+    const int si = in_splits(cfg), sd = down_splits(cfg);
+    // h0 = x W_in^T (split K), then n1 = RMSNorm(h0)
+    if ((s = gemm<kPartial>(x, wt(L.w_in), B, m, d, si, part, nullptr, nullptr, st)) != RAC_OK) return s;
+    if ((s = row(nullptr, part, si, B, m, wt(L.g1), h0, n, st)) != RAC_OK) return s;
+    // q, k, v; attention over the window; h1 = h0 + o W_o^T; n2 = RMSNorm(h1)
+    if ((s = gemm<kStore>(n, wt(L.w_qkv), B, 3 * m, m, 1, qkv, nullptr, nullptr, st)) != RAC_OK) return s;
+    {
+        AttnArgs a{qkv, static_cast<uint16_t*>(cache), pos, B, m, cfg->heads, cfg->window, o};
+        void* args[] = {&a};
+        if (hipLaunchKernel(reinterpret_cast<const void*>(pred_attn), dim3((unsigned)(B * cfg->heads)), dim3(kW),
+                            args, 0, st) != hipSuccess)
+            return RAC_ERR_HIP;
+    }
+    if ((s = gemm<kPartial>(o, wt(L.w_o), B, m, m, 1, part, nullptr, nullptr, st)) != RAC_OK) return s;
+    if ((s = row(h0, part, 1, B, m, wt(L.g2), h1, n, st)) != RAC_OK) return s;
+    // SwiGLU; h2 = h1 + g W_down^T; n3 = RMSNorm(h2)
+    if ((s = gemm<kSwiglu>(n, wt(L.w_gu), B, 2 * f, m, 1, nullptr, gg, nullptr, st)) != RAC_OK) return s;
+    if ((s = gemm<kPartial>(gg, wt(L.w_down), B, m, f, sd, part, nullptr, nullptr, st)) != RAC_OK) return s;
+    if ((s = row(h1, part, sd, B, m, wt(L.g3), h2, n, st)) != RAC_OK) return s;
+    // R = x + n3 W_out^T (bf16)
+    return gemm<kResidOut>(n, wt(L.w_out), B, d, m, 1, nullptr, static_cast<uint16_t*>(ref_out), x, st);
+}
+
+}  // extern "C"

@@ -175,3 +175,37 @@ def long_context(seed: int = 0, rows=None, group: int = 128, tokens: int = 32768
     rc = AffineRecipe(tokens, hidden, group, noise="student_t3", noise_scale=0.05,
                       zero_ref_frac=0.5, tag=5)
     return affine_pair(rc, seed, rows)
+
+
+# ---- Decode-phase reference predictor -------------------------------------
+
+PREDICTOR_SECTIONS = ("w_in", "g1", "w_qkv", "w_o", "g2", "w_gu", "w_down", "g3", "w_out")
+
+
+def predictor_weights(hidden: int, model: int, ffn: int, seed: int = 0) -> dict:
+    """Random weights of the one-layer predictor (the trained ones are not
+    available), as bf16 patterns: every matrix [outputs][inputs] drawn
+    N(0, 1/inputs), every RMSNorm gain 1 + N(0, 0.1^2).  W_gu interleaves the
+    gate (even rows) and up (odd rows) projections."""
+    g = np.random.default_rng([seed, 6])
+    mat = lambda o, i: f32_to_bf16_bits(g.standard_normal((o, i), dtype=np.float32) / np.float32(np.sqrt(i)))
+    gain = lambda n: f32_to_bf16_bits(1.0 + 0.1 * g.standard_normal(n, dtype=np.float32))
+    return {"w_in": mat(model, hidden), "g1": gain(model), "w_qkv": mat(3 * model, model),
+            "w_o": mat(model, model), "g2": gain(model), "w_gu": mat(2 * ffn, model),
+            "w_down": mat(model, ffn), "g3": gain(model), "w_out": mat(hidden, model)}
+
+
+def decode_sequence(batch: int, steps: int, seed: int = 0, hidden: int = 4096):
+    """Boundary states of `batch` sequences over `steps` decode steps
+    (GLM-4-9B-shaped, 4096 hidden): a per-channel scale s_c ~ LogNormal(0, 0.5)
+    and a state that drifts, x_t = 0.95 x_{t-1} + 0.3 N(0, 1) s_c, as bf16
+    [steps][batch][hidden]."""
+    g = np.random.default_rng([seed, 7, batch])
+    s_c = g.lognormal(0.0, 0.5, size=hidden).astype(np.float32)
+    x = g.standard_normal((batch, hidden), dtype=np.float32) * s_c
+    out = np.empty((steps, batch, hidden), dtype=np.uint16)
+    for t in range(steps):
+        if t:
+            x = np.float32(0.95) * x + np.float32(0.3) * g.standard_normal((batch, hidden), dtype=np.float32) * s_c
+        out[t] = f32_to_bf16_bits(x)
+    return out

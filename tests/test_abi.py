@@ -39,7 +39,9 @@ def test_exports_every_declared_symbol(lib):
                           "rac_status_string", "rac_span_index_create", "rac_span_index_destroy",
                           "rac_span_index_add", "rac_span_select", "rac_encode_pooled",
                           "rac_saturation_summary", "rac_recon_error_workspace", "rac_recon_error",
-                          "rac_calibrate_workspace", "rac_calibrate", "rac_recon_error_noalloc"}
+                          "rac_calibrate_workspace", "rac_calibrate", "rac_recon_error_noalloc",
+                          "rac_predictor_layout", "rac_predictor_cache_bytes", "rac_predictor_workspace_bytes",
+                          "rac_predictor_step"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -346,3 +348,32 @@ def test_saturation_summary_reads_the_infinity_marks_of_oracle_wires(lib):
     rc, wire, _ = oracle.encode(xb, None, np.full(8, 1.0, np.float32), want_xhat=False, **c)
     # rows 0 and 2: outlier values past the range; row 3: beta; no scale section
     assert rac.rac_saturation_summary(rac.RacConfig(**c), wire) == (3, 5)
+
+
+def test_predictor_layout_is_the_documented_one_and_errors_are_synchronous(lib):
+    up = lambda v: (v + 255) // 256 * 256
+    cfg = rac.PredictorConfig(4096, 512, 8, 2048, 64, 256)
+    lay = rac.rac_predictor_layout(cfg)
+    d, m, f = 4096, 512, 2048
+    o, want = 0, {}
+    for name, n in (("w_in", m * d), ("g1", m), ("w_qkv", 3 * m * m), ("w_o", m * m), ("g2", m),
+                    ("w_gu", 2 * f * m), ("w_down", m * f), ("g3", m), ("w_out", d * m)):
+        want[name] = o
+        o = up(o + 2 * n)
+    want["total"] = o
+    assert lay == want
+    assert rac.rac_predictor_cache_bytes(cfg) == 256 * 64 * 2 * 512 * 2
+    assert rac.rac_predictor_workspace_bytes(cfg) > 0
+    for bad in (rac.PredictorConfig(4000, 512, 8, 2048, 64, 8), rac.PredictorConfig(4096, 512, 4, 2048, 64, 8),
+                rac.PredictorConfig(4096, 512, 8, 2000, 64, 8), rac.PredictorConfig(4096, 512, 8, 2048, 0, 8),
+                rac.PredictorConfig(4096, 512, 8, 2048, 64, 257), rac.PredictorConfig(4096, 192, 3, 2048, 64, 8)):
+        assert rac.rac_predictor_workspace_bytes(bad) == 0
+        with pytest.raises(rac.RacError):
+            rac.rac_predictor_layout(bad)
+    L = rac.library()
+    step = lambda B=4, w=FAKE, c=FAKE, p=FAKE, x=FAKE, r=FAKE, ws=FAKE, cap=1 << 40: L.rac_predictor_step(
+        ctypes.byref(cfg._c()), w, c, p, B, x, r, ws, cap, 0)
+    assert step(B=257) == 1 and step(B=-1) == 1 and step(w=None) == 1 and step(p=None) == 1
+    assert step(w=FAKE + 16) == 2 and step(x=FAKE + 8) == 2 and step(p=FAKE + 2) == 2 and step(ws=FAKE + 64) == 2
+    assert step(cap=rac.rac_predictor_workspace_bytes(cfg) - 1) == 3
+    assert step(B=0, w=None, p=None) == 0      # an empty batch enqueues nothing
