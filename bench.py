@@ -26,9 +26,10 @@ Prints ONE JSON line:
                prefill uplink (4096 x 4096, k = 8), the long context
                (32768 x 4096 at groups 64/128 and 2/3/4/8 bits, k = 16) and the
                tiny case, each with its fraction of 8 TB/s; decode-phase
-               microseconds per call at batch 1/16/64/256; the per-group
-               outlier modes, gathered reference, span selection and pooled fit
-               on the uplink inputs.
+               microseconds per call at batch 1/16/64/256; the decode-phase
+               reference predictor's step time at the same batches; the
+               per-group outlier modes, gathered reference, span selection and
+               pooled fit on the uplink inputs.
 
 --profile WORKLOAD runs only that workload's launches (back-to-back encodes,
 then back-to-back decodes, over rotating buffers) and prints their event
@@ -181,7 +182,7 @@ def main():
                          "climbs for the first ~20 ms of sustained load")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true")
-    ap.add_argument("--profile", choices=["downlink", "uplink", "long_context", "decode_step", "tiny"],
+    ap.add_argument("--profile", choices=["downlink", "uplink", "long_context", "decode_step", "tiny", "predictor"],
                     help="run only this workload's back-to-back encodes and decodes and print their timings")
     ap.add_argument("--iters", type=int, default=20, help="back-to-back launches per kernel in --profile runs")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -266,11 +267,10 @@ def main():
 
     enc_alg = C.alg()
     achieved = enc_alg / (enc_us * 1e-6) / 1e9
-    traffic = None
-    if os.path.exists(TRAFFIC_FILE):
-        t = json.load(open(TRAFFIC_FILE))
-        if t.get("kernel_source_sha256_16") == rocprof_summary.source_hash():
-            traffic = round(t["bytes_per_launch"])
+    # HBM bytes per launch from the committed counter runs of this workload,
+    # while they were taken on the current kernel source
+    traffic = rocprof_summary.block_traffic(TRAFFIC_FILE, "downlink_65536x3584_g128_b4_k4 encode")
+    traffic = round(traffic) if traffic is not None else None
     out = {
         "metric": "encode+reconstruct GB/s of bf16 activation & % HBM peak; decode-step µs/call",
         "value": round(value, 2),
@@ -348,6 +348,7 @@ def all_extras(torch, rac, wl, stream):
     ex["long_context_32768x4096_k16"] = long_context_rates(torch, rac, wl, stream)
     ex["tiny_64x512_g64_b4"] = tiny_rates(torch, rac, wl, stream)
     ex["decode_step"] = decode_step_latency(torch, rac, wl, stream)
+    ex["decode_predictor"] = predictor_latency(torch, rac, wl, stream)
     # graph-replayed encode + decode pair, µs, across the bit widths and with
     # one scale per token row (quantization group = hidden)
     ex["decode_step_graph_pair_us"] = {
@@ -656,10 +657,60 @@ def profile_run(torch, rac, wl, stream, workload, iters):
         out.update(long_context_rates(torch, rac, wl, stream, iters))
     elif workload == "tiny":
         out.update(tiny_rates(torch, rac, wl, stream, iters))
+    elif workload == "predictor":
+        out.update(predictor_latency(torch, rac, wl, stream, iters=iters))
     else:
         for bits, gq in ((2, 128), (4, 128), (8, 128), (4, 4096)):
-            out[f"b{bits}_gq{gq}"] = decode_step_latency(torch, rac, wl, stream, bits, gq, detail=True)
+            for B, v in decode_step_latency(torch, rac, wl, stream, bits, gq, detail=True).items():
+                out[f"b{bits}_gq{gq}_{B}"] = v
     log(f"[bench] profile {workload} done")
+    return out
+
+
+def predictor_latency(torch, rac, wl, stream, batches=(1, 16, 64, 256), iters=50):
+    """Decode-phase reference predictor (one-layer causal Transformer, width
+    512, 8 heads, SwiGLU 2048, window 64, on 4096-wide boundary states):
+    microseconds per step with back-to-back launches (HIP events) and per
+    step replayed from a HIP graph of 20 steps; the weight stream (bytes per
+    step / time) and the matrix-core rate (2 * batch * parameters / time)."""
+    cfg = rac.PredictorConfig(4096, 512, 8, 2048, 64, 256)
+    weights = wl.predictor_weights(cfg.hidden, cfg.model, cfg.ffn, 0)
+    blob = torch.from_numpy(rac.predictor_pack(cfg, weights)).cuda()
+    params = sum(int(v.size) for v in weights.values())
+    cache = torch.zeros(rac.rac_predictor_cache_bytes(cfg) // 2, dtype=torch.int16, device="cuda")
+    ws = torch.empty(rac.rac_predictor_workspace_bytes(cfg), dtype=torch.uint8, device="cuda")
+    out = {"config": "hidden 4096, model 512, 8 heads, ffn 2048, window 64", "weight_bytes": params * 2}
+    for B in batches:
+        x = torch.from_numpy(wl.decode_sequence(B, 1, 0)[0].view(np.int16)).cuda()
+        r = torch.empty_like(x)
+        pos = torch.arange(B, dtype=torch.int32, device="cuda") % 64 + 63
+        step = lambda: rac.rac_predictor_step(cfg, blob, cache, pos, x, r, ws, B, stream=stream)
+        for _ in range(20):
+            step()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for _ in range(iters):
+            step()
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        eager = ev[0].elapsed_time(ev[1]) / iters * 1e3
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(20):
+                rac.rac_predictor_step(cfg, blob, cache, pos, x, r, ws, B)
+        g.replay()
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for _ in range(5):
+            g.replay()
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        graph = ev[0].elapsed_time(ev[1]) * 1e3 / 100
+        out[f"B{B}"] = {"eager_us_per_step": round(eager, 2), "graph_us_per_step": round(graph, 2),
+                        "weight_GBps_graph": round(params * 2 / graph / 1e3, 1),
+                        "mfma_TFLOPs_graph": round(2 * B * params / graph / 1e6, 2)}
+        log(f"[bench] predictor B{B}: {out[f'B{B}']}")
     return out
 
 

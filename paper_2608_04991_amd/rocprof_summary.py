@@ -15,6 +15,11 @@
       configuration (LABELS.json: the bench's --profile output, whose
       configurations appear in launch order, two blocks each, or a list).
 
+  python -m paper_2608_04991_amd.rocprof_summary grids DIR SUBSTR OUT.txt "COMMAND"
+      per-shape statistics of the kernels whose name holds SUBSTR: one line
+      per (kernel, workgroup count), for kernels that interleave with others
+      (each launch of a multi-kernel step has its own grid).
+
   python -m paper_2608_04991_amd.rocprof_summary traffic FETCH_DIR WRITE_DIR \
          COPY_FETCH_DIR COPY_WRITE_DIR COPY_BYTES MIN OUT.json "COMMANDS" [LABELS.json]
       HBM bytes per launch of every block (as above) from two `--pmc` runs of
@@ -133,6 +138,20 @@ def blocks(dirpath: str, min_len: str, out: str, command: str, labels: str = "")
     print("\n".join(lines))
 
 
+def grids(dirpath: str, substr: str, out: str, command: str) -> None:
+    acc = defaultdict(list)
+    for d in _trace_dispatches(dirpath):
+        if substr in d["name"]:
+            acc[(d["name"], d["blocks"])].append(d["us"])
+    lines = ["# rocprofv3 kernel trace, per kernel and workgroup count", f"# command: {command}", "",
+             f"{'calls':>6} {'avg_us':>10} {'median_us':>10} {'min_us':>10} {'wgs':>6}  kernel"]
+    for (name, wgs), us in acc.items():
+        u = sorted(us)
+        lines.append(f"{len(u):>6} {sum(u) / len(u):>10.2f} {u[len(u) // 2]:>10.2f} {u[0]:>10.2f} {wgs:>6}  {name[:100]}")
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def _counter_dispatches(dirpath: str, counter: str):
     rows = list(csv.DictReader(open(_one(os.path.join(dirpath, "**", "*counter_collection.csv")))))
     vals, names, grid = defaultdict(float), {}, {}
@@ -195,6 +214,8 @@ if __name__ == "__main__":
         stats(*sys.argv[2:5], *(int(a) for a in sys.argv[5:6]))
     elif len(sys.argv) > 1 and sys.argv[1] == "blocks":
         blocks(*sys.argv[2:7])
+    elif len(sys.argv) > 1 and sys.argv[1] == "grids":
+        grids(*sys.argv[2:6])
     elif len(sys.argv) > 1 and sys.argv[1] == "traffic":
         traffic(*sys.argv[2:11])
     else:
