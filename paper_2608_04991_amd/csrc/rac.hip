@@ -636,26 +636,9 @@ __device__ __forceinline__ Rsrc xhat_row(const Args& A, uint32_t row) {
 // the launch gives every workgroup at most kMaxGatherRows rows, so all of
 // them are loaded once, before the row loop (a load inside the loop would
 // make the compiler's wait counts conservative for the prefetched rows).
-//
-// LDS copy (the outlier kernel): slot i holds the index of the workgroup's
-// row i, that is token row blockIdx.x + i * gridDim.x (-1 past the last
-// token); filled by the first wavefront before a barrier.
-__device__ __forceinline__ void fill_ref_rows(const Args& A, int32_t* rix) {
-    if (!A.ref_rows) return;
-    if (threadIdx.x < (uint32_t)kWave) {
-        const uint64_t r = (uint64_t)blockIdx.x + (uint64_t)threadIdx.x * gridDim.x;
-        rix[threadIdx.x] = r < A.tokens ? A.ref_rows[r] : -1;
-    }
-    __syncthreads();
-}
-
-__device__ __forceinline__ int32_t ref_index(const Args& A, const int32_t* rix, uint32_t n) {
-    return A.ref_rows ? rix[n & (uint32_t)(kWave - 1)] : 0;
-}
-
-// Register copy (the other kernels): each wavefront holds the same indices in
-// one register, lane i for row i; reading one is a lane read, with no memory
-// wait and no barrier.
+// Each wavefront holds the indices in one register, lane i for the
+// workgroup's row i (token row blockIdx.x + i * gridDim.x, -1 past the last
+// token); reading one is a lane read, with no memory wait and no barrier.
 __device__ __forceinline__ int32_t load_ref_rows_v(const Args& A, uint32_t lane) {
     const uint64_t r = (uint64_t)blockIdx.x + (uint64_t)lane * gridDim.x;
     return (A.ref_rows && r < A.tokens) ? A.ref_rows[r] : -1;
@@ -666,7 +649,7 @@ __device__ __forceinline__ int32_t ref_index_v(const Args& A, int32_t cache, uin
 }
 
 // The index of the workgroup's first row, read directly (a scalar load), so
-// that the first row's loads need not wait for the LDS copy.
+// that the first row's loads need not wait for the register copy's lane read.
 __device__ __forceinline__ int32_t first_ref_index(const Args& A) {
     return (A.ref_rows && blockIdx.x < A.tokens) ? A.ref_rows[blockIdx.x] : 0;
 }
@@ -1265,6 +1248,8 @@ void rac_encode_kernel(Args A) {
 constexpr int kRowsWaves = 4;               // wavefronts per row
 constexpr int kRowsMaxD = 16 * kChunk;       // channels per row (4 chunks per wavefront)
 constexpr int kKeyChBits = 13;               // channel bits of the exact search's key (d <= 8192)
+constexpr int kTop1 = 16;  // largest k whose first threshold comes from one maximum per lane
+constexpr int kTop2 = 48;  // largest k whose first threshold takes two per wavefront lane
 
 template <int NW>
 struct alignas(16) GroupShared {
@@ -1275,6 +1260,7 @@ struct alignas(16) GroupShared {
     uint32_t crw[kCandCap];   // their ref word (the bf16 pair holding the channel)
     uint32_t ccf[kCandCap];   // their group's coefficient pair
     uint32_t smax[NW][kWave]; // lane maxima of |E| of each wavefront
+    uint32_t smax2[NW][kWave];// the lanes' second largest |E| (kTop1 < k <= kTop2)
     uint32_t cnt[2];          // candidate count (LDS atomic), by row parity
     uint32_t xn[2];           // count of the rebuilt list (exact search), by row parity
 };
@@ -1387,7 +1373,7 @@ void rac_encode_rows_kernel(Args A) {
     // first channel of the wavefront's i-th chunk: chunks are dealt round the
     // wavefronts, so a row of fewer than NW * CPW chunks stays balanced
     auto chunk_at = [&](int i) { return (w + i * NW) * kChunk; };
-    __shared__ int32_t RIX[kWave];  // store rows of the reference (gathered references only)
+    const int32_t rix = load_ref_rows_v(A, lane);  // store rows of the gathered reference
     if (w == 0 && lane < 2u) {
         S.cnt[lane] = 0u;
         S.xn[lane] = 0u;
@@ -1410,7 +1396,6 @@ void rac_encode_rows_kernel(Args A) {
             rp[i] = bload128(rr, off);
         }
     }
-    fill_ref_rows(A, RIX);
     // A store that the range check drops, so that stores are outstanding at
     // the loop entry as they are at the end of every row: the compiler's wait
     // analysis then keeps the memory operations in order across the loop and
@@ -1435,7 +1420,7 @@ void rac_encode_rows_kernel(Args A) {
         const uint32_t nrow = row + gridDim.x;
         const bool more = nrow < A.tokens;
         const uint64_t on = (uint64_t)nrow * (uint64_t)d;
-        const Rsrc nx = rsrc(A.x, on, more ? row_bytes : 0u), nr = ref_row(A, nrow, more, ref_index(A, RIX, n + 1u));
+        const Rsrc nx = rsrc(A.x, on, more ? row_bytes : 0u), nr = ref_row(A, nrow, more, ref_index_v(A, rix, n + 1u));
         uint32_t cf[CPW];
 #pragma unroll
         for (int i = 0; i < CPW; ++i) cf[i] = 0u;
@@ -1488,8 +1473,31 @@ void rac_encode_rows_kernel(Args A) {
         // Threshold L: the k-th largest of the 64 maxima of |E| over lane l
         // of all wavefronts, cut to its top 16 bits (which can only lower
         // it); each of >= k such groups holds an element >= L, so every
-        // outlier has |E| >= L.
+        // outlier has |E| >= L.  For kTop1 < k <= kTop2 the groups are the
+        // NW * 64 (wavefront, lane) pairs and each gives its two largest |E|
+        // (two distinct elements): L is the k-th largest of those
+        // 2 * NW * 64 values, again with >= k elements >= L, and on rows
+        // whose large |E| crowd into some channels far fewer elements pass it
+        // (fewer rows overflow the candidate list).  Beyond kTop2 most rows
+        // overflow the list either way and the cheaper bound is kept.
         S.smax[w][lane] = __float_as_uint(lmx);
+        const bool two = k > kTop1 && k <= kTop2;
+        if (two) {
+            uint32_t m1 = 0u, m2 = 0u;
+#pragma unroll
+            for (int i = 0; i < CPW; ++i) {
+                if (chunk_at(i) >= d) continue;
+                float e[8];
+                get8(EL[w][i], lane, e);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const uint32_t b = __float_as_uint(e[j]) & 0x7FFFFFFFu;
+                    m2 = __builtin_elementwise_max(m2, __builtin_elementwise_min(m1, b));
+                    m1 = __builtin_elementwise_max(m1, b);
+                }
+            }
+            S.smax2[w][lane] = m2;
+        }
         __syncthreads();
         // the other buffer was last read by the previous row, which every
         // wavefront has left: reset its candidate count for the next row
@@ -1501,10 +1509,29 @@ void rac_encode_rows_kernel(Args A) {
 #pragma unroll
         for (int ww = 1; ww < NW; ++ww) v = __builtin_elementwise_max(v, S.smax[ww][lane]);
         uint32_t L = 0u;
+        if (!two) {
 #pragma unroll
-        for (int bit = 30; bit >= 15; --bit) {
-            const uint32_t cnd = L | (1u << bit);
-            if ((uint32_t)__builtin_popcountll(ballot(v >= cnd)) >= (uint32_t)k) L = cnd;
+            for (int bit = 30; bit >= 15; --bit) {
+                const uint32_t cnd = L | (1u << bit);
+                if ((uint32_t)__builtin_popcountll(ballot(v >= cnd)) >= (uint32_t)k) L = cnd;
+            }
+        } else {
+            uint32_t v1[NW], v2[NW];
+#pragma unroll
+            for (int ww = 0; ww < NW; ++ww) {
+                v1[ww] = S.smax[ww][lane];
+                v2[ww] = S.smax2[ww][lane];
+            }
+#pragma unroll 1
+            for (int bit = 30; bit >= 15; --bit) {
+                const uint32_t cnd = L | (1u << bit);
+                uint32_t c = 0u;
+#pragma unroll
+                for (int ww = 0; ww < NW; ++ww)
+                    c += (uint32_t)__builtin_popcountll(ballot(v1[ww] >= cnd)) +
+                         (uint32_t)__builtin_popcountll(ballot(v2[ww] >= cnd));
+                if (c >= (uint32_t)k) L = cnd;
+            }
         }
         opaque_n(rp);
         const float Lf = __uint_as_float(L);

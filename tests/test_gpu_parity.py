@@ -110,6 +110,17 @@ def _signed_zero_rows(T, d, distinct):
     return wl.f32_to_bf16_bits(x), wl.f32_to_bf16_bits(np.full((T, d), -1.0, np.float32))
 
 
+def _mixed_tie_rows(T, d, g):
+    """Even rows from the uplink workload with their references, odd rows
+    integer rows full of ties with a zero reference: some wavefronts of a
+    launch find their groups' k_g-th largest untied, others do not."""
+    x, r, _ = wl.prefill_uplink(5, rows=(0, T))
+    xt = wl.f32_to_bf16_bits(_zero_sum_integer_rows(T, d, g, 2, 3.0, 9))
+    x, r = x.copy(), r.copy()
+    x[1::2], r[1::2] = xt[1::2], 0
+    return x, r
+
+
 CASES = {
     "tiny_64x512_g64_b4": (cfgd(64, 512, 64, 64, 4), lambda: wl.tiny(0)[:2]),
     "uplink_37x4096_g128_b4_k8": (cfgd(37, 4096, 128, 128, 4, 8),
@@ -124,7 +135,8 @@ CASES = {
     "long_13x4096_g128_b8_k16": (cfgd(13, 4096, 128, 128, 8, 16),
                                  lambda: wl.long_context(2, rows=(500, 513), group=128)[:2]),
     # Uplink rows with more than 64 elements above the first threshold (about
-    # a quarter of them at g = 64, k = 16, most of them at k = 32 and k = 64),
+    # a quarter of them at g = 64, k = 16 and most at k = 64; at k = 32 the
+    # threshold from the two largest of each wavefront lane leaves few),
     # whose outliers come from the histogram search
     "overflow_uplink_32x4096_g64_b4_k16": (cfgd(32, 4096, 64, 64, 4, 16),
                                            lambda: wl.prefill_uplink(0, rows=(0, 32))[:2]),
@@ -132,7 +144,12 @@ CASES = {
                                             lambda: wl.prefill_uplink(0, rows=(40, 64))[:2]),
     "overflow_uplink_16x4096_g64_b8_k64": (cfgd(16, 4096, 64, 64, 8, 64),
                                            lambda: wl.prefill_uplink(2, rows=(64, 80))[:2]),
-    # rows of 4097..8192 channels (the one-wavefront-per-chunk kernel)
+    # k > 16 with ties everywhere: the two-per-lane threshold, then the
+    # histogram search
+    "ties_heavy_zero_ref_6x4096_g128_k24": (cfgd(6, 4096, 128, 128, 4, 24),
+                                            lambda: (wl.f32_to_bf16_bits(_zero_sum_integer_rows(6, 4096, 128, 0, 0.0, 2)), None)),
+    "uplink_17x4096_g128_b4_k20": (cfgd(17, 4096, 128, 128, 4, 20), lambda: wl.prefill_uplink(4, rows=(200, 217))[:2]),
+    # rows of 4097..8192 channels (four chunks per wavefront)
     "wide_uplink_12x8192_g128_b4_k16": (cfgd(12, 8192, 128, 128, 4, 16),
                                         lambda: wl.prefill_uplink(0, rows=(0, 12), hidden=8192)[:2]),
     "wide_overflow_8x8192_g64_b4_k64": (cfgd(8, 8192, 64, 64, 4, 64),
@@ -198,6 +215,25 @@ CASES = {
     "group_signed_zero_6x1024_g128_b4_kg3": (cfgd(6, 1024, 128, 128, 4, 3, GRP),
                                              lambda: _signed_zero_rows(6, 1024, False)),
     "group_smallest_5x8_b4_kg2": (cfgd(5, 8, 8, 8, 4, 2, GRP), lambda: _affine(5, 8, 8)),
+    # k_g <= 4: the k_g-th largest first, and the round-by-round choice where
+    # a tie crosses it (every group here, some rows or some groups there)
+    "group_ties_zero_ref_6x4096_g128_kg1": (cfgd(6, 4096, 128, 128, 4, 1, GRP),
+                                            lambda: (wl.f32_to_bf16_bits(_zero_sum_integer_rows(6, 4096, 128, 0, 0.0, 3)), None)),
+    "group_ties_zero_ref_6x4096_g128_kg4": (cfgd(6, 4096, 128, 128, 4, 4, GRP),
+                                            lambda: (wl.f32_to_bf16_bits(_zero_sum_integer_rows(6, 4096, 128, 0, 0.0, 4)), None)),
+    "group_tied_pairs_9x4096_g128_kg2": (cfgd(9, 4096, 128, 128, 4, 2, GRP),
+                                         lambda: (wl.f32_to_bf16_bits(_zero_sum_integer_rows(9, 4096, 128, 5, 3.0, 5)), None)),
+    "group_tied_pairs_9x4096_g128_kg3": (cfgd(9, 4096, 128, 128, 4, 3, GRP),
+                                         lambda: (wl.f32_to_bf16_bits(_zero_sum_integer_rows(9, 4096, 128, 5, 3.0, 6)), None)),
+    "group_mixed_tie_rows_16x4096_g128_kg4": (cfgd(16, 4096, 128, 128, 4, 4, GRP), lambda: _mixed_tie_rows(16, 4096, 128)),
+    "group_mixed_tie_rows_16x4096_g128_kg1": (cfgd(16, 4096, 128, 128, 4, 1, GRP), lambda: _mixed_tie_rows(16, 4096, 128)),
+    "group_ties_g256_4x4096_kg4": (cfgd(4, 4096, 256, 256, 4, 4, GRP),
+                                   lambda: (wl.f32_to_bf16_bits(_zero_sum_integer_rows(4, 4096, 256, 3, 5.0, 7)), None)),
+    "group_g256_9x8192_kg3": (cfgd(9, 8192, 128, 256, 4, 3, GRP), lambda: _affine(9, 8192, 128, seed=2)),
+    "group_ties_g8_6x1024_kg2": (cfgd(6, 1024, 8, 8, 4, 2, GRP),
+                                 lambda: (wl.f32_to_bf16_bits(_zero_sum_integer_rows(6, 1024, 8, 0, 0.0, 8)), None)),
+    "group_g16_11x2880_ga64_b4_kg3": (cfgd(11, 2880, 64, 16, 4, 3, GRP), lambda: _affine(11, 2880, 64, seed=3)),
+    "group_g32_13x2880_ga64_b4_kg4": (cfgd(13, 2880, 64, 32, 4, 4, GRP), lambda: _affine(13, 2880, 64, seed=4)),
 }
 
 
