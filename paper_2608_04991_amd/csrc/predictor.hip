@@ -82,14 +82,26 @@ __global__ __launch_bounds__(kW * kGemmWaves) void pred_gemm(Gemm g) {
     for (int r = 0; r < kRt; ++r) acc[r] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     const bool rows_in[kRt] = {m0 + (lane & 15) < g.M, m0 + 16 + (lane & 15) < g.M, m0 + 32 + (lane & 15) < g.M,
                                m0 + 48 + (lane & 15) < g.M};
-    for (int k = 0; k < kq; k += 32) {
-        const bf16x8 bw = *reinterpret_cast<const bf16x8*>(wrow + k);
+    // four 32-wide steps at a time: their weight loads (the HBM stream) are
+    // all issued before the first product waits, then the activation tiles
+    // (read by every column tile, so cache hits) step by step
+    for (int k0 = 0; k0 < kq; k0 += 4 * 32) {
+        bf16x8 bw[4];
 #pragma unroll
-        for (int r = 0; r < kRt; ++r) {
-            bf16x8 av = bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
-            if (rows_in[r])
-                av = *reinterpret_cast<const bf16x8*>(g.a + (size_t)(m0 + 16 * r + (lane & 15)) * g.K + kbeg + kl + k);
-            acc[r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bw, acc[r], 0, 0, 0);
+        for (int u = 0; u < 4; ++u)
+            bw[u] = k0 + 32 * u < kq ? *reinterpret_cast<const bf16x8*>(wrow + k0 + 32 * u)
+                                     : bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            if (k0 + 32 * u >= kq) break;
+            const int k = k0 + 32 * u;
+#pragma unroll
+            for (int r = 0; r < kRt; ++r) {
+                bf16x8 av = bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
+                if (rows_in[r])
+                    av = *reinterpret_cast<const bf16x8*>(g.a + (size_t)(m0 + 16 * r + (lane & 15)) * g.K + kbeg + kl + k);
+                acc[r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bw[u], acc[r], 0, 0, 0);
+            }
         }
     }
     // the four wavefronts' sums, added in the order ((w0 + w1) + w2) + w3
@@ -145,23 +157,33 @@ struct RowArgs {
     uint16_t* n;         // bf16 [M][m]
 };
 
+constexpr int kMaxSplits = 16;  // hidden / 512 and ffn / 512 at their largest
+
 __global__ __launch_bounds__(kRowThreads) void pred_row(RowArgs a) {
-    __shared__ float red[kRowThreads];
+    __shared__ float red[kRowThreads / kW];
     const int b = blockIdx.x, t = threadIdx.x;
     float ss = 0.0f;
     for (int c = t; c < a.m; c += kRowThreads) {
+        // every partial loaded before the first add, then summed in order
+        float pv[kMaxSplits];
+#pragma unroll
+        for (int s = 0; s < kMaxSplits; ++s) pv[s] = s < a.splits ? a.part[((size_t)s * a.M + b) * a.m + c] : 0.0f;
         float v = a.resid ? a.resid[(size_t)b * a.m + c] : 0.0f;
-        for (int s = 0; s < a.splits; ++s) v = v + a.part[((size_t)s * a.M + b) * a.m + c];
+#pragma unroll
+        for (int s = 0; s < kMaxSplits; ++s)
+            if (s < a.splits) v = v + pv[s];
         a.h[(size_t)b * a.m + c] = v;
         ss = ss + v * v;
     }
-    red[t] = ss;
+    // the sum of squares: a butterfly in each wavefront, then the
+    // wavefronts' sums in order
+    for (int o = kW / 2; o > 0; o >>= 1) ss = ss + __shfl_xor(ss, o);
+    if ((t & (kW - 1)) == 0) red[t / kW] = ss;
     __syncthreads();
-    for (int st = kRowThreads / 2; st > 0; st >>= 1) {
-        if (t < st) red[t] = red[t] + red[t + st];
-        __syncthreads();
-    }
-    const float inv = 1.0f / __builtin_sqrtf(red[0] / (float)a.m + kEps);
+    float tot = red[0];
+#pragma unroll
+    for (int w = 1; w < kRowThreads / kW; ++w) tot = tot + red[w];
+    const float inv = 1.0f / __builtin_sqrtf(tot / (float)a.m + kEps);
     for (int c = t; c < a.m; c += kRowThreads)
         a.n[(size_t)b * a.m + c] = to_bf(a.h[(size_t)b * a.m + c] * inv * bf(a.gain[c]));
 }
@@ -171,8 +193,14 @@ __global__ __launch_bounds__(kRowThreads) void pred_row(RowArgs a) {
 // the head: q and k get the rotary position (pairs (2i, 2i + 1) turned by
 // pos * 10000^(-2i/64), angles in binary64), k and v go to the cache slot
 // pos mod W (bf16), and the output is the softmax-weighted sum of the values
-// of positions max(0, pos - W + 1) .. pos, the current one taken from
-// registers (it is never read back from memory in the same launch).
+// of positions max(0, pos - W + 1) .. pos, the current one taken from LDS
+// (it is never read back from memory in the same launch).
+//
+// Scores: lane j takes position first + j (64 positions per pass), its key
+// row (128 bytes) as eight 16-byte loads, against q read from LDS.  Output:
+// lane d sums channels 8 (d % 8) .. 8 (d % 8) + 7 over positions d / 8,
+// d / 8 + 8, ... (one 16-byte load of the value row each), then the eight
+// lanes holding the same channels add their sums.
 struct AttnArgs {
     const float* qkv;    // [B][3m]: q | k | v
     uint16_t* cache;     // [B][W][2][m] bf16
@@ -180,6 +208,17 @@ struct AttnArgs {
     int32_t B, m, heads, window;
     uint16_t* o;         // [B][m] bf16
 };
+
+__device__ __forceinline__ void widen8(const uint4& v, float* f) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        f[2 * i] = __uint_as_float(w[i] << 16);
+        f[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+}
+
+constexpr int kMaxWindow = 1024;
 
 __global__ __launch_bounds__(kW) void pred_attn(AttnArgs a) {
     const int b = blockIdx.x / a.heads, hh = blockIdx.x % a.heads, d = threadIdx.x;
@@ -198,35 +237,40 @@ __global__ __launch_bounds__(kW) void pred_attn(AttnArgs a) {
     }
     const uint16_t kb = to_bf(k), vb = to_bf(v);
     const int slot = p % a.window;
-    uint16_t* cs = a.cache + ((size_t)b * a.window + slot) * 2 * a.m + hh * kHd;
-    cs[d] = kb;
-    cs[a.m + d] = vb;
-    // scores of the window, 64 positions per pass: lane j takes position
-    // first + j; the current position's key is bf16(k) in registers
+    const size_t rowk = (size_t)2 * a.m;  // cache elements per (sequence, slot)
+    uint16_t* const base = a.cache + (size_t)b * a.window * rowk + hh * kHd;
+    base[(size_t)slot * rowk + d] = kb;
+    base[(size_t)slot * rowk + a.m + d] = vb;
     const int first = p - a.window + 1 < 0 ? 0 : p - a.window + 1;
     const int n = p - first + 1;
-    __shared__ float qs[kHd], sc[1024];
-    __shared__ uint16_t kcur[kHd];
+    __shared__ float qs[kHd], sc[kMaxWindow];
+    __shared__ alignas(16) uint16_t kcur[kHd], vcur[kHd];
     qs[d] = q;
     kcur[d] = kb;
+    vcur[d] = vb;
     __syncthreads();
     float mx = -INFINITY;
     for (int j0 = 0; j0 < n; j0 += kW) {
         const int j = j0 + d;
-        float sdot = -INFINITY;
         if (j < n) {
             const int pp = first + j;
+            const uint4* kr = pp == p ? reinterpret_cast<const uint4*>(kcur)
+                                      : reinterpret_cast<const uint4*>(base + (size_t)(pp % a.window) * rowk);
+            uint4 kv[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) kv[i] = kr[i];
             float acc = 0.0f;
-            if (pp == p) {
-                for (int c = 0; c < kHd; ++c) acc = acc + qs[c] * bf(kcur[c]);
-            } else {
-                const uint16_t* kr = a.cache + ((size_t)b * a.window + pp % a.window) * 2 * a.m + hh * kHd;
-                for (int c = 0; c < kHd; ++c) acc = acc + qs[c] * bf(kr[c]);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                float kf[8];
+                widen8(kv[i], kf);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) acc = acc + qs[8 * i + e] * kf[e];
             }
-            sdot = acc * 0.125f;  // 1 / sqrt(64)
+            const float sdot = acc * 0.125f;  // 1 / sqrt(64)
+            sc[j] = sdot;
+            mx = __builtin_fmaxf(mx, sdot);
         }
-        if (j < n) sc[j] = sdot;
-        mx = __builtin_fmaxf(mx, sdot);
     }
     for (int o = 1; o < kW; o <<= 1) mx = __builtin_fmaxf(mx, __shfl_xor(mx, o));
     __syncthreads();
@@ -238,14 +282,33 @@ __global__ __launch_bounds__(kW) void pred_attn(AttnArgs a) {
     }
     for (int o = 1; o < kW; o <<= 1) den = den + __shfl_xor(den, o);
     __syncthreads();
-    float acc = 0.0f;
-    for (int j = 0; j < n; ++j) {
+    const int t = d >> 3, cb = d & 7;
+    float acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
+    for (int j = t; j < n; j += 8) {
         const int pp = first + j;
-        const float vv = pp == p ? bf(vb)
-                                 : bf(a.cache[((size_t)b * a.window + pp % a.window) * 2 * a.m + a.m + hh * kHd + d]);
-        acc = acc + sc[j] * vv;
+        const uint4 vv = pp == p ? reinterpret_cast<const uint4*>(vcur)[cb]
+                                 : reinterpret_cast<const uint4*>(base + (size_t)(pp % a.window) * rowk + a.m)[cb];
+        float vf[8];
+        widen8(vv, vf);
+        const float w = sc[j];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = acc[e] + w * vf[e];
     }
-    a.o[(size_t)b * a.m + hh * kHd + d] = to_bf(acc / den);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        acc[e] = acc[e] + __shfl_xor(acc[e], 8);
+        acc[e] = acc[e] + __shfl_xor(acc[e], 16);
+        acc[e] = acc[e] + __shfl_xor(acc[e], 32);
+    }
+    if (t == 0) {
+        uint32_t w[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            w[i] = (uint32_t)to_bf(acc[2 * i] / den) | ((uint32_t)to_bf(acc[2 * i + 1] / den) << 16);
+        reinterpret_cast<uint4*>(a.o + (size_t)b * a.m + hh * kHd)[cb] = uint4{w[0], w[1], w[2], w[3]};
+    }
 }
 
 // ---------------------------------------------------------------------------
