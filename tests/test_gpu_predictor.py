@@ -97,3 +97,14 @@ def test_predictor_single_and_full_batches(batch):
     cfg = rac.PredictorConfig(4096, 512, 8, 2048, 64, 256)
     say(f"[gpu] predictor batch {batch}, 3 steps")
     _run(cfg, batch, 3, lambda s, b: s + 100 * (b % 2), seed=1)
+
+
+@pytest.mark.parametrize("window,start", [(300, 400), (1024, 1500)])
+def test_predictor_windows_longer_than_one_pass_of_64_positions(window, start):
+    # sequences start deep into their positions, so the window reaches back
+    # over slots never written (zero on both sides) and spans several passes
+    # of 64 positions in the score loop
+    cfg = rac.PredictorConfig(512, 128, 2, 256, window, 8)
+    say(f"[gpu] predictor 512/128/2/256, window {window}, batch 8, 4 steps from position {start}")
+    _run(cfg, 8, 4, lambda s, b: start + s + 37 * b, seed=2)
+
