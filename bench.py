@@ -53,6 +53,7 @@ HBM_PEAK_GBPS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
 # calibrated HBM traffic per launch of the headline encode, from rocprofv3
 # FETCH_SIZE / WRITE_SIZE runs (see paper_2608_04991_amd/rocprof_summary.py)
+LLC_BYTES = 256 << 20    # MI355X last-level (Infinity) cache
 TRAFFIC_FILE = os.path.join(PROFILES, "rac_encode_prefill_downlink_65536x3584_traffic.json")
 HEADLINE_KERNEL = "rac_encode_rows_kernel<4, 4, 4, 4, 2, false>"
 
@@ -318,12 +319,16 @@ def main():
 
 
 def prefill_uplink(torch, rac, wl, stream):
-    """The 4096 x 4096 uplink on rotating buffer sets (> 1.2 GB in total)."""
+    """The 4096 x 4096 uplink on rotating buffer sets: enough of them that a
+    pass of decodes (each reading its wire and reference) and a pass of
+    encodes (each reading x and the reference) read at least twice the
+    256 MiB last-level cache, so no set is still cached when it comes round
+    again (the reconstruction stores are non-temporal and do not evict it)."""
     T, d = 4096, 4096
     cfg = rac.RacConfig(T, d, 128, 128, 4, 8)
     xb, rb, _ = wl.prefill_uplink(0)
-    set_bytes = 2 * T * d * 2 + 2 * T * d * 4 + rac.rac_wire_size(cfg)
-    nsets = max(2, int(np.ceil(1.2e9 / set_bytes)))
+    dec_read = T * d * 2 + rac.rac_wire_size(cfg)
+    nsets = max(2, int(np.ceil(2 * LLC_BYTES / dec_read)))
     return Codec(torch, rac, cfg, to_dev(torch, xb), to_dev(torch, rb), nsets, stream), rb
 
 
