@@ -70,9 +70,10 @@ struct alignas(8) Args {
     int32_t lg_cpg_q;
     int32_t k;          // outliers per row, or per group with gout
     int32_t gout;       // per-group outlier mode
-    int32_t cf_given;   // the wire already holds every row's (alpha, beta) (pooled fit)
+    int32_t cf_given;   // pooled fit: the pairs are given (see pool_first_rows)
     int32_t segments;   // pooled fit: segment count and row starts [segments + 1]
     const int32_t* seg_start;
+    int32_t pool_first_rows;  // pooled fit: a segment's pair is in its first row only
     int32_t fixed;
     int32_t xhat_bf16;
     float inv_ga;       // 1 / g_a (exact, power of two)
@@ -1358,6 +1359,34 @@ __device__ __forceinline__ void append_bound(G& S, uint32_t* counter, const floa
     }
 }
 
+// Pooled fit: the first row of the segment holding token row `row`, that is
+// seg_start[s] for the largest s < segments with seg_start[s] <= row.  The
+// search takes 64 starts per level (one vector load, then the highest lane of
+// a ballot: the sorted starts at or below the row are a prefix of the
+// lanes), so up to 64 segments take one level and 4096 two.  The result is
+// clamped to [0, tokens - 1]: whatever the starts hold, the row read stays in
+// the coefficient section.
+__device__ __forceinline__ uint32_t seg_first_row(const Args& A, uint32_t row) {
+    const uint32_t lane = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+    int64_t base = 0, span = A.segments;
+    int32_t f = 0;
+    for (;;) {
+        const int64_t stride = (span + kWave - 1) / kWave;
+        const int64_t idx = base + (int64_t)lane * stride;
+        const int32_t v = idx < base + span ? A.seg_start[idx] : INT32_MAX;
+        const uint64_t le = ballot(v <= (int32_t)row);
+        const int c = le ? 63 - __builtin_clzll(le) : 0;
+        base += (int64_t)c * stride;
+        if (stride == 1) {
+            f = (int32_t)rdlane((uint32_t)v, c);
+            break;
+        }
+        span = stride < A.segments - base ? stride : A.segments - base;
+    }
+    f = f < 0 ? 0 : f;
+    return (uint32_t)f < A.tokens ? (uint32_t)f : A.tokens - 1u;
+}
+
 // Hide held ref values from the optimizer before they are widened again (a
 // reused widening would keep 8 more registers per chunk alive across the row).
 template <int N>
@@ -1447,6 +1476,9 @@ void rac_encode_rows_kernel(Args A) {
         // a2-a3 per chunk: fit of the lane's group, E; lane maxima of |E|
         // (per chunk, and over the wavefront's chunks)
         const Rsrc rcoef = rsrc(A.coef, (uint64_t)row * nga, nga * 4u);
+        // pooled fit: the pair is read from the first row of the row's segment
+        const uint32_t frow = GIVEN ? seg_first_row(A, row) : row;
+        const Rsrc rgiven = rsrc(A.coef, (uint64_t)frow * nga, GIVEN ? nga * 4u : 0u);
         float lmc[CPW];
 #pragma unroll
         for (int i = 0; i < CPW; ++i) lmc[i] = 0.0f;
@@ -1467,7 +1499,8 @@ void rac_encode_rows_kernel(Args A) {
             }
             const float crr = lsum<GA>(tree8(uu), lv_a), crx = lsum<GA>(tree8(uv), lv_a);
             if constexpr (GIVEN) {
-                cf[i] = bload32(rcoef, (c0 >> A.lg_a) * 4u);
+                cf[i] = bload32(rgiven, (c0 >> A.lg_a) * 4u);
+                bstore32(rcoef, first_a ? (c0 >> A.lg_a) * 4u : kOut, cf[i]);
             } else {
                 cf[i] = fit_coef(crr, crx, mr, mx);
                 bstore32(rcoef, first_a ? (c0 >> A.lg_a) * 4u : kOut, cf[i]);
@@ -2049,8 +2082,15 @@ __global__ __launch_bounds__(kWave * kPoolWaves) void rac_pool_kernel(Args A, co
     }
     __syncthreads();
     const uint32_t cf = cf_shared;
-    for (int64_t t = lo + threadIdx.x; t < hi; t += (int64_t)kWave * kPoolWaves)
-        bstore32(rsrc(A.coef, (uint64_t)t * nga, nga * 4u), j * 4u, cf);
+    if (A.pool_first_rows) {
+        // the outlier encode takes the pair from the segment's first row and
+        // writes every row's slot itself (4-byte stores from each segment's
+        // 32 or more workgroups into shared lines cost 4 us here)
+        if (threadIdx.x == 0u && lo < hi) bstore32(rsrc(A.coef, (uint64_t)lo * nga, nga * 4u), j * 4u, cf);
+    } else {
+        for (int64_t t = lo + threadIdx.x; t < hi; t += (int64_t)kWave * kPoolWaves)
+            bstore32(rsrc(A.coef, (uint64_t)t * nga, nga * 4u), j * 4u, cf);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -2660,6 +2700,7 @@ rac_status rac_encode_pooled(const rac_config* cfg, const void* x, const void* r
     A.segments = (int32_t)segments;
     A.seg_start = seg_start;
     float4* mom = reinterpret_cast<float4*>(A.codes);
+    A.pool_first_rows = use_rows_kernel(A) ? 1 : 0;
     // 1. row moments
     const int threads = A.nch * kWave;
     void* margs[] = {&A, &mom};

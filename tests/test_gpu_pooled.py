@@ -69,7 +69,17 @@ CASES = {
                                     lambda: wl.prefill_uplink(5, rows=(0, 66))[:2]),
     "ragged_chunk_23x2880_ga64_gq32_b4": (cfgd(23, 2880, 64, 32, 4), [0, 7, 23],
                                           lambda: wl.affine_pair(wl.AffineRecipe(23, 2880, 64), 0)[:2]),
+    # the outlier encode finds each row's segment 64 starts at a time: about
+    # 100 segments take two levels of that search, 4100 one-row segments three
+    "many_segments_300x1024_g128_b4_k4": (cfgd(300, 1024, 128, 128, 4, 4),
+                                          np.unique(np.concatenate([[0, 300], np.cumsum(
+                                              np.random.default_rng(21).integers(1, 6, 120))]))[:None],
+                                          lambda: wl.prefill_uplink(7, rows=(0, 300), hidden=1024)[:2]),
+    "one_row_segments_4100x512_g64_b4_k2": (cfgd(4100, 512, 64, 64, 4, 2), np.arange(4101),
+                                            lambda: wl.long_context(1, rows=(0, 4100), group=64, hidden=512)[:2]),
 }
+_c, _s, _g = CASES["many_segments_300x1024_g128_b4_k4"]
+CASES["many_segments_300x1024_g128_b4_k4"] = (_c, _s[_s <= 300], _g)
 
 
 @pytest.mark.parametrize("name", list(CASES))
