@@ -1281,6 +1281,7 @@ struct alignas(16) GroupShared {
     uint32_t ccf[kCandCap];   // their group's coefficient pair
     uint32_t smax[NW][kWave]; // lane maxima of |E| of each wavefront
     uint32_t smax2[NW][kWave];// the lanes' second largest |E| (kTop1 < k <= kTop2)
+    uint32_t thr;             // that threshold, from wavefront 0
     uint32_t cnt[2];          // candidate count (LDS atomic), by row parity
     uint32_t xn[2];           // count of the rebuilt list (exact search), by row parity
 };
@@ -1397,7 +1398,10 @@ __device__ __forceinline__ void opaque_n(uint4 (&r)[N]) {
 
 // GIVEN: the wire already holds every row's (alpha, beta) (pooled fit), which
 // is read instead of fitted.
-template <int BITS, int GA, int GQ, int NW, int CPW, bool GIVEN>
+// TWO: the first outlier threshold from the two largest |E| of each
+// (wavefront, lane) (for kTop1 < k <= kTop2; a separate kernel, so that the
+// other k keep the code and registers of the one-value bound).
+template <int BITS, int GA, int GQ, int NW, int CPW, bool GIVEN, bool TWO>
 __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(CPW == 2 ? 7 : 4)))
 void rac_encode_rows_kernel(Args A) {
     // (a row's lists are read before the next row's first barrier and
@@ -1533,8 +1537,8 @@ void rac_encode_rows_kernel(Args A) {
         // (fewer rows overflow the candidate list).  Beyond kTop2 most rows
         // overflow the list either way and the cheaper bound is kept.
         S.smax[w][lane] = __float_as_uint(lmx);
-        const bool two = k > kTop1 && k <= kTop2;
-        if (two) {
+        constexpr bool two = TWO;
+        if constexpr (two) {
             uint32_t m1 = 0u, m2 = 0u;
 #pragma unroll
             for (int i = 0; i < CPW; ++i) {
@@ -1561,29 +1565,37 @@ void rac_encode_rows_kernel(Args A) {
 #pragma unroll
         for (int ww = 1; ww < NW; ++ww) v = __builtin_elementwise_max(v, S.smax[ww][lane]);
         uint32_t L = 0u;
-        if (!two) {
+        if constexpr (!two) {
 #pragma unroll
             for (int bit = 30; bit >= 15; --bit) {
                 const uint32_t cnd = L | (1u << bit);
                 if ((uint32_t)__builtin_popcountll(ballot(v >= cnd)) >= (uint32_t)k) L = cnd;
             }
         } else {
-            uint32_t v1[NW], v2[NW];
+            // wavefront 0 alone searches (its ballot counts are scalar work,
+            // and the compute unit's scalar unit is shared by all its
+            // wavefronts), then hands L over through LDS
+            if (w == 0) {
+                uint32_t v1[NW], v2[NW];
 #pragma unroll
-            for (int ww = 0; ww < NW; ++ww) {
-                v1[ww] = S.smax[ww][lane];
-                v2[ww] = S.smax2[ww][lane];
-            }
+                for (int ww = 0; ww < NW; ++ww) {
+                    v1[ww] = S.smax[ww][lane];
+                    v2[ww] = S.smax2[ww][lane];
+                }
 #pragma unroll 1
-            for (int bit = 30; bit >= 15; --bit) {
-                const uint32_t cnd = L | (1u << bit);
-                uint32_t c = 0u;
+                for (int bit = 30; bit >= 15; --bit) {
+                    const uint32_t cnd = L | (1u << bit);
+                    uint32_t c = 0u;
 #pragma unroll
-                for (int ww = 0; ww < NW; ++ww)
-                    c += (uint32_t)__builtin_popcountll(ballot(v1[ww] >= cnd)) +
-                         (uint32_t)__builtin_popcountll(ballot(v2[ww] >= cnd));
-                if (c >= (uint32_t)k) L = cnd;
+                    for (int ww = 0; ww < NW; ++ww)
+                        c += (uint32_t)__builtin_popcountll(ballot(v1[ww] >= cnd)) +
+                             (uint32_t)__builtin_popcountll(ballot(v2[ww] >= cnd));
+                    if (c >= (uint32_t)k) L = cnd;
+                }
+                if (lane == 0u) S.thr = L;
             }
+            __syncthreads();
+            L = uniform(S.thr);
         }
         opaque_n(rp);
         const float Lf = __uint_as_float(L);
@@ -2359,20 +2371,25 @@ KernelFn pick_encode(const Args& A, int bits) {
     return encode_for<-1, -1>(bits, om);
 }
 
-template <int GA, int GQ, int CPW, bool GIVEN>
+template <int GA, int GQ, int CPW, bool GIVEN, bool TWO>
 KernelFn rows_for_bits(int bits) {
     switch (bits) {
-        case 2: return rac_encode_rows_kernel<2, GA, GQ, kRowsWaves, CPW, GIVEN>;
-        case 3: return rac_encode_rows_kernel<3, GA, GQ, kRowsWaves, CPW, GIVEN>;
-        case 4: return rac_encode_rows_kernel<4, GA, GQ, kRowsWaves, CPW, GIVEN>;
-        default: return rac_encode_rows_kernel<8, GA, GQ, kRowsWaves, CPW, GIVEN>;
+        case 2: return rac_encode_rows_kernel<2, GA, GQ, kRowsWaves, CPW, GIVEN, TWO>;
+        case 3: return rac_encode_rows_kernel<3, GA, GQ, kRowsWaves, CPW, GIVEN, TWO>;
+        case 4: return rac_encode_rows_kernel<4, GA, GQ, kRowsWaves, CPW, GIVEN, TWO>;
+        default: return rac_encode_rows_kernel<8, GA, GQ, kRowsWaves, CPW, GIVEN, TWO>;
     }
 }
 
 // Rows of up to 4096 channels: two chunks per wavefront; up to 8192: four.
+// The two-value threshold for kTop1 < k <= kTop2 (not with given pairs,
+// which keep the one-value bound: either bound is exact).
 template <int GA, int GQ, bool GIVEN = false>
-KernelFn rows_for(int bits, int d) {
-    return d <= kRowsWaves * 2 * kChunk ? rows_for_bits<GA, GQ, 2, GIVEN>(bits) : rows_for_bits<GA, GQ, 4, GIVEN>(bits);
+KernelFn rows_for(int bits, int d, int k) {
+    const bool two = !GIVEN && k > kTop1 && k <= kTop2;
+    if (d <= kRowsWaves * 2 * kChunk)
+        return two ? rows_for_bits<GA, GQ, 2, GIVEN, !GIVEN>(bits) : rows_for_bits<GA, GQ, 2, GIVEN, false>(bits);
+    return two ? rows_for_bits<GA, GQ, 4, GIVEN, !GIVEN>(bits) : rows_for_bits<GA, GQ, 4, GIVEN, false>(bits);
 }
 
 // Rows with outliers take the NW-wavefront kernel when it holds the whole
@@ -2385,15 +2402,15 @@ bool use_rows_kernel(const Args& A) {
 KernelFn pick_rows(const Args& A, int bits) {
     // given pairs (pooled fit): the fixed 128 and 64 shapes and the generic one
     if (A.cf_given) {
-        if (A.lane_lv_a == 4 && A.lane_lv_q == 4) return rows_for<4, 4, true>(bits, A.d);
-        if (A.lane_lv_a == 3 && A.lane_lv_q == 3) return rows_for<3, 3, true>(bits, A.d);
-        return rows_for<-1, -1, true>(bits, A.d);
+        if (A.lane_lv_a == 4 && A.lane_lv_q == 4) return rows_for<4, 4, true>(bits, A.d, A.k);
+        if (A.lane_lv_a == 3 && A.lane_lv_q == 3) return rows_for<3, 3, true>(bits, A.d, A.k);
+        return rows_for<-1, -1, true>(bits, A.d, A.k);
     }
-    if (A.lane_lv_a == 3 && A.lane_lv_q == 3) return rows_for<3, 3>(bits, A.d);
-    if (A.lane_lv_a == 4 && A.lane_lv_q == 4) return rows_for<4, 4>(bits, A.d);
-    if (A.lane_lv_a == 3 && A.lane_lv_q == 4) return rows_for<3, 4>(bits, A.d);
-    if (A.lane_lv_a == 4 && A.lane_lv_q == 3) return rows_for<4, 3>(bits, A.d);
-    return rows_for<-1, -1>(bits, A.d);
+    if (A.lane_lv_a == 3 && A.lane_lv_q == 3) return rows_for<3, 3>(bits, A.d, A.k);
+    if (A.lane_lv_a == 4 && A.lane_lv_q == 4) return rows_for<4, 4>(bits, A.d, A.k);
+    if (A.lane_lv_a == 3 && A.lane_lv_q == 4) return rows_for<3, 4>(bits, A.d, A.k);
+    if (A.lane_lv_a == 4 && A.lane_lv_q == 3) return rows_for<4, 3>(bits, A.d, A.k);
+    return rows_for<-1, -1>(bits, A.d, A.k);
 }
 
 template <int OM, bool BF16>
