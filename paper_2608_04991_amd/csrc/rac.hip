@@ -1529,13 +1529,14 @@ void rac_encode_rows_kernel(Args A) {
         // Threshold L: the k-th largest of the 64 maxima of |E| over lane l
         // of all wavefronts, cut to its top 16 bits (which can only lower
         // it); each of >= k such groups holds an element >= L, so every
-        // outlier has |E| >= L.  For kTop1 < k <= kTop2 the groups are the
-        // NW * 64 (wavefront, lane) pairs and each gives its two largest |E|
-        // (two distinct elements): L is the k-th largest of those
-        // 2 * NW * 64 values, again with >= k elements >= L, and on rows
-        // whose large |E| crowd into some channels far fewer elements pass it
-        // (fewer rows overflow the candidate list).  Beyond kTop2 most rows
-        // overflow the list either way and the cheaper bound is kept.
+        // outlier has |E| >= L.  For kTop1 < k <= kTop2 each of the 64 groups
+        // gives its two largest |E| (two distinct elements; from the two
+        // largest of each wavefront's 16 channels of the lane): L is the
+        // k-th largest of those 128 values, again with >= k elements >= L,
+        // and on rows whose large |E| crowd into some channels far fewer
+        // elements pass it (fewer rows overflow the candidate list).  Beyond
+        // kTop2 most rows overflow the list either way and the cheaper bound
+        // is kept.
         S.smax[w][lane] = __float_as_uint(lmx);
         constexpr bool two = TWO;
         if constexpr (two) {
@@ -1576,20 +1577,22 @@ void rac_encode_rows_kernel(Args A) {
             // and the compute unit's scalar unit is shared by all its
             // wavefronts), then hands L over through LDS
             if (w == 0) {
-                uint32_t v1[NW], v2[NW];
+                // the two largest of the lane's 2 * NW values: two distinct
+                // elements of the 64 channels of lane l in all wavefronts
+                uint32_t a1 = 0u, a2 = 0u;
 #pragma unroll
                 for (int ww = 0; ww < NW; ++ww) {
-                    v1[ww] = S.smax[ww][lane];
-                    v2[ww] = S.smax2[ww][lane];
+                    const uint32_t u1 = S.smax[ww][lane], u2 = S.smax2[ww][lane];
+                    a2 = __builtin_elementwise_max(a2, __builtin_elementwise_min(a1, u1));
+                    a1 = __builtin_elementwise_max(a1, u1);
+                    a2 = __builtin_elementwise_max(a2, __builtin_elementwise_min(a1, u2));
+                    a1 = __builtin_elementwise_max(a1, u2);
                 }
-#pragma unroll 1
+#pragma unroll
                 for (int bit = 30; bit >= 15; --bit) {
                     const uint32_t cnd = L | (1u << bit);
-                    uint32_t c = 0u;
-#pragma unroll
-                    for (int ww = 0; ww < NW; ++ww)
-                        c += (uint32_t)__builtin_popcountll(ballot(v1[ww] >= cnd)) +
-                             (uint32_t)__builtin_popcountll(ballot(v2[ww] >= cnd));
+                    const uint32_t c = (uint32_t)__builtin_popcountll(ballot(a1 >= cnd)) +
+                                       (uint32_t)__builtin_popcountll(ballot(a2 >= cnd));
                     if (c >= (uint32_t)k) L = cnd;
                 }
                 if (lane == 0u) S.thr = L;
