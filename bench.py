@@ -348,6 +348,7 @@ def all_extras(torch, rac, wl, stream):
     ex["gathered_reference"] = gather_rates(torch, rac, U, 50)
     ex["pooled_fit"] = pooled_rates(torch, rac, U, 50)
     ex["span_selection"] = span_selection_cost(rac, 4096)
+    ex["calibration"] = calibration_rates(torch, rac, wl, U)
     U.free()
     del U
     ex["long_context_32768x4096_k16"] = long_context_rates(torch, rac, wl, stream)
@@ -486,6 +487,51 @@ def pooled_rates(torch, rac, U, steps):
     return {"segments": int(seg.numel()) - 1, "encode_us": round(us, 2),
             "hbm_frac_by_encode_bytes": frac(algorithmic_bytes(T, d, wb), us),
             "hbm_frac_by_own_bytes": frac(own, us)}
+
+
+def calibration_rates(torch, rac, wl, U, steps=20):
+    """The offline calibration's two costs.  rac_recon_error over the
+    uplink's 4096 x 4096 reconstruction (reads x, bf16, and the fp32
+    reconstruction once: 6 bytes per element), back to back over the rotating
+    buffer sets; and one rac_calibrate over a grid of 108 candidates
+    (g_a, g_q in {64, 128, 256}, b in {2, 3, 4, 8}, k_g in {0, 1, 2}) on 1024
+    uplink rows, host time of the whole call (it synchronizes to read its
+    results back)."""
+    T, d = U.cfg.tokens, U.cfg.hidden
+    ws = torch.empty(rac.rac_recon_error_workspace(T), dtype=torch.uint8, device="cuda")
+    stats = torch.empty(3, dtype=torch.float64, device="cuda")
+    for i in range(U.n):
+        U.enc(i)
+    for i in range(2 * U.n):
+        s = U.sets[i % U.n]
+        rac.rac_recon_error(T, d, s["x"], s["xhat"], stats, ws, stream=U.stream)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    ev[0].record(U.stream)
+    for i in range(steps):
+        s = U.sets[i % U.n]
+        rac.rac_recon_error(T, d, s["x"], s["xhat"], stats, ws, stream=U.stream)
+    ev[1].record(U.stream)
+    torch.cuda.synchronize()
+    err_us = ev[0].elapsed_time(ev[1]) / steps * 1e3
+    n = 1024
+    xs, rs = U.sets[0]["x"][:n].contiguous(), U.sets[0]["ref"][:n].contiguous()
+    grp = rac.RAC_FLAG_GROUP_OUTLIERS
+    configs = [rac.RacConfig(n, d, ga, gq, b, kg, grp if kg else 0)
+               for ga in (64, 128, 256) for gq in (64, 128, 256) for b in (2, 3, 4, 8) for kg in (0, 1, 2)]
+    wsc = torch.empty(rac.rac_calibrate_workspace(configs), dtype=torch.uint8, device="cuda")
+    rac.rac_calibrate(xs, rs, configs, 1e-3, workspace=wsc, stream=U.stream)
+    times = []
+    for _ in range(3):
+        t0 = time.perf_counter()
+        chosen, res = rac.rac_calibrate(xs, rs, configs, 1e-3, workspace=wsc, stream=U.stream)
+        times.append(time.perf_counter() - t0)
+    c = configs[chosen]
+    return {"recon_error_4096x4096_us": round(err_us, 2),
+            "recon_error_hbm_frac": frac(T * d * 6, err_us),
+            "calibrate_1024x4096_108_candidates_ms": round(min(times) * 1e3, 2),
+            "chosen_for_nmse_1e-3": {"g_a": c.group_align, "g_q": c.group_quant, "bits": c.bits, "k_g": c.outlier_k,
+                                     "wire_bytes": res[chosen]["wire_bytes"], "nmse": res[chosen]["nmse"]}}
 
 
 def span_selection_cost(rac, T, window=16, n_hist=7):
