@@ -27,6 +27,8 @@
 // in a fixed order, by the row kernel that follows).  Every weight byte is
 // read once per 64 batch rows.
 #include <hip/hip_runtime.h>
+
+#include <cmath>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -191,7 +193,8 @@ __global__ __launch_bounds__(kRowThreads) void pred_row(RowArgs a) {
 // ---------------------------------------------------------------------------
 // Attention of one (sequence, head) per wavefront.  Lane d holds channel d of
 // the head: q and k get the rotary position (pairs (2i, 2i + 1) turned by
-// pos * 10000^(-2i/64), angles in binary64), k and v go to the cache slot
+// pos * 10000^(-2i/64): the angle formed and reduced in binary64, its sine
+// and cosine in binary32), k and v go to the cache slot
 // pos mod W (bf16), and the output is the softmax-weighted sum of the values
 // of positions max(0, pos - W + 1) .. pos, the current one taken from LDS
 // (it is never read back from memory in the same launch).
@@ -207,6 +210,7 @@ struct AttnArgs {
     const int32_t* pos;  // [B]
     int32_t B, m, heads, window;
     uint16_t* o;         // [B][m] bf16
+    double theta[kHd / 2];  // 10000^(-2i/64), i < 32 (binary64, from the host's pow)
 };
 
 __device__ __forceinline__ void widen8(const uint4& v, float* f) {
@@ -227,9 +231,14 @@ __global__ __launch_bounds__(kW) void pred_attn(AttnArgs a) {
     float q = row[d], k = row[a.m + d];
     const float v = row[2 * a.m + d];
     {
-        const int i = d >> 1;
-        const double th = (double)p * exp2(-(double)(2 * i) / (double)kHd * 13.287712379549449);  // 10000^(-2i/64)
-        const float c = (float)cos(th), sn = (float)sin(th);
+        // the angle pos * theta_i in binary64, reduced to [-pi, pi] there (the
+        // product k * 2 pi is exact to far below a binary32 ulp for any int32
+        // position), then a binary32 sincos
+        const double th = (double)p * a.theta[d >> 1];
+        const double kTwoPi = 6.283185307179586476925;
+        const float r = (float)(th - kTwoPi * rint(th / kTwoPi));
+        float sn, c;
+        sincosf(r, &sn, &c);
         const float qo = __shfl_xor(q, 1), ko = __shfl_xor(k, 1);
         // (a, b) -> (a cos - b sin, a sin + b cos): the even lane holds a
         q = (d & 1) ? qo * sn + q * c : q * c - qo * sn;
@@ -286,15 +295,27 @@ __global__ __launch_bounds__(kW) void pred_attn(AttnArgs a) {
     float acc[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
-    for (int j = t; j < n; j += 8) {
-        const int pp = first + j;
-        const uint4 vv = pp == p ? reinterpret_cast<const uint4*>(vcur)[cb]
-                                 : reinterpret_cast<const uint4*>(base + (size_t)(pp % a.window) * rowk + a.m)[cb];
-        float vf[8];
-        widen8(vv, vf);
-        const float w = sc[j];
+    // positions t, t + 8, ...: eight value rows loaded before any is added
+    // (the sums run in that order)
+    for (int j0 = t; j0 < n; j0 += 64) {
+        uint4 vv[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] = acc[e] + w * vf[e];
+        for (int u = 0; u < 8; ++u) {
+            const int j = j0 + 8 * u, pp = first + j;
+            vv[u] = j >= n ? uint4{0u, 0u, 0u, 0u}
+                  : pp == p ? reinterpret_cast<const uint4*>(vcur)[cb]
+                            : reinterpret_cast<const uint4*>(base + (size_t)(pp % a.window) * rowk + a.m)[cb];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int j = j0 + 8 * u;
+            if (j >= n) break;
+            float vf[8];
+            widen8(vv[u], vf);
+            const float w = sc[j];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[e] = acc[e] + w * vf[e];
+        }
     }
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -461,7 +482,8 @@ rac_status rac_predictor_step(const rac_predictor_config* cfg, const void* weigh
     // q, k, v; attention over the window; h1 = h0 + o W_o^T; n2 = RMSNorm(h1)
     if ((s = gemm<kStore>(n, wt(L.w_qkv), B, 3 * m, m, 1, qkv, nullptr, nullptr, st)) != RAC_OK) return s;
     {
-        AttnArgs a{qkv, static_cast<uint16_t*>(cache), pos, B, m, cfg->heads, cfg->window, o};
+        AttnArgs a{qkv, static_cast<uint16_t*>(cache), pos, B, m, cfg->heads, cfg->window, o, {}};
+        for (int i = 0; i < kHd / 2; ++i) a.theta[i] = std::pow(10000.0, -2.0 * i / kHd);
         void* args[] = {&a};
         if (hipLaunchKernel(reinterpret_cast<const void*>(pred_attn), dim3((unsigned)(B * cfg->heads)), dim3(kW),
                             args, 0, st) != hipSuccess)
