@@ -454,12 +454,13 @@ def outlier_mode_rates(torch, rac, U, steps):
     return res
 
 
-def pooled_rates(torch, rac, U, steps):
+def pooled_rates(torch, rac, U, steps, reps=5):
     """rac_encode_pooled on the uplink inputs, with segments standing for
     retrieved spans (random lengths of 1 to 600 rows): average time of the
-    whole call (its three launches) over `steps` back-to-back calls, and the
-    fraction of 8 TB/s by the per-token encode's algorithmic bytes and by the
-    pooled call's own (the moments pass reads x and ref a second time)."""
+    whole call (its three launches) over `steps` back-to-back calls (the
+    median of `reps` such timings), and the fraction of 8 TB/s by the
+    per-token encode's algorithmic bytes and by the pooled call's own (the
+    moments pass reads x and ref a second time)."""
     cfg, sets, nsets, stream = U.cfg, U.sets, U.n, U.stream
     T, d = cfg.tokens, cfg.hidden
     rng = np.random.default_rng(12)
@@ -475,13 +476,16 @@ def pooled_rates(torch, rac, U, steps):
     for i in range(2 * nsets):
         enc(i)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    torch.cuda.synchronize()
-    ev[0].record(stream)
-    for i in range(steps):
-        enc(i)
-    ev[1].record(stream)
-    torch.cuda.synchronize()
-    us = ev[0].elapsed_time(ev[1]) / steps * 1e3
+    times = []
+    for _ in range(reps):
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for i in range(steps):
+            enc(i)
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        times.append(ev[0].elapsed_time(ev[1]) / steps * 1e3)
+    us = float(np.median(times))
     del wires
     own = algorithmic_bytes(T, d, wb) + T * d * 4
     return {"segments": int(seg.numel()) - 1, "encode_us": round(us, 2),
@@ -570,7 +574,7 @@ def span_selection_cost(rac, T, window=16, n_hist=7):
             "covered_fraction": round(cov / T, 4)}
 
 
-def gather_rates(torch, rac, U, steps):
+def gather_rates(torch, rac, U, steps, reps=7):
     """rac_encode_gather / rac_decode_gather on the uplink configuration,
     each row's reference read from an 8192-row bf16 store of earlier rows
     (one store per buffer set), for two index patterns: span runs (what
@@ -579,9 +583,11 @@ def gather_rates(torch, rac, U, steps):
     (every row at a random store row: the worst case for locality).  The
     workload's rows without a reference name no row (a zero reference), the
     others a store row holding their own reference, so the codec sees the
-    materialized call's data.  Average launch time over
-    `steps` back-to-back launches; the materialized calls on the same inputs
-    are timed alongside."""
+    materialized call's data.  Average launch time over `steps` back-to-back
+    launches, for the materialized calls on the same inputs and the two
+    patterns in turn, `reps` times over; each figure is the median of its
+    repetitions (the clock drifts under sustained load, so a single timing
+    of each, taken one after the other, would mostly measure that drift)."""
     cfg, sets, nsets, stream = U.cfg, U.sets, U.n, U.stream
     T, d = cfg.tokens, cfg.hidden
     # the rows without a reference (ref = 0 in the workload, a fifth of
@@ -610,7 +616,7 @@ def gather_rates(torch, rac, U, steps):
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
 
     def timed(enc, dec):
-        for i in range(2 * nsets):
+        for i in range(nsets):
             enc(i)
             dec(i)
         torch.cuda.synchronize()
@@ -622,17 +628,14 @@ def gather_rates(torch, rac, U, steps):
             dec(i)
         ev[2].record(stream)
         torch.cuda.synchronize()
-        return round(ev[0].elapsed_time(ev[1]) / steps * 1e3, 2), round(ev[1].elapsed_time(ev[2]) / steps * 1e3, 2)
+        return ev[0].elapsed_time(ev[1]) / steps * 1e3, ev[1].elapsed_time(ev[2]) / steps * 1e3
 
-    out = {"store_rows": 2 * T}
-    e, dcd = timed(U.enc, U.dec)
-    out["materialized"] = {"encode_us": e, "decode_us": dcd}
-    for name, pos in (("span_runs", runs), ("random_rows", rand)):
+    def gathered(pos):
         idx = torch.from_numpy(pos).cuda()
+        ok = idx >= 0
         stores = []
         for i in range(nsets):
             st = torch.zeros(2 * T, d, dtype=torch.int16, device="cuda")
-            ok = idx >= 0
             st[idx[ok].long()] = sets[i]["ref"][ok]
             stores.append(st)
 
@@ -644,16 +647,23 @@ def gather_rates(torch, rac, U, steps):
         def dec(i):
             s = sets[i % nsets]
             rac.rac_decode_gather(cfg, wires[i % nsets], stores[i % nsets], idx, None, s["xdec"], stream=stream)
+        return enc, dec
 
-        e, dcd = timed(enc, dec)
-        assert torch.equal(sets[0]["xhat"], sets[0]["xdec"])
-        out[name] = {"miss_fraction": round(float((pos < 0).mean()), 4), "encode_us": e, "decode_us": dcd}
-        del stores
-    # the materialized calls again: the clock drifts under sustained load, so
-    # the gathered figures are compared with both
-    e, dcd = timed(U.enc, U.dec)
-    out["materialized_after"] = {"encode_us": e, "decode_us": dcd}
-    del wires
+    calls = {"materialized": (U.enc, U.dec), "span_runs": gathered(runs), "random_rows": gathered(rand)}
+    times = {name: [] for name in calls}
+    for _ in range(reps):
+        for name, (enc, dec) in calls.items():
+            times[name].append(timed(enc, dec))
+            if name != "materialized":
+                assert torch.equal(sets[0]["xhat"], sets[0]["xdec"])
+    out = {"store_rows": 2 * T, "repetitions": reps}
+    for name, tv in times.items():
+        a = np.asarray(tv)
+        out[name] = {"encode_us": round(float(np.median(a[:, 0])), 2),
+                     "decode_us": round(float(np.median(a[:, 1])), 2)}
+        if name != "materialized":
+            out[name]["miss_fraction"] = round(float(((runs if name == "span_runs" else rand) < 0).mean()), 4)
+    del calls, wires
     return out
 
 

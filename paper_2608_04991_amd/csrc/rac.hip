@@ -668,10 +668,14 @@ __device__ __forceinline__ int32_t ref_index_v(const Args& A, int32_t cache, uin
     return A.ref_rows ? __builtin_amdgcn_readlane(cache, (int)(n & (uint32_t)(kWave - 1))) : 0;
 }
 
-// The index of the workgroup's first row, read directly (a scalar load), so
-// that the first row's loads need not wait for the register copy's lane read.
+// The index of the workgroup's first row, read directly, so that the first
+// row's loads need not wait for the register copy.  Read through the constant
+// address space (the array is read-only for the whole launch): that makes it a
+// scalar load, which is waited for apart from the vector loads, and the kernels
+// issue it first, before any store or barrier.
 __device__ __forceinline__ int32_t first_ref_index(const Args& A) {
-    return (A.ref_rows && blockIdx.x < A.tokens) ? A.ref_rows[blockIdx.x] : 0;
+    using cptr = const __attribute__((address_space(4))) int32_t*;
+    return (A.ref_rows && blockIdx.x < A.tokens) ? ((cptr)A.ref_rows)[blockIdx.x] : 0;
 }
 
 // Buffer resource of token row `row`'s reference: row `row` of ref, or, with
@@ -1061,6 +1065,7 @@ void rac_encode_kernel(Args A) {
     const bool act = c0 < d;
     constexpr float q = (float)((1 << (BITS - 1)) - 1);
     constexpr float inv_q = 1.0f / q;
+    const int32_t fix = first_ref_index(A);  // store row of the first row's reference
     if (A.write_header && blockIdx.x == 0 && w == 0) write_header(A, lane);
     const bool dword3 = (d & 31) == 0;
     const bool multi_a = GA == 7 || (GA < 0 && A.lg_cpg_a > 0);
@@ -1102,7 +1107,7 @@ void rac_encode_kernel(Args A) {
     uint32_t row = blockIdx.x;
     uint4 nx, nr;
     const int32_t rix = load_ref_rows_v(A, lane);  // store rows of the gathered reference
-    load_row(row, first_ref_index(A), nx, nr);
+    load_row(row, fix, nx, nr);
     // Let the first row land before the loop: then the loop head holds no
     // wait, and inside the loop only the prefetched loads are waited for
     // (never the stores of the row before).
@@ -1426,6 +1431,7 @@ void rac_encode_rows_kernel(Args A) {
     // wavefronts, so a row of fewer than NW * CPW chunks stays balanced
     auto chunk_at = [&](int i) { return (w + i * NW) * kChunk; };
     const int32_t rix = load_ref_rows_v(A, lane);  // store rows of the gathered reference
+    const int32_t fix = first_ref_index(A);
     if (w == 0 && lane < 2u) {
         S.cnt[lane] = 0u;
         S.xn[lane] = 0u;
@@ -1440,7 +1446,7 @@ void rac_encode_rows_kernel(Args A) {
         const uint32_t row = blockIdx.x;
         const bool any = row < A.tokens;
         const uint64_t o = (uint64_t)row * (uint64_t)d;
-        const Rsrc rx = rsrc(A.x, o, any ? row_bytes : 0u), rr = ref_row(A, row, any, first_ref_index(A));
+        const Rsrc rx = rsrc(A.x, o, any ? row_bytes : 0u), rr = ref_row(A, row, any, fix);
 #pragma unroll
         for (int i = 0; i < CPW; ++i) {
             const uint32_t off = ((uint32_t)(chunk_at(i)) + lane * 8u) * 2u;  // past the row: reads 0
@@ -1834,6 +1840,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
     const uint32_t sh_fixed = (A.fixed && act) ? step_roundup(A.steps[grp_q]) : 0u;
     constexpr bool OUTL = OM == 1;
     const int32_t rix = load_ref_rows_v(A, lane);  // store rows of the gathered reference
+    const int32_t fix = first_ref_index(A);        // and of the first row
     // per-group outliers: entries per row, this chunk's first entry and count
     const uint32_t gent = (uint32_t)k * ngq;
     const uint32_t gfirst = ((uint32_t)(w * kChunk) >> A.lg_q) * (uint32_t)k;
@@ -1930,7 +1937,7 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_decode_kernel(Args A) {
     // for a prefetch before its row starts.
     const uint32_t G = gridDim.x;
     uint32_t row = blockIdx.x;
-    In p = load(row, first_ref_index(A)), q;
+    In p = load(row, fix), q;
     // (a store that the range check drops, so that stores are outstanding at
     // the loop entry as at the end of every row; the compiler's wait analysis
     // then keeps later waits exact instead of waiting for everything)
