@@ -143,6 +143,30 @@ def test_full_prefill_uplink_4096x4096_gathered_sampled():
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("k,flags", [(4, 0), (2, GRP)])
+def test_many_rows_gathered_65536x512(k, flags):
+    """65536 rows of 512 channels: more rows than six per resident workgroup
+    for every kernel at this width, so the launch takes one workgroup per row
+    (the strided grid covers the smaller cases above).  The whole output must
+    equal the materialized call's; sampled rows must equal the oracle's."""
+    import torch
+    T, d = 65536, 512
+    c = cfgd(T, d, 128, 128, 4, k, flags)
+    say(f"[gpu] gather {T}x{d} k{k} flags {flags}: generating")
+    xb, rb, _ = wl.prefill_uplink(3, tokens=T, hidden=d)
+    store, idx = _history(xb, rb, 4096, seed=13)
+    ref = _gathered(store, idx)
+    gw, gx, gd = _gpu_gather(c, xb, store, idx)
+    assert np.array_equal(gx, gd)
+    mw, mx, _, _ = gpu_run(c, xb, ref)
+    assert np.array_equal(mw, gw) and np.array_equal(mx, gx)
+    rng = np.random.default_rng(6)
+    rows = np.unique(np.concatenate([[0, 1, T - 2, T - 1], rng.choice(T, 60, replace=False)]))
+    ow, ox = oracle_run(dict(c, tokens=rows.size), xb[rows], ref[rows])
+    assert_parity(c, gw, gx, ow, ox, g_rows=rows, o_rows=slice(None))
+    torch.cuda.empty_cache()
+
+
 def test_selected_spans_end_to_end():
     """Prompt tokens -> native span selection -> gathered encode and decode
     on the GPU, against the selection oracle -> host gather -> codec oracle.
