@@ -39,6 +39,7 @@ profiles/ were taken with.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -152,6 +153,24 @@ class Codec:
     def free(self):
         del self.sets
         self.torch.cuda.empty_cache()
+
+
+def launch_shape_rates(torch, rac, C, iters):
+    """Encode and decode times of one workload under each launch shape: the
+    default choice and the two shapes forced by the launch hints (the strided
+    grid of resident workgroups, one workgroup per row).  The outputs are
+    identical under every hint (checked by the GPU tests); medians of
+    back-to-back blocks."""
+    base = C.cfg
+    out = {}
+    for name, hint in (("default", 0), ("strided", rac.RAC_FLAG_LAUNCH_STRIDED),
+                       ("per_row", rac.RAC_FLAG_LAUNCH_PER_ROW)):
+        C.cfg = dataclasses.replace(base, flags=base.flags | hint)
+        C.warm(30)
+        e, d = C.steady(iters, reps=3)
+        out[name] = {"encode_us": round(e, 2), "decode_us": round(d, 2)}
+    C.cfg = base
+    return out
 
 
 def to_dev(torch, a):
@@ -310,6 +329,7 @@ def main():
         # the encode kernel in a kernel trace are those of the timed steps)
         C.warm()
         e_us, d_us = C.steady(args.steps)
+        extras["launch_shapes"] = launch_shape_rates(torch, rac, C, args.steps)
         extras.update({"encode_us_back_to_back": round(e_us, 2),
                        "encode_hbm_frac_back_to_back": frac(enc_alg, e_us),
                        "decode_us_back_to_back": round(d_us, 2),
@@ -351,6 +371,7 @@ def all_extras(torch, rac, wl, stream):
         "wire_over_bf16": round(U.wbytes / (4096 * 4096 * 2), 4),
         "encode_kernel": "rac_encode_rows_kernel<4, 4, 4, 4, 2, false>"}
     log(f"[bench] uplink: {ex['prefill_uplink_4096x4096_g128_b4_k8']}")
+    ex["launch_shapes_4096x4096_g128_b4_k8"] = launch_shape_rates(torch, rac, U, 50)
     ex["outlier_modes_4096x4096_g128_b4"] = outlier_mode_rates(torch, rac, U, 50)
     ex["gathered_reference"] = gather_rates(torch, rac, U, 50)
     ex["pooled_fit"] = pooled_rates(torch, rac, U, 50)

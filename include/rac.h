@@ -113,7 +113,17 @@ enum {
     /* Outliers per quantization group (the outlier paragraph's mask M_j):
      * outlier_k is k_g, the number taken from every group of g_q channels
      * (ties to the lower channel), 1 <= k_g <= min(16, g_q/4), g_q <= 256. */
-    RAC_FLAG_GROUP_OUTLIERS = 1u << 2
+    RAC_FLAG_GROUP_OUTLIERS = 1u << 2,
+    /* Launch hints; neither changes the wire or any result, only how rows are
+     * spread over workgroups, and neither is recorded in the wire.  By default
+     * more than 256 rows run on a grid of the workgroups the device holds at
+     * once, each taking rows in strides with its next row prefetched, unless
+     * that would give each more than six rows; then one workgroup per row
+     * (over many rows the strided workgroups drift apart and the HBM writes
+     * lose locality).  STRIDED always takes the strided grid, PER_ROW always
+     * one workgroup per row; setting both is RAC_ERR_INVALID. */
+    RAC_FLAG_LAUNCH_STRIDED = 1u << 3,
+    RAC_FLAG_LAUNCH_PER_ROW = 1u << 4
 };
 
 typedef struct {

@@ -33,6 +33,8 @@ __all__ = [
 RAC_FLAG_FIXED_STEP = 1
 RAC_FLAG_XHAT_BF16 = 2
 RAC_FLAG_GROUP_OUTLIERS = 4
+RAC_FLAG_LAUNCH_STRIDED = 8    # launch hints: change no result, only the launch shape
+RAC_FLAG_LAUNCH_PER_ROW = 16
 STATUS = {0: "RAC_OK", 1: "RAC_ERR_INVALID", 2: "RAC_ERR_ALIGN", 3: "RAC_ERR_CAPACITY",
           4: "RAC_ERR_HIP", 5: "RAC_ERR_FORMAT", 6: "RAC_ERR_UNSUPPORTED", 7: "RAC_ERR_NOMEM"}
 

@@ -78,6 +78,7 @@ struct alignas(8) Args {
     int32_t fixed;
     int32_t xhat_bf16;
     float inv_ga;       // 1 / g_a (exact, power of two)
+    int32_t launch_shape;  // (read by the host only) 0 by rows per workgroup, 1 strided, 2 one workgroup per row
     // header and padding (written once, by the first wavefront)
     int32_t write_header;
     uint8_t* wire;
@@ -2232,7 +2233,10 @@ bool config_valid(const rac_config* c) {
         c->hidden % c->group_quant != 0)
         return false;
     if (c->bits != 2 && c->bits != 3 && c->bits != 4 && c->bits != 8) return false;
-    if (c->flags & ~uint32_t(RAC_FLAG_FIXED_STEP | RAC_FLAG_XHAT_BF16 | RAC_FLAG_GROUP_OUTLIERS)) return false;
+    if (c->flags & ~uint32_t(RAC_FLAG_FIXED_STEP | RAC_FLAG_XHAT_BF16 | RAC_FLAG_GROUP_OUTLIERS |
+                             RAC_FLAG_LAUNCH_STRIDED | RAC_FLAG_LAUNCH_PER_ROW))
+        return false;
+    if ((c->flags & RAC_FLAG_LAUNCH_STRIDED) && (c->flags & RAC_FLAG_LAUNCH_PER_ROW)) return false;
     if (c->flags & RAC_FLAG_GROUP_OUTLIERS) {
         if (c->group_quant > 256) return false;  // u8 in-group offsets
         if (c->outlier_k < 1 || c->outlier_k > 16 || c->outlier_k > c->group_quant / 4) return false;
@@ -2297,6 +2301,7 @@ Args make_args(const rac_config* c, const Sizes& S) {
     A.fixed = (c->flags & RAC_FLAG_FIXED_STEP) ? 1 : 0;
     A.xhat_bf16 = (c->flags & RAC_FLAG_XHAT_BF16) ? 1 : 0;
     A.inv_ga = 1.0f / (float)c->group_align;
+    A.launch_shape = (c->flags & RAC_FLAG_LAUNCH_STRIDED) ? 1 : (c->flags & RAC_FLAG_LAUNCH_PER_ROW) ? 2 : 0;
     return A;
 }
 
@@ -2494,7 +2499,8 @@ rac_status device_cus(int* cus) {
 // workgroups as the device keeps resident (at most max_per_cu per compute
 // unit), each taking rows in strides (and prefetching its next row); small
 // counts, and counts that would give every resident workgroup more than
-// kStridedRowsMax rows, launch one workgroup per row.  (Over many rows the
+// kStridedRowsMax rows, launch one workgroup per row.  The launch flags of the
+// configuration override that choice for more than 256 rows.  (Over many rows the
 // strided workgroups drift apart, so the rows in flight spread over the
 // tensors and the HBM writes lose locality; with one workgroup per row the
 // dispatcher hands rows out in order as workgroups finish, which keeps them
@@ -2512,7 +2518,8 @@ rac_status launch(KernelFn fn, Args A, hipStream_t stream, int threads = 0, int 
         int cus = 0, per_cu = 0;
         if (resident(reinterpret_cast<const void*>(fn), threads, lds, &cus, &per_cu) != RAC_OK) return RAC_ERR_HIP;
         const int64_t fits = (int64_t)cus * (per_cu > 0 ? per_cu : 1);  // workgroups the device holds at once
-        if (rows <= kStridedRowsMax * fits) {
+        const bool strided = A.launch_shape == 1 || (A.launch_shape == 0 && rows <= kStridedRowsMax * fits);
+        if (strided) {
             if (max_per_cu > 0 && per_cu > max_per_cu) per_cu = max_per_cu;
             int64_t resident = (int64_t)cus * (per_cu > 0 ? per_cu : 1);
             // a gathered reference: at most kMaxGatherRows rows per workgroup,

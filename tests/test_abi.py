@@ -84,7 +84,7 @@ def test_payload_ratio_of_the_prefill_uplink_shape(lib):
 
 @pytest.mark.parametrize("bad", [dict(bits=5), dict(group_align=96), dict(group_quant=4),
                                  dict(hidden=100), dict(outlier_k=65), dict(tokens=-1),
-                                 dict(tokens=2**31), dict(flags=16), dict(group_align=1024)])
+                                 dict(tokens=2**31), dict(flags=32), dict(flags=24), dict(group_align=1024)])
 def test_invalid_configs_are_rejected(lib, bad):
     c = dict(tokens=4, hidden=512, group_align=64, group_quant=64, bits=4)
     c.update(bad)
@@ -93,6 +93,15 @@ def test_invalid_configs_are_rejected(lib, bad):
     with pytest.raises(rac.RacError) as e:
         rac.rac_wire_layout(cfg)
     assert e.value.status == 1
+
+
+@pytest.mark.parametrize("hint", [rac.RAC_FLAG_LAUNCH_STRIDED, rac.RAC_FLAG_LAUNCH_PER_ROW])
+def test_launch_hints_leave_the_wire_layout_alone(lib, hint):
+    for c in CFGS:
+        plain = rac.RacConfig(**c)
+        hinted = rac.RacConfig(**dict(c, flags=c.get("flags", 0) | hint))
+        assert rac.rac_wire_size(hinted) == rac.rac_wire_size(plain) > 0
+        assert rac.rac_wire_layout(hinted) == rac.rac_wire_layout(plain)
 
 
 def test_parse_header_reads_oracle_headers(lib):
