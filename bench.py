@@ -29,12 +29,14 @@ Prints ONE JSON line:
                microseconds per call at batch 1/16/64/256; the decode-phase
                reference predictor's step time at the same batches; the
                per-group outlier modes, gathered reference, span selection and
-               pooled fit on the uplink inputs.
+               pooled fit on the uplink inputs; the headline and uplink
+               workloads under each launch shape (the launch hints).
 
 --profile WORKLOAD runs only that workload's launches (back-to-back encodes,
 then back-to-back decodes, over rotating buffers) and prints their event
 timings: the command the rocprofv3 kernel traces and counter runs under
-profiles/ were taken with.
+profiles/ were taken with.  --profile launch_shapes instead times encode and
+decode under each launch shape over 2048 to 65536 rows of random inputs.
 """
 from __future__ import annotations
 
@@ -163,6 +165,7 @@ def launch_shape_rates(torch, rac, C, iters):
     back-to-back blocks."""
     base = C.cfg
     out = {}
+    C.warm(100)
     for name, hint in (("default", 0), ("strided", rac.RAC_FLAG_LAUNCH_STRIDED),
                        ("per_row", rac.RAC_FLAG_LAUNCH_PER_ROW)):
         C.cfg = dataclasses.replace(base, flags=base.flags | hint)
@@ -170,6 +173,32 @@ def launch_shape_rates(torch, rac, C, iters):
         e, d = C.steady(iters, reps=3)
         out[name] = {"encode_us": round(e, 2), "decode_us": round(d, 2)}
     C.cfg = base
+    return out
+
+
+def launch_shape_sweep(torch, rac, stream, iters):
+    """Encode and decode µs under each launch shape over 2048 to 65536 rows at
+    4096 channels (k = 8) and 3584 channels (k = 4), group 128, 4-bit, on
+    random inputs (x ~ N(0, 0.25) with every 97th channel scaled x12, ref = x
+    plus N(0, 0.0025)), generated on the device."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(0)
+    out = {}
+    for d, k in ((4096, 8), (3584, 4)):
+        for T in (2048, 4096, 8192, 16384, 32768, 65536):
+            cfg = rac.RacConfig(T, d, 128, 128, 4, k)
+            x = torch.randn(T, d, device="cuda", generator=g) * 0.5
+            x[:, ::97] *= 12.0
+            ref = (x + 0.05 * torch.randn(T, d, device="cuda", generator=g)).bfloat16().view(torch.int16)
+            x = x.bfloat16().view(torch.int16)
+            nsets = max(2, int(np.ceil(2 * LLC_BYTES / (T * d * 8))))
+            C = Codec(torch, rac, cfg, x, ref, nsets, stream)
+            res = launch_shape_rates(torch, rac, C, iters)
+            out[f"{T}x{d}_k{k}"] = res
+            log(f"[bench] launch shapes {T}x{d}: {res}")
+            C.free()
+            del C, x, ref
+            torch.cuda.empty_cache()
     return out
 
 
@@ -208,7 +237,8 @@ def main():
                          "climbs for the first ~20 ms of sustained load")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true")
-    ap.add_argument("--profile", choices=["downlink", "uplink", "long_context", "decode_step", "tiny", "predictor"],
+    ap.add_argument("--profile", choices=["downlink", "uplink", "long_context", "decode_step", "tiny", "predictor",
+                                            "launch_shapes"],
                     help="run only this workload's back-to-back encodes and decodes and print their timings")
     ap.add_argument("--iters", type=int, default=20, help="back-to-back launches per kernel in --profile runs")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -788,6 +818,8 @@ def profile_run(torch, rac, wl, stream, workload, iters):
         out.update(tiny_rates(torch, rac, wl, stream, iters))
     elif workload == "predictor":
         out.update(predictor_latency(torch, rac, wl, stream, iters=iters))
+    elif workload == "launch_shapes":
+        out.update(launch_shape_sweep(torch, rac, stream, iters))
     else:
         for bits, gq in ((2, 128), (4, 128), (8, 128), (4, 4096)):
             for B, v in decode_step_latency(torch, rac, wl, stream, bits, gq, detail=True).items():
