@@ -2,13 +2,14 @@
 Student-t residual noise, half the rows without a reference, 16 outliers per
 token) at every group size and bit width the benchmark times.
 
-At this row count every kernel runs as a persistent grid whose workgroups
-stride over rows, prefetch the next row and alternate row buffers; small
-cases launch one workgroup per row and never reach that loop.  The GPU codes
-all 32768 rows; the oracle recomputes sampled rows one by one (rows are
-independent), and the wire sections and the sender reconstruction of those
-rows must be bit-identical.  Decode and reconstruct are checked bitwise
-against the sender reconstruction on every row, on the device.
+At this row count the default launch is one workgroup per row.  Every
+configuration is also run on the strided grid (RAC_FLAG_LAUNCH_STRIDED),
+whose workgroups stride over rows, prefetch the next row and alternate row
+buffers, and must give the same bytes.  The GPU codes all 32768 rows; the
+oracle recomputes sampled rows one by one (rows are independent), and the
+wire sections and the sender reconstruction of those rows must be
+bit-identical.  Decode and reconstruct are checked bitwise against the sender
+reconstruction on every row, on the device.
 """
 from __future__ import annotations
 
@@ -44,7 +45,7 @@ def _data(group):
 
 def _rows(seed):
     rng = np.random.default_rng(seed)
-    # the first and last rows of the grid's first and last rounds, and random ones
+    # rows at the strided grid's round boundaries, the ends, and random ones
     fixed = [0, 1, 2, 1791, 1792, 2047, 2048, T - 513, T - 512, T - 2, T - 1]
     return np.unique(np.concatenate([fixed, rng.choice(T, 36, replace=False)]))
 
@@ -63,3 +64,6 @@ def test_long_context_full_sampled(group, bits):
     assert n == rows.size
     h = wirefmt.header(gw)
     assert h["tokens"] == T and wirefmt.padding_is_zero(gw)
+    say(f"[gpu] long context g{group} b{bits}: the same on the strided grid")
+    sw, sx = gpu_run_rows(dict(c, flags=rac.RAC_FLAG_LAUNCH_STRIDED), xb, rb, rows)
+    assert np.array_equal(sw, gw) and np.array_equal(sx.view(np.uint8), gx.view(np.uint8))

@@ -40,6 +40,8 @@ CASES = {
     # no outliers, bf16 reconstruction, a ragged chunk (1536 = 3 chunks)
     "none_bf16_2600x1536_g128_b8": (cfgd(2600, 1536, 128, 128, 8, 0, rac.RAC_FLAG_XHAT_BF16), 2),
     "per_token_1000x4096_g64_b2_k16": (cfgd(1000, 4096, 64, 64, 2, 16), 3),
+    # 16 < k <= 48: the two-value threshold variant of the rows kernel
+    "per_token_1500x2048_g128_b4_k32": (cfgd(1500, 2048, 128, 128, 4, 32), 5),
 }
 
 
