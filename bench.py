@@ -30,7 +30,8 @@ Prints ONE JSON line:
                reference predictor's step time at the same batches; the
                per-group outlier modes, gathered reference, span selection and
                pooled fit on the uplink inputs; the headline and uplink
-               workloads under each launch shape (the launch hints).
+               workloads under each launch shape (the launch hints); a plain
+               1 GiB device copy as the memory system's reference.
 
 --profile WORKLOAD runs only that workload's launches (back-to-back encodes,
 then back-to-back decodes, over rotating buffers) and prints their event
@@ -389,8 +390,35 @@ def prefill_uplink(torch, rac, wl, stream):
     return Codec(torch, rac, cfg, to_dev(torch, xb), to_dev(torch, rb), nsets, stream), rb
 
 
+def copy_reference(torch, stream, nbytes=1 << 30, iters=10, reps=5):
+    """What the memory system gives a plain copy: a 1 GiB device-to-device
+    copy (the HIP runtime's copy kernel, through torch), timed back to back;
+    bytes moved = read + write.  The median of `reps` blocks."""
+    src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    times = []
+    for _ in range(reps):
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for _ in range(iters):
+            dst.copy_(src)
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        times.append(ev[0].elapsed_time(ev[1]) / iters * 1e3)
+    us = float(np.median(times))
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"bytes_per_copy": 2 * nbytes, "us": round(us, 1), "GBps": round(2 * nbytes / us / 1e3, 1),
+            "hbm_frac": frac(2 * nbytes, us)}
+
+
 def all_extras(torch, rac, wl, stream):
     ex = {}
+    ex["copy_reference_1GiB"] = copy_reference(torch, stream)
+    log(f"[bench] device copy: {ex['copy_reference_1GiB']}")
     log("[bench] prefill uplink 4096 x 4096")
     U, rb = prefill_uplink(torch, rac, wl, stream)
     U.warm()
