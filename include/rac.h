@@ -98,7 +98,8 @@ typedef enum {
     RAC_ERR_HIP = 4,         /* the HIP runtime refused the kernel launch        */
     RAC_ERR_FORMAT = 5,      /* a wire header does not parse                     */
     RAC_ERR_UNSUPPORTED = 6, /* valid codec configuration the kernels do not
-                                implement (hidden above 8192)                   */
+                                implement (hidden above 8192; a gathered call
+                                of more than 268,435,392 rows may be refused)   */
     RAC_ERR_NOMEM = 7        /* host memory exhausted (span index only)          */
 } rac_status;
 
@@ -218,7 +219,9 @@ rac_status rac_decode(const rac_config* cfg, const void* wire, const void* ref,
  *                token a zero reference row (no span hit); the kernels never
  *                read outside the store.
  * Errors as rac_encode, plus RAC_ERR_INVALID for a store without ref_rows or
- * store_rows out of range.  One kernel launch. */
+ * store_rows out of range, and RAC_ERR_UNSUPPORTED for more token rows than
+ * 64 per workgroup of the largest grid one dispatch holds (2^32 work-items);
+ * that never happens for T <= 268,435,392.  One kernel launch. */
 rac_status rac_encode_gather(const rac_config* cfg, const void* x, const void* ref_store, int64_t store_rows,
                              const int32_t* ref_rows, const float* fixed_steps, void* wire, size_t wire_cap,
                              void* xhat, rac_stream_t stream);

@@ -2529,6 +2529,13 @@ rac_status launch(KernelFn fn, Args A, hipStream_t stream, int threads = 0, int 
             if (blocks > resident) blocks = resident;
         }
     }
+    // A dispatch holds fewer than 2^32 work-items per dimension: beyond that
+    // the workgroups stride over the rows (every kernel takes rows in strides
+    // of the grid).  A gathered reference allows at most kMaxGatherRows rows
+    // per workgroup.
+    const int64_t max_blocks = (int64_t)(0xFFFFFFFFu / (uint32_t)threads);
+    if (blocks > max_blocks) blocks = max_blocks;
+    if (A.ref_rows && blocks * kMaxGatherRows < rows) return RAC_ERR_UNSUPPORTED;
     void* args[] = {&A};
     const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(fn), dim3((unsigned)blocks),
                                          dim3((unsigned)threads), args, lds, stream);

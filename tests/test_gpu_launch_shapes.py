@@ -100,3 +100,54 @@ def test_launch_shapes_gathered_and_pooled():
     gref[ok] = store[idx[ok]]
     ow, ox = oracle_run(c, xb, gref)
     assert_parity(c, res[0][0], res[0][1], ow, ox)
+
+
+def test_more_rows_than_one_dispatch_holds():
+    """17,000,000 rows of 8 channels: one workgroup per row would exceed the
+    2^32 work-items of a dispatch for the 256-thread outlier encode, so its
+    grid stops at 16,777,215 workgroups and some take a second row.  Sampled
+    rows (the ends of the grid and past it) must equal the oracle's, decode
+    and reconstruct the sender's on every row, and a gathered call with a
+    fifth of its rows missing the same bytes as the materialized call."""
+    import torch
+    from tests.gpu_util import gpu_run_rows
+    T, d = 17_000_000, 8
+    c = cfgd(T, d, 8, 8, 4, 2)
+    say(f"[gpu] {T}x{d} k2: generating")
+    # the tiny recipe's distribution, drawn in bulk: x = a ref + b + noise with
+    # (a, b) per row, a fifth of the rows against a zero reference
+    rng = np.random.default_rng(11)
+    ref = rng.standard_normal((T, d), dtype=np.float32)
+    x = (rng.uniform(0.8, 1.2, (T, 1)).astype(np.float32) * ref
+         + (0.1 * rng.standard_normal((T, 1))).astype(np.float32)
+         + np.float32(0.05) * rng.standard_normal((T, d), dtype=np.float32))
+    ref[rng.random(T) < 0.2] = 0.0
+    xb, rb = wl.f32_to_bf16_bits(x), wl.f32_to_bf16_bits(ref)
+    del x, ref
+    cap = 0xFFFFFFFF // 256
+    rows = np.unique(np.concatenate([[0, 1, cap - 1, cap, cap + 1, T - 2, T - 1],
+                                     rng.choice(T, 40, replace=False)]))
+    say(f"[gpu] {T}x{d} k2: encode, decode, reconstruct")
+    gw, gx = gpu_run_rows(c, xb, rb, rows)
+    ow, ox = oracle_run(dict(c, tokens=rows.size), xb[rows], rb[rows])
+    assert_parity(c, gw, gx, ow, ox, g_rows=rows, o_rows=slice(None), g_xhat_sampled=True)
+    # gathered: the store is the reference itself, and a fifth of the rows
+    # name no row (their reference is zero in the materialized call)
+    miss = rng.random(T) < 0.2
+    idx = np.arange(T, dtype=np.int32)
+    idx[miss] = -1
+    rz = rb.copy()
+    rz[miss] = 0
+    say(f"[gpu] {T}x{d} k2: gathered against materialized")
+    cfg = rac.RacConfig(**c)
+    x, st, ix = to_dev(xb), to_dev(rb), torch.from_numpy(idx).cuda()
+    wg = torch.empty(rac.rac_wire_size(cfg), dtype=torch.uint8, device="cuda")
+    rac.rac_encode_gather(cfg, x, st, ix, None, wg, None, store_rows=T)
+    torch.cuda.synchronize()
+    del st
+    wm = torch.empty_like(wg)
+    rac.rac_encode(cfg, x, to_dev(rz), None, wm, None)
+    torch.cuda.synchronize()
+    assert torch.equal(wg, wm)
+    del x, ix, wg, wm
+    torch.cuda.empty_cache()
