@@ -40,6 +40,7 @@ constexpr int kMaxWaves = 16;     // rows up to 8192 channels
 constexpr int kCandCap = 64;      // outlier candidates ranked by one wavefront
 constexpr int kMaxGatherRows = 64; // rows per workgroup with a gathered reference
 constexpr int kStridedRowsMax = 6; // beyond this many rows per resident workgroup: one workgroup per row
+constexpr uint32_t kMaxDispatchItems = 0xFFFFFFFFu;  // work-items one dispatch holds (per dimension)
 constexpr float kMagic = 12582912.0f;  // 1.5 * 2^23: adding it rounds to an integer (RNE)
 // Quotients t' = E * (1/s) within this distance of a half-integer are
 // recomputed with the correctly rounded division E / s.  |t' - E/s| is below
@@ -2012,7 +2013,9 @@ __global__ __launch_bounds__(kWave * kMaxWaves) void rac_moments_kernel(Args A, 
     }
 }
 
-// One workgroup of kPoolWaves wavefronts per (segment, alignment group):
+// One workgroup of kPoolWaves wavefronts per (segment, alignment group)
+// (beyond the largest grid one dispatch holds, workgroups take further pairs
+// in strides of the grid):
 // merges the segment's row moments over the binary-decomposition tree (a
 // range of n rows splits into its first p rows, p the largest power of two
 // below n, and the rest).  Rows are taken in blocks of 64, one block per
@@ -2035,11 +2038,8 @@ __global__ __launch_bounds__(kWave * kPoolWaves) void rac_pool_kernel(Args A, co
     __shared__ uint32_t cf_shared;
     const uint32_t lane = threadIdx.x & (kWave - 1), wv = threadIdx.x / kWave;
     const uint32_t nga = (uint32_t)A.d >> A.lg_a;
-    const uint32_t s = blockIdx.x / nga, j = blockIdx.x % nga;
+    const uint32_t pairs = (uint32_t)A.segments * nga;  // < 2^31
     const int64_t T = (int64_t)A.tokens;
-    int64_t lo = A.seg_start[s], hi = A.seg_start[s + 1];
-    lo = lo < 0 ? 0 : (lo > T ? T : lo);
-    hi = hi < lo ? lo : (hi > T ? T : hi);
     const float gn = (float)(1 << A.lg_a);
     // bottom-up tree over the first m lanes' moments (result in lane 0)
     auto lane_tree = [&](Mom v, uint32_t m, int levels) {
@@ -2056,64 +2056,71 @@ __global__ __launch_bounds__(kWave * kPoolWaves) void rac_pool_kernel(Args A, co
         }
         return v;
     };
-    int top = 0;  // (thread 0's)
-    for (int64_t p0 = lo; p0 < hi; p0 += (int64_t)kWave * kPoolWaves) {
-        const int64_t b0 = p0 + (int64_t)wv * kWave;
-        const int64_t left = hi - b0;
-        const uint32_t m = left <= 0 ? 0u : (left < kWave ? (uint32_t)left : (uint32_t)kWave);
-        Mom v{0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
-        if (lane < m) {
-            const float4 f = mom[(uint64_t)(b0 + lane) * nga + j];
-            v = Mom{gn, f.x, f.y, f.z, f.w};
-        }
-        v = lane_tree(v, m, 6);
-        if (lane == 0u) {
-            blk[wv] = v;
-            bsz[wv] = m;
-        }
-        __syncthreads();
-        if (wv == 0u) {
-            // the pass's blocks: whole 64-row blocks, possibly a partial last one
-            uint32_t nb = 0u, rows = 0u;
-            for (int b = 0; b < kPoolWaves; ++b) {
-                nb += bsz[b] != 0u ? 1u : 0u;
-                rows += bsz[b];
+    for (uint32_t pair = blockIdx.x; pair < pairs; pair += gridDim.x) {
+        const uint32_t s = pair / nga, j = pair % nga;
+        int64_t lo = A.seg_start[s], hi = A.seg_start[s + 1];
+        lo = lo < 0 ? 0 : (lo > T ? T : lo);
+        hi = hi < lo ? lo : (hi > T ? T : hi);
+        int top = 0;  // (thread 0's)
+        for (int64_t p0 = lo; p0 < hi; p0 += (int64_t)kWave * kPoolWaves) {
+            const int64_t b0 = p0 + (int64_t)wv * kWave;
+            const int64_t left = hi - b0;
+            const uint32_t m = left <= 0 ? 0u : (left < kWave ? (uint32_t)left : (uint32_t)kWave);
+            Mom v{0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+            if (lane < m) {
+                const float4 f = mom[(uint64_t)(b0 + lane) * nga + j];
+                v = Mom{gn, f.x, f.y, f.z, f.w};
             }
-            Mom u{0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
-            if (lane < nb) u = blk[lane];
-            u = lane_tree(u, nb, 4);
+            v = lane_tree(v, m, 6);
             if (lane == 0u) {
-                stk[top] = u;
-                ssz[top] = rows;
-                ++top;
-                while (top >= 2 && ssz[top - 1] == ssz[top - 2]) {
-                    stk[top - 2] = mom_merge(stk[top - 2], stk[top - 1]);
-                    ssz[top - 2] *= 2u;
-                    --top;
+                blk[wv] = v;
+                bsz[wv] = m;
+            }
+            __syncthreads();
+            if (wv == 0u) {
+                // the pass's blocks: whole 64-row blocks, possibly a partial last one
+                uint32_t nb = 0u, rows = 0u;
+                for (int b = 0; b < kPoolWaves; ++b) {
+                    nb += bsz[b] != 0u ? 1u : 0u;
+                    rows += bsz[b];
+                }
+                Mom u{0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+                if (lane < nb) u = blk[lane];
+                u = lane_tree(u, nb, 4);
+                if (lane == 0u) {
+                    stk[top] = u;
+                    ssz[top] = rows;
+                    ++top;
+                    while (top >= 2 && ssz[top - 1] == ssz[top - 2]) {
+                        stk[top - 2] = mom_merge(stk[top - 2], stk[top - 1]);
+                        ssz[top - 2] *= 2u;
+                        --top;
+                    }
                 }
             }
+            __syncthreads();
+        }
+        if (threadIdx.x == 0u) {
+            uint32_t cf = 0u;
+            if (top > 0) {
+                Mom r = stk[top - 1];
+                for (int i = top - 2; i >= 0; --i) r = mom_merge(stk[i], r);
+                cf = fit_coef(r.crr, r.crx, r.mr, r.mx);
+            }
+            cf_shared = cf;
         }
         __syncthreads();
-    }
-    if (threadIdx.x == 0u) {
-        uint32_t cf = 0u;
-        if (top > 0) {
-            Mom r = stk[top - 1];
-            for (int i = top - 2; i >= 0; --i) r = mom_merge(stk[i], r);
-            cf = fit_coef(r.crr, r.crx, r.mr, r.mx);
+        const uint32_t cf = cf_shared;
+        if (A.pool_first_rows) {
+            // the outlier encode takes the pair from the segment's first row and
+            // writes every row's slot itself (4-byte stores from each segment's
+            // 32 or more workgroups into shared lines cost 4 us here)
+            if (threadIdx.x == 0u && lo < hi) bstore32(rsrc(A.coef, (uint64_t)lo * nga, nga * 4u), j * 4u, cf);
+        } else {
+            for (int64_t t = lo + threadIdx.x; t < hi; t += (int64_t)kWave * kPoolWaves)
+                bstore32(rsrc(A.coef, (uint64_t)t * nga, nga * 4u), j * 4u, cf);
         }
-        cf_shared = cf;
-    }
-    __syncthreads();
-    const uint32_t cf = cf_shared;
-    if (A.pool_first_rows) {
-        // the outlier encode takes the pair from the segment's first row and
-        // writes every row's slot itself (4-byte stores from each segment's
-        // 32 or more workgroups into shared lines cost 4 us here)
-        if (threadIdx.x == 0u && lo < hi) bstore32(rsrc(A.coef, (uint64_t)lo * nga, nga * 4u), j * 4u, cf);
-    } else {
-        for (int64_t t = lo + threadIdx.x; t < hi; t += (int64_t)kWave * kPoolWaves)
-            bstore32(rsrc(A.coef, (uint64_t)t * nga, nga * 4u), j * 4u, cf);
+        __syncthreads();  // the next pair reuses the shared state
     }
 }
 
@@ -2154,35 +2161,41 @@ __device__ __forceinline__ ErrSums err_tree(ErrSums v, double (*sh)[kErrThreads]
 __global__ __launch_bounds__(kErrThreads) void rac_error_kernel(const uint16_t* x, const void* xhat, int32_t bf16,
                                                                 uint32_t tokens, int32_t d, double* part) {
     __shared__ double sh[3][kErrThreads];
-    const uint64_t row0 = (uint64_t)blockIdx.x * kErrRows;
-    const uint64_t rows = tokens - row0 < (uint64_t)kErrRows ? tokens - row0 : (uint64_t)kErrRows;
-    const uint64_t base = row0 * (uint64_t)d, n = rows * (uint64_t)d;  // n is a multiple of 8
-    ErrSums v{0.0, 0.0, 0.0};
-    for (uint64_t e = (uint64_t)threadIdx.x * 8u; e < n; e += (uint64_t)kErrThreads * 8u) {
-        float xf[8], hf[8];
-        widen8(*reinterpret_cast<const uint4*>(x + base + e), xf);
-        if (bf16) {
-            widen8(*reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(xhat) + base + e), hf);
-        } else {
-            const float4* hp = reinterpret_cast<const float4*>(static_cast<const float*>(xhat) + base + e);
-            const float4 a = hp[0], b = hp[1];
-            hf[0] = a.x; hf[1] = a.y; hf[2] = a.z; hf[3] = a.w;
-            hf[4] = b.x; hf[5] = b.y; hf[6] = b.z; hf[7] = b.w;
+    const uint32_t parts = (uint32_t)(((uint64_t)tokens + kErrRows - 1) / kErrRows);
+    // (beyond the largest grid one dispatch holds, blocks take further parts
+    // in strides of the grid; each part's sum is the same either way)
+    for (uint32_t pt = blockIdx.x; pt < parts; pt += gridDim.x) {
+        const uint64_t row0 = (uint64_t)pt * kErrRows;
+        const uint64_t rows = tokens - row0 < (uint64_t)kErrRows ? tokens - row0 : (uint64_t)kErrRows;
+        const uint64_t base = row0 * (uint64_t)d, n = rows * (uint64_t)d;  // n is a multiple of 8
+        ErrSums v{0.0, 0.0, 0.0};
+        for (uint64_t e = (uint64_t)threadIdx.x * 8u; e < n; e += (uint64_t)kErrThreads * 8u) {
+            float xf[8], hf[8];
+            widen8(*reinterpret_cast<const uint4*>(x + base + e), xf);
+            if (bf16) {
+                widen8(*reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(xhat) + base + e), hf);
+            } else {
+                const float4* hp = reinterpret_cast<const float4*>(static_cast<const float*>(xhat) + base + e);
+                const float4 a = hp[0], b = hp[1];
+                hf[0] = a.x; hf[1] = a.y; hf[2] = a.z; hf[3] = a.w;
+                hf[4] = b.x; hf[5] = b.y; hf[6] = b.z; hf[7] = b.w;
+            }
+    #pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const double xv = (double)xf[j];
+                const double dd = xv - (double)hf[j];
+                v.se = v.se + dd * dd;
+                v.sx = v.sx + xv * xv;
+                v.mx = __builtin_fmax(v.mx, __builtin_fabs(dd));
+            }
         }
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const double xv = (double)xf[j];
-            const double dd = xv - (double)hf[j];
-            v.se = v.se + dd * dd;
-            v.sx = v.sx + xv * xv;
-            v.mx = __builtin_fmax(v.mx, __builtin_fabs(dd));
+        const ErrSums r = err_tree(v, sh);
+        if (threadIdx.x == 0) {
+            part[3u * pt + 0u] = r.se;
+            part[3u * pt + 1u] = r.sx;
+            part[3u * pt + 2u] = r.mx;
         }
-    }
-    const ErrSums r = err_tree(v, sh);
-    if (threadIdx.x == 0) {
-        part[3u * blockIdx.x + 0u] = r.se;
-        part[3u * blockIdx.x + 1u] = r.sx;
-        part[3u * blockIdx.x + 2u] = r.mx;
+        __syncthreads();  // the next part reuses sh
     }
 }
 
@@ -2533,7 +2546,7 @@ rac_status launch(KernelFn fn, Args A, hipStream_t stream, int threads = 0, int 
     // the workgroups stride over the rows (every kernel takes rows in strides
     // of the grid).  A gathered reference allows at most kMaxGatherRows rows
     // per workgroup.
-    const int64_t max_blocks = (int64_t)(0xFFFFFFFFu / (uint32_t)threads);
+    const int64_t max_blocks = (int64_t)(kMaxDispatchItems / (uint32_t)threads);
     if (blocks > max_blocks) blocks = max_blocks;
     if (A.ref_rows && blocks * kMaxGatherRows < rows) return RAC_ERR_UNSUPPORTED;
     void* args[] = {&A};
@@ -2763,7 +2776,9 @@ rac_status rac_encode_pooled(const rac_config* cfg, const void* x, const void* r
         return RAC_ERR_HIP;
     // 2. merge per (segment, group) into every row's coefficient slot
     void* pargs[] = {&A, &mom};
-    if (hipLaunchKernel(reinterpret_cast<const void*>(rac_pool_kernel), dim3((unsigned)pblocks),
+    const uint64_t pgrid = pblocks < kMaxDispatchItems / (kWave * kPoolWaves) ? pblocks
+                                                                              : kMaxDispatchItems / (kWave * kPoolWaves);
+    if (hipLaunchKernel(reinterpret_cast<const void*>(rac_pool_kernel), dim3((unsigned)pgrid),
                         dim3(kWave * kPoolWaves), pargs, 0, stream) != hipSuccess)
         return RAC_ERR_HIP;
     // 3. the encode with the pairs given
@@ -2805,7 +2820,8 @@ rac_status run_error(int64_t tokens, int32_t hidden, uint32_t flags, const void*
     if (P > 0) {
         uint32_t rows = T;
         void* a[] = {(void*)&xp, (void*)&xhat, (void*)&bf16, (void*)&rows, (void*)&hidden, (void*)&part};
-        if (hipLaunchKernel(reinterpret_cast<const void*>(rac_error_kernel), dim3(P), dim3(kErrThreads), a, 0,
+        const uint32_t grid = P < kMaxDispatchItems / kErrThreads ? P : (uint32_t)(kMaxDispatchItems / kErrThreads);
+        if (hipLaunchKernel(reinterpret_cast<const void*>(rac_error_kernel), dim3(grid), dim3(kErrThreads), a, 0,
                             stream) != hipSuccess)
             return RAC_ERR_HIP;
     }

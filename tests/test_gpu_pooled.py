@@ -105,6 +105,33 @@ def test_one_row_segments_equal_the_per_token_encode():
     assert np.array_equal(gw, tw) and np.array_equal(gx.view(np.uint32), tx.view(np.uint32))
 
 
+def test_more_segment_groups_than_one_dispatch_holds():
+    """4,300,000 one-row segments of 32 channels (one alignment group each):
+    more (segment, group) pairs than merge workgroups one dispatch holds
+    (2^32 work-items over 1024 per workgroup), so some workgroups merge a
+    second pair.  One-row segments must still give the per-token encode's
+    bytes (header flag aside) and reconstruction."""
+    T, d = 4_300_000, 32
+    c = cfgd(T, d, 32, 32, 4, 2)
+    say(f"[gpu] pooled, {T} one-row segments of {d} channels: generating")
+    rng = np.random.default_rng(21)
+    ref = rng.standard_normal((T, d), dtype=np.float32)
+    x = (rng.uniform(0.8, 1.2, (T, 1)).astype(np.float32) * ref
+         + (0.1 * rng.standard_normal((T, 1))).astype(np.float32)
+         + np.float32(0.05) * rng.standard_normal((T, d), dtype=np.float32))
+    xb, rb = wl.f32_to_bf16_bits(x), wl.f32_to_bf16_bits(ref)
+    del x, ref
+    assert T > 0xFFFFFFFF // 1024
+    say(f"[gpu] pooled, {T} one-row segments: encode and decode")
+    gw, gx, gd = _gpu_pooled(c, xb, rb, np.arange(T + 1))
+    assert np.array_equal(gx.view(np.uint32), gd.view(np.uint32))
+    tw, tx, _, _ = gpu_run(c, xb, rb)
+    assert gw[6] == tw[6] | 16
+    gw = gw.copy()
+    gw[6] = tw[6]
+    assert np.array_equal(gw, tw) and np.array_equal(gx.view(np.uint32), tx.view(np.uint32))
+
+
 def test_full_prefill_uplink_4096x4096_pooled_over_spans():
     """The benchmark shape with segments standing for retrieved spans (random
     lengths between 1 and 600 rows), every row compared with the oracle."""
