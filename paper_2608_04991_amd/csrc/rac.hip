@@ -1279,14 +1279,25 @@ constexpr int kKeyChBits = 13;               // channel bits of the exact search
 constexpr int kTop1 = 16;  // largest k whose first threshold comes from one maximum per lane
 constexpr int kTop2 = 48;  // largest k whose first threshold takes two per wavefront lane
 
+// The third and fourth largest |E| of each (wavefront, lane), kept only with
+// the larger candidate list.
+template <int NW, bool MORE>
+struct LaneMaxMore {
+    uint32_t smax3[NW][kWave];
+    uint32_t smax4[NW][kWave];
+};
 template <int NW>
-struct alignas(16) GroupShared {
+struct LaneMaxMore<NW, false> {};
+
+template <int NW, int CAP = kCandCap>
+struct alignas(16) GroupShared : LaneMaxMore<NW, (CAP > kCandCap)> {
+    static constexpr int cap = CAP;  // candidate list capacity
     // (ckey and cval, contiguous, also hold the exact search's three
     // 64-bin histograms while the list is dropped)
-    uint64_t ckey[kCandCap];  // candidates: |E| bits << 32 | (0xFFFF - channel)
-    uint32_t cval[kCandCap];  // their E bits
-    uint32_t crw[kCandCap];   // their ref word (the bf16 pair holding the channel)
-    uint32_t ccf[kCandCap];   // their group's coefficient pair
+    uint64_t ckey[CAP];  // candidates: |E| bits << 32 | (0xFFFF - channel)
+    uint32_t cval[CAP];  // their E bits
+    uint32_t crw[CAP];   // their ref word (the bf16 pair holding the channel)
+    uint32_t ccf[CAP];   // their group's coefficient pair
     uint32_t smax[NW][kWave]; // lane maxima of |E| of each wavefront
     uint32_t smax2[NW][kWave];// the lanes' second largest |E| (kTop1 < k <= kTop2)
     uint32_t thr;             // that threshold, from wavefront 0
@@ -1300,8 +1311,8 @@ static_assert(offsetof(GroupShared<4>, cval) == sizeof(uint64_t) * kCandCap &&
 // Append this lane's elements of one chunk whose |E| pattern is >= lo (and,
 // with use_key, whose key is >= kmin) to the shared candidate list, with
 // what R~ is formed from (the loaded ref word and the coefficient pair
-// cfv); one LDS atomic per wavefront reserves the slots, entries beyond
-// kCandCap are counted but not stored.
+// cfv); one LDS atomic per wavefront reserves the slots, entries beyond the
+// list's capacity are counted but not stored.
 template <class G>
 __device__ __forceinline__ void append_shared(G& S, uint32_t* counter,
                                               const float* e, const uint4& rpk, uint32_t cfv, bool act, uint32_t c0,
@@ -1324,7 +1335,7 @@ __device__ __forceinline__ void append_shared(G& S, uint32_t* counter,
         const uint64_t m = ballot(p[j]);
         if (m) {
             const uint32_t pos = base + mbcnt64(m);
-            if (p[j] & (pos < (uint32_t)kCandCap)) {
+            if (p[j] & (pos < (uint32_t)G::cap)) {
                 S.ckey[pos] = cand_key(__float_as_uint(e[j]), c0 + j);
                 S.cval[pos] = __float_as_uint(e[j]);
                 S.crw[pos] = rw[j >> 1];
@@ -1357,7 +1368,7 @@ __device__ __forceinline__ void append_bound(G& S, uint32_t* counter, const floa
         const uint64_t m = ballot(__builtin_fabsf(e[j]) >= Lf) & actm;
         if (m) {
             const uint32_t pos = base + mbcnt64(m);
-            if (act & (__builtin_fabsf(e[j]) >= Lf) & (pos < (uint32_t)kCandCap)) {
+            if (act & (__builtin_fabsf(e[j]) >= Lf) & (pos < (uint32_t)G::cap)) {
                 S.ckey[pos] = cand_key(__float_as_uint(e[j]), c0 + j);
                 S.cval[pos] = __float_as_uint(e[j]);
                 S.crw[pos] = rw[j >> 1];
@@ -1409,12 +1420,15 @@ __device__ __forceinline__ void opaque_n(uint4 (&r)[N]) {
 // TWO: the first outlier threshold from the two largest |E| of each
 // (wavefront, lane) (for kTop1 < k <= kTop2; a separate kernel, so that the
 // other k keep the code and registers of the one-value bound).
-template <int BITS, int GA, int GQ, int NW, int CPW, bool GIVEN, bool TWO>
-__global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(CPW == 2 ? 7 : 4)))
+// BIG: the same threshold and a candidate list of 2 * kCandCap entries,
+// ranked two per lane (for k > kTop2, whose rows would overflow the smaller
+// list almost always).
+template <int BITS, int GA, int GQ, int NW, int CPW, bool GIVEN, bool TWO, bool BIG = false>
+__global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(CPW == 2 ? (BIG ? 6 : 7) : 4)))
 void rac_encode_rows_kernel(Args A) {
     // (a row's lists are read before the next row's first barrier and
     // written after it; only the count is reset early, so it alternates)
-    __shared__ GroupShared<NW> S;
+    __shared__ GroupShared<NW, BIG ? 2 * kCandCap : kCandCap> S;
     // E of each wavefront's chunks (one slice per chunk), later the staging
     // of the chunk's reconstruction
     __shared__ float4 EL[NW][CPW][kSlice];
@@ -1544,11 +1558,32 @@ void rac_encode_rows_kernel(Args A) {
         // k-th largest of those 128 values, again with >= k elements >= L,
         // and on rows whose large |E| crowd into some channels far fewer
         // elements pass it (fewer rows overflow the candidate list).  Beyond
-        // kTop2 most rows overflow the list either way and the cheaper bound
-        // is kept.
+        // kTop2 (BIG) each group gives its four largest, L is the k-th
+        // largest of those 256 values, and the list holds 2 * kCandCap.
         S.smax[w][lane] = __float_as_uint(lmx);
-        constexpr bool two = TWO;
-        if constexpr (two) {
+        constexpr bool two = TWO || BIG;
+        if constexpr (BIG) {
+            // the four largest (a multiset: ties count separately), each
+            // value entering at the top and the smaller one moving down
+            uint32_t m1 = 0u, m2 = 0u, m3 = 0u, m4 = 0u;
+#pragma unroll
+            for (int i = 0; i < CPW; ++i) {
+                if (chunk_at(i) >= d) continue;
+                float e[8];
+                get8(EL[w][i], lane, e);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    uint32_t t = __float_as_uint(e[j]) & 0x7FFFFFFFu, hi;
+                    hi = __builtin_elementwise_max(m1, t); t = __builtin_elementwise_min(m1, t); m1 = hi;
+                    hi = __builtin_elementwise_max(m2, t); t = __builtin_elementwise_min(m2, t); m2 = hi;
+                    hi = __builtin_elementwise_max(m3, t); t = __builtin_elementwise_min(m3, t); m3 = hi;
+                    m4 = __builtin_elementwise_max(m4, t);
+                }
+            }
+            S.smax2[w][lane] = m2;
+            S.smax3[w][lane] = m3;
+            S.smax4[w][lane] = m4;
+        } else if constexpr (two) {
             uint32_t m1 = 0u, m2 = 0u;
 #pragma unroll
             for (int i = 0; i < CPW; ++i) {
@@ -1586,22 +1621,38 @@ void rac_encode_rows_kernel(Args A) {
             // and the compute unit's scalar unit is shared by all its
             // wavefronts), then hands L over through LDS
             if (w == 0) {
-                // the two largest of the lane's 2 * NW values: two distinct
-                // elements of the 64 channels of lane l in all wavefronts
-                uint32_t a1 = 0u, a2 = 0u;
+                // the two (with BIG four) largest of the lane's values from
+                // every wavefront: distinct elements of the 64 channels of
+                // lane l in all wavefronts
+                uint32_t a1 = 0u, a2 = 0u, a3 = 0u, a4 = 0u;
+                auto insert = [&](uint32_t t) {
+                    uint32_t hi;
+                    hi = __builtin_elementwise_max(a1, t); t = __builtin_elementwise_min(a1, t); a1 = hi;
+                    if constexpr (BIG) {
+                        hi = __builtin_elementwise_max(a2, t); t = __builtin_elementwise_min(a2, t); a2 = hi;
+                        hi = __builtin_elementwise_max(a3, t); t = __builtin_elementwise_min(a3, t); a3 = hi;
+                        a4 = __builtin_elementwise_max(a4, t);
+                    } else {
+                        a2 = __builtin_elementwise_max(a2, t);
+                    }
+                };
 #pragma unroll
                 for (int ww = 0; ww < NW; ++ww) {
-                    const uint32_t u1 = S.smax[ww][lane], u2 = S.smax2[ww][lane];
-                    a2 = __builtin_elementwise_max(a2, __builtin_elementwise_min(a1, u1));
-                    a1 = __builtin_elementwise_max(a1, u1);
-                    a2 = __builtin_elementwise_max(a2, __builtin_elementwise_min(a1, u2));
-                    a1 = __builtin_elementwise_max(a1, u2);
+                    insert(S.smax[ww][lane]);
+                    insert(S.smax2[ww][lane]);
+                    if constexpr (BIG) {
+                        insert(S.smax3[ww][lane]);
+                        insert(S.smax4[ww][lane]);
+                    }
                 }
 #pragma unroll
                 for (int bit = 30; bit >= 15; --bit) {
                     const uint32_t cnd = L | (1u << bit);
-                    const uint32_t c = (uint32_t)__builtin_popcountll(ballot(a1 >= cnd)) +
-                                       (uint32_t)__builtin_popcountll(ballot(a2 >= cnd));
+                    uint32_t c = (uint32_t)__builtin_popcountll(ballot(a1 >= cnd)) +
+                                 (uint32_t)__builtin_popcountll(ballot(a2 >= cnd));
+                    if constexpr (BIG)
+                        c += (uint32_t)__builtin_popcountll(ballot(a3 >= cnd)) +
+                             (uint32_t)__builtin_popcountll(ballot(a4 >= cnd));
                     if (c >= (uint32_t)k) L = cnd;
                 }
                 if (lane == 0u) S.thr = L;
@@ -1621,19 +1672,32 @@ void rac_encode_rows_kernel(Args A) {
             append_bound(S, cnt, e, rp[i], cf[i], c0 < (uint32_t)d, c0, Lf, lane);
         }
         __syncthreads();
-        // k-th largest of the first Cn listed keys (Cn <= kCandCap; lane i
-        // ranks key i by the number of larger keys, which are distinct; LDS
-        // broadcast reads, two keys at a time); `key` gets lane i's key
-        auto kth_key = [&](uint32_t Cn, uint64_t& key) -> uint64_t {
-            const bool have = lane < Cn;
+        // k-th largest of the first Cn listed keys (Cn <= S.cap; lane i
+        // ranks key i, and with BIG key i + 64 as well, by the number of
+        // larger keys, which are distinct; LDS broadcast reads, two keys at a
+        // time); `key` and `key2` get lane i's keys
+        auto kth_key = [&](uint32_t Cn, uint64_t& key, uint64_t& key2) -> uint64_t {
+            const bool have = lane < Cn, have2 = BIG && lane + (uint32_t)kWave < Cn;
             key = have ? S.ckey[lane] : 0ull;
-            uint32_t rank = 0;
+            key2 = have2 ? S.ckey[lane + kWave] : 0ull;
+            uint32_t rank = 0, rank2 = 0;
             for (uint32_t j = 0; j < Cn; j += 2) {
                 const ulonglong2 kk = *reinterpret_cast<const ulonglong2*>(&S.ckey[j]);
+                const bool y = j + 1u < Cn;
                 rank += (kk.x > key) ? 1u : 0u;
-                rank += (j + 1u < Cn && kk.y > key) ? 1u : 0u;
+                rank += (y && kk.y > key) ? 1u : 0u;
+                if constexpr (BIG) {
+                    rank2 += (kk.x > key2) ? 1u : 0u;
+                    rank2 += (y && kk.y > key2) ? 1u : 0u;
+                }
             }
             const uint64_t at = ballot(have && rank == (uint32_t)(k - 1));
+            if constexpr (BIG) {
+                if (!at) {
+                    const uint64_t at2 = ballot(have2 && rank2 == (uint32_t)(k - 1));
+                    return rdlane64(key2, at2 ? (int)__builtin_ctzll(at2) : 0);
+                }
+            }
             return rdlane64(key, at ? (int)__builtin_ctzll(at) : 0);
         };
         // (values read from LDS are the same in every lane: readfirstlane
@@ -1641,7 +1705,7 @@ void rac_encode_rows_kernel(Args A) {
         uint32_t C = uniform(*cnt);
         uint64_t key = 0ull;
         uint64_t kst = 0ull;  // the outliers are the listed keys >= kst
-        if (C > (uint32_t)kCandCap) {
+        if (C > (uint32_t)S.cap) {
             // More candidates than the list holds: they are narrowed by a
             // radix search over a 49-bit key (|E| pattern, 8191 - channel,
             // 5 zero bits; a larger key ranks higher), from the top digit
@@ -1649,7 +1713,7 @@ void rac_encode_rows_kernel(Args A) {
             // Each digit (6 bits, the last one narrower) is taken from a
             // 64-bin histogram of the candidates that share the digits found
             // so far: the bin holding the k-th largest.  Once the keys in
-            // that bin or above number at most kCandCap, the list is rebuilt
+            // that bin or above number at most S.cap, the list is rebuilt
             // from them and ranked as usual; keys are distinct, so at worst
             // the last digit gets there.  The histograms (three, in turn,
             // each cleared two levels before it is filled, so one barrier
@@ -1699,7 +1763,7 @@ void rac_encode_rows_kernel(Args A) {
                 prefix = (prefix << width) | (uint64_t)(kWave - 1 - ls);
                 need -= above;
                 // keys in this bin or above: k - need + nb
-                if ((uint32_t)k - need + nb <= (uint32_t)kCandCap || shift == 0) break;
+                if ((uint32_t)k - need + nb <= (uint32_t)S.cap || shift == 0) break;
                 width = shift >= 6 ? 6 : shift;
                 shift -= width;
             }
@@ -1718,15 +1782,16 @@ void rac_encode_rows_kernel(Args A) {
                 append_shared(S, xc, e, rp[i], cf[i], c0 < (uint32_t)d, c0, pm, true, kmin, lane);
             }
             __syncthreads();
-            C = uniform(*xc);  // k <= C <= kCandCap
+            C = uniform(*xc);  // k <= C <= S.cap
         }
-        kst = kth_key(C, key);
+        uint64_t key2 = 0ull;
+        kst = kth_key(C, key, key2);
         const bool have = lane < C;
-        // Candidate lane i holds one chosen outlier (or none): its channel
-        // and its reconstruction R~ + fp16(E), which phase C writes over
-        // the staged value of that channel.  Every outlier is a candidate
-        // and keys are distinct, so the outliers are exactly the candidate
-        // keys >= kst.
+        // Candidate lane i holds one chosen outlier (or none; with BIG two,
+        // entries i and i + 64): its channel and its reconstruction
+        // R~ + fp16(E), which phase C writes over the staged value of that
+        // channel.  Every outlier is a candidate and keys are distinct, so
+        // the outliers are exactly the candidate keys >= kst.
         const bool chosen = have && key >= kst;
         const uint32_t och = chosen ? key_channel(key) : 0xFFFFFFFFu;
         uint32_t oval = 0u;
@@ -1737,17 +1802,38 @@ void rac_encode_rows_kernel(Args A) {
             const float r = (och & 1u) ? bf16_hi(rw) : bf16_lo(rw);
             ohat = __builtin_fmaf(f16_wire(cfc & 0xFFFFu), r, f16_wire(cfc >> 16)) + f16_wire(oval);
         }
+        bool chosen2 = false;
+        uint32_t och2 = 0xFFFFFFFFu, oval2 = 0u;
+        float ohat2 = 0.0f;
+        if constexpr (BIG) {
+            chosen2 = lane + (uint32_t)kWave < C && key2 >= kst;
+            if (chosen2) {
+                const uint32_t i2 = lane + (uint32_t)kWave;
+                och2 = key_channel(key2);
+                oval2 = f16_rne(__uint_as_float(S.cval[i2]));
+                const uint32_t rw = S.crw[i2], cfc = S.ccf[i2];
+                const float r = (och2 & 1u) ? bf16_hi(rw) : bf16_lo(rw);
+                ohat2 = __builtin_fmaf(f16_wire(cfc & 0xFFFFu), r, f16_wire(cfc >> 16)) + f16_wire(oval2);
+            }
+        }
         if (w == 0) {
             // the row's outliers in ascending channel order (slot = number of
             // chosen keys of a lower channel, i.e. of a larger low word)
-            uint32_t slot = 0;
+            uint32_t slot = 0, slot2 = 0;
             for (uint32_t j = 0; j < C; j += 2) {
                 const ulonglong2 kk = *reinterpret_cast<const ulonglong2*>(&S.ckey[j]);
-                slot += (kk.x >= kst && (uint32_t)kk.x > (uint32_t)key) ? 1u : 0u;
-                slot += (j + 1u < C && kk.y >= kst && (uint32_t)kk.y > (uint32_t)key) ? 1u : 0u;
+                const bool cx = kk.x >= kst, cy = j + 1u < C && kk.y >= kst;
+                slot += (cx && (uint32_t)kk.x > (uint32_t)key) ? 1u : 0u;
+                slot += (cy && (uint32_t)kk.y > (uint32_t)key) ? 1u : 0u;
+                if constexpr (BIG) {
+                    slot2 += (cx && (uint32_t)kk.x > (uint32_t)key2) ? 1u : 0u;
+                    slot2 += (cy && (uint32_t)kk.y > (uint32_t)key2) ? 1u : 0u;
+                }
             }
             const Rsrc outl = rsrc(A.outl, (uint64_t)row * (uint64_t)k, (uint32_t)k * 4u);
             bstore32(outl, (chosen && slot < (uint32_t)k) ? slot * 4u : kOut, key_channel(key) | (oval << 16));
+            if constexpr (BIG)
+                bstore32(outl, (chosen2 && slot2 < (uint32_t)k) ? slot2 * 4u : kOut, key_channel(key2) | (oval2 << 16));
         }
 
         // E^d: E with the outliers set to 0, in place (each wavefront
@@ -1756,6 +1842,10 @@ void rac_encode_rows_kernel(Args A) {
         for (int i = 0; i < CPW; ++i) {
             const uint32_t oc = och - (uint32_t)(chunk_at(i));
             if (oc < (uint32_t)kChunk) reinterpret_cast<float*>(EL[w][i])[slice_float(oc)] = 0.0f;
+            if constexpr (BIG) {
+                const uint32_t oc2 = och2 - (uint32_t)(chunk_at(i));
+                if (oc2 < (uint32_t)kChunk) reinterpret_cast<float*>(EL[w][i])[slice_float(oc2)] = 0.0f;
+            }
         }
         wave_lds_sync();
 
@@ -1816,6 +1906,8 @@ void rac_encode_rows_kernel(Args A) {
             put8(st, lane, H);
             wave_lds_sync();
             if (och - chunk0 < (uint32_t)kChunk) reinterpret_cast<float*>(st)[slice_float(och - chunk0)] = ohat;
+            if constexpr (BIG)
+                if (och2 - chunk0 < (uint32_t)kChunk) reinterpret_cast<float*>(st)[slice_float(och2 - chunk0)] = ohat2;
             wave_lds_sync();
             emit_xhat(rxh, A.xhat_bf16 != 0, chunk0, l8 >> 3, st);
         }
@@ -2400,25 +2492,35 @@ KernelFn pick_encode(const Args& A, int bits) {
     return encode_for<-1, -1>(bits, om);
 }
 
-template <int GA, int GQ, int CPW, bool GIVEN, bool TWO>
+template <int GA, int GQ, int CPW, bool GIVEN, bool TWO, bool BIG>
 KernelFn rows_for_bits(int bits) {
     switch (bits) {
-        case 2: return rac_encode_rows_kernel<2, GA, GQ, kRowsWaves, CPW, GIVEN, TWO>;
-        case 3: return rac_encode_rows_kernel<3, GA, GQ, kRowsWaves, CPW, GIVEN, TWO>;
-        case 4: return rac_encode_rows_kernel<4, GA, GQ, kRowsWaves, CPW, GIVEN, TWO>;
-        default: return rac_encode_rows_kernel<8, GA, GQ, kRowsWaves, CPW, GIVEN, TWO>;
+        case 2: return rac_encode_rows_kernel<2, GA, GQ, kRowsWaves, CPW, GIVEN, TWO, BIG>;
+        case 3: return rac_encode_rows_kernel<3, GA, GQ, kRowsWaves, CPW, GIVEN, TWO, BIG>;
+        case 4: return rac_encode_rows_kernel<4, GA, GQ, kRowsWaves, CPW, GIVEN, TWO, BIG>;
+        default: return rac_encode_rows_kernel<8, GA, GQ, kRowsWaves, CPW, GIVEN, TWO, BIG>;
+    }
+}
+
+template <int GA, int GQ, int CPW, bool GIVEN>
+KernelFn rows_for_cpw(int bits, int k) {
+    if constexpr (GIVEN) {
+        return rows_for_bits<GA, GQ, CPW, true, false, false>(bits);
+    } else {
+        if (k > kTop2) return rows_for_bits<GA, GQ, CPW, false, false, true>(bits);
+        if (k > kTop1) return rows_for_bits<GA, GQ, CPW, false, true, false>(bits);
+        return rows_for_bits<GA, GQ, CPW, false, false, false>(bits);
     }
 }
 
 // Rows of up to 4096 channels: two chunks per wavefront; up to 8192: four.
-// The two-value threshold for kTop1 < k <= kTop2 (not with given pairs,
-// which keep the one-value bound: either bound is exact).
+// The two-value threshold for kTop1 < k <= kTop2, and with the larger
+// candidate list beyond (not with given pairs, which keep the one-value
+// bound and the smaller list: every bound and list size is exact).
 template <int GA, int GQ, bool GIVEN = false>
 KernelFn rows_for(int bits, int d, int k) {
-    const bool two = !GIVEN && k > kTop1 && k <= kTop2;
-    if (d <= kRowsWaves * 2 * kChunk)
-        return two ? rows_for_bits<GA, GQ, 2, GIVEN, !GIVEN>(bits) : rows_for_bits<GA, GQ, 2, GIVEN, false>(bits);
-    return two ? rows_for_bits<GA, GQ, 4, GIVEN, !GIVEN>(bits) : rows_for_bits<GA, GQ, 4, GIVEN, false>(bits);
+    if (d <= kRowsWaves * 2 * kChunk) return rows_for_cpw<GA, GQ, 2, GIVEN>(bits, k);
+    return rows_for_cpw<GA, GQ, 4, GIVEN>(bits, k);
 }
 
 // Rows with outliers take the NW-wavefront kernel when it holds the whole

@@ -134,10 +134,11 @@ CASES = {
                                  lambda: wl.long_context(0, rows=(0, 29), group=128)[:2]),
     "long_13x4096_g128_b8_k16": (cfgd(13, 4096, 128, 128, 8, 16),
                                  lambda: wl.long_context(2, rows=(500, 513), group=128)[:2]),
-    # Uplink rows with more than 64 elements above the first threshold (about
-    # a quarter of them at g = 64, k = 16 and most at k = 64; at k = 32 the
-    # threshold from the two largest of each wavefront lane leaves few),
-    # whose outliers come from the histogram search
+    # Uplink rows with more candidates above the first threshold than the
+    # list holds (about a quarter of them at g = 64, k = 16; at k = 32 the
+    # threshold from the two largest of each wavefront lane leaves few, and
+    # k = 64 ranks a list of 128), whose outliers come from the histogram
+    # search
     "overflow_uplink_32x4096_g64_b4_k16": (cfgd(32, 4096, 64, 64, 4, 16),
                                            lambda: wl.prefill_uplink(0, rows=(0, 32))[:2]),
     "overflow_uplink_24x4096_g128_b4_k32": (cfgd(24, 4096, 128, 128, 4, 32),
@@ -149,6 +150,15 @@ CASES = {
     "ties_heavy_zero_ref_6x4096_g128_k24": (cfgd(6, 4096, 128, 128, 4, 24),
                                             lambda: (wl.f32_to_bf16_bits(_zero_sum_integer_rows(6, 4096, 128, 0, 0.0, 2)), None)),
     "uplink_17x4096_g128_b4_k20": (cfgd(17, 4096, 128, 128, 4, 20), lambda: wl.prefill_uplink(4, rows=(200, 217))[:2]),
+    # k > 48: the list of 128 candidates, two per lane; with ties everywhere
+    # it overflows into the histogram search
+    "ties_heavy_zero_ref_6x4096_g128_k60": (cfgd(6, 4096, 128, 128, 4, 60),
+                                            lambda: (wl.f32_to_bf16_bits(_zero_sum_integer_rows(6, 4096, 128, 0, 0.0, 4)), None)),
+    "uplink_23x4096_g128_b4_k49": (cfgd(23, 4096, 128, 128, 4, 49), lambda: wl.prefill_uplink(6, rows=(300, 323))[:2]),
+    "uplink_19x2048_g128_b4_k64": (cfgd(19, 2048, 128, 128, 4, 64),
+                                   lambda: wl.prefill_uplink(7, rows=(0, 19), hidden=2048)[:2]),
+    "long_300x4096_g64_b2_k56": (cfgd(300, 4096, 64, 64, 2, 56),
+                                 lambda: wl.long_context(3, rows=(1000, 1300), group=64)[:2]),
     # rows of 4097..8192 channels (four chunks per wavefront)
     "wide_uplink_12x8192_g128_b4_k16": (cfgd(12, 8192, 128, 128, 4, 16),
                                         lambda: wl.prefill_uplink(0, rows=(0, 12), hidden=8192)[:2]),
@@ -383,6 +393,19 @@ def test_full_prefill_uplink_4096x4096_sampled():
     n = assert_parity(c, gw, gx, ow, ox, g_rows=rows, o_rows=slice(None))
     assert n == rows.size
     assert wirefmt.padding_is_zero(gw) and wirefmt.header(gw)["tokens"] == 4096
+
+
+def test_full_prefill_uplink_4096x4096_k64_sampled():
+    """k = 64 at the uplink's full size: the list of 128 candidates ranked two
+    per lane, on the strided grid."""
+    c = cfgd(4096, 4096, 128, 128, 4, 64)
+    say("[gpu] full prefill uplink 4096x4096, k = 64: generating")
+    xb, rb, _ = wl.prefill_uplink(0)
+    gw, gx, gd, _ = gpu_run(c, xb, rb)
+    assert np.array_equal(gx, gd)
+    rows = _sample(4096, 48, seed=3)
+    ow, ox = oracle_run(dict(c, tokens=rows.size), xb[rows], rb[rows])
+    assert_parity(c, gw, gx, ow, ox, g_rows=rows, o_rows=slice(None))
 
 
 def test_full_prefill_uplink_4096x4096_group_outliers_sampled():
