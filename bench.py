@@ -59,7 +59,7 @@ PROFILES = os.path.join(ROOT, "profiles")
 # FETCH_SIZE / WRITE_SIZE runs (see paper_2608_04991_amd/rocprof_summary.py)
 LLC_BYTES = 256 << 20    # MI355X last-level (Infinity) cache
 TRAFFIC_FILE = os.path.join(PROFILES, "rac_encode_prefill_downlink_65536x3584_traffic.json")
-HEADLINE_KERNEL = "rac_encode_rows_kernel<4, 4, 4, 4, 2, false>"
+HEADLINE_KERNEL = "rac_encode_rows_kernel<4, 4, 4, 4, 2, false, false, false>"
 
 
 def log(msg):
@@ -427,7 +427,7 @@ def all_extras(torch, rac, wl, stream):
         "encode_us": round(e, 2), "encode_hbm_frac": frac(U.alg(), e),
         "decode_us": round(dcd, 2), "decode_hbm_frac": frac(U.alg(False), dcd),
         "wire_over_bf16": round(U.wbytes / (4096 * 4096 * 2), 4),
-        "encode_kernel": "rac_encode_rows_kernel<4, 4, 4, 4, 2, false>"}
+        "encode_kernel": "rac_encode_rows_kernel<4, 4, 4, 4, 2, false, false, false>"}
     log(f"[bench] uplink: {ex['prefill_uplink_4096x4096_g128_b4_k8']}")
     ex["launch_shapes_4096x4096_g128_b4_k8"] = launch_shape_rates(torch, rac, U, 50)
     ex["outlier_modes_4096x4096_g128_b4"] = outlier_mode_rates(torch, rac, U, 50)
