@@ -62,17 +62,31 @@ __device__ __forceinline__ uint16_t to_bf(float v) {  // round to nearest even (
 enum Epi { kPartial = 0, kStore = 1, kSwiglu = 2, kResidOut = 3 };
 
 struct Gemm {
-    const uint16_t* a;   // [M][K]
+    const uint16_t* a;   // [M][K] (not read with NORM)
     const uint16_t* w;   // [N][K]
     int32_t M, N, K, ksplit;   // K range per split
     float* out;          // kPartial: [splits][M][N]; kStore: [M][N]
     uint16_t* out16;     // kSwiglu: [M][N/2]; kResidOut: [M][N]
     const uint16_t* resid;     // kResidOut: bf16 [M][N] added to the product
+    // NORM (M <= kFuseRows, one K range, K <= kFuseK): the activations are
+    // bf16(h / sqrt(mean(h^2) + eps) * gain), h = nres + sum_s npart[s] added
+    // in order, formed by every workgroup in LDS (the norm of the step's row
+    // kernel, folded into the product that consumes it)
+    const float* nres;      // [M][K], or null
+    const float* npart;     // [nsplits][M][K]
+    int32_t nsplits;
+    const uint16_t* ngain;  // bf16 [K]
+    float* nh;              // [M][K]: h, written by the first workgroup; or null
 };
 
-template <int EPI>
+constexpr int kFuseRows = kGemmWaves;  // batch rows whose norm a product forms itself (one per wavefront)
+constexpr int kFuseK = 2048;           // the widest such row (the model width)
+constexpr int kNormPad = 8;            // bf16 padding per LDS row (spreads the rows over the banks)
+
+template <int EPI, bool NORM = false>
 __global__ __launch_bounds__(kW * kGemmWaves) void pred_gemm(Gemm g) {
     __shared__ f32x4 red[kGemmWaves - 1][kRt][kW];
+    extern __shared__ uint4 an4[];  // NORM: the normalized rows, [M][K + kNormPad] bf16
     const int lane = threadIdx.x & (kW - 1), w = threadIdx.x / kW;
     const int n0 = blockIdx.x * kNt, s = blockIdx.y, m0 = blockIdx.z * (kRt * 16);
     const int kq = g.ksplit / kGemmWaves;                // this wavefront's share (multiple of 32)
@@ -87,12 +101,88 @@ __global__ __launch_bounds__(kW * kGemmWaves) void pred_gemm(Gemm g) {
     // four 32-wide steps at a time: their weight loads (the HBM stream) are
     // all issued before the first product waits, then the activation tiles
     // (read by every column tile, so cache hits) step by step
-    for (int k0 = 0; k0 < kq; k0 += 4 * 32) {
-        bf16x8 bw[4];
+    bf16x8 bw[4];
+    auto load_w = [&](int k0) {
 #pragma unroll
         for (int u = 0; u < 4; ++u)
             bw[u] = k0 + 32 * u < kq ? *reinterpret_cast<const bf16x8*>(wrow + k0 + 32 * u)
                                      : bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
+    };
+    load_w(0);
+    uint16_t* const an = reinterpret_cast<uint16_t*>(an4);
+    const int pitch = g.K + kNormPad;
+    if constexpr (NORM) {
+        // wavefront w forms row w (while the first weights are in flight):
+        // lane l holds channels 512 i + 8 l .. + 7
+        if (w < g.M) {
+            const int b = w;
+            const bool writer = g.nh && blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0;
+            float hv[kFuseK / 512][8];
+            float ss = 0.0f;
+#pragma unroll
+            for (int i = 0; i < kFuseK / 512; ++i) {
+                const int c = 512 * i + 8 * lane;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) hv[i][j] = 0.0f;
+                if (c >= g.K) continue;
+                if (g.nres) {
+                    const float4 r0 = *reinterpret_cast<const float4*>(g.nres + (size_t)b * g.K + c);
+                    const float4 r1 = *reinterpret_cast<const float4*>(g.nres + (size_t)b * g.K + c + 4);
+                    hv[i][0] = r0.x; hv[i][1] = r0.y; hv[i][2] = r0.z; hv[i][3] = r0.w;
+                    hv[i][4] = r1.x; hv[i][5] = r1.y; hv[i][6] = r1.z; hv[i][7] = r1.w;
+                }
+                // the partials four at a time, every load of a group issued
+                // before its adds, which run in split order
+                for (int s0 = 0; s0 < g.nsplits; s0 += 4) {
+                    float4 pp[4][2];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        if (s0 + u < g.nsplits) {
+                            const float* q = g.npart + ((size_t)(s0 + u) * g.M + b) * g.K + c;
+                            pp[u][0] = *reinterpret_cast<const float4*>(q);
+                            pp[u][1] = *reinterpret_cast<const float4*>(q + 4);
+                        }
+                    }
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        if (s0 + u < g.nsplits) {
+                            hv[i][0] = hv[i][0] + pp[u][0].x; hv[i][1] = hv[i][1] + pp[u][0].y;
+                            hv[i][2] = hv[i][2] + pp[u][0].z; hv[i][3] = hv[i][3] + pp[u][0].w;
+                            hv[i][4] = hv[i][4] + pp[u][1].x; hv[i][5] = hv[i][5] + pp[u][1].y;
+                            hv[i][6] = hv[i][6] + pp[u][1].z; hv[i][7] = hv[i][7] + pp[u][1].w;
+                        }
+                    }
+                }
+                if (writer) {
+                    float* q = g.nh + (size_t)b * g.K + c;
+                    *reinterpret_cast<float4*>(q) = make_float4(hv[i][0], hv[i][1], hv[i][2], hv[i][3]);
+                    *reinterpret_cast<float4*>(q + 4) = make_float4(hv[i][4], hv[i][5], hv[i][6], hv[i][7]);
+                }
+#pragma unroll
+                for (int j = 0; j < 8; ++j) ss = ss + hv[i][j] * hv[i][j];
+            }
+            for (int o = kW / 2; o > 0; o >>= 1) ss = ss + __shfl_xor(ss, o);
+            const float inv = 1.0f / __builtin_sqrtf(ss / (float)g.K + kEps);
+#pragma unroll
+            for (int i = 0; i < kFuseK / 512; ++i) {
+                const int c = 512 * i + 8 * lane;
+                if (c >= g.K) continue;
+                const uint4 gw = *reinterpret_cast<const uint4*>(g.ngain + c);
+                const uint32_t gv[4] = {gw.x, gw.y, gw.z, gw.w};
+                uint32_t o[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const uint32_t lo = to_bf(hv[i][2 * j] * inv * __uint_as_float(gv[j] << 16));
+                    const uint32_t hi = to_bf(hv[i][2 * j + 1] * inv * __uint_as_float(gv[j] & 0xFFFF0000u));
+                    o[j] = lo | (hi << 16);
+                }
+                *reinterpret_cast<uint4*>(an + (size_t)b * pitch + c) = make_uint4(o[0], o[1], o[2], o[3]);
+            }
+        }
+        __syncthreads();
+    }
+    for (int k0 = 0; k0 < kq; k0 += 4 * 32) {
+        if (k0 > 0) load_w(k0);
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             if (k0 + 32 * u >= kq) break;
@@ -100,8 +190,12 @@ __global__ __launch_bounds__(kW * kGemmWaves) void pred_gemm(Gemm g) {
 #pragma unroll
             for (int r = 0; r < kRt; ++r) {
                 bf16x8 av = bf16x8{0, 0, 0, 0, 0, 0, 0, 0};
-                if (rows_in[r])
+                if constexpr (NORM) {
+                    if (r == 0 && rows_in[0])
+                        av = *reinterpret_cast<const bf16x8*>(an + (size_t)(lane & 15) * pitch + kbeg + kl + k);
+                } else if (rows_in[r]) {
                     av = *reinterpret_cast<const bf16x8*>(g.a + (size_t)(m0 + 16 * r + (lane & 15)) * g.K + kbeg + kl + k);
+                }
                 acc[r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bw[u], acc[r], 0, 0, 0);
             }
         }
@@ -396,11 +490,26 @@ PWork pwork(const rac_predictor_config* c, int B) {
 template <int EPI>
 rac_status gemm(const uint16_t* a, const uint16_t* w, int M, int N, int K, int splits, float* out, uint16_t* out16,
                 const uint16_t* resid, hipStream_t st) {
-    Gemm g{a, w, M, N, K, K / splits, out, out16, resid};
+    Gemm g{a, w, M, N, K, K / splits, out, out16, resid, nullptr, nullptr, 0, nullptr, nullptr};
     void* args[] = {&g};
     const dim3 grid((unsigned)(N / kNt), (unsigned)splits, (unsigned)((M + kRt * 16 - 1) / (kRt * 16)));
     return hipLaunchKernel(reinterpret_cast<const void*>(pred_gemm<EPI>), grid, dim3(kW * kGemmWaves), args, 0, st) ==
                    hipSuccess
+               ? RAC_OK
+               : RAC_ERR_HIP;
+}
+
+// The product of the normalized rows h = nres + sum_s npart[s] (one K range,
+// M <= kFuseRows, K <= kFuseK): every workgroup forms the norm in LDS.
+template <int EPI>
+rac_status gemm_norm(const float* nres, const float* npart, int nsplits, const uint16_t* gain, float* nh,
+                     const uint16_t* w, int M, int N, int K, float* out, uint16_t* out16, const uint16_t* resid,
+                     hipStream_t st) {
+    Gemm g{nullptr, w, M, N, K, K, out, out16, resid, nres, npart, nsplits, gain, nh};
+    void* args[] = {&g};
+    const size_t lds = (size_t)M * (size_t)(K + kNormPad) * 2u;
+    return hipLaunchKernel(reinterpret_cast<const void*>(pred_gemm<EPI, true>), dim3((unsigned)(N / kNt), 1u, 1u),
+                           dim3(kW * kGemmWaves), args, lds, st) == hipSuccess
                ? RAC_OK
                : RAC_ERR_HIP;
 }
@@ -411,6 +520,17 @@ rac_status row(const float* resid, const float* part, int splits, int M, int m, 
     void* args[] = {&r};
     return hipLaunchKernel(reinterpret_cast<const void*>(pred_row), dim3((unsigned)M), dim3(kRowThreads), args, 0,
                            st) == hipSuccess
+               ? RAC_OK
+               : RAC_ERR_HIP;
+}
+
+rac_status attention(const rac_predictor_config* cfg, const float* qkv, void* cache, const int32_t* pos, int B,
+                     uint16_t* o, hipStream_t st) {
+    AttnArgs a{qkv, static_cast<uint16_t*>(cache), pos, B, cfg->model, cfg->heads, cfg->window, o, {}};
+    for (int i = 0; i < kHd / 2; ++i) a.theta[i] = std::pow(10000.0, -2.0 * i / kHd);
+    void* args[] = {&a};
+    return hipLaunchKernel(reinterpret_cast<const void*>(pred_attn), dim3((unsigned)(B * cfg->heads)), dim3(kW), args,
+                           0, st) == hipSuccess
                ? RAC_OK
                : RAC_ERR_HIP;
 }
@@ -476,19 +596,28 @@ rac_status rac_predictor_step(const rac_predictor_config* cfg, const void* weigh
     hipStream_t st = stream;
     rac_status s;
     const int si = in_splits(cfg), sd = down_splits(cfg);
+    if (B <= kFuseRows && m <= kFuseK) {
+        // small batches: each norm is formed by the product that consumes
+        // it (seven launches instead of ten)
+        if ((s = gemm<kPartial>(x, wt(L.w_in), B, m, d, si, part, nullptr, nullptr, st)) != RAC_OK) return s;
+        if ((s = gemm_norm<kStore>(nullptr, part, si, wt(L.g1), h0, wt(L.w_qkv), B, 3 * m, m, qkv, nullptr, nullptr,
+                                   st)) != RAC_OK)
+            return s;
+        if ((s = attention(cfg, qkv, cache, pos, B, o, st)) != RAC_OK) return s;
+        if ((s = gemm<kPartial>(o, wt(L.w_o), B, m, m, 1, part, nullptr, nullptr, st)) != RAC_OK) return s;
+        if ((s = gemm_norm<kSwiglu>(h0, part, 1, wt(L.g2), h1, wt(L.w_gu), B, 2 * f, m, nullptr, gg, nullptr, st)) !=
+            RAC_OK)
+            return s;
+        if ((s = gemm<kPartial>(gg, wt(L.w_down), B, m, f, sd, part, nullptr, nullptr, st)) != RAC_OK) return s;
+        return gemm_norm<kResidOut>(h1, part, sd, wt(L.g3), nullptr, wt(L.w_out), B, d, m, nullptr,
+                                    static_cast<uint16_t*>(ref_out), x, st);
+    }
     // h0 = x W_in^T (split K), then n1 = RMSNorm(h0)
     if ((s = gemm<kPartial>(x, wt(L.w_in), B, m, d, si, part, nullptr, nullptr, st)) != RAC_OK) return s;
     if ((s = row(nullptr, part, si, B, m, wt(L.g1), h0, n, st)) != RAC_OK) return s;
     // q, k, v; attention over the window; h1 = h0 + o W_o^T; n2 = RMSNorm(h1)
     if ((s = gemm<kStore>(n, wt(L.w_qkv), B, 3 * m, m, 1, qkv, nullptr, nullptr, st)) != RAC_OK) return s;
-    {
-        AttnArgs a{qkv, static_cast<uint16_t*>(cache), pos, B, m, cfg->heads, cfg->window, o, {}};
-        for (int i = 0; i < kHd / 2; ++i) a.theta[i] = std::pow(10000.0, -2.0 * i / kHd);
-        void* args[] = {&a};
-        if (hipLaunchKernel(reinterpret_cast<const void*>(pred_attn), dim3((unsigned)(B * cfg->heads)), dim3(kW),
-                            args, 0, st) != hipSuccess)
-            return RAC_ERR_HIP;
-    }
+    if ((s = attention(cfg, qkv, cache, pos, B, o, st)) != RAC_OK) return s;
     if ((s = gemm<kPartial>(o, wt(L.w_o), B, m, m, 1, part, nullptr, nullptr, st)) != RAC_OK) return s;
     if ((s = row(h0, part, 1, B, m, wt(L.g2), h1, n, st)) != RAC_OK) return s;
     // SwiGLU; h2 = h1 + g W_down^T; n3 = RMSNorm(h2)

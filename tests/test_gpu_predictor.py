@@ -108,3 +108,15 @@ def test_predictor_windows_longer_than_one_pass_of_64_positions(window, start):
     say(f"[gpu] predictor 512/128/2/256, window {window}, batch 8, 4 steps from position {start}")
     _run(cfg, 8, 4, lambda s, b: start + s + 37 * b, seed=2)
 
+
+
+@pytest.mark.parametrize("hidden,model,heads,ffn,window,batch", [
+    (4096, 512, 8, 2048, 64, 2), (4096, 512, 8, 2048, 64, 4),
+    (1024, 2048, 32, 512, 16, 3), (512, 128, 2, 256, 5, 4)])
+def test_predictor_small_batches_fold_the_norms(hidden, model, heads, ffn, window, batch):
+    # batches of at most four rows form each norm inside the product that
+    # consumes it; widths 128 to 2048, including a down projection of one
+    # K range (ffn 256 and 512)
+    cfg = rac.PredictorConfig(hidden, model, heads, ffn, window, 4)
+    say(f"[gpu] predictor {hidden}/{model}/{heads}/{ffn}, window {window}, batch {batch}, 6 steps")
+    _run(cfg, batch, 6, lambda s, b: s + 3 * b, seed=4)
