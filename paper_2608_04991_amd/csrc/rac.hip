@@ -14,7 +14,12 @@
 // packing and the fused sender reconstruction, so every byte of x/ref is read
 // from HBM once and every output byte written once.  Work that spans chunks
 // (the per-token outlier choice, groups wider than 512 channels) goes through
-// LDS with workgroup barriers; everything else is wave-local.
+// LDS with workgroup barriers; everything else is wave-local.  (The
+// per-token outlier encode deals a row's chunks round four wavefronts, two or
+// four chunks each.)  Up to a few rows per resident workgroup the grid is the
+// resident workgroups, taking rows in strides with the next row prefetched;
+// beyond that, one workgroup per row, which keeps the rows in flight close
+// together in memory.
 //
 // Exactness.  The sums of the fit follow a fixed pairwise tree over channel
 // order: a lane-local tree over its 8 contiguous channels, a butterfly across
@@ -37,7 +42,7 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kChunk = 512;       // channels per wavefront (8 per lane)
 constexpr int kMaxWaves = 16;     // rows up to 8192 channels
-constexpr int kCandCap = 64;      // outlier candidates ranked by one wavefront
+constexpr int kCandCap = 64;      // outlier candidates ranked by one wavefront (twice that for k > 48)
 constexpr int kMaxGatherRows = 64; // rows per workgroup with a gathered reference
 constexpr int kStridedRowsMax = 6; // beyond this many rows per resident workgroup: one workgroup per row
 constexpr uint32_t kMaxDispatchItems = 0xFFFFFFFFu;  // work-items one dispatch holds (per dimension)
@@ -1277,7 +1282,7 @@ constexpr int kRowsWaves = 4;               // wavefronts per row
 constexpr int kRowsMaxD = 16 * kChunk;       // channels per row (4 chunks per wavefront)
 constexpr int kKeyChBits = 13;               // channel bits of the exact search's key (d <= 8192)
 constexpr int kTop1 = 16;  // largest k whose first threshold comes from one maximum per lane
-constexpr int kTop2 = 48;  // largest k whose first threshold takes two per wavefront lane
+constexpr int kTop2 = 48;  // largest k whose first threshold takes two per wavefront lane (beyond: four)
 
 // The third and fourth largest |E| of each (wavefront, lane), kept only with
 // the larger candidate list.
@@ -1299,7 +1304,7 @@ struct alignas(16) GroupShared : LaneMaxMore<NW, (CAP > kCandCap)> {
     uint32_t crw[CAP];   // their ref word (the bf16 pair holding the channel)
     uint32_t ccf[CAP];   // their group's coefficient pair
     uint32_t smax[NW][kWave]; // lane maxima of |E| of each wavefront
-    uint32_t smax2[NW][kWave];// the lanes' second largest |E| (kTop1 < k <= kTop2)
+    uint32_t smax2[NW][kWave];// the lanes' second largest |E| (k > kTop1)
     uint32_t thr;             // that threshold, from wavefront 0
     uint32_t cnt[2];          // candidate count (LDS atomic), by row parity
     uint32_t xn[2];           // count of the rebuilt list (exact search), by row parity
@@ -1420,9 +1425,9 @@ __device__ __forceinline__ void opaque_n(uint4 (&r)[N]) {
 // TWO: the first outlier threshold from the two largest |E| of each
 // (wavefront, lane) (for kTop1 < k <= kTop2; a separate kernel, so that the
 // other k keep the code and registers of the one-value bound).
-// BIG: the same threshold and a candidate list of 2 * kCandCap entries,
-// ranked two per lane (for k > kTop2, whose rows would overflow the smaller
-// list almost always).
+// BIG: the first threshold from the four largest |E| of each (wavefront,
+// lane) and a candidate list of 2 * kCandCap entries, ranked two per lane
+// (for k > kTop2, whose rows would overflow the smaller list almost always).
 template <int BITS, int GA, int GQ, int NW, int CPW, bool GIVEN, bool TWO, bool BIG = false>
 __global__ __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(CPW == 2 ? (BIG ? 6 : 7) : 4)))
 void rac_encode_rows_kernel(Args A) {
