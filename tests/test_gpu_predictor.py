@@ -92,8 +92,9 @@ def test_predictor_ragged_batch_with_staggered_and_restarted_positions():
     _run(cfg, 37, 12, pos)
 
 
-@pytest.mark.parametrize("batch", [1, 256])
+@pytest.mark.parametrize("batch", [1, 100, 256])
 def test_predictor_single_and_full_batches(batch):
+    # (100: the wide products with a ragged second tile of 64 rows)
     cfg = rac.PredictorConfig(4096, 512, 8, 2048, 64, 256)
     say(f"[gpu] predictor batch {batch}, 3 steps")
     _run(cfg, batch, 3, lambda s, b: s + 100 * (b % 2), seed=1)
