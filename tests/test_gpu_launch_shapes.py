@@ -42,6 +42,8 @@ CASES = {
     "per_token_1000x4096_g64_b2_k16": (cfgd(1000, 4096, 64, 64, 2, 16), 3),
     # 16 < k <= 48: the two-value threshold variant of the rows kernel
     "per_token_1500x2048_g128_b4_k32": (cfgd(1500, 2048, 128, 128, 4, 32), 5),
+    # k > 48: the four-value threshold and the list of 128 candidates
+    "per_token_2100x4096_g128_b4_k64": (cfgd(2100, 4096, 128, 128, 4, 64), 6),
 }
 
 
