@@ -158,6 +158,9 @@ class Codec:
         self.torch.cuda.empty_cache()
 
 
+SHAPE_REPS = 3  # back-to-back blocks per launch shape (their median is reported)
+
+
 def launch_shape_rates(torch, rac, C, iters):
     """Encode and decode times of one workload under each launch shape: the
     default choice and the two shapes forced by the launch hints (the strided
@@ -171,7 +174,7 @@ def launch_shape_rates(torch, rac, C, iters):
                        ("per_row", rac.RAC_FLAG_LAUNCH_PER_ROW)):
         C.cfg = dataclasses.replace(base, flags=base.flags | hint)
         C.warm(30)
-        e, d = C.steady(iters, reps=3)
+        e, d = C.steady(iters, reps=SHAPE_REPS)
         out[name] = {"encode_us": round(e, 2), "decode_us": round(d, 2)}
     C.cfg = base
     return out
@@ -847,6 +850,7 @@ def profile_run(torch, rac, wl, stream, workload, iters):
     elif workload == "predictor":
         out.update(predictor_latency(torch, rac, wl, stream, iters=iters))
     elif workload == "launch_shapes":
+        out["reps"] = SHAPE_REPS
         out.update(launch_shape_sweep(torch, rac, stream, iters))
     else:
         for bits, gq in ((2, 128), (4, 128), (8, 128), (4, 4096)):

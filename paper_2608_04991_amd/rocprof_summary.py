@@ -15,6 +15,12 @@
       configuration (LABELS.json: the bench's --profile output, whose
       configurations appear in launch order, two blocks each, or a list).
 
+  python -m paper_2608_04991_amd.rocprof_summary merged DIR MIN OUT.txt "COMMAND" LABELS.json
+      the blocks as above, merged by label (the launch-shape sweep repeats
+      each configuration's blocks): per label the number of blocks, the
+      median of their average durations, the range of those averages and
+      the workgroup count.
+
   python -m paper_2608_04991_amd.rocprof_summary grids DIR SUBSTR OUT.txt "COMMAND"
       per-shape statistics of the kernels whose name holds SUBSTR: one line
       per (kernel, workgroup count), for kernels that interleave with others
@@ -85,16 +91,22 @@ def stats(dirpath: str, out: str, command: str, last: int = 0) -> None:
 def _labels(path):
     """Configuration labels in launch order: a list, or the bench's --profile
     output (its configuration keys in order, each giving an encode block and
-    a decode block)."""
+    a decode block; a configuration whose entries are themselves per launch
+    shape gives, per shape, `reps` encode and decode blocks in turn)."""
     if not path:
         return None
     d = json.load(open(path))
     if isinstance(d, list):
         return d
+    reps = int(d.get("reps", 1))
     out = []
     for k, v in d.items():
         if isinstance(v, dict):
-            out += [f"{k} encode", f"{k} decode"]
+            if v and all(isinstance(x, dict) for x in v.values()):
+                for shape in v:
+                    out += [f"{k} {shape} encode", f"{k} {shape} decode"] * reps
+            else:
+                out += [f"{k} encode", f"{k} decode"]
     return out
 
 
@@ -134,6 +146,29 @@ def blocks(dirpath: str, min_len: str, out: str, command: str, labels: str = "")
         tag = lab[i] if lab and i < len(lab) else ""
         lines.append(f"{i:>5} {len(r):>6} {sum(us) / len(us):>10.2f} {min(us):>10.2f} {max(us):>10.2f} "
                      f"{r[0]['blocks']:>6}  {tag} | {r[0]['name'][:100]}")
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def merged(dirpath: str, min_len: str, out: str, command: str, labels: str) -> None:
+    runs = _runs(_trace_dispatches(dirpath), lambda d: (d["name"], d["blocks"]), int(min_len))
+    lab = _labels(labels)
+    if len(lab) != len(runs):
+        raise ValueError(f"{len(runs)} blocks in the trace but {len(lab)} labels")
+    acc = {}
+    for tag, r in zip(lab, runs):
+        e = acc.setdefault(tag, dict(avgs=[], wgs=r[0]["blocks"], name=r[0]["name"]))
+        if (r[0]["blocks"], r[0]["name"]) != (e["wgs"], e["name"]):
+            raise ValueError(f"blocks labelled {tag!r} launched different kernels or grids")
+        e["avgs"].append(sum(d["us"] for d in r) / len(r))
+    kern = lambda n: n.split("(anonymous namespace)::", 1)[-1].split("(")[0]
+    lines = ["# rocprofv3 kernel trace, blocks of back-to-back dispatches merged by label",
+             f"# command: {command}", "",
+             f"{'blocks':>6} {'median_us':>10} {'lo_us':>8} {'hi_us':>8} {'wgs':>6}  label | kernel"]
+    for tag, e in acc.items():
+        a = sorted(e["avgs"])
+        lines.append(f"{len(a):>6} {a[len(a) // 2]:>10.2f} {a[0]:>8.2f} {a[-1]:>8.2f} {e['wgs']:>6}  "
+                     f"{tag} | {kern(e['name'])}")
     open(out, "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
@@ -214,6 +249,8 @@ if __name__ == "__main__":
         stats(*sys.argv[2:5], *(int(a) for a in sys.argv[5:6]))
     elif len(sys.argv) > 1 and sys.argv[1] == "blocks":
         blocks(*sys.argv[2:7])
+    elif len(sys.argv) > 1 and sys.argv[1] == "merged":
+        merged(*sys.argv[2:7])
     elif len(sys.argv) > 1 and sys.argv[1] == "grids":
         grids(*sys.argv[2:6])
     elif len(sys.argv) > 1 and sys.argv[1] == "traffic":

@@ -63,3 +63,60 @@ def test_runs_keep_only_long_runs_of_codec_kernels():
     key = lambda d: (d["name"], d["blocks"])
     runs = rs._runs(items, key, 2)
     assert [(r[0]["name"], r[0]["blocks"], len(r)) for r in runs] == [("rac_a", 1, 2), ("rac_b", 1, 2)]
+
+
+def test_labels_expand_launch_shapes_into_repeated_blocks(tmp_path):
+    # the launch-shape sweep gives, per configuration and shape, `reps`
+    # back-to-back encode and decode blocks
+    p = tmp_path / "shapes.json"
+    p.write_text(json.dumps({"profile": "launch_shapes", "iters": 20, "reps": 2,
+                             "a": {"default": {"encode_us": 1.0}, "per_row": {"encode_us": 2.0}},
+                             "b": {"strided": {"encode_us": 3.0}}}))
+    assert rs._labels(str(p)) == ["a default encode", "a default decode"] * 2 + \
+        ["a per_row encode", "a per_row decode"] * 2 + ["b strided encode", "b strided decode"] * 2
+    assert rs._labels(None) is None
+    q = tmp_path / "list.json"
+    q.write_text(json.dumps(["x", "y"]))
+    assert rs._labels(str(q)) == ["x", "y"]
+
+
+def _trace(dirpath, dispatches):
+    """A kernel_trace.csv of (kernel, workgroups, µs) dispatches back to back."""
+    os.makedirs(os.path.join(dirpath, "run"), exist_ok=True)
+    f = ["Dispatch_Id", "Kernel_Name", "Workgroup_Size_X", "Workgroup_Size_Y", "Workgroup_Size_Z",
+         "Grid_Size_X", "Grid_Size_Y", "Grid_Size_Z", "Start_Timestamp", "End_Timestamp"]
+    with open(os.path.join(dirpath, "run", "p_kernel_trace.csv"), "w", newline="") as fh:
+        w = csv.DictWriter(fh, fieldnames=f)
+        w.writeheader()
+        t = 1000
+        for i, (name, wgs, us) in enumerate(dispatches):
+            w.writerow(dict(zip(f, [i + 1, name, 256, 1, 1, wgs * 256, 1, 1, t, t + int(us * 1000)])))
+            t += int(us * 1000) + 500
+
+
+def test_merged_takes_the_median_block_per_label(tmp_path):
+    enc = "void (anonymous namespace)::rac_encode_rows_kernel<4, 4>((anonymous namespace)::Args)"
+    dec = "void (anonymous namespace)::rac_decode_kernel<4, 1>((anonymous namespace)::Args)"
+    d = []
+    for rep, (e_us, d_us) in enumerate([(10.0, 6.0), (12.0, 5.0), (11.0, 7.0)]):
+        d += [(enc, 100, e_us)] * 4 + [(dec, 50, d_us)] * 4
+    d += [("at::native::fill", 1, 1.0)] * 4           # not a codec kernel: no block
+    d += [(enc, 200, 20.0)] * 4 + [(dec, 200, 9.0)] * 4
+    _trace(tmp_path / "t", d)
+    lab = tmp_path / "l.json"
+    lab.write_text(json.dumps({"profile": "launch_shapes", "reps": 3,
+                               "c": {"default": {}}, "e": {"per_row": {}}}))
+    # three repetitions of "c" but one of "e": the label count does not match
+    try:
+        rs.merged(str(tmp_path / "t"), "3", str(tmp_path / "o.txt"), "cmd", str(lab))
+        raise AssertionError("expected a label count mismatch")
+    except ValueError as err:
+        assert "8 blocks" in str(err) and "12 labels" in str(err)
+    d += [(enc, 200, 22.0)] * 4 + [(dec, 200, 8.0)] * 4 + [(enc, 200, 21.0)] * 4 + [(dec, 200, 10.0)] * 4
+    _trace(tmp_path / "t", d)
+    rs.merged(str(tmp_path / "t"), "3", str(tmp_path / "o.txt"), "cmd", str(lab))
+    rows = [l.split() for l in open(tmp_path / "o.txt").read().splitlines()[4:]]
+    got = {" ".join(r[5:8]): (int(r[0]), float(r[1]), float(r[2]), float(r[3]), int(r[4])) for r in rows}
+    assert got == {"c default encode": (3, 11.0, 10.0, 12.0, 100), "c default decode": (3, 6.0, 5.0, 7.0, 50),
+                   "e per_row encode": (3, 21.0, 20.0, 22.0, 200), "e per_row decode": (3, 9.0, 8.0, 10.0, 200)}
+    assert all(r[9].startswith("rac_") for r in rows)
