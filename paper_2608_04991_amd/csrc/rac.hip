@@ -796,13 +796,16 @@ __device__ __forceinline__ uint64_t block_starts(int lv) {
     }
 }
 
-// The lowest set bit of every aligned block of 2^lv bits of a lane mask
-// (scalar work: an OR-prefix inside the blocks, then the bits with nothing
-// set below them in their block).
+// The lowest set bit of every aligned block of 2^lv bits of a lane mask.
+// Each block less one, without a borrow crossing into the next block (the
+// blocks' top bits are set before the subtraction and put right after it),
+// clears the block's lowest set bit and sets the bits below it, so x & ~(x - 1)
+// per block is that bit; a zero block gives zero.  Six scalar instructions.
 __device__ __forceinline__ uint64_t block_firsts(uint64_t x, int lv, uint64_t starts) {
-    uint64_t p = x;
-    for (int s = 1; s < (1 << lv); s <<= 1) p |= (p << s) & ~(starts * ((1ull << s) - 1ull));
-    return x & ~((p << 1) & ~starts);
+    if (lv == 0) return x;
+    const uint64_t tops = starts << ((1 << lv) - 1);
+    const uint64_t less = ((x | tops) - starts) ^ (tops & ~x);
+    return x & ~less;
 }
 
 // Chooses the k_g outliers of the lane's group and returns the lane's mask of
@@ -810,11 +813,12 @@ __device__ __forceinline__ uint64_t block_firsts(uint64_t x, int lv, uint64_t st
 // group's largest remaining |E| and, among the channels holding it, the
 // lowest.  Magnitudes are compared as the integer patterns of |E|, a chosen
 // channel drops to -1, so a zero residual still outranks it, and k_g < g_q
-// leaves every round a candidate.  The tie-break is scalar work on the
-// wave-wide masks of lanes whose channel j holds the group maximum.  The
-// entries, (fp16 value | in-group offset << 16), go to `st` at their position
-// in the chunk's part of the row: group by group, ascending offset inside a
-// group.
+// leaves every round a candidate.  The lanes holding the group maximum are
+// those whose own maximum equals it; the lowest of them in each group keeps
+// its lowest channel holding it, a scalar walk over the wave-wide masks of
+// the lanes whose channel j does.  The entries, (fp16 value | in-group offset
+// << 16), go to `st` at their position in the chunk's part of the row: group
+// by group, ascending offset inside a group.
 template <int LV>
 __device__ __forceinline__ uint32_t select_group_outliers(const float* e, int lv, int kg, uint32_t lane,
                                                           uint32_t* st) {
@@ -823,32 +827,22 @@ __device__ __forceinline__ uint32_t select_group_outliers(const float* e, int lv
 #pragma unroll
     for (int j = 0; j < 8; ++j) a[j] = (int32_t)(__float_as_uint(e[j]) & 0x7FFFFFFFu);
     const uint64_t starts = block_starts(L);
-    uint64_t sel[8], pick[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) sel[j] = pick[j] = 0ull;
     for (int i = 0; i < kg; ++i) {
-        if (i > 0) {
-#pragma unroll
-            for (int j = 0; j < 8; ++j) a[j] = __builtin_amdgcn_inverse_ballot_w64(pick[j]) ? -1 : a[j];
-        }
         int32_t lb = a[0];
 #pragma unroll
         for (int j = 1; j < 8; ++j) lb = lb > a[j] ? lb : a[j];
         const int32_t m = imax_lanes<LV>(lb, L);
-        uint64_t hit[8], any = 0ull;
+        uint64_t lanes = block_firsts(ballot(lb == m), L, starts);  // one lane per group
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            hit[j] = ballot(a[j] == m);
-            any |= hit[j];
-        }
-        uint64_t free_lanes = block_firsts(any, L, starts);  // one lane per group
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            pick[j] = hit[j] & free_lanes;
-            free_lanes &= ~pick[j];
-            sel[j] |= pick[j];
+            const uint64_t hit = ballot(a[j] == m);
+            a[j] = __builtin_amdgcn_inverse_ballot_w64(hit & lanes) ? -1 : a[j];
+            lanes &= ~hit;
         }
     }
+    uint64_t sel[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sel[j] = ballot(a[j] == -1);
     uint32_t selm = 0u;
 #pragma unroll
     for (int j = 0; j < 8; ++j) selm |= __builtin_amdgcn_inverse_ballot_w64(sel[j]) ? (1u << j) : 0u;
