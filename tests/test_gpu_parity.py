@@ -244,6 +244,14 @@ CASES = {
                                  lambda: (wl.f32_to_bf16_bits(_zero_sum_integer_rows(6, 1024, 8, 0, 0.0, 8)), None)),
     "group_g16_11x2880_ga64_b4_kg3": (cfgd(11, 2880, 64, 16, 4, 3, GRP), lambda: _affine(11, 2880, 64, seed=3)),
     "group_g32_13x2880_ga64_b4_kg4": (cfgd(13, 2880, 64, 32, 4, 4, GRP), lambda: _affine(13, 2880, 64, seed=4)),
+    # ties at the largest k_g of each lane-block width (2, 4 and 32 lanes per
+    # group): every round of the choice meets several lanes holding the maximum
+    "group_ties_g16_8x2048_ga64_kg4": (cfgd(8, 2048, 64, 16, 4, 4, GRP),
+                                       lambda: (wl.f32_to_bf16_bits(_zero_sum_integer_rows(8, 2048, 16, 9, 3.0, 10)), None)),
+    "group_ties_g32_6x2048_ga64_kg8": (cfgd(6, 2048, 64, 32, 4, 8, GRP),
+                                       lambda: (wl.f32_to_bf16_bits(_zero_sum_integer_rows(6, 2048, 32, 7, 4.0, 11)), None)),
+    "group_ties_g256_4x4096_kg16": (cfgd(4, 4096, 256, 256, 4, 16, GRP),
+                                    lambda: (wl.f32_to_bf16_bits(_zero_sum_integer_rows(4, 4096, 256, 3, 5.0, 12)), None)),
 }
 
 
