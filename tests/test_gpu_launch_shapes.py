@@ -4,7 +4,8 @@ byte of the output.  Above 256 rows a launch runs either on the strided grid
 its next row prefetched) or on one workgroup per row; the default picks by
 rows per workgroup.  Each case runs the default, RAC_FLAG_LAUNCH_STRIDED and
 RAC_FLAG_LAUNCH_PER_ROW and requires identical wires and reconstructions; the
-default is also held to the oracle.
+default is also held to the oracle.  The cases cover the outlier modes, the
+bf16 reconstruction and a step table.
 """
 from __future__ import annotations
 
@@ -44,7 +45,21 @@ CASES = {
     "per_token_1500x2048_g128_b4_k32": (cfgd(1500, 2048, 128, 128, 4, 32), 5),
     # k > 48: the four-value threshold and the list of 128 candidates
     "per_token_2100x4096_g128_b4_k64": (cfgd(2100, 4096, 128, 128, 4, 64), 6),
+    # bf16 reconstruction from the rows kernel (one and two threshold values)
+    "per_token_bf16_2000x2048_g128_b4_k8": (cfgd(2000, 2048, 128, 128, 4, 8, rac.RAC_FLAG_XHAT_BF16), 7),
+    "per_token_bf16_1100x4096_g128_b3_k32": (cfgd(1100, 4096, 128, 128, 3, 32, rac.RAC_FLAG_XHAT_BF16), 8),
+    # a step table (the chunk kernel's per-token and per-group selections;
+    # codes clip by design)
+    "fixed_step_per_token_1800x2048_g128_b4_k4": (cfgd(1800, 2048, 128, 128, 4, 4, rac.RAC_FLAG_FIXED_STEP), 9),
+    "fixed_step_per_group_1500x1024_g64_b4_kg2": (cfgd(1500, 1024, 64, 64, 4, 2, rac.RAC_FLAG_FIXED_STEP | GRP), 10),
 }
+
+
+def _steps(c, seed):
+    """A step per quantization group for the step-table cases (None otherwise)."""
+    if not c["flags"] & rac.RAC_FLAG_FIXED_STEP:
+        return None
+    return np.random.default_rng(seed).uniform(0.01, 0.2, c["hidden"] // c["group_quant"]).astype(np.float32)
 
 
 @pytest.mark.parametrize("name", list(CASES))
@@ -52,14 +67,15 @@ def test_launch_shapes_give_identical_bytes(name):
     c, seed = CASES[name]
     T, d = c["tokens"], c["hidden"]
     xb, rb, _ = wl.prefill_uplink(seed, tokens=T, hidden=d)
+    steps = _steps(c, seed)
     outs = []
     for hint in HINTS:
         say(f"[gpu] launch shapes {name}: hint {hint}")
-        outs.append(gpu_run(dict(c, flags=c["flags"] | hint), xb, rb))
+        outs.append(gpu_run(dict(c, flags=c["flags"] | hint), xb, rb, steps))
     for o in outs[1:]:
         for a, b in zip(outs[0], o):
             assert np.array_equal(_bytes(a), _bytes(b))
-    ow, ox = oracle_run(c, xb, rb)
+    ow, ox = oracle_run(c, xb, rb, steps)
     assert_parity(c, outs[0][0], outs[0][1], ow, ox)
 
 
